@@ -1,0 +1,355 @@
+#!/usr/bin/env python3
+"""Benchmark of the OffQ W4A4 online path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+One step = the whole online path of one quantized linear layer on one batch:
+fused rotate + quantize of the bf16 activations (offq_rotate_quantize), then
+the int4 x int4 GEMM with the dequantising epilogue (offq_w4a4_gemm).  The
+default workload is the attention-projection prefill layer
+X bf16 [2048, 4096] -> Y bf16 [2048, 4096] with W int4 [4096, 4096] and a
+4096-point Hadamard.  Inputs are synthetic (seeded), resident in HBM before
+the timed region; several input/weight sets whose total exceeds the 256 MB
+last-level cache are cycled so that every step reads from HBM.
+
+Prints ONE JSON line: the step throughput (integer TOP/s of the GEMM work per
+step time), per-kernel times from HIP events recorded on the launch stream,
+the roofline of the dominant kernel, and the CPU oracle timed on the host.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "W4A4 offset-GEMM int TOPS (prefill) + quantize/decode HBM GB/s vs peak"
+PEAK_INT8_TOPS = 5000.0     # MI355X dense int8 MFMA, 5.0 POP/s
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, 8 TB/s
+LLC_BYTES = 256 << 20       # MI355X Infinity Cache
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", default="attn_proj_prefill",
+                   choices=["attn_proj_prefill", "mlp_prefill", "decode", "kv_chain"])
+    p.add_argument("--decode-m", type=int, default=16)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args()
+
+
+def rq_bytes(M, K, g):
+    """Algorithmic HBM bytes of rotate-quantize: bf16 read, 4-bit codes, fp16 scale + int16 zero."""
+    return M * K * 2 + M * K // 2 + 4 * M * (K // g)
+
+
+def gemv_bytes(M, N, K, g):
+    """Algorithmic HBM bytes of the decode GEMV (weights dominate)."""
+    G = K // g
+    return N * K // 2 + 2 * N + 4 * G * N + M * K // 2 + 4 * M * G + 2 * M * N
+
+
+def source_hash(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(kernel_key):
+    """HBM bytes per launch measured with rocprofv3 counters (profiles/traffic.json),
+    or None when the kernel source changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    e = d.get(kernel_key)
+    if not e:
+        return None
+    if e.get("source_hash") != source_hash(e["sources"]):
+        return None
+    return e.get("bytes_per_launch")
+
+
+class Sets:
+    """Several independent input/output buffer sets, cycled per step."""
+
+    def __init__(self, make, bytes_per_set):
+        self.n = max(3, -(-2 * LLC_BYTES // max(bytes_per_set, 1)))
+        self.n = min(self.n, 16)
+        self.sets = [make(i) for i in range(self.n)]
+
+    def __getitem__(self, i):
+        return self.sets[i % self.n]
+
+
+def make_layer_set(offq, inputs, torch, M, K, N, g, seed, spec):
+    x = inputs.activations_device(M, K, seed=seed, device="cuda", **spec)
+    w = inputs.weights_device(N, K, seed=seed, device="cuda")
+    wc, ws, wcs = offq.offq_pack_weights(w, g)
+    del w
+    return dict(x=x, wc=wc, ws=ws, wcs=wcs,
+                codes=torch.empty((M, K // 2), dtype=torch.uint8, device="cuda"),
+                scale=torch.empty((M, K // g), dtype=torch.float16, device="cuda"),
+                zero=torch.empty((M, K // g), dtype=torch.int16, device="cuda"),
+                y=torch.empty((M, N), dtype=torch.bfloat16, device="cuda"),
+                M=M, K=K, N=N, g=g)
+
+
+def run_rq(lib, s, stream):
+    return lib.offq_rotate_quantize_raw(s["x"].data_ptr(), s["M"], s["K"], s["K"], s["g"], 1,
+                                        s["codes"].data_ptr(), s["scale"].data_ptr(),
+                                        s["zero"].data_ptr(), None, stream)
+
+
+def run_gemm(lib, s, stream):
+    return lib.offq_w4a4_gemm_raw(s["codes"].data_ptr(), s["scale"].data_ptr(), s["zero"].data_ptr(),
+                                  s["wc"].data_ptr(), s["ws"].data_ptr(), s["wcs"].data_ptr(),
+                                  s["M"], s["N"], s["K"], s["g"], s["y"].data_ptr(), s["N"], None,
+                                  stream)
+
+
+def cpu_baseline(M, K, N, g, spec, seed):
+    """The CPU oracle on the same workload (full step, repeated to >= 10 s)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import gemm as OG
+    from oracle import hadamard as OH
+    from oracle import quantizer as OQ
+    from paper_2606_07116_amd import inputs
+
+    x = inputs.activations(M, K, seed=seed, **spec)
+    w = inputs.weights(N, K, seed=seed)
+    q_w, sw = OQ.quantize_weights(w)          # offline weight prep: not timed
+    cs = OQ.colsum(q_w, g)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        y = OH.rotate(x, g).astype(np.float32)
+        q, s, z = OQ.quantize_groups(y, g)
+        acc = OG.int_gemm_groups(q, q_w, g)
+        out = OG.epilogue(acc, s, z, sw, cs)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= 10.0 or reps >= 50:
+            break
+    del out
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": round(2.0 * M * N * K * reps / el / 1e12, 4), "unit": "TOPS",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"full step (rotate fp64, quantize, int GEMM via fp64 BLAS, epilogue) "
+                      f"on M={M},K={K},N={N}, {reps} repetition(s) in {el:.1f} s; BLAS "
+                      f"threads={threads}, elementwise stages single-threaded"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "multi-GPU sharding is described in DESIGN.md but not built", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2606_07116_amd as offq
+    from paper_2606_07116_amd import _lib, inputs
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    wl = args.workload
+
+    def check(st, what):
+        if st != 0:
+            raise RuntimeError(f"{what}: {_lib.status_name(st)}: {_lib.last_error()}")
+
+    kernels = {}   # name -> list of (start_event, end_event)
+    steps = []     # list of callables producing one step (each records its own events)
+
+    if wl in ("attn_proj_prefill", "kv_chain"):
+        cfg = inputs.WORKLOADS["attn_proj_prefill" if wl == "attn_proj_prefill" else "kv_chain_proj"]
+        M, K, N, g = cfg["M"], cfg["K"], cfg["N"], cfg["g"]
+        spec = dict(n_outliers=cfg["n_outliers"], lo=cfg["lo"], hi=cfg["hi"])
+        per_set = M * K * 2 + N * K // 2 + M * K // 2 + M * N * 2
+        sets = Sets(lambda i: make_layer_set(offq, inputs, torch, M, K, N, g, cfg["seed"] + 100 * i,
+                                             spec), per_set)
+        layers = [("rotate_quantize", "w4a4_gemm", sets)]
+        work_ops = 2.0 * M * N * K
+        config = {"workload": wl, "M": M, "K": K, "N": N, "g": g,
+                  "step": "rotate_quantize + w4a4_gemm", "input_sets": sets.n}
+        if wl == "kv_chain":
+            kc = inputs.WORKLOADS["kv_cache"]
+            B, H, S, Dh = kc["B"], kc["H"], kc["S"], kc["Dh"]
+            kv = [inputs.kv_cache_device(B, H, S, Dh, seed=kc["seed"] + j, device="cuda",
+                                         n_outliers=kc["n_outliers"], lo=kc["lo"], hi=kc["hi"])
+                  for j in range(2)]
+            R = B * H * S
+            kvo = [dict(codes=torch.empty((R, Dh // 2), dtype=torch.uint8, device="cuda"),
+                        scale=torch.empty((R,), dtype=torch.float16, device="cuda"),
+                        zero=torch.empty((R,), dtype=torch.int16, device="cuda")) for _ in range(2)]
+            config.update({"kv_shape": [B, H, S, Dh], "step": "kv_quantize(K) + kv_quantize(V) + "
+                           "rotate_quantize + w4a4_gemm"})
+    elif wl == "mlp_prefill":
+        up = inputs.WORKLOADS["mlp_up_gate_prefill"]
+        dn = inputs.WORKLOADS["mlp_down_prefill"]
+        spec_u = dict(n_outliers=up["n_outliers"], lo=up["lo"], hi=up["hi"],
+                      spike_frac=up["spike_frac"], spike_mult=up["spike_mult"])
+        spec_d = dict(n_outliers=dn["n_outliers"], lo=dn["lo"], hi=dn["hi"],
+                      spike_frac=dn["spike_frac"], spike_mult=dn["spike_mult"])
+        per_u = up["M"] * up["K"] * 2 + up["N"] * up["K"] + up["M"] * up["N"] * 4
+        per_d = dn["M"] * dn["K"] * 2 + dn["N"] * dn["K"] // 2 + dn["M"] * dn["N"] * 2
+        su = Sets(lambda i: make_layer_set(offq, inputs, torch, up["M"], up["K"], 2 * up["N"], up["g"],
+                                           up["seed"] + 100 * i, spec_u), per_u)
+        sd = Sets(lambda i: make_layer_set(offq, inputs, torch, dn["M"], dn["K"], dn["N"], dn["g"],
+                                           dn["seed"] + 100 * i, spec_d), per_d)
+        layers = [("rotate_quantize_up", "w4a4_gemm_upgate", su),
+                  ("rotate_quantize_down", "w4a4_gemm_down", sd)]
+        work_ops = 2.0 * up["M"] * 2 * up["N"] * up["K"] + 2.0 * dn["M"] * dn["N"] * dn["K"]
+        config = {"workload": wl, "up_gate": [up["M"], up["K"], 2 * up["N"], up["g"]],
+                  "down": [dn["M"], dn["K"], dn["N"], dn["g"]],
+                  "step": "rotate_quantize + gemm(up|gate, N=28672) + rotate_quantize(g=512) + gemm(down)",
+                  "input_sets": [su.n, sd.n]}
+    else:  # decode
+        up = inputs.WORKLOADS["decode_up"]
+        dn = inputs.WORKLOADS["decode_down"]
+        Md = args.decode_m
+        spec = dict(n_outliers=up["n_outliers"], lo=up["lo"], hi=up["hi"])
+        per = up["N"] * up["K"] // 2 * 2
+        su = Sets(lambda i: make_layer_set(offq, inputs, torch, Md, up["K"], up["N"], up["g"],
+                                           up["seed"] + 100 * i, spec), per)
+        sd = Sets(lambda i: make_layer_set(offq, inputs, torch, Md, dn["K"], dn["N"], dn["g"],
+                                           dn["seed"] + 100 * i, spec), per)
+        layers = [("rotate_quantize_up", "w4a4_gemv_up", su), ("rotate_quantize_down", "w4a4_gemv_down", sd)]
+        work_ops = None
+        gbytes = gemv_bytes(Md, up["N"], up["K"], up["g"]) + gemv_bytes(Md, dn["N"], dn["K"], dn["g"])
+        config = {"workload": wl, "M": Md, "up": [up["K"], up["N"], up["g"]],
+                  "down": [dn["K"], dn["N"], dn["g"]], "step": "(rotate_quantize + w4a4_gemv) x2",
+                  "input_sets": [su.n, sd.n]}
+
+    torch.cuda.synchronize()
+
+    def record(name, fn):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        check(fn(), name)
+        b.record(stream)
+        kernels.setdefault(name, []).append((a, b))
+
+    def one_step(i, timed):
+        if wl == "kv_chain":
+            for j in range(2):
+                fn = (lambda j=j: _lib.offq_kv_quantize_raw(kv[j].data_ptr(), R, Dh, Dh, 1,
+                                                            kvo[j]["codes"].data_ptr(),
+                                                            kvo[j]["scale"].data_ptr(),
+                                                            kvo[j]["zero"].data_ptr(), None, sp))
+                if timed:
+                    record("kv_quantize", fn)
+                else:
+                    check(fn(), "kv_quantize")
+        for rq_name, mm_name, sets_ in layers:
+            s = sets_[i]
+            if timed:
+                record(rq_name, lambda: run_rq(_lib, s, sp))
+                record(mm_name, lambda: run_gemm(_lib, s, sp))
+            else:
+                check(run_rq(_lib, s, sp), rq_name)
+                check(run_gemm(_lib, s, sp), mm_name)
+
+    for i in range(args.warmup):
+        one_step(i, False)
+    torch.cuda.synchronize()
+    kernels.clear()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for i in range(args.steps):
+        one_step(args.warmup + i, True)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms = t_start.elapsed_time(t_end) / args.steps
+
+    comp = {}
+    for name, evs in kernels.items():
+        times = sorted(a.elapsed_time(b) for a, b in evs)
+        us = 1000.0 * sum(times) / len(times)
+        comp[name] = {"us": round(us, 3), "us_p10": round(1000 * times[len(times) // 10], 3),
+                      "us_p90": round(1000 * times[(9 * len(times)) // 10], 3)}
+
+    def ann_rq(name, M, K, g, n=1):
+        b = rq_bytes(M, K, g) * n
+        comp[name]["alg_bytes"] = b
+        comp[name]["GBs"] = round(b / (comp[name]["us"] * 1e-6) / 1e9, 1)
+        comp[name]["frac_hbm"] = round(comp[name]["GBs"] / PEAK_HBM_GBS, 4)
+
+    def ann_mm(name, M, N, K):
+        ops = 2.0 * M * N * K
+        comp[name]["alg_ops"] = ops
+        comp[name]["TOPS"] = round(ops / (comp[name]["us"] * 1e-6) / 1e12, 1)
+        comp[name]["frac_int8_peak"] = round(comp[name]["TOPS"] / PEAK_INT8_TOPS, 4)
+
+    gemm_src = ["paper_2606_07116_amd/csrc/w4a4_gemm.hip", "paper_2606_07116_amd/csrc/common.h"]
+    rq_src = ["paper_2606_07116_amd/csrc/rotate_quantize.hip", "paper_2606_07116_amd/csrc/common.h"]
+    if wl in ("attn_proj_prefill", "kv_chain"):
+        ann_rq("rotate_quantize", M, K, g)
+        ann_mm("w4a4_gemm", M, N, K)
+        if wl == "kv_chain":
+            ann_rq("kv_quantize", R, Dh, Dh)
+        value = work_ops / (ms * 1e-3) / 1e12
+        unit = "TOPS"
+        dom = "w4a4_gemm"
+        roof = {"bound": "mfma", "achieved": comp[dom]["TOPS"], "peak": PEAK_INT8_TOPS,
+                "unit": "TOP/s", "frac": comp[dom]["frac_int8_peak"],
+                "traffic": traffic_for(f"w4a4_gemm:{wl}"), "kernel": dom,
+                "alg_ops_per_launch": comp[dom]["alg_ops"], "avg_launch_us": comp[dom]["us"]}
+    elif wl == "mlp_prefill":
+        ann_rq("rotate_quantize_up", up["M"], up["K"], up["g"])
+        ann_rq("rotate_quantize_down", dn["M"], dn["K"], dn["g"])
+        ann_mm("w4a4_gemm_upgate", up["M"], 2 * up["N"], up["K"])
+        ann_mm("w4a4_gemm_down", dn["M"], dn["N"], dn["K"])
+        value = work_ops / (ms * 1e-3) / 1e12
+        unit = "TOPS"
+        dom = "w4a4_gemm_upgate"
+        roof = {"bound": "mfma", "achieved": comp[dom]["TOPS"], "peak": PEAK_INT8_TOPS,
+                "unit": "TOP/s", "frac": comp[dom]["frac_int8_peak"],
+                "traffic": traffic_for(f"w4a4_gemm:{wl}"), "kernel": dom,
+                "alg_ops_per_launch": comp[dom]["alg_ops"], "avg_launch_us": comp[dom]["us"]}
+    else:
+        ann_rq("rotate_quantize_up", Md, up["K"], up["g"])
+        ann_rq("rotate_quantize_down", Md, dn["K"], dn["g"])
+        for name, c in (("w4a4_gemv_up", up), ("w4a4_gemv_down", dn)):
+            b = gemv_bytes(Md, c["N"], c["K"], c["g"])
+            comp[name]["alg_bytes"] = b
+            comp[name]["GBs"] = round(b / (comp[name]["us"] * 1e-6) / 1e9, 1)
+            comp[name]["frac_hbm"] = round(comp[name]["GBs"] / PEAK_HBM_GBS, 4)
+        value = gbytes / (ms * 1e-3) / 1e9
+        unit = "GB/s"
+        dom = "w4a4_gemv_up"
+        roof = {"bound": "hbm", "achieved": comp[dom]["GBs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": comp[dom]["frac_hbm"], "traffic": traffic_for(f"w4a4_gemv:{wl}"),
+                "kernel": dom, "alg_bytes_per_launch": comp[dom]["alg_bytes"],
+                "avg_launch_us": comp[dom]["us"]}
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": unit, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int4 codes on i8 MFMA (i32 accumulate), fp32 rotation",
+        "data": "synthetic (seeded Llama-shaped activations with structured outliers; random weights)",
+        "config": config, "roofline": roof, "components": comp,
+    }
+    if not args.no_cpu_baseline and wl in ("attn_proj_prefill",):
+        out["cpu_baseline"] = cpu_baseline(M, K, N, g, spec, cfg["seed"])
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,170 @@
+/*
+ * offq.h -- C ABI of the MI355X (gfx950) OffQ W4A4KV4 online path.
+ *
+ * OffQ ("Taming Structured Outliers in LLM Quantization by Offsetting")
+ * concentrates the structured activation outliers into the first channel of
+ * each channel group (top-1 PCA rotation and grouping permutation, fused into
+ * the weights offline), then applies an online Hadamard rotation whose first
+ * row is all ones, so that this channel becomes a constant offset of the group
+ * (sec. 3.2, Eq. 4 and Eq. 5), and absorbs that offset into the integer
+ * zero-point of a per-group asymmetric 4-bit quantizer (sec. 3, Eq. 1).  All
+ * matrix products then run on 4-bit integer codes.
+ *
+ * This library implements the online part only: the fused rotate + quantize
+ * of activations, the int4 x int4 GEMM (and its decode-shape GEMV) with the
+ * dequantising epilogue, the KV-cache quantizer, and an offline helper that
+ * packs weights into the operand format the GEMM reads.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All data pointers are DEVICE pointers, allocated and freed by the caller;
+ *   the library allocates nothing and keeps no per-call state.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   Every call only enqueues work on `stream` and returns without
+ *   synchronising; device faults surface at the caller's next sync.
+ * - Arguments are validated on the host before anything is enqueued; a call
+ *   that returns an error has enqueued nothing.  `offq_last_error()` gives a
+ *   message for the last failing call of the calling thread.
+ * - bf16 and fp16 tensors are passed as uint16_t bit patterns.
+ * - Packed 4-bit codes: two per byte, channel 2j in the low nibble of byte j,
+ *   channel 2j+1 in the high nibble.  Activation codes are unsigned 0..15;
+ *   weight codes are 4-bit two's complement -8..7.
+ * - Numerics: inputs are assumed finite.  NaN/Inf inputs give unspecified
+ *   codes and outputs but never an out-of-bounds access.
+ * - M == 0 (or rows == 0) is valid and enqueues nothing; the data pointers
+ *   may then be NULL.
+ *
+ * The quantizer (sec. 3, Eq. 1, with 16-bit scale and 16-bit zero-point as in
+ * sec. 3.4), for every group y[0..g) of fp32 values:
+ *     mx = max y, mn = min y
+ *     s  = fl32(fl32(mx - mn) / 15); if mx == mn: s = |mn| (1 if mn == 0)
+ *     s16 = fp16_rne(clamp(s, 2^-24, 65504)),  sq = (float)s16,  r = fl32(1/sq)
+ *     z  = clamp(rne(-mn * r), -32768, 32767)         (exact product)
+ *     q  = clamp(rne(y * r) + z, 0, 15)               (exact product)
+ * and x_hat = sq * (q - z) reconstructs y.
+ */
+#ifndef OFFQ_H
+#define OFFQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OFFQ_OK = 0,
+  OFFQ_ERR_INVALID = 1,      /* bad pointer, size, stride or alignment        */
+  OFFQ_ERR_UNSUPPORTED = 2,  /* valid but unsupported: g out of range, not gfx950 */
+  OFFQ_ERR_HIP = 3           /* the HIP runtime reported an error at launch     */
+} offq_status_t;
+
+/* Version of this ABI; bumped on any incompatible change. */
+#define OFFQ_ABI_VERSION 1
+int offq_abi_version(void);
+
+/* Static, human-readable name of a status code. */
+const char* offq_status_string(int status);
+
+/* Message describing the last failing call made by the calling thread
+ * (empty string if none).  Valid until the next call on that thread. */
+const char* offq_last_error(void);
+
+/*
+ * offq_rotate_quantize -- fused online block-Hadamard rotation + per-group
+ * 4-bit quantization of activations (sec. 3.2 Eq. 4 and group-wise offsetting;
+ * sec. 3 Eq. 1; sec. 3.3 step 2(4) for the online group-wise H4).
+ *
+ *   For every row m and group b (channels [b*g, (b+1)*g)):
+ *     y = x[m, group b] * H_g * c   if apply_hadamard   (H_g Sylvester, c = fl32(1/sqrt(g)))
+ *     y = x[m, group b]             otherwise
+ *   then the quantizer above on y.  The first channel of each group becomes
+ *   the group's constant offset, which the zero-point absorbs.
+ *
+ *   x        bf16 [M, K], row stride ldx elements (ldx >= K, ldx % 8 == 0),
+ *            16-byte aligned.
+ *   M, K     rows (tokens) and channels; K % g == 0.
+ *   g        group = Hadamard block size, power of two, 16 <= g <= 8192
+ *            (g == K: one group per token).
+ *   apply_hadamard  1 = rotate then quantize, 0 = quantize only (inputs whose
+ *            rotation is already fused into the producing weights).
+ *   codes    uint8 [M, K/2] packed unsigned codes, contiguous, 4-byte aligned.
+ *   scale    fp16  [M, K/g] scales sq, contiguous.
+ *   zero     int16 [M, K/g] zero-points z, contiguous.
+ *   y_debug  nullable fp32 [M, K] contiguous, 16-byte aligned: if non-NULL,
+ *            receives exactly the fp32 values that were quantized.
+ */
+int offq_rotate_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
+                         int32_t g, int32_t apply_hadamard,
+                         uint8_t* codes, uint16_t* scale, int16_t* zero,
+                         float* y_debug, void* stream);
+
+/*
+ * offq_w4a4_gemm -- int4 x int4 GEMM with int32 accumulation and the
+ * dequantising epilogue that follows from Eq. 1 (x_hat = s (q_a - z),
+ * w_hat = sw q_w):
+ *
+ *   acc_b[m, n] = sum_{k in group b} q_a[m, k] * q_w[n, k]           (int32)
+ *   Y[m, n]     = sw[n] * sum_b s[m, b] * (acc_b[m, n] - z[m, b] * colsum[b, n])
+ *
+ *   The z * colsum term is the zero-point (offset) correction through
+ *   per-column weight sums.  Y is rounded to bf16 (nearest even).  Shapes with
+ *   M <= 16 (decode) take a weight-streaming GEMV path; larger M the MFMA
+ *   GEMM path.  Results are identical up to fp32 summation order.
+ *
+ *   a_codes  uint8 [M, K/2] (from offq_rotate_quantize), 16-byte aligned.
+ *   a_scale  fp16  [M, K/g];  a_zero int16 [M, K/g].
+ *   w_codes  uint8 [N, K/2] two's-complement int4, 16-byte aligned.
+ *   w_scale  fp16  [N] per-output-channel symmetric scale sw.
+ *   w_colsum int32 [K/g, N]: colsum[b, n] = sum_{k in group b} q_w[n, k].
+ *   M, N, K  K % g == 0; g power of two, 64 <= g <= 8192.
+ *   y        bf16 [M, N], row stride ldy >= N elements.
+ *   acc_debug nullable int32 [K/g, M, N] contiguous: if non-NULL, receives
+ *            every per-group integer accumulator acc_b.
+ */
+int offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale,
+                   const int16_t* a_zero, const uint8_t* w_codes,
+                   const uint16_t* w_scale, const int32_t* w_colsum,
+                   int64_t M, int64_t N, int64_t K, int32_t g,
+                   uint16_t* y, int64_t ldy, int32_t* acc_debug, void* stream);
+
+/*
+ * offq_kv_quantize -- 4-bit KV-cache quantization: one row = one (batch,
+ * head, position); group = head_dim (sec. 4.2, "Number of Groups").  With
+ * apply_hadamard = 1 the row first receives the per-head online Hadamard H3
+ * (sec. 3.3 step 2(3), keys after RoPE); values, whose rotation R2 is fused
+ * offline (sec. 3.3 step 2(2)), use apply_hadamard = 0.
+ *
+ *   kv        bf16 [rows, head_dim], row stride row_stride elements
+ *             (>= head_dim, % 8 == 0), 16-byte aligned.
+ *   head_dim  power of two, 16 <= head_dim <= 8192 (128 for Llama-class).
+ *   codes     uint8 [rows, head_dim/2]; scale fp16 [rows]; zero int16 [rows].
+ *   y_debug   nullable fp32 [rows, head_dim].
+ */
+int offq_kv_quantize(const uint16_t* kv, int64_t rows, int32_t head_dim,
+                     int64_t row_stride, int32_t apply_hadamard,
+                     uint8_t* codes, uint16_t* scale, int16_t* zero,
+                     float* y_debug, void* stream);
+
+/*
+ * offq_pack_weights -- offline helper: per-output-channel symmetric 4-bit
+ * weight quantization (sec. 4, implementation: per-channel symmetric weights)
+ * into the operand format of offq_w4a4_gemm.
+ *
+ *   sw[n]  = fp16_rne(clamp(max_k |w[n,k]| / 7, 2^-24, 65504))  (1 for a zero row)
+ *   q[n,k] = clamp(rne(w[n,k] / sw[n]), -8, 7)                   (exact quotient)
+ *   colsum[b, n] = sum_{k in group b} q[n, k]
+ *
+ *   w        fp32 [N, K] contiguous, 16-byte aligned.
+ *   g        group size the activations will use (power of two, 64..8192, K % g == 0).
+ *   w_codes  uint8 [N, K/2]; w_scale fp16 [N]; w_colsum int32 [K/g, N].
+ */
+int offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g,
+                      uint8_t* w_codes, uint16_t* w_scale, int32_t* w_colsum,
+                      void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OFFQ_H */

@@ -1,1 +1,24 @@
-"""MI355X-native OffQ W4A4KV4 online path (HIP kernels behind a C ABI)."""
+"""MI355X-native OffQ W4A4KV4 online path (HIP kernels behind a C ABI).
+
+The compute lives in ``liboffq.so`` (HIP, gfx950); this package only marshals
+arguments.  Entry points (same names as ``include/offq.h``):
+
+    offq_rotate_quantize(x, g, apply_hadamard=True, debug=False)
+    offq_w4a4_gemm(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, g, debug=False)
+    offq_kv_quantize(kv, apply_hadamard=True, debug=False)
+    offq_pack_weights(w, g)
+
+Importing the package loads the library and raises if it has not been built.
+"""
+
+from ._lib import (  # noqa: F401
+    ABI_VERSION,
+    EXPORTED,
+    OffqError,
+    last_error,
+    offq_kv_quantize,
+    offq_pack_weights,
+    offq_rotate_quantize,
+    offq_w4a4_gemm,
+    status_name,
+)

@@ -1,0 +1,218 @@
+"""ctypes binding of liboffq.so (argument marshalling only).
+
+Every entry point of ``include/offq.h`` is exposed under the same name.  The
+``*_raw`` functions take plain integers (device addresses, sizes, a stream
+handle) exactly like the C functions; the tensor-level wrappers take torch
+device tensors, check dtype/shape/contiguity, allocate outputs with torch and
+pass ``data_ptr()`` and the current HIP stream.  All arithmetic happens in the
+HIP kernels of the library; if the library is missing, importing this module
+raises -- there is no fallback path.
+"""
+
+import ctypes
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "liboffq.so")
+
+OFFQ_OK = 0
+OFFQ_ERR_INVALID = 1
+OFFQ_ERR_UNSUPPORTED = 2
+OFFQ_ERR_HIP = 3
+
+EXPORTED = (
+    "offq_abi_version",
+    "offq_status_string",
+    "offq_last_error",
+    "offq_rotate_quantize",
+    "offq_w4a4_gemm",
+    "offq_kv_quantize",
+    "offq_pack_weights",
+)
+
+
+class OffqError(RuntimeError):
+    def __init__(self, status, fn, msg):
+        super().__init__(f"{fn}: {status_name(status)}: {msg}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2606_07116_amd.build` "
+            "(there is no non-HIP fallback)")
+    # torch ships its own HIP runtime (SONAME libamdhip64.so.7).  Import it
+    # first so that the library binds to that same runtime: a second runtime in
+    # the process would not understand torch's stream handles or allocations.
+    import torch  # noqa: F401
+
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+    lib.offq_abi_version.restype = ctypes.c_int
+    lib.offq_abi_version.argtypes = []
+    lib.offq_status_string.restype = ctypes.c_char_p
+    lib.offq_status_string.argtypes = [ctypes.c_int]
+    lib.offq_last_error.restype = ctypes.c_char_p
+    lib.offq_last_error.argtypes = []
+    lib.offq_rotate_quantize.restype = ctypes.c_int
+    lib.offq_rotate_quantize.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp]
+    lib.offq_w4a4_gemm.restype = ctypes.c_int
+    lib.offq_w4a4_gemm.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i32, vp, i64, vp, vp]
+    lib.offq_kv_quantize.restype = ctypes.c_int
+    lib.offq_kv_quantize.argtypes = [vp, i64, i32, i64, i32, vp, vp, vp, vp, vp]
+    lib.offq_pack_weights.restype = ctypes.c_int
+    lib.offq_pack_weights.argtypes = [vp, i64, i64, i32, vp, vp, vp, vp]
+    return lib
+
+
+lib = _load()
+ABI_VERSION = lib.offq_abi_version()
+
+
+def status_name(status):
+    return lib.offq_status_string(int(status)).decode()
+
+
+def last_error():
+    return lib.offq_last_error().decode()
+
+
+def _check(status, fn):
+    if status != OFFQ_OK:
+        raise OffqError(status, fn, last_error())
+
+
+# ---------------------------------------------------------------- raw C calls
+def offq_rotate_quantize_raw(x, M, K, ldx, g, apply_hadamard, codes, scale, zero, y_debug, stream):
+    return lib.offq_rotate_quantize(x, M, K, ldx, g, apply_hadamard, codes, scale, zero, y_debug, stream)
+
+
+def offq_w4a4_gemm_raw(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, g, y, ldy,
+                       acc_debug, stream):
+    return lib.offq_w4a4_gemm(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, g, y,
+                              ldy, acc_debug, stream)
+
+
+def offq_kv_quantize_raw(kv, rows, head_dim, row_stride, apply_hadamard, codes, scale, zero,
+                         y_debug, stream):
+    return lib.offq_kv_quantize(kv, rows, head_dim, row_stride, apply_hadamard, codes, scale, zero,
+                                y_debug, stream)
+
+
+def offq_pack_weights_raw(w, N, K, g, w_codes, w_scale, w_colsum, stream):
+    return lib.offq_pack_weights(w, N, K, g, w_codes, w_scale, w_colsum, stream)
+
+
+# ------------------------------------------------------------ tensor wrappers
+def _torch():
+    import torch
+    return torch
+
+
+def _stream():
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _need(t, dtype, name, ndim=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims")
+
+
+def offq_rotate_quantize(x, g, apply_hadamard=True, debug=False):
+    """x: bf16 [M, K] (last dim contiguous).  Returns (codes u8 [M, K/2],
+    scale fp16 [M, K/g], zero int16 [M, K/g], y fp32 [M, K] or None)."""
+    torch = _torch()
+    _need(x, torch.bfloat16, "x", 2)
+    if x.stride(1) != 1:
+        raise ValueError("x must have a contiguous last dimension")
+    M, K = x.shape
+    dev = x.device
+    codes = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+    scale = torch.empty((M, K // g), dtype=torch.float16, device=dev)
+    zero = torch.empty((M, K // g), dtype=torch.int16, device=dev)
+    y = torch.empty((M, K), dtype=torch.float32, device=dev) if debug else None
+    _check(lib.offq_rotate_quantize(_ptr(x), M, K, x.stride(0), int(g), int(bool(apply_hadamard)),
+                                    _ptr(codes), _ptr(scale), _ptr(zero), _ptr(y), _stream()),
+           "offq_rotate_quantize")
+    return codes, scale, zero, y
+
+
+def offq_w4a4_gemm(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, g, debug=False, out=None):
+    """Returns (y bf16 [M, N], acc int32 [K/g, M, N] or None)."""
+    torch = _torch()
+    _need(a_codes, torch.uint8, "a_codes", 2)
+    _need(a_scale, torch.float16, "a_scale", 2)
+    _need(a_zero, torch.int16, "a_zero", 2)
+    _need(w_codes, torch.uint8, "w_codes", 2)
+    _need(w_scale, torch.float16, "w_scale", 1)
+    _need(w_colsum, torch.int32, "w_colsum", 2)
+    for t, n in ((a_codes, "a_codes"), (a_scale, "a_scale"), (a_zero, "a_zero"), (w_codes, "w_codes"),
+                 (w_scale, "w_scale"), (w_colsum, "w_colsum")):
+        if not t.is_contiguous():
+            raise ValueError(f"{n} must be contiguous")
+    M, Kh = a_codes.shape
+    N = w_codes.shape[0]
+    K = 2 * Kh
+    if w_codes.shape[1] != Kh or a_scale.shape != (M, K // g) or a_zero.shape != (M, K // g) \
+            or w_scale.shape != (N,) or w_colsum.shape != (K // g, N):
+        raise ValueError("operand shapes do not match")
+    dev = a_codes.device
+    y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    _need(y, torch.bfloat16, "out", 2)
+    acc = torch.empty((K // g, M, N), dtype=torch.int32, device=dev) if debug else None
+    _check(lib.offq_w4a4_gemm(_ptr(a_codes), _ptr(a_scale), _ptr(a_zero), _ptr(w_codes), _ptr(w_scale),
+                              _ptr(w_colsum), M, N, K, int(g), _ptr(y), y.stride(0), _ptr(acc),
+                              _stream()), "offq_w4a4_gemm")
+    return y, acc
+
+
+def offq_kv_quantize(kv, apply_hadamard=True, debug=False):
+    """kv: bf16 [..., head_dim] (rows contiguous in the last dim; leading dims
+    flattened).  Returns (codes u8 [rows, Dh/2], scale fp16 [rows],
+    zero int16 [rows], y fp32 [rows, Dh] or None)."""
+    torch = _torch()
+    _need(kv, torch.bfloat16, "kv")
+    Dh = kv.shape[-1]
+    rows2d = kv.reshape(-1, Dh)
+    if rows2d.stride(1) != 1:
+        raise ValueError("kv must have a contiguous last dimension")
+    R = rows2d.shape[0]
+    dev = kv.device
+    codes = torch.empty((R, Dh // 2), dtype=torch.uint8, device=dev)
+    scale = torch.empty((R,), dtype=torch.float16, device=dev)
+    zero = torch.empty((R,), dtype=torch.int16, device=dev)
+    y = torch.empty((R, Dh), dtype=torch.float32, device=dev) if debug else None
+    _check(lib.offq_kv_quantize(_ptr(rows2d), R, Dh, rows2d.stride(0), int(bool(apply_hadamard)),
+                                _ptr(codes), _ptr(scale), _ptr(zero), _ptr(y), _stream()),
+           "offq_kv_quantize")
+    return codes, scale, zero, y
+
+
+def offq_pack_weights(w, g):
+    """w: fp32 [N, K] contiguous.  Returns (w_codes u8 [N, K/2], w_scale fp16 [N],
+    w_colsum int32 [K/g, N])."""
+    torch = _torch()
+    _need(w, torch.float32, "w", 2)
+    if not w.is_contiguous():
+        raise ValueError("w must be contiguous")
+    N, K = w.shape
+    dev = w.device
+    wc = torch.empty((N, K // 2), dtype=torch.uint8, device=dev)
+    ws = torch.empty((N,), dtype=torch.float16, device=dev)
+    cs = torch.empty((K // g, N), dtype=torch.int32, device=dev)
+    _check(lib.offq_pack_weights(_ptr(w), N, K, int(g), _ptr(wc), _ptr(ws), _ptr(cs), _stream()),
+           "offq_pack_weights")
+    return wc, ws, cs

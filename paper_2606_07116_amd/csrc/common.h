@@ -1,0 +1,78 @@
+// Shared device/host helpers of the OffQ HIP library (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace offq {
+
+// bf16 bit pattern -> fp32 (exact).
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 bit pattern, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float fp16_bits_to_f32(uint16_t h) {
+  _Float16 v = __builtin_bit_cast(_Float16, h);
+  return (float)v;
+}
+
+// Per-group quantizer parameters of Eq. 1 (sec. 3) with a 16-bit scale and a
+// 16-bit integer zero-point (sec. 3.4), from the group's max and min:
+//   s = fl32(fl32(mx - mn) / 15)  (degenerate mx == mn: s = |mn|, or 1)
+//   s16 = fp16_rne(clamp(s, 2^-24, 65504)), r = fl32(1 / f32(s16))
+//   z = clamp(rne(-mn * r), -32768, 32767), the product taken exactly.
+// Codes are then q = clamp(rne(y * r) + z, 0, 15) with the exact product,
+// evaluated as described at quant_code().
+struct QParams {
+  float r;          // 1 / sq
+  float lo;         // MAGIC - z       (exact integer in [2^23, 2^24))
+  float hi;         // MAGIC - z + 15
+  uint16_t s16;     // stored scale (fp16 bits)
+  int16_t z;        // stored zero-point
+};
+
+// 1.5 * 2^23: fma(y, r, MAGIC) = MAGIC + rne(y * r) exactly when |y r| < 2^22,
+// because every float in [2^23, 2^24) is an integer and MAGIC is even.
+#define OFFQ_MAGIC 12582912.0f
+
+__device__ __forceinline__ QParams quant_params(float mx, float mn) {
+#pragma clang fp contract(off)
+  float s;
+  if (mx > mn) {
+    s = (mx - mn) / 15.0f;             // IEEE fp32 division
+  } else {
+    s = (mn != 0.0f) ? fabsf(mn) : 1.0f;
+  }
+  s = fminf(fmaxf(s, 0x1p-24f), 65504.0f);
+  _Float16 h = (_Float16)s;            // round to nearest even
+  float sq = (float)h;
+  float r = 1.0f / sq;                 // IEEE fp32 division
+  double zd = __builtin_rint(-(double)mn * (double)r);  // exact product, RNE
+  zd = fmin(fmax(zd, -32768.0), 32767.0);
+  int z = (int)zd;
+  QParams p;
+  p.r = r;
+  p.lo = OFFQ_MAGIC - (float)z;
+  p.hi = p.lo + 15.0f;
+  p.s16 = __builtin_bit_cast(uint16_t, h);
+  p.z = (int16_t)z;
+  return p;
+}
+
+// Returns bits(clamp(MAGIC + rne(y r), lo, hi)); subtracting bits(lo) gives the
+// code clamp(rne(y r) + z, 0, 15).  Correct for every finite y: when
+// |y r| >= 2^22 the fma result lies outside [lo, hi] on the correct side, and
+// the clamp to [lo, hi] then yields code 0 or 15 exactly as the definition.
+__device__ __forceinline__ uint32_t quant_bits(float y, const QParams& p) {
+  float u = __builtin_fmaf(y, p.r, OFFQ_MAGIC);
+  u = __builtin_amdgcn_fmed3f(u, p.lo, p.hi);
+  return __float_as_uint(u);
+}
+
+}  // namespace offq

@@ -1,0 +1,35 @@
+// Host-side launchers shared between the kernel files and the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace offq {
+
+// Fused rotate + quantize over n_groups groups of g channels.  Group q lives at
+// row q / G, channels [(q % G) * g, (q % G + 1) * g) of x (row stride ldx).
+hipError_t launch_rotate_quantize(const uint16_t* x, int64_t n_groups, int G,
+                                  int64_t ldx, int log2g, bool hadamard,
+                                  uint8_t* codes, int64_t ldc_bytes,
+                                  uint16_t* scale, int16_t* zero, float* y_debug,
+                                  int64_t ldy, hipStream_t stream);
+
+hipError_t launch_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale,
+                            const int16_t* a_zero, const uint8_t* w_codes,
+                            const uint16_t* w_scale, const int32_t* w_colsum,
+                            int64_t M, int64_t N, int64_t K, int log2g,
+                            uint16_t* y, int64_t ldy, int32_t* acc_debug,
+                            hipStream_t stream);
+
+hipError_t launch_w4a4_gemv(const uint8_t* a_codes, const uint16_t* a_scale,
+                            const int16_t* a_zero, const uint8_t* w_codes,
+                            const uint16_t* w_scale, const int32_t* w_colsum,
+                            int64_t M, int64_t N, int64_t K, int log2g,
+                            uint16_t* y, int64_t ldy, int32_t* acc_debug,
+                            hipStream_t stream);
+
+hipError_t launch_pack_weights(const float* w, int64_t N, int64_t K, int log2g,
+                               uint8_t* w_codes, uint16_t* w_scale,
+                               int32_t* w_colsum, hipStream_t stream);
+
+}  // namespace offq

@@ -1,0 +1,180 @@
+// C ABI of the OffQ library: argument validation, device check, dispatch.
+// Every entry point validates on the host before enqueuing anything and
+// returns a status code; nothing here allocates device memory.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/offq.h"
+#include "internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int ok() {
+  g_last_error[0] = '\0';
+  return OFFQ_OK;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int ilog2_pow2(int64_t v) {
+  if (v <= 0 || (v & (v - 1))) return -1;
+  int l = 0;
+  while ((int64_t(1) << l) < v) ++l;
+  return l;
+}
+
+// The kernels are built for gfx950 only; refuse other devices up front.
+int check_device() {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(OFFQ_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  static thread_local int cached_dev = -1;
+  static thread_local bool cached_ok = false;
+  if (dev != cached_dev) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess)
+      return fail(OFFQ_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+    cached_dev = dev;
+    cached_ok = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+    if (!cached_ok)
+      return fail(OFFQ_ERR_UNSUPPORTED, "device %d is %s; this library is built for gfx950",
+                  dev, prop.gcnArchName);
+  }
+  if (!cached_ok) return fail(OFFQ_ERR_UNSUPPORTED, "device %d is not gfx950", dev);
+  return OFFQ_OK;
+}
+
+int launched(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(OFFQ_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+constexpr int64_t kMaxGroups = int64_t(1) << 31;
+
+}  // namespace
+
+extern "C" {
+
+int offq_abi_version(void) { return OFFQ_ABI_VERSION; }
+
+const char* offq_status_string(int status) {
+  switch (status) {
+    case OFFQ_OK: return "OFFQ_OK";
+    case OFFQ_ERR_INVALID: return "OFFQ_ERR_INVALID";
+    case OFFQ_ERR_UNSUPPORTED: return "OFFQ_ERR_UNSUPPORTED";
+    case OFFQ_ERR_HIP: return "OFFQ_ERR_HIP";
+    default: return "OFFQ_ERR_UNKNOWN";
+  }
+}
+
+const char* offq_last_error(void) { return g_last_error; }
+
+int offq_rotate_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, int32_t g,
+                         int32_t apply_hadamard, uint8_t* codes, uint16_t* scale,
+                         int16_t* zero, float* y_debug, void* stream) {
+  if (M < 0 || K <= 0) return fail(OFFQ_ERR_INVALID, "M must be >= 0 and K > 0");
+  const int lg = ilog2_pow2(g);
+  if (lg < 0) return fail(OFFQ_ERR_INVALID, "g = %d is not a power of two", g);
+  if (lg < 4 || lg > 13) return fail(OFFQ_ERR_UNSUPPORTED, "g = %d outside [16, 8192]", g);
+  if (K % g) return fail(OFFQ_ERR_INVALID, "K = %lld is not a multiple of g = %d", (long long)K, g);
+  if (ldx < K || ldx % 8) return fail(OFFQ_ERR_INVALID, "ldx must be >= K and a multiple of 8");
+  if (apply_hadamard != 0 && apply_hadamard != 1)
+    return fail(OFFQ_ERR_INVALID, "apply_hadamard must be 0 or 1");
+  if (M == 0) return ok();  // empty: pointers may be NULL
+  if (!x || !codes || !scale || !zero) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(x, 16) || !aligned(codes, 4) || !aligned(scale, 2) || !aligned(zero, 2) ||
+      (y_debug && !aligned(y_debug, 16)))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (x, y_debug: 16 B; codes: 4 B)");
+  if (M * (K / g) >= kMaxGroups) return fail(OFFQ_ERR_UNSUPPORTED, "too many groups");
+  if (int s = check_device()) return s;
+  return launched(offq::launch_rotate_quantize(x, M * (K / g), (int)(K / g), ldx, lg,
+                                               apply_hadamard != 0, codes, K / 2, scale, zero,
+                                               y_debug, K, (hipStream_t)stream),
+                  "rotate_quantize");
+}
+
+int offq_kv_quantize(const uint16_t* kv, int64_t rows, int32_t head_dim, int64_t row_stride,
+                     int32_t apply_hadamard, uint8_t* codes, uint16_t* scale, int16_t* zero,
+                     float* y_debug, void* stream) {
+  if (rows < 0) return fail(OFFQ_ERR_INVALID, "rows must be >= 0");
+  const int lg = ilog2_pow2(head_dim);
+  if (lg < 0) return fail(OFFQ_ERR_INVALID, "head_dim = %d is not a power of two", head_dim);
+  if (lg < 4 || lg > 13) return fail(OFFQ_ERR_UNSUPPORTED, "head_dim outside [16, 8192]");
+  if (row_stride < head_dim || row_stride % 8)
+    return fail(OFFQ_ERR_INVALID, "row_stride must be >= head_dim and a multiple of 8");
+  if (apply_hadamard != 0 && apply_hadamard != 1)
+    return fail(OFFQ_ERR_INVALID, "apply_hadamard must be 0 or 1");
+  if (rows == 0) return ok();  // empty: pointers may be NULL
+  if (!kv || !codes || !scale || !zero) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(kv, 16) || !aligned(codes, 4) || !aligned(scale, 2) || !aligned(zero, 2) ||
+      (y_debug && !aligned(y_debug, 16)))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (kv, y_debug: 16 B; codes: 4 B)");
+  if (rows >= kMaxGroups) return fail(OFFQ_ERR_UNSUPPORTED, "too many rows");
+  if (int s = check_device()) return s;
+  return launched(offq::launch_rotate_quantize(kv, rows, 1, row_stride, lg, apply_hadamard != 0,
+                                               codes, head_dim / 2, scale, zero, y_debug,
+                                               head_dim, (hipStream_t)stream),
+                  "kv_quantize");
+}
+
+int offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale, const int16_t* a_zero,
+                   const uint8_t* w_codes, const uint16_t* w_scale, const int32_t* w_colsum,
+                   int64_t M, int64_t N, int64_t K, int32_t g, uint16_t* y, int64_t ldy,
+                   int32_t* acc_debug, void* stream) {
+  if (M < 0 || N <= 0 || K <= 0) return fail(OFFQ_ERR_INVALID, "need M >= 0, N > 0, K > 0");
+  const int lg = ilog2_pow2(g);
+  if (lg < 0) return fail(OFFQ_ERR_INVALID, "g = %d is not a power of two", g);
+  if (lg < 6 || lg > 13) return fail(OFFQ_ERR_UNSUPPORTED, "g = %d outside [64, 8192]", g);
+  if (K % g) return fail(OFFQ_ERR_INVALID, "K = %lld is not a multiple of g = %d", (long long)K, g);
+  if (ldy < N) return fail(OFFQ_ERR_INVALID, "ldy must be >= N");
+  if (M > (1 << 30) || N > (1 << 30) || K > (1 << 30))
+    return fail(OFFQ_ERR_UNSUPPORTED, "dimension too large");
+  if (M == 0) return ok();  // empty: pointers may be NULL
+  if (!a_codes || !a_scale || !a_zero || !w_codes || !w_scale || !w_colsum || !y)
+    return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(a_codes, 16) || !aligned(w_codes, 16) || !aligned(a_scale, 2) ||
+      !aligned(a_zero, 2) || !aligned(w_scale, 2) || !aligned(w_colsum, 4) || !aligned(y, 2) ||
+      (acc_debug && !aligned(acc_debug, 4)))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (codes: 16 B)");
+  if (int s = check_device()) return s;
+  hipError_t e;
+  if (M <= 16)
+    e = offq::launch_w4a4_gemv(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, lg,
+                               y, ldy, acc_debug, (hipStream_t)stream);
+  else
+    e = offq::launch_w4a4_gemm(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, lg,
+                               y, ldy, acc_debug, (hipStream_t)stream);
+  return launched(e, M <= 16 ? "w4a4_gemv" : "w4a4_gemm");
+}
+
+int offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g, uint8_t* w_codes,
+                      uint16_t* w_scale, int32_t* w_colsum, void* stream) {
+  if (N <= 0 || K <= 0) return fail(OFFQ_ERR_INVALID, "need N > 0, K > 0");
+  const int lg = ilog2_pow2(g);
+  if (lg < 0) return fail(OFFQ_ERR_INVALID, "g = %d is not a power of two", g);
+  if (lg < 6 || lg > 13) return fail(OFFQ_ERR_UNSUPPORTED, "g = %d outside [64, 8192]", g);
+  if (K % g) return fail(OFFQ_ERR_INVALID, "K = %lld is not a multiple of g = %d", (long long)K, g);
+  if (K / g > 512) return fail(OFFQ_ERR_UNSUPPORTED, "K / g must be <= 512");
+  if (N >= kMaxGroups) return fail(OFFQ_ERR_UNSUPPORTED, "N too large");
+  if (!w || !w_codes || !w_scale || !w_colsum) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(w, 16) || !aligned(w_codes, 4) || !aligned(w_scale, 2) || !aligned(w_colsum, 4))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (w: 16 B; w_codes: 4 B)");
+  if (int s = check_device()) return s;
+  return launched(offq::launch_pack_weights(w, N, K, lg, w_codes, w_scale, w_colsum,
+                                            (hipStream_t)stream),
+                  "pack_weights");
+}
+
+}  // extern "C"

@@ -1,0 +1,109 @@
+"""Host-only checks of the C ABI: the library loads, exports every symbol the
+header declares, and rejects bad arguments before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_07116_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    src = open(os.path.join(ROOT, "include", "offq.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(offq_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = _header_functions()
+    assert "offq_rotate_quantize" in names and "offq_w4a4_gemm" in names
+    assert "offq_kv_quantize" in names and "offq_pack_weights" in names
+    lib = ctypes.CDLL(_lib.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(_lib.EXPORTED) == names
+
+
+def test_version_and_status_strings():
+    assert _lib.ABI_VERSION == 1
+    assert _lib.status_name(0) == "OFFQ_OK"
+    assert _lib.status_name(1) == "OFFQ_ERR_INVALID"
+    assert _lib.status_name(2) == "OFFQ_ERR_UNSUPPORTED"
+    assert _lib.status_name(3) == "OFFQ_ERR_HIP"
+    assert _lib.status_name(99) == "OFFQ_ERR_UNKNOWN"
+
+
+P = 0x10000  # a fake, 64 KiB-aligned address: never dereferenced (validation fails first)
+
+
+@pytest.mark.parametrize("args,expect", [
+    # (x, M, K, ldx, g, had, codes, scale, zero, ydbg)
+    ((P, 4, 256, 256, 100, 1, P, P, P, None), _lib.OFFQ_ERR_INVALID),      # g not power of 2
+    ((P, 4, 256, 256, 8, 1, P, P, P, None), _lib.OFFQ_ERR_UNSUPPORTED),    # g too small
+    ((P, 4, 32768, 32768, 16384, 1, P, P, P, None), _lib.OFFQ_ERR_UNSUPPORTED),  # g too large
+    ((P, 4, 384, 384, 256, 1, P, P, P, None), _lib.OFFQ_ERR_INVALID),      # K % g
+    ((P, 4, 256, 200, 256, 1, P, P, P, None), _lib.OFFQ_ERR_INVALID),      # ldx < K
+    ((P, 4, 256, 260, 256, 1, P, P, P, None), _lib.OFFQ_ERR_INVALID),      # ldx % 8
+    ((P, 4, 256, 256, 256, 2, P, P, P, None), _lib.OFFQ_ERR_INVALID),      # bad flag
+    ((None, 4, 256, 256, 256, 1, P, P, P, None), _lib.OFFQ_ERR_INVALID),   # null x
+    ((P + 8, 4, 256, 256, 256, 1, P, P, P, None), _lib.OFFQ_ERR_INVALID),  # misaligned x
+    ((P, 4, 256, 256, 256, 1, P + 2, P, P, None), _lib.OFFQ_ERR_INVALID),  # misaligned codes
+    ((P, -1, 256, 256, 256, 1, P, P, P, None), _lib.OFFQ_ERR_INVALID),     # M < 0
+    ((P, 0, 256, 256, 256, 1, P, P, P, None), _lib.OFFQ_OK),               # empty: no-op
+])
+def test_rotate_quantize_validation(args, expect):
+    st = _lib.offq_rotate_quantize_raw(*args, None)
+    assert st == expect, _lib.last_error()
+    if st != _lib.OFFQ_OK:
+        assert _lib.last_error()
+
+
+@pytest.mark.parametrize("args,expect", [
+    # (a, as, az, w, ws, cs, M, N, K, g, y, ldy, acc)
+    ((P, P, P, P, P, P, 4, 8, 256, 32, P, 8, None), _lib.OFFQ_ERR_UNSUPPORTED),  # g < 64
+    ((P, P, P, P, P, P, 4, 8, 256, 96, P, 8, None), _lib.OFFQ_ERR_INVALID),      # g not pow2
+    ((P, P, P, P, P, P, 4, 8, 320, 256, P, 8, None), _lib.OFFQ_ERR_INVALID),     # K % g
+    ((P, P, P, P, P, P, 4, 8, 256, 256, P, 4, None), _lib.OFFQ_ERR_INVALID),     # ldy < N
+    ((P, P, P, P, P, P, 4, 0, 256, 256, P, 8, None), _lib.OFFQ_ERR_INVALID),     # N = 0
+    ((P, P, P, None, P, P, 4, 8, 256, 256, P, 8, None), _lib.OFFQ_ERR_INVALID),  # null w
+    ((P + 4, P, P, P, P, P, 4, 8, 256, 256, P, 8, None), _lib.OFFQ_ERR_INVALID), # misaligned
+    ((P, P, P, P, P, P, 0, 8, 256, 256, P, 8, None), _lib.OFFQ_OK),              # M = 0
+])
+def test_gemm_validation(args, expect):
+    st = _lib.offq_w4a4_gemm_raw(*args, None)
+    assert st == expect, _lib.last_error()
+
+
+@pytest.mark.parametrize("args,expect", [
+    # (kv, rows, Dh, stride, had, codes, scale, zero, ydbg)
+    ((P, 10, 96, 96, 1, P, P, P, None), _lib.OFFQ_ERR_INVALID),
+    ((P, 10, 128, 120, 1, P, P, P, None), _lib.OFFQ_ERR_INVALID),
+    ((P, 10, 128, 132, 1, P, P, P, None), _lib.OFFQ_ERR_INVALID),
+    ((P, 10, 8, 8, 1, P, P, P, None), _lib.OFFQ_ERR_UNSUPPORTED),
+    ((P, 0, 128, 128, 1, P, P, P, None), _lib.OFFQ_OK),
+])
+def test_kv_validation(args, expect):
+    st = _lib.offq_kv_quantize_raw(*args, None)
+    assert st == expect, _lib.last_error()
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((P, 8, 256, 48, P, P, P), _lib.OFFQ_ERR_INVALID),
+    ((P, 8, 65536, 64, P, P, P), _lib.OFFQ_ERR_UNSUPPORTED),   # K/g > 512
+    ((P, 0, 256, 64, P, P, P), _lib.OFFQ_ERR_INVALID),
+    ((P + 4, 8, 256, 64, P, P, P), _lib.OFFQ_ERR_INVALID),
+])
+def test_pack_weights_validation(args, expect):
+    st = _lib.offq_pack_weights_raw(*args, None)
+    assert st == expect, _lib.last_error()
+
+
+def test_valid_call_without_gpu_reports_hip_error():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    st = _lib.offq_rotate_quantize_raw(P, 4, 256, 256, 256, 1, P, P, P, None, None)
+    assert st == _lib.OFFQ_ERR_HIP

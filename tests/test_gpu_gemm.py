@@ -1,0 +1,105 @@
+"""GPU parity: W4A4 GEMM / GEMV (offq_w4a4_gemm) and weight packing vs the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_07116_amd as offq
+from oracle import gemm as OG
+from oracle import quantizer as OQ
+from paper_2606_07116_amd import inputs
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def _layer(M, N, K, g, seed, layout="concentrated", n_out=4):
+    x = inputs.activations(M, K, seed=seed, n_outliers=n_out, lo=50, hi=200, layout=layout, g=g)
+    w = inputs.weights(N, K, seed=seed)
+    (q, s, z), (codes, scale, zero) = P.rotate_quantize_and_check(x, g, True)
+    q_w, sw, cs, packed = P.oracle_weights(w, g)
+    wc, ws, wcs = P.upload_weights(packed, sw, cs)
+    y, acc = offq.offq_w4a4_gemm(codes, scale, zero, wc, ws, wcs, g, debug=True)
+    y2, _ = offq.offq_w4a4_gemm(codes, scale, zero, wc, ws, wcs, g, debug=False)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+    acc_ref = OG.int_gemm_groups(q, q_w, g)
+    acc_gpu = P.host(acc)
+    if not np.array_equal(acc_gpu, acc_ref):
+        bad = np.argwhere(acc_gpu != acc_ref)
+        raise AssertionError(f"accumulator mismatch at {bad[:5].tolist()} (of {len(bad)})")
+    P.check_output(P.host(y.float()), acc_ref, s, z, sw, cs)
+    return y
+
+
+@pytest.mark.parametrize("M,N,K,g", [
+    (17, 8, 256, 256), (128, 128, 512, 512), (130, 136, 1024, 256), (200, 250, 256, 64),
+    (257, 384, 2048, 512), (64, 512, 4096, 4096), (40, 96, 8192, 8192), (33, 64, 512, 128),
+])
+def test_gemm_shapes(M, N, K, g):
+    _layer(M, N, K, g, seed=M * 7 + N)
+
+
+@pytest.mark.parametrize("M", [1, 2, 4, 5, 16])
+@pytest.mark.parametrize("K,g", [(256, 256), (2048, 512), (8192, 8192), (1024, 64)])
+def test_gemv_shapes(M, K, g):
+    _layer(M, 200, K, g, seed=M + K)
+
+
+def test_raw_layout_and_spikes():
+    _layer(150, 192, 1024, 1024, seed=5, layout="raw", n_out=6)
+
+
+def test_output_row_stride():
+    M, N, K, g = 140, 72, 512, 256
+    x = inputs.activations(M, K, seed=3, n_outliers=2, lo=50, hi=60, layout="concentrated", g=g)
+    w = inputs.weights(N, K, seed=3)
+    (q, s, z), (codes, scale, zero) = P.rotate_quantize_and_check(x, g, True)
+    q_w, sw, cs, packed = P.oracle_weights(w, g)
+    wc, ws, wcs = P.upload_weights(packed, sw, cs)
+    big = torch.full((M, 100), 7.0, dtype=torch.bfloat16, device=P.DEV)
+    offq.offq_w4a4_gemm(codes, scale, zero, wc, ws, wcs, g, out=big[:, 10:10 + N])
+    torch.cuda.synchronize()
+    yb = P.host(big.float())
+    assert np.all(yb[:, :10] == 7.0) and np.all(yb[:, 10 + N:] == 7.0)
+    P.check_output(yb[:, 10:10 + N], OG.int_gemm_groups(q, q_w, g), s, z, sw, cs)
+
+
+def test_extreme_codes_and_zero_points():
+    """All-15 activation codes against all -8 weights with large zero-points."""
+    M, N, K, g = 130, 66, 1024, 512
+    codes = torch.full((M, K // 2), 0xFF, dtype=torch.uint8, device=P.DEV)
+    scale = torch.full((M, K // g), 0.5, dtype=torch.float16, device=P.DEV)
+    zero = torch.full((M, K // g), -32768, dtype=torch.int16, device=P.DEV)
+    q_w = np.full((N, K), -8, np.int8)
+    sw = np.full(N, 0.25, np.float16)
+    cs = OQ.colsum(q_w, g)
+    wc, ws, wcs = P.upload_weights(OQ.pack_nibbles(q_w), sw, cs)
+    y, acc = offq.offq_w4a4_gemm(codes, scale, zero, wc, ws, wcs, g, debug=True)
+    torch.cuda.synchronize()
+    acc_ref = OG.int_gemm_groups(np.full((M, K), 15, np.uint8), q_w, g)
+    assert np.array_equal(P.host(acc), acc_ref)
+    P.check_output(P.host(y.float()), acc_ref, P.host(scale), P.host(zero), sw, cs)
+
+
+def test_empty_m_is_noop():
+    g, K, N = 256, 256, 8
+    e = torch.empty((0, K // 2), dtype=torch.uint8, device=P.DEV)
+    y, _ = offq.offq_w4a4_gemm(e, torch.empty((0, 1), dtype=torch.float16, device=P.DEV),
+                               torch.empty((0, 1), dtype=torch.int16, device=P.DEV),
+                               torch.zeros((N, K // 2), dtype=torch.uint8, device=P.DEV),
+                               torch.ones(N, dtype=torch.float16, device=P.DEV),
+                               torch.zeros((1, N), dtype=torch.int32, device=P.DEV), g)
+    assert y.shape == (0, N)
+
+
+@pytest.mark.parametrize("N,K,g", [(7, 256, 64), (300, 4096, 4096), (64, 28672, 512), (33, 8192, 8192)])
+def test_pack_weights(N, K, g):
+    w = inputs.weights(N, K, seed=N)
+    w[0] = 0.0                      # all-zero row -> scale 1
+    w[1, 5] = 3.0                   # one large weight
+    q_w, sw, cs, packed = P.oracle_weights(w, g)
+    wc, ws, wcs = offq.offq_pack_weights(torch.from_numpy(w).to(P.DEV), g)
+    torch.cuda.synchronize()
+    assert np.array_equal(P.fp16_bits(P.host(ws)), P.fp16_bits(sw))
+    assert np.array_equal(P.host(wc), packed)
+    assert np.array_equal(P.host(wcs), cs)
