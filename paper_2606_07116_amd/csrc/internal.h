@@ -21,6 +21,14 @@ hipError_t launch_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale,
                             uint16_t* y, int64_t ldy, int32_t* acc_debug,
                             hipStream_t stream);
 
+// One group per row (g == K): MFMA GEMM with 128 x 128 wave tiles.
+bool gemm_1g_supported(int64_t M, int64_t N, int64_t K);
+hipError_t launch_w4a4_gemm_1g(const uint8_t* a_codes, const uint16_t* a_scale,
+                               const int16_t* a_zero, const uint8_t* w_codes,
+                               const uint16_t* w_scale, const int32_t* w_colsum, int64_t M,
+                               int64_t N, int64_t K, uint16_t* y, int64_t ldy,
+                               int32_t* acc_debug, hipStream_t stream);
+
 hipError_t launch_w4a4_gemv(const uint8_t* a_codes, const uint16_t* a_scale,
                             const int16_t* a_zero, const uint8_t* w_codes,
                             const uint16_t* w_scale, const int32_t* w_colsum,
