@@ -17,6 +17,14 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// two fp32 -> packed bf16 (lo = a, hi = b), round to nearest even
+// (v_cvt_pk_bf16_f32 on gfx950).
+typedef __bf16 offq_bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16x2_rne(float a, float b) {
+  const offq_bf16x2 r = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, r);
+}
+
 __device__ __forceinline__ float fp16_bits_to_f32(uint16_t h) {
   _Float16 v = __builtin_bit_cast(_Float16, h);
   return (float)v;

@@ -15,23 +15,29 @@
 //   SPLITK = 2: two 128-row sub-tiles x two k-slots -> 256 x 128 workgroup
 //   tile; the two k-slots are summed through LDS at the end.  Used when the
 //   256 x 256 tiling leaves compute units idle.
-// * Per stage every wave consumes 128 k (64 packed bytes per row); the stage
-//   (A: 256 rows, B: 256 or 128 rows, 64 * SPLITK bytes each) is staged
-//   through registers into a double-buffered LDS ring.  Rows are stored as
-//   16-byte chunks whose order is XOR-swizzled with the row so that the
-//   fragment reads (one row per lane, 8 lanes per LDS cycle) hit 8 different
-//   bank groups.
+// * Per stage every wave consumes 128 k (64 packed bytes per row).  Stages go
+//   global -> registers -> a 3-deep LDS ring: while stage st is multiplied,
+//   stage st + 2 is written to LDS, stage st + 3 is loaded into registers and
+//   the first fragments of stage st + 1 are read, so one barrier per stage
+//   (with an LDS-only fence, which does not wait for the global prefetch) is
+//   the only synchronisation.  Rows are 16-byte chunks XOR-swizzled with the
+//   row, so the fragment reads (one row per lane) are free of bank conflicts.
 // * The MFMA takes the weight fragment as its row operand and the activation
-//   fragment as its column operand, i.e. it accumulates the transposed tile, so
-//   that each lane ends with four consecutive output columns of one row.
+//   fragment as its column operand, i.e. it accumulates the transposed tile.
 // * Operands: activation codes (0..15) feed the signed i8 MFMA unchanged;
 //   weight nibbles are widened to 16 * q (high nibble by a mask, low nibble by
 //   a shift and a mask).  Each lane's 16-byte chunk gives two MFMA operands
 //   (low nibbles, high nibbles): the same k-permutation on both operands.
-//   The accumulator holds 16 * acc exactly.
+//   The accumulator holds 16 * acc exactly.  The unpacking of the high
+//   nibbles is interleaved with the 16 MFMAs on the low nibbles.
+// * Epilogue: the bf16 tile goes through LDS (8-byte units XOR-swizzled by
+//   row, 64 rows at a time) so that every lane stores 16 contiguous bytes and
+//   every store instruction covers 4 full 256-byte row segments.
 // * Tile order: consecutive workgroups are dispatched to different XCDs, so
 //   the linear id is first regrouped per XCD and then walked in groups of 4
 //   tile rows, keeping each XCD's A and B panels within its own L2.
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -46,13 +52,13 @@ struct Cfg {
   static constexpr int BM = 256;
   static constexpr int BN = SPLITK == 1 ? 256 : 128;
   static constexpr int NC = 4 * SPLITK;            // 16-byte chunks per row and stage
-  static constexpr int ROWB = 16 * NC;             // bytes per row and stage
   static constexpr int A_SLOTS = BM * NC;          // 16-byte slots of the A stage
   static constexpr int B_SLOTS = BN * NC;
   static constexpr int STAGE_SLOTS = A_SLOTS + B_SLOTS;
   static constexpr int A_LD = A_SLOTS / 256;       // loads per thread and stage
   static constexpr int B_LD = B_SLOTS / 256;
   static constexpr int KSTAGE = 128 * SPLITK;      // k per stage
+  static constexpr int NBUF = 3;                   // LDS ring depth
 };
 
 template <int NC>
@@ -78,7 +84,13 @@ __device__ __forceinline__ v4i wgt_hi16(uint4 d) {
              (int)(d.w & 0xf0f0f0f0u)};
 }
 
-__device__ __forceinline__ int acc_row(int i, int h) { return ((i >> 2) << 3) + (h << 2) + (i & 3); }
+// Workgroup barrier whose fence covers LDS only: outstanding global loads
+// (the register prefetch of later stages) are not waited for.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
 // Linear workgroup id -> (tile row, tile column): per-XCD regrouping, then
 // groups of 4 tile rows walked column by column.
@@ -103,7 +115,7 @@ __global__ __launch_bounds__(256) void w4a4_gemm_1g_kernel(
     const uint16_t* __restrict__ w_scale, const int32_t* __restrict__ w_colsum, int M, int N,
     int K, uint16_t* __restrict__ Y, int64_t ldy, int32_t* __restrict__ acc_dbg) {
   using C = Cfg<SPLITK>;
-  __shared__ uint4 lds[2 * C::STAGE_SLOTS];
+  __shared__ uint4 lds[C::NBUF * C::STAGE_SLOTS];
   __shared__ __attribute__((aligned(16))) float sS[C::BM];
   __shared__ __attribute__((aligned(16))) int sZ[C::BM];
   __shared__ __attribute__((aligned(16))) float sSW[C::BN];
@@ -168,6 +180,19 @@ __global__ __launch_bounds__(256) void w4a4_gemm_1g_kernel(
 #pragma unroll
     for (int i = 0; i < C::B_LD; ++i) base[C::A_SLOTS + tid + 256 * i] = rb[i];
   };
+  // fragment chunk jj (0/1: which 16 bytes of this lane's 32 per row) of stage buffer buf
+  auto fread = [&](int buf, int jj, uint4* pa, uint4* pb) {
+    const uint4* As = lds + buf * C::STAGE_SLOTS;
+    const uint4* Bs = As + C::A_SLOTS;
+    const int c = ks * 4 + 2 * h + jj;
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+      const int ra_ = wm * 128 + f * 32 + fr;
+      const int rb_ = wn * 128 + f * 32 + fr;
+      pa[f] = As[ra_ * C::NC + swz<C::NC>(ra_, c)];
+      pb[f] = Bs[rb_ * C::NC + swz<C::NC>(rb_, c)];
+    }
+  };
 
   v16i acc[4][4];
 #pragma unroll
@@ -175,94 +200,84 @@ __global__ __launch_bounds__(256) void w4a4_gemm_1g_kernel(
 #pragma unroll
     for (int b = 0; b < 4; ++b) acc[a][b] = v16i{};
 
+  // two k-steps (low and high nibbles of one 16-byte chunk per fragment)
+  auto mma2 = [&](const uint4* pa, const uint4* pb) {
+    v4i ua[4], ub[4];
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+      ua[f] = act_lo(pa[f]);
+      ub[f] = wgt_lo16(pb[f]);
+    }
+    v4i na[4], nb[4];
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+      na[f] = act_hi(pa[f]);
+      nb[f] = wgt_hi16(pb[f]);
+    }
+#pragma unroll
+    for (int fm = 0; fm < 4; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < 4; ++fn)
+        acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub[fn], ua[fm], acc[fm][fn], 0, 0, 0);
+    // interleave: each of the 16 MFMAs above is followed by up to 2 of the
+    // 24 VALU ops that unpack the high nibbles
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+    }
+#pragma unroll
+    for (int fm = 0; fm < 4; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < 4; ++fn)
+        acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(nb[fn], na[fm], acc[fm][fn], 0, 0, 0);
+  };
+
+  // prologue: stages 0 and 1 into the ring, stage 2 into registers
   gload(0);
   lstore(0);
-  __syncthreads();
+  if (nst > 1) {
+    gload(1);
+    lstore(1);
+  }
+  if (nst > 2) gload(2);
+  lds_barrier();
+  uint4 pc_a[4], pc_b[4];
+  fread(0, 0, pc_a, pc_b);
 
   for (int st = 0; st < nst; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < nst) gload(st + 1);
-    const uint4* As = lds + buf * C::STAGE_SLOTS;
-    const uint4* Bs = As + C::A_SLOTS;
-#pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-      const int c = ks * 4 + 2 * h + jj;
-      uint4 pa[4], pb[4];
-#pragma unroll
-      for (int f = 0; f < 4; ++f) {
-        const int ra_ = wm * 128 + f * 32 + fr;
-        const int rb_ = wn * 128 + f * 32 + fr;
-        pa[f] = As[ra_ * C::NC + swz<C::NC>(ra_, c)];
-        pb[f] = Bs[rb_ * C::NC + swz<C::NC>(rb_, c)];
-      }
-#pragma unroll
-      for (int sel = 0; sel < 2; ++sel) {
-        v4i a[4], b[4];
-#pragma unroll
-        for (int f = 0; f < 4; ++f) {
-          a[f] = sel ? act_hi(pa[f]) : act_lo(pa[f]);
-          b[f] = sel ? wgt_hi16(pb[f]) : wgt_lo16(pb[f]);
-        }
-#pragma unroll
-        for (int fm = 0; fm < 4; ++fm)
-#pragma unroll
-          for (int fn = 0; fn < 4; ++fn)
-            acc[fm][fn] =
-                __builtin_amdgcn_mfma_i32_32x32x32_i8(b[fn], a[fm], acc[fm][fn], 0, 0, 0);
-      }
+    const int buf = st % C::NBUF;
+    if (st + 2 < nst) {
+      lstore((st + 2) % C::NBUF);
+      if (st + 3 < nst) gload(st + 3);
     }
-    if (st + 1 < nst) lstore(buf ^ 1);
-    __syncthreads();
+    uint4 p1_a[4], p1_b[4];
+    fread(buf, 1, p1_a, p1_b);
+    mma2(pc_a, pc_b);
+    if (st + 1 < nst) fread((st + 1) % C::NBUF, 0, pc_a, pc_b);
+    mma2(p1_a, p1_b);
+    lds_barrier();
   }
 
-  if constexpr (SPLITK == 2) {
-    // sum the two k-slots: waves of slot 1 hand their accumulators to slot 0,
-    // 16 bytes per lane and access, in two rounds of two fragment rows
-    v4i* red = reinterpret_cast<v4i*>(lds);
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      if (ks == 1) {
-#pragma unroll
-        for (int f2 = 0; f2 < 2; ++f2)
-#pragma unroll
-          for (int fn = 0; fn < 4; ++fn)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const v16i& t = acc[half * 2 + f2][fn];
-              red[((((wm * 2 + f2) * 4 + fn) * 4 + q) * 64) + lane] =
-                  v4i{t[4 * q], t[4 * q + 1], t[4 * q + 2], t[4 * q + 3]};
-            }
-      }
-      __syncthreads();
-      if (ks == 0) {
-#pragma unroll
-        for (int f2 = 0; f2 < 2; ++f2)
-#pragma unroll
-          for (int fn = 0; fn < 4; ++fn)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const v4i o = red[((((wm * 2 + f2) * 4 + fn) * 4 + q) * 64) + lane];
-              acc[half * 2 + f2][fn][4 * q + 0] += o[0];
-              acc[half * 2 + f2][fn][4 * q + 1] += o[1];
-              acc[half * 2 + f2][fn][4 * q + 2] += o[2];
-              acc[half * 2 + f2][fn][4 * q + 3] += o[3];
-            }
-      }
-      __syncthreads();
-    }
-    if (ks == 1) return;
-  }
+  // ---- epilogue --------------------------------------------------------
+  // Y = sw * s * ((acc >> 4) - z * colsum) -> bf16.  Lane column fr is output
+  // row m of fragment row fm; register i of fragment (fm, fn) is output column
+  // fn*32 + 8*(i/4) + 4*h + i%4.  Per half of 64 rows (fm = 2 HF, 2 HF + 1),
+  // each wave writes its bf16 rows to a private 16 KB LDS area in 8-byte
+  // units (unit u of row r stored at u ^ (r & 15), which spreads 16 rows over
+  // all banks), then reads 16-byte pieces back row by row for coalesced
+  // stores.  With split-K each k-slot wave finishes one half.
+  uint32_t* ot = reinterpret_cast<uint32_t*>(lds) + wave * (64 * 64);
+  const int row_base = tm + wm * 128;
+  const int col_base = tn + wn * 128;
+  const bool full = (tm + C::BM <= M) && (tn + C::BN <= N);
+  const bool vec = full && (ldy % 8 == 0) && ((reinterpret_cast<uintptr_t>(Y) & 15) == 0);
 
-  // epilogue: Y = sw * s * ((acc >> 4) - z * colsum) -> bf16.  The MFMA
-  // computes the transposed tile (weights as the row operand), so lane column
-  // fr is output row m and register i of fragment (fm, fn) is output column
-  // fn*32 + 8*(i/4) + 4*h + i%4: four consecutive columns per 4 registers,
-  // stored as one 8-byte write.
-  if constexpr (DBG) {
-    // accumulator-only launch: store acc (int32), four consecutive columns per
-    // 4 registers; the output Y comes from a second, regular launch
+  auto store_acc_half = [&](auto HFC) {  // debug: raw accumulators of one half
+    constexpr int HF = decltype(HFC)::value;
 #pragma unroll
-    for (int fm = 0; fm < 4; ++fm) {
+    for (int f2 = 0; f2 < 2; ++f2) {
+      const int fm = HF * 2 + f2;
       const int row = tm + wm * 128 + fm * 32 + fr;
       if (row >= M) continue;
 #pragma unroll
@@ -275,18 +290,17 @@ __global__ __launch_bounds__(256) void w4a4_gemm_1g_kernel(
             if (c0 + e < N) acc_dbg[(int64_t)row * N + c0 + e] = acc[fm][fn][q * 4 + e] >> 4;
         }
     }
-    return;
-  }
-  const bool full = (tm + C::BM <= M) && (tn + C::BN <= N);
-  const bool vec = full && (ldy % 4 == 0) && ((reinterpret_cast<uintptr_t>(Y) & 7) == 0);
-  if (vec) {
-    // interior tile: no bounds checks, 8-byte stores
+  };
+
+  auto out_half = [&](auto HFC) {
+    constexpr int HF = decltype(HFC)::value;
 #pragma unroll
-    for (int fm = 0; fm < 4; ++fm) {
+    for (int f2 = 0; f2 < 2; ++f2) {
+      const int fm = HF * 2 + f2;
       const int lr = wm * 128 + fm * 32 + fr;
       const float rs = sS[lr];
-      const int rz = sZ[lr];
-      uint16_t* yrow = Y + (int64_t)(tm + lr) * ldy + tn + wn * 128 + h * 4;
+      const int nz = -sZ[lr];
+      const int r = f2 * 32 + fr;  // row within the half
 #pragma unroll
       for (int fn = 0; fn < 4; ++fn) {
 #pragma unroll
@@ -296,45 +310,91 @@ __global__ __launch_bounds__(256) void w4a4_gemm_1g_kernel(
           const float4 s4 = *reinterpret_cast<const float4*>(&sSW[lc]);
           const int cs[4] = {c4.x, c4.y, c4.z, c4.w};
           const float sw[4] = {s4.x, s4.y, s4.z, s4.w};
-          uint32_t v[4];
+          float yv[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int a = acc[fm][fn][q * 4 + e] >> 4;
             float d;
-            if constexpr (!WIDE) d = (float)(a - rz * cs[e]);
-            else d = (float)((long long)a - (long long)rz * (long long)cs[e]);
-            v[e] = f32_to_bf16_rne(sw[e] * (rs * d));
+            // |z|, |colsum| < 2^23: one 24-bit multiply-add; exact for K <= 4096
+            if constexpr (!WIDE) d = (float)(__mul24(nz, cs[e]) + a);
+            else d = (float)((long long)a + (long long)nz * (long long)cs[e]);
+            yv[e] = sw[e] * (rs * d);
           }
-          *reinterpret_cast<uint2*>(yrow + fn * 32 + q * 8) =
-              make_uint2(v[0] | (v[1] << 16), v[2] | (v[3] << 16));
+          const int u = fn * 8 + q * 2 + h;  // 8-byte unit within the 256-byte row
+          *reinterpret_cast<uint2*>(ot + r * 64 + ((u ^ (r & 15)) * 2)) =
+              make_uint2(bf16x2_rne(yv[0], yv[1]), bf16x2_rne(yv[2], yv[3]));
         }
       }
     }
-    return;
-  }
-  // edge tiles: checked scalar stores
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    // 16-byte pieces: lane l of pass p covers row 4p + l/16, units 2(l%16), 2(l%16)+1
+#pragma unroll 4
+    for (int p = 0; p < 16; ++p) {
+      const int r = 4 * p + (lane >> 4);
+      const int k = lane & 15;
+      const int pu = (2 * k) ^ (r & 15);   // physical unit of logical unit 2k
+      uint4 d = *reinterpret_cast<const uint4*>(ot + r * 64 + (pu & ~1) * 2);
+      if (pu & 1) d = make_uint4(d.z, d.w, d.x, d.y);  // the pair came swapped
+      const int row = row_base + HF * 64 + r;
+      const int col = col_base + 8 * k;
+      if (vec) {
+        *reinterpret_cast<uint4*>(Y + (int64_t)row * ldy + col) = d;
+      } else if (row < M) {
+        const uint32_t w4[4] = {d.x, d.y, d.z, d.w};
 #pragma unroll
-  for (int fm = 0; fm < 4; ++fm) {
-    const int lr = wm * 128 + fm * 32 + fr;
-    const int row = tm + lr;
-    if (row >= M) continue;
-    const float rs = sS[lr];
-    const int rz = sZ[lr];
-#pragma unroll
-    for (int fn = 0; fn < 4; ++fn) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int col = tn + wn * 128 + fn * 32 + acc_row(i, h);
-        if (col < N) {
-          const int a = acc[fm][fn][i] >> 4;
-          const int cs = sCS[col - tn];
-          const float sw = sSW[col - tn];
-          float d;
-          if constexpr (!WIDE) d = (float)(a - rz * cs);
-          else d = (float)((long long)a - (long long)rz * (long long)cs);
-          Y[(int64_t)row * ldy + col] = f32_to_bf16_rne(sw * (rs * d));
-        }
+        for (int e = 0; e < 8; ++e)
+          if (col + e < N) Y[(int64_t)row * ldy + col + e] = (uint16_t)(w4[e >> 1] >> (16 * (e & 1)));
       }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+  };
+
+  if constexpr (SPLITK == 2) {
+    // sum the two k-slots: slot 0 keeps fm 0-1, slot 1 keeps fm 2-3; each
+    // hands the other half to its partner through LDS (16 bytes per access).
+    v4i* red = reinterpret_cast<v4i*>(lds);
+    auto finish = [&](auto KC) {
+      constexpr int KEEP = decltype(KC)::value, GIVE = 1 - KEEP;
+#pragma unroll
+      for (int f2 = 0; f2 < 2; ++f2)
+#pragma unroll
+        for (int fn = 0; fn < 4; ++fn)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const v16i& t = acc[GIVE * 2 + f2][fn];
+            red[(((((GIVE * 2 + wm) * 2 + f2) * 4 + fn) * 4 + q) * 64) + lane] =
+                v4i{t[4 * q], t[4 * q + 1], t[4 * q + 2], t[4 * q + 3]};
+          }
+      lds_barrier();
+#pragma unroll
+      for (int f2 = 0; f2 < 2; ++f2)
+#pragma unroll
+        for (int fn = 0; fn < 4; ++fn)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const v4i o = red[(((((KEEP * 2 + wm) * 2 + f2) * 4 + fn) * 4 + q) * 64) + lane];
+            acc[KEEP * 2 + f2][fn][4 * q + 0] += o[0];
+            acc[KEEP * 2 + f2][fn][4 * q + 1] += o[1];
+            acc[KEEP * 2 + f2][fn][4 * q + 2] += o[2];
+            acc[KEEP * 2 + f2][fn][4 * q + 3] += o[3];
+          }
+      lds_barrier();
+      if constexpr (DBG) store_acc_half(std::integral_constant<int, KEEP>{});
+      else out_half(std::integral_constant<int, KEEP>{});
+    };
+    if (ks == 0) finish(std::integral_constant<int, 0>{});
+    else finish(std::integral_constant<int, 1>{});
+  } else {
+    if constexpr (DBG) {
+      store_acc_half(std::integral_constant<int, 0>{});
+      store_acc_half(std::integral_constant<int, 1>{});
+    } else {
+      out_half(std::integral_constant<int, 0>{});
+      out_half(std::integral_constant<int, 1>{});
     }
   }
 }
