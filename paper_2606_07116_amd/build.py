@@ -29,6 +29,14 @@ FLAGS = [
 ]
 
 
+# Per-file additions.  rotate_quantize: inputs are finite by contract, so NaN
+# semantics are not honoured and the IEEE mode bit is off; max / min then take
+# lane-permuted (DPP) operands directly instead of canonicalising them first.
+EXTRA = {
+    "rotate_quantize.hip": ["-fno-honor-nans", "-mno-amdgpu-ieee"],
+}
+
+
 def hipcc():
     for c in (os.environ.get("HIPCC"), shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
         if c and os.path.exists(c):
@@ -38,7 +46,7 @@ def hipcc():
 
 def _compile(src):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [hipcc()] + FLAGS + ["-c", src, "-o", obj]
+    cmd = [hipcc()] + FLAGS + EXTRA.get(os.path.basename(src), []) + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

@@ -8,32 +8,75 @@
 // becomes the group's constant offset (Eq. 5), absorbed by the zero-point.
 //
 // Work decomposition: one wavefront owns a tile of T = 64 * E consecutive
-// elements (E = 64 registers per lane; E = 128 for g = 8192), i.e. T / g whole
-// groups.  Tile element i sits in
-//   layout A: lane i[8:3], register i[2:0] | i[high:9] << 3   (16-byte chunks:
-//             coalesced bf16 loads, packed code stores)
-//   layout B: lane i[2:0] | i[11:9] << 3, register i[8:3] | i[12] << 6
-// The Walsh-Hadamard butterflies for index bits held in registers run in
-// registers: bits {0,1,2,9,..} in layout A, bits {3..8} in layout B.  The
-// two layouts are exchanged through a swizzled LDS buffer (no cross-lane
-// arithmetic, no workgroup barrier beyond the wave itself).  Group max/min use
-// in-register max/min plus xor-shuffles over the lanes of a group; the codes
-// are produced with one fma + one med3 per element and packed 8 per dword.
+// elements of the group sequence, i.e. T / g whole groups, with E registers
+// per lane: E = max(16, min(64, g / 8)), and 128 for g = 8192.  Tile element i
+// sits in
+//   layout A: lane i[8:3], register i[2:0] | i[high:9] << 3
+//             (16-byte chunks: coalesced bf16 loads, packed code stores)
+//   layout B: lane i[2:0] | i[S+2:S] << 3, register i[S-1:3] (| i[12] << 6
+//             when E = 128), with S = 3 + min(log2 E, 6)
+// The Walsh-Hadamard butterflies for the index bits held in registers run in
+// registers: bits {0, 1, 2, 9, ...} in layout A, then bits {3, ..., S-1} in
+// layout B, which completes every group.  Group statistics, parameters and
+// codes are computed in layout B for g >= 128 (a lane then holds 16 or more
+// elements of a single group), in layout A for smaller groups.  The codes
+// return to layout A through LDS and are packed 8 per dword.  The layouts are
+// exchanged through a padded LDS buffer; one wave per workgroup.
 #include "common.h"
 #include "internal.h"
 
 namespace offq {
 namespace {
 
-// LDS word for tile element i: xor-swizzle so that both the layout-A 16-byte
-// accesses and the layout-B 4-byte accesses are free of bank conflicts.
-__device__ __forceinline__ int lds_index(int i) {
-  return i ^ (((i >> 9) & 7) << 3) ^ (((i >> 5) & 1) << 2);
-}
+template <int LOGG>
+struct Geom {
+  static constexpr int LOGE = LOGG <= 7 ? 4 : LOGG == 8 ? 5 : LOGG <= 12 ? 6 : 7;
+  static constexpr int E = 1 << LOGE;
+  static constexpr int T = 64 * E;
+  static constexpr int NCH = E / 8;      // 16-byte chunks per lane in layout A
+  static constexpr int GPT = T >> LOGG;  // groups per tile
+  static constexpr int SH = (LOGE < 6 ? LOGE : 6) + 3;
+  // LDS word of tile element i: 4 words of padding after every 32 elements and
+  // 8 after every 2^SH.  A layout-B 4-byte access then puts the 64 lanes in 64
+  // distinct banks (32 distinct per half-wave), each 8-lane phase of a
+  // layout-A 16-byte access covers 32 distinct banks, and every address is a
+  // per-lane base plus a compile-time offset.
+  static constexpr int word(int i) { return i + 4 * (i >> 5) + 8 * (i >> SH); }
+  static constexpr int WORDS = word(T - 1) + 1;
+  // layout A: element (lane, chunk ch, j) is i = 512 ch + 8 lane + j
+  static constexpr int elem_a(int lane, int ch, int j) { return 512 * ch + 8 * lane + j; }
+  static constexpr int a_base(int lane) {
+    return 8 * lane + 4 * (lane >> 2) + 8 * (lane >> (SH - 3));
+  }
+  static constexpr int a_off(int ch) { return 576 * ch + 8 * ((512 * ch) >> SH); }
+  // layout B: element (lane, register r)
+  static constexpr int elem_b(int lane, int r) {
+    return (lane & 7) + 8 * (r & 63) + (1 << SH) * (lane >> 3) + 4096 * (r >> 6);
+  }
+  static constexpr int b_base(int lane) {
+    return (lane & 7) + ((1 << SH) + (1 << (SH - 3)) + 8) * (lane >> 3);
+  }
+  static constexpr int b_off(int r) {
+    return 8 * (r & 63) + 4 * ((r & 63) >> 2) + word(4096) * (r >> 6);
+  }
+};
 
-__device__ __forceinline__ int elem_B(int lane, int r) {
-  return (lane & 7) | ((r & 63) << 3) | (((lane >> 3) & 7) << 9) | ((r >> 6) << 12);
+// The affine address maps agree with word(element) for every lane, chunk and
+// register of every tile shape.
+template <int LOGG>
+constexpr bool maps_ok() {
+  using Gm = Geom<LOGG>;
+  for (int lane = 0; lane < 64; ++lane) {
+    for (int ch = 0; ch < Gm::NCH; ++ch)
+      for (int j = 0; j < 8; j += 4)
+        if (Gm::word(Gm::elem_a(lane, ch, j)) != Gm::a_base(lane) + Gm::a_off(ch) + j)
+          return false;
+    for (int r = 0; r < Gm::E; ++r)
+      if (Gm::word(Gm::elem_b(lane, r)) != Gm::b_base(lane) + Gm::b_off(r)) return false;
+  }
+  return true;
 }
+static_assert(maps_ok<7>() && maps_ok<8>() && maps_ok<9>() && maps_ok<13>(), "LDS maps");
 
 template <int E, int RB>
 __device__ __forceinline__ void butterfly(float* v) {
@@ -47,8 +90,23 @@ __device__ __forceinline__ void butterfly(float* v) {
   }
 }
 
+// A butterfly stage with the normalisation c folded in:
+// (a + b) c and (a - b) c evaluated as fma(a, c, +-(b c)).
+template <int E, int RB>
+__device__ __forceinline__ void butterfly_scaled(float* v, float c) {
+#pragma unroll
+  for (int r = 0; r < E; ++r) {
+    if (!(r & (1 << RB))) {
+      const float a = v[r], bc = v[r | (1 << RB)] * c;
+      v[r] = __builtin_fmaf(a, c, bc);
+      v[r | (1 << RB)] = __builtin_fmaf(a, c, -bc);
+    }
+  }
+}
+
 // Butterflies over the index bits held in registers in layout A, except bit 0
-// (that stage is done while the bf16 input is converted).
+// (that stage is done while the bf16 input is converted): register bits 1, 2
+// and 3.. (index bits 9..).
 template <int LOGE, int LOGG>
 __device__ __forceinline__ void stages_A(float* v) {
   constexpr int E = 1 << LOGE;
@@ -57,25 +115,72 @@ __device__ __forceinline__ void stages_A(float* v) {
   if constexpr (LOGG > 9) butterfly<E, 3>(v);   // index bit 9
   if constexpr (LOGG > 10) butterfly<E, 4>(v);  // index bit 10
   if constexpr (LOGG > 11) butterfly<E, 5>(v);  // index bit 11
-  if constexpr (LOGG > 12) {                    // index bit 12
-    static_assert(LOGE >= 7, "g = 8192 needs 128 registers per lane");
-    butterfly<E, 6>(v);
+  if constexpr (LOGG > 12) butterfly<E, 6>(v);  // index bit 12
+}
+
+// Butterflies over index bits 3 .. min(log2 g, 9) - 1, held in registers
+// 0, 1, .. of layout B.  They complete the transform, so the last one applies
+// the factor c when SCALED.
+template <int LOGE, int LOGG, bool SCALED, int K>
+__device__ __forceinline__ void stage_B(float* v, float c) {
+  constexpr int E = 1 << LOGE;
+  constexpr int LAST = (LOGG < 9 ? LOGG : 9) - 4;
+  if constexpr (K < LAST || (K == LAST && !SCALED)) butterfly<E, K>(v);
+  if constexpr (K == LAST && SCALED) butterfly_scaled<E, K>(v, c);
+}
+template <int LOGE, int LOGG, bool SCALED>
+__device__ __forceinline__ void stages_B(float* v, float c) {
+  stage_B<LOGE, LOGG, SCALED, 0>(v, c);
+  stage_B<LOGE, LOGG, SCALED, 1>(v, c);
+  stage_B<LOGE, LOGG, SCALED, 2>(v, c);
+  stage_B<LOGE, LOGG, SCALED, 3>(v, c);
+  stage_B<LOGE, LOGG, SCALED, 4>(v, c);
+  stage_B<LOGE, LOGG, SCALED, 5>(v, c);
+}
+
+// a.lo * b.lo + a.hi * b.hi for two packed bf16 pairs, fp32 result.  The
+// three-operand encoding with an inline zero addend avoids the accumulator
+// copy that the two-operand form would need.
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b) {
+  float r;
+  asm("v_dot2_f32_bf16 %0, %1, %2, 0" : "=v"(r) : "v"(a), "s"(b));
+  return r;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(float,
+                            __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xf, 0xf, true));
+}
+
+// max / min over the lanes that differ in lane bits 0 .. NB-1 (all get it)
+template <int NB>
+__device__ __forceinline__ void lane_reduce(float& mx, float& mn) {
+  if constexpr (NB > 0) {
+    mx = fmaxf(mx, dpp<0xb1>(mx));  // quad_perm [1,0,3,2]
+    mn = fminf(mn, dpp<0xb1>(mn));
+  }
+  if constexpr (NB > 1) {
+    mx = fmaxf(mx, dpp<0x4e>(mx));  // quad_perm [2,3,0,1]
+    mn = fminf(mn, dpp<0x4e>(mn));
+  }
+  if constexpr (NB > 2) {
+    mx = fmaxf(mx, dpp<0x141>(mx));  // row_half_mirror
+    mn = fminf(mn, dpp<0x141>(mn));
+  }
+  if constexpr (NB > 3) {
+    mx = fmaxf(mx, dpp<0x140>(mx));  // row_mirror
+    mn = fminf(mn, dpp<0x140>(mn));
+  }
+  if constexpr (NB > 4) {
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mn = fminf(mn, __shfl_xor(mn, 16));
+  }
+  if constexpr (NB > 5) {
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mn = fminf(mn, __shfl_xor(mn, 32));
   }
 }
-
-// Butterflies over index bits 3..8, held in registers 0..5 of layout B.
-template <int LOGE, int LOGG>
-__device__ __forceinline__ void stages_B(float* v) {
-  constexpr int E = 1 << LOGE;
-  if constexpr (LOGG > 3) butterfly<E, 0>(v);
-  if constexpr (LOGG > 4) butterfly<E, 1>(v);
-  if constexpr (LOGG > 5) butterfly<E, 2>(v);
-  if constexpr (LOGG > 6) butterfly<E, 3>(v);
-  if constexpr (LOGG > 7) butterfly<E, 4>(v);
-  if constexpr (LOGG > 8) butterfly<E, 5>(v);
-}
-
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 // Where group q lives: row q / G and first channel (q % G) * g.  G == 1 is
 // the common case (one group per row, and every KV row); otherwise q / G is
@@ -93,38 +198,76 @@ __device__ __forceinline__ void group_loc(uint32_t q, int G, uint32_t m, int sh,
   }
 }
 
-template <int LOGE, int LOGG, bool HAD, bool DBG, bool G1>
+template <int LOGG, bool HAD, bool DBG, bool G1>
 __global__ __launch_bounds__(64) void rotate_quantize_kernel(
     const uint16_t* __restrict__ x, int64_t n_groups, int G, uint32_t dm, int dsh, int64_t ldx,
     uint8_t* __restrict__ codes, int64_t ldc, uint16_t* __restrict__ scale,
     int16_t* __restrict__ zero, float* __restrict__ ydbg, int64_t ldy, float cnorm) {
-  constexpr int E = 1 << LOGE;
-  constexpr int T = 64 * E;
-  constexpr int NCH = E / 8;
-  constexpr int GPT = T >> LOGG;  // groups per tile (>= 1)
+  using Gm = Geom<LOGG>;
+  constexpr int LOGE = Gm::LOGE, E = Gm::E, NCH = Gm::NCH, GPT = Gm::GPT;
   static_assert(GPT >= 1, "tile smaller than a group");
   // With an even log2(g) the normalisation 1/sqrt(g) is a power of two: the
   // butterflies' output is kept unscaled and the factor is folded into the
   // quantizer's reciprocal scale, which gives bit-identical codes.
   constexpr bool FOLD = HAD && (LOGG % 2 == 0);
-  __shared__ __attribute__((aligned(16))) float lds[T];
+  constexpr bool STATS_B = LOGG >= 7;
+  __shared__ __attribute__((aligned(16))) float lds[Gm::WORDS];
+  __shared__ uint32_t s_lo[STATS_B ? GPT : 1];
 
   const int lane = threadIdx.x;
   const int64_t gbase = (int64_t)blockIdx.x * GPT;
   const bool full = gbase + GPT <= n_groups;
+  float* const la = lds + Gm::a_base(lane);
+  float* const lb = lds + Gm::b_base(lane);
 
-  // per chunk: row and first channel of the 8 elements this lane holds
-  uint32_t crow[NCH], ccol[NCH];
+  // Per chunk: element offset into x and byte offset into the codes of the 8
+  // elements this lane holds in layout A.  For g >= 512 the chunk's group is
+  // the same for every lane (scalar arithmetic).  Groups past the end are
+  // clamped to the last one: read, never stored.
+  int64_t xoff[NCH], coff[NCH];
+  if constexpr (LOGG < 9 && G1) {
+    // group (= row) gbase + (ch << (9 - log2 g)) + (lane >> (log2 g - 3))
+    const int lr = lane >> (LOGG - 3);
+    const int c = 8 * (lane & ((1 << (LOGG - 3)) - 1));
+    if (full) {
+      const int64_t x0 = (gbase + lr) * ldx + c, c0 = (gbase + lr) * ldc + (c >> 1);
 #pragma unroll
-  for (int ch = 0; ch < NCH; ++ch) {
-    const int i = (ch << 9) | (lane << 3);
-    int64_t q = gbase + (i >> LOGG);
-    if (q >= n_groups) q = n_groups - 1;  // clamp: only read, never stored
-    uint32_t row, col0;
-    group_loc<G1>((uint32_t)q, G, dm, dsh, LOGG, row, col0);
-    crow[ch] = row;
-    ccol[ch] = col0 + (i & ((1 << LOGG) - 1));
+      for (int ch = 0; ch < NCH; ++ch) {
+        xoff[ch] = x0 + (int64_t)(ch << (9 - LOGG)) * ldx;
+        coff[ch] = c0 + (int64_t)(ch << (9 - LOGG)) * ldc;
+      }
+    } else {
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        int64_t q = gbase + (ch << (9 - LOGG)) + lr;
+        if (q >= n_groups) q = n_groups - 1;
+        xoff[ch] = q * ldx + c;
+        coff[ch] = q * ldc + (c >> 1);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      int64_t q;
+      int c;  // channel of the chunk's first element inside its group
+      if constexpr (LOGG >= 9) {
+        q = gbase + (ch >> (LOGG - 9));
+        c = ((ch & ((1 << (LOGG - 9)) - 1)) << 9) + 8 * lane;
+      } else {
+        q = gbase + (ch << (9 - LOGG)) + (lane >> (LOGG - 3));
+        c = 8 * (lane & ((1 << (LOGG - 3)) - 1));
+      }
+      if (q >= n_groups) q = n_groups - 1;
+      uint32_t row, col0;
+      group_loc<G1>((uint32_t)q, G, dm, dsh, LOGG, row, col0);
+      xoff[ch] = (int64_t)row * ldx + col0 + c;
+      coff[ch] = (int64_t)row * ldc + ((col0 + c) >> 1);
+    }
   }
+  auto stored = [&](int ch) -> bool {
+    const int64_t q = gbase + (((ch << 9) | (lane << 3)) >> LOGG);
+    return full || q < n_groups;
+  };
 
   float v[E];
 
@@ -134,148 +277,155 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
   // for the sum and the difference.
 #pragma unroll
   for (int ch = 0; ch < NCH; ++ch) {
-    uint4 d = *reinterpret_cast<const uint4*>(x + (int64_t)crow[ch] * ldx + ccol[ch]);
+    uint4 d = *reinterpret_cast<const uint4*>(x + xoff[ch]);
     const uint32_t w[4] = {d.x, d.y, d.z, d.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       if constexpr (HAD) {
-        const bf16x2_t b = __builtin_bit_cast(bf16x2_t, w[j]);
-        const bf16x2_t pp = {(__bf16)1.0f, (__bf16)1.0f};
-        const bf16x2_t pm = {(__bf16)1.0f, (__bf16)-1.0f};
-        v[ch * 8 + 2 * j] = __builtin_amdgcn_fdot2_f32_bf16(b, pp, 0.0f, false);
-        v[ch * 8 + 2 * j + 1] = __builtin_amdgcn_fdot2_f32_bf16(b, pm, 0.0f, false);
+        v[ch * 8 + 2 * j] = dot2_bf16(w[j], 0x3f803f80u);      // (1, 1)
+        v[ch * 8 + 2 * j + 1] = dot2_bf16(w[j], 0xbf803f80u);  // (1, -1)
       } else {
         v[ch * 8 + 2 * j] = bf16_lo(w[j]);
         v[ch * 8 + 2 * j + 1] = bf16_hi(w[j]);
       }
     }
   }
+  if constexpr (HAD) stages_A<LOGE, LOGG>(v);
 
-  if constexpr (HAD) {
-    stages_A<LOGE, LOGG>(v);
-    // A -> B through LDS
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      const int i0 = (ch << 9) | (lane << 3);
-      *reinterpret_cast<float4*>(&lds[lds_index(i0)]) =
-          make_float4(v[ch * 8 + 0], v[ch * 8 + 1], v[ch * 8 + 2], v[ch * 8 + 3]);
-      *reinterpret_cast<float4*>(&lds[lds_index(i0 | 4)]) =
-          make_float4(v[ch * 8 + 4], v[ch * 8 + 5], v[ch * 8 + 6], v[ch * 8 + 7]);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < E; ++r) v[r] = lds[lds_index(elem_B(lane, r))];
-    __syncthreads();
-    stages_B<LOGE, LOGG>(v);
-    // B -> A
-#pragma unroll
-    for (int r = 0; r < E; ++r) lds[lds_index(elem_B(lane, r))] = v[r];
-    __syncthreads();
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      const int i0 = (ch << 9) | (lane << 3);
-      const float4 a = *reinterpret_cast<const float4*>(&lds[lds_index(i0)]);
-      const float4 b = *reinterpret_cast<const float4*>(&lds[lds_index(i0 | 4)]);
-      const float c = FOLD ? 1.0f : cnorm;
-      v[ch * 8 + 0] = a.x * c;
-      v[ch * 8 + 1] = a.y * c;
-      v[ch * 8 + 2] = a.z * c;
-      v[ch * 8 + 3] = a.w * c;
-      v[ch * 8 + 4] = b.x * c;
-      v[ch * 8 + 5] = b.y * c;
-      v[ch * 8 + 6] = b.z * c;
-      v[ch * 8 + 7] = b.w * c;
-    }
-  }
-
-  // ---- group max / min ---------------------------------------------------
-  float cmx[NCH], cmn[NCH];
+  // ---- A -> B ---------------------------------------------------------------
 #pragma unroll
   for (int ch = 0; ch < NCH; ++ch) {
-    float a = v[ch * 8], b = v[ch * 8];
-#pragma unroll
-    for (int j = 1; j < 8; ++j) {
-      a = fmaxf(a, v[ch * 8 + j]);
-      b = fminf(b, v[ch * 8 + j]);
-    }
-    cmx[ch] = a;
-    cmn[ch] = b;
+    *reinterpret_cast<float4*>(la + Gm::a_off(ch)) =
+        make_float4(v[ch * 8 + 0], v[ch * 8 + 1], v[ch * 8 + 2], v[ch * 8 + 3]);
+    *reinterpret_cast<float4*>(la + Gm::a_off(ch) + 4) =
+        make_float4(v[ch * 8 + 4], v[ch * 8 + 5], v[ch * 8 + 6], v[ch * 8 + 7]);
   }
-  if constexpr (LOGG >= 9) {
-    constexpr int S = 1 << (LOGG - 9);  // chunks per group within a lane
+  __syncthreads();
 #pragma unroll
-    for (int ch = 0; ch < NCH; ch += S) {
+  for (int r = 0; r < E; ++r) v[r] = lb[Gm::b_off(r)];
+  if constexpr (HAD) stages_B<LOGE, LOGG, !FOLD>(v, cnorm);
+  // v now holds y in layout B (y / cnorm when folded)
+
+  if constexpr (DBG) {
+    // y to global through LDS, in layout A (16-byte stores)
+    const float c = FOLD ? cnorm : 1.0f;
+    __syncthreads();
 #pragma unroll
-      for (int j = 1; j < S; ++j) {
-        cmx[ch] = fmaxf(cmx[ch], cmx[ch + j]);
-        cmn[ch] = fminf(cmn[ch], cmn[ch + j]);
-      }
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        cmx[ch] = fmaxf(cmx[ch], __shfl_xor(cmx[ch], off));
-        cmn[ch] = fminf(cmn[ch], __shfl_xor(cmn[ch], off));
-      }
-#pragma unroll
-      for (int j = 1; j < S; ++j) {
-        cmx[ch + j] = cmx[ch];
-        cmn[ch + j] = cmn[ch];
-      }
-    }
-  } else {
+    for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = v[r] * c;
+    __syncthreads();
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
-#pragma unroll
-      for (int off = 1; off < (1 << (LOGG - 3)); off <<= 1) {
-        cmx[ch] = fmaxf(cmx[ch], __shfl_xor(cmx[ch], off));
-        cmn[ch] = fminf(cmn[ch], __shfl_xor(cmn[ch], off));
+      if (stored(ch)) {
+        const int64_t row = xoff[ch] / ldx;
+        float* yp = ydbg + row * ldy + (xoff[ch] - row * ldx);
+        *reinterpret_cast<float4*>(yp) = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
+        *reinterpret_cast<float4*>(yp + 4) =
+            *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
       }
     }
   }
 
-  // ---- parameters, codes, stores ------------------------------------------
-  constexpr int SP = LOGG >= 9 ? (1 << (LOGG - 9)) : 1;
+  uint32_t corr[NCH];  // per chunk: bits(lo) * 0x11111111 of its group
+  if constexpr (STATS_B) {
+    // ---- statistics, parameters and codes in layout B ----------------------
+    // All E registers of a lane belong to one group, which spans lane bits
+    // 0 .. NB-1: group lane >> 3 of the tile when g <= 512, lane >> (log2 g - 6)
+    // when g >= 1024.
+    constexpr int NB = LOGG <= 9 ? 3 : LOGG - 6;
+    float mx = v[0], mn = v[0];
 #pragma unroll
-  for (int cg = 0; cg < NCH; cg += SP) {
-    // group max / min of the quantized values y (= v * cnorm, exact when folded)
-    QParams P = FOLD ? quant_params(cmx[cg] * cnorm, cmn[cg] * cnorm)
-                     : quant_params(cmx[cg], cmn[cg]);
+    for (int r = 1; r < E; ++r) {
+      mx = fmaxf(mx, v[r]);
+      mn = fminf(mn, v[r]);
+    }
+    lane_reduce<NB < 6 ? NB : 6>(mx, mn);
+    QParams P = FOLD ? quant_params(mx * cnorm, mn * cnorm) : quant_params(mx, mn);
     if constexpr (FOLD) P.r *= cnorm;  // exact: cnorm is a power of two
-    const uint32_t corr = __float_as_uint(P.lo) * 0x11111111u;
-#pragma unroll
-    for (int ch = cg; ch < cg + SP; ++ch) {
-      const int i = (ch << 9) | (lane << 3);
-      const int64_t q = gbase + (i >> LOGG);
-      uint32_t w = 0;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) w += quant_bits(v[ch * 8 + j], P) << (4 * j);
-      w -= corr;
-      if (full || q < n_groups) {
-        *reinterpret_cast<uint32_t*>(codes + (int64_t)crow[ch] * ldc + (ccol[ch] >> 1)) = w;
-        if constexpr (DBG) {
-          const float c = FOLD ? cnorm : 1.0f;
-          float* yp = ydbg + (int64_t)crow[ch] * ldy + ccol[ch];
-          *reinterpret_cast<float4*>(yp) = make_float4(v[ch * 8 + 0] * c, v[ch * 8 + 1] * c,
-                                                       v[ch * 8 + 2] * c, v[ch * 8 + 3] * c);
-          *reinterpret_cast<float4*>(yp + 4) = make_float4(v[ch * 8 + 4] * c, v[ch * 8 + 5] * c,
-                                                           v[ch * 8 + 6] * c, v[ch * 8 + 7] * c);
-        }
-        const bool writer = (LOGG >= 9) ? (lane == 0 && ch == cg)
-                                        : ((lane & ((1 << (LOGG >= 9 ? 0 : LOGG - 3)) - 1)) == 0);
-        if (writer) {
-          scale[q] = P.s16;
-          zero[q] = P.z;
-        }
+    const int gi = lane >> NB;
+    if ((lane & ((1 << NB) - 1)) == 0) {
+      s_lo[gi] = __float_as_uint(P.lo);
+      if (full || gbase + gi < n_groups) {
+        scale[gbase + gi] = P.s16;
+        zero[gbase + gi] = P.z;
       }
     }
+    // codes as float bits, back to layout A
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = __uint_as_float(quant_bits(v[r], P));
+    __syncthreads();
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      const float4 a = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
+      const float4 b = *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
+      v[ch * 8 + 0] = a.x;
+      v[ch * 8 + 1] = a.y;
+      v[ch * 8 + 2] = a.z;
+      v[ch * 8 + 3] = a.w;
+      v[ch * 8 + 4] = b.x;
+      v[ch * 8 + 5] = b.y;
+      v[ch * 8 + 6] = b.z;
+      v[ch * 8 + 7] = b.w;
+      corr[ch] = s_lo[((ch << 9) | (lane << 3)) >> LOGG] * 0x11111111u;
+    }
+  } else {
+    // ---- back to layout A; statistics, parameters and codes there ----------
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = v[r];
+    __syncthreads();
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      const float4 a = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
+      const float4 b = *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
+      v[ch * 8 + 0] = a.x;
+      v[ch * 8 + 1] = a.y;
+      v[ch * 8 + 2] = a.z;
+      v[ch * 8 + 3] = a.w;
+      v[ch * 8 + 4] = b.x;
+      v[ch * 8 + 5] = b.y;
+      v[ch * 8 + 6] = b.z;
+      v[ch * 8 + 7] = b.w;
+    }
+    // a group is 2^(log2 g - 3) consecutive lanes of one chunk
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      float mx = v[ch * 8], mn = v[ch * 8];
+#pragma unroll
+      for (int j = 1; j < 8; ++j) {
+        mx = fmaxf(mx, v[ch * 8 + j]);
+        mn = fminf(mn, v[ch * 8 + j]);
+      }
+      lane_reduce<LOGG - 3>(mx, mn);
+      QParams P = FOLD ? quant_params(mx * cnorm, mn * cnorm) : quant_params(mx, mn);
+      if constexpr (FOLD) P.r *= cnorm;
+      const int64_t q = gbase + (((ch << 9) | (lane << 3)) >> LOGG);
+      if ((lane & ((1 << (LOGG - 3)) - 1)) == 0 && (full || q < n_groups)) {
+        scale[q] = P.s16;
+        zero[q] = P.z;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[ch * 8 + j] = __uint_as_float(quant_bits(v[ch * 8 + j], P));
+      corr[ch] = __float_as_uint(P.lo) * 0x11111111u;
+    }
+  }
+
+  // ---- pack 8 codes per dword and store (layout A) -------------------------
+#pragma unroll
+  for (int ch = 0; ch < NCH; ++ch) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w += __float_as_uint(v[ch * 8 + j]) << (4 * j);
+    w -= corr[ch];
+    if (stored(ch)) *reinterpret_cast<uint32_t*>(codes + coff[ch]) = w;
   }
 }
 
-template <int LOGE, int LOGG>
+template <int LOGG>
 hipError_t launch_t(const uint16_t* x, int64_t n_groups, int G, int64_t ldx, bool had,
                     uint8_t* codes, int64_t ldc, uint16_t* scale, int16_t* zero, float* ydbg,
                     int64_t ldy, hipStream_t stream) {
-  constexpr int T = 64 << LOGE;
-  constexpr int GPT = T >> LOGG;
+  constexpr int GPT = Geom<LOGG>::GPT;
   const int64_t nblk = (n_groups + GPT - 1) / GPT;
   const dim3 grid((unsigned)nblk), block(64);
   const float cnorm = (float)(1.0 / __builtin_sqrt((double)(1 << LOGG)));
@@ -284,9 +434,9 @@ hipError_t launch_t(const uint16_t* x, int64_t n_groups, int G, int64_t ldx, boo
   while ((1 << lg) < G) ++lg;
   const int dsh = 31 + lg;
   const uint32_t dm = (uint32_t)(((uint64_t(1) << dsh) + (uint64_t)G - 1) / (uint64_t)G);
-#define OFFQ_RQ(HD, DB, G1)                                                                     \
-  hipLaunchKernelGGL((rotate_quantize_kernel<LOGE, LOGG, HD, DB, G1>), grid, block, 0, stream, \
-                     x, n_groups, G, dm, dsh, ldx, codes, ldc, scale, zero, ydbg, ldy,         \
+#define OFFQ_RQ(HD, DB, G1)                                                                  \
+  hipLaunchKernelGGL((rotate_quantize_kernel<LOGG, HD, DB, G1>), grid, block, 0, stream, x, \
+                     n_groups, G, dm, dsh, ldx, codes, ldc, scale, zero, ydbg, ldy,         \
                      HD ? cnorm : 1.0f)
 #define OFFQ_RQ_G(HD, DB) \
   if (G == 1) OFFQ_RQ(HD, DB, true); else OFFQ_RQ(HD, DB, false);
@@ -307,21 +457,21 @@ hipError_t launch_rotate_quantize(const uint16_t* x, int64_t n_groups, int G,
                                   uint8_t* codes, int64_t ldc_bytes,
                                   uint16_t* scale, int16_t* zero, float* y_debug,
                                   int64_t ldy, hipStream_t stream) {
-#define OFFQ_RQ_CASE(L, LE)                                                          \
-  case L:                                                                            \
-    return launch_t<LE, L>(x, n_groups, G, ldx, hadamard, codes, ldc_bytes, scale, \
-                           zero, y_debug, ldy, stream);
+#define OFFQ_RQ_CASE(L)                                                                        \
+  case L:                                                                                      \
+    return launch_t<L>(x, n_groups, G, ldx, hadamard, codes, ldc_bytes, scale, zero, y_debug, \
+                       ldy, stream);
   switch (log2g) {
-    OFFQ_RQ_CASE(4, 6)
-    OFFQ_RQ_CASE(5, 6)
-    OFFQ_RQ_CASE(6, 6)
-    OFFQ_RQ_CASE(7, 6)
-    OFFQ_RQ_CASE(8, 6)
-    OFFQ_RQ_CASE(9, 6)
-    OFFQ_RQ_CASE(10, 6)
-    OFFQ_RQ_CASE(11, 6)
-    OFFQ_RQ_CASE(12, 6)
-    OFFQ_RQ_CASE(13, 7)
+    OFFQ_RQ_CASE(4)
+    OFFQ_RQ_CASE(5)
+    OFFQ_RQ_CASE(6)
+    OFFQ_RQ_CASE(7)
+    OFFQ_RQ_CASE(8)
+    OFFQ_RQ_CASE(9)
+    OFFQ_RQ_CASE(10)
+    OFFQ_RQ_CASE(11)
+    OFFQ_RQ_CASE(12)
+    OFFQ_RQ_CASE(13)
     default:
       return hipErrorInvalidValue;
   }
