@@ -11,15 +11,22 @@
 // Organisation
 // * 4 waves per workgroup in a 2 x 2 arrangement, each owning 128 tokens x 64
 //   output channels (4 x 2 MFMA tiles of 32 x 32): 128 int32 accumulators for
-//   the current group and 128 fp32 running sums; workgroup tile 256 x 128.
-// * Operand staging, fragment reads, unpacking and the transposed MFMA are
-//   those of the one-group kernel: stages of 128 k through a 3-deep LDS ring,
-//   one LDS-only barrier per stage.
-// * At the end of each group (g / 128 stages) every accumulator is folded into
-//   its running sum, F += (s / 16) * acc + (-s z) * colsum, in fp32, and the
-//   first MFMA of the next group starts from a zero accumulator.  The row
-//   parameters (s / 16, -s z) and the column sums of a group are staged in LDS
-//   one group ahead (double buffered).
+//   the current group and 128 fp32 running sums F; workgroup tile 256 x 128.
+// * Stages of 128 k go from global memory straight into a 4-deep LDS ring
+//   (buffer loads with the LDS destination, 3 stages ahead; rows past the end
+//   read as zero), so no registers hold staged data.  One barrier per stage,
+//   preceded by a wait for the stage two ahead only.  The stage loop is
+//   unrolled by the ring depth so that every LDS access names its ring buffer
+//   at compile time.
+// * Fragment reads, unpacking and the transposed MFMA are those of the
+//   one-group kernel.
+// * At the end of each group (g / 128 stages) the accumulators are folded
+//   into the running sums, F += (s / 16) * acc in fp32 (s / 16 undoes the 16x
+//   widening of the weight codes), and the first MFMA of the next group starts
+//   from a zero accumulator.  The row scales of a group are staged in LDS one
+//   group ahead.
+// * After the last group the zero-point terms are added with one fp32 MFMA
+//   per pair of groups: F += sum_b (-s z)[m, b] * colsum[b, n].
 // * Epilogue: Y = sw * F -> bf16 through LDS for 16-byte coalesced stores.
 #include <type_traits>
 
@@ -42,23 +49,57 @@ struct GCfg {
   static constexpr int A_LD = A_SLOTS / 256;       // loads per thread and stage
   static constexpr int B_LD = B_SLOTS / 256;
   static constexpr int KSTAGE = 128;               // k per stage
-  static constexpr int NBUF = 3;                   // LDS ring depth
+  static constexpr int NBUF = 4;                   // LDS ring depth
+  static constexpr int GMAX = 28;                  // groups whose parameters fit in LDS
 };
 
-template <bool DBG>
+// s_waitcnt with only the vector-memory counter bounded (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// 16 bytes per lane from a buffer straight into LDS: lane l writes bytes
+// [lds + 16 l, lds + 16 l + 16) (lds is the wave-uniform LDS byte address).
+// Issued as inline assembly, so the compiler neither tracks these writes nor
+// inserts waits for them: the ring's own vmcnt waits and barriers order them.
+__device__ __forceinline__ void buffer_to_lds16(__amdgpu_buffer_rsrc_t rsrc, uint32_t lds,
+                                                int voff, int soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
+}
+
+// Workgroup barrier for the ring: waits for the wave's own LDS operations,
+// synchronises, and is a compiler-level memory barrier.  The buffer-to-LDS
+// loads a stage needs are waited for with wait_vmcnt before it.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+// MODE: stages per group: 1, 2, 4, or a multiple of 8 (MODE 8).
+template <bool DBG, int MODE>
 __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
     const uint8_t* __restrict__ A, const uint16_t* __restrict__ a_scale,
     const int16_t* __restrict__ a_zero, const uint8_t* __restrict__ W,
     const uint16_t* __restrict__ w_scale, const int32_t* __restrict__ w_colsum, int M, int N,
     int K, int log2g, uint16_t* __restrict__ Y, int64_t ldy, int32_t* __restrict__ acc_dbg) {
   using C = GCfg;
-  __shared__ uint4 lds[C::NBUF * C::STAGE_SLOTS];
-  __shared__ __attribute__((aligned(16))) float2 sRP[2][C::BM];  // (s / 16, -s z) per row
-  __shared__ __attribute__((aligned(16))) float sCS[2][C::BN];   // colsum per column
+  __shared__ uint4 ring[C::NBUF * C::STAGE_SLOTS];
+  // per group b: s / 16 and z of the tile's rows, colsum of its columns
+  __shared__ float sRS[C::GMAX][C::BM];
+  __shared__ short sZ[C::GMAX][C::BM];
+  __shared__ float sCS[C::GMAX][C::BN];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int h = lane >> 5, fr = lane & 31;
   const int wm = wave & 1, wn = wave >> 1;
 
@@ -72,28 +113,6 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
   const int G = K >> log2g;
   const int spg = 1 << (log2g - 7);  // stages per group
 
-  // ---- per-group parameters, staged one group ahead ----------------------
-  float p_s = 0.0f, p_z = 0.0f, p_c = 0.0f;
-  auto param_load = [&](int b) {
-    const int row = tm + tid;
-    if (row < M) {
-      p_s = fp16_bits_to_f32(a_scale[(int64_t)row * G + b]);
-      p_z = (float)a_zero[(int64_t)row * G + b];
-    } else {
-      p_s = 0.0f;
-      p_z = 0.0f;
-    }
-    if (tid < C::BN) {
-      const int col = tn + tid;
-      p_c = col < N ? (float)w_colsum[(int64_t)b * N + col] : 0.0f;
-    }
-  };
-  auto param_store = [&](int b) {
-    // s / 16 undoes the 16x widening of the weight codes (exact)
-    sRP[b & 1][tid] = make_float2(p_s * 0.0625f, -(p_s * p_z));
-    if (tid < C::BN) sCS[b & 1][tid] = p_c;
-  };
-
   constexpr int RSTEP = 256 / C::NC;
   const int row0 = tid / C::NC;
   const int chunk = swz<C::NC>(row0, tid % C::NC);
@@ -103,107 +122,82 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
       (void*)(W + (int64_t)tn * ldk), 0, (int)((int64_t)(N - tn) * ldk), 0x00020000);
   const int voff = row0 * (int)ldk + chunk * 16;
   const int vstep = RSTEP * (int)ldk;
+  const uint32_t ring_lds = lds_addr(ring) + wave * 64 * 16;
 
-  v4i ra[C::A_LD], rb[C::B_LD];
-  auto gload = [&](int st) {
+  // stage st into ring buffer J: this thread's slots tid + 256 i, written by
+  // each wave as 64 consecutive 16-byte slots per load
+  auto dma = [&](int J, int st) __attribute__((always_inline)) {
+    const uint32_t base = ring_lds + J * (C::STAGE_SLOTS * 16);
     const int soff = st * (C::KSTAGE / 2);
 #pragma unroll
     for (int i = 0; i < C::A_LD; ++i)
-      ra[i] = __builtin_amdgcn_raw_buffer_load_b128(arsrc, voff + i * vstep, soff, 0);
+      buffer_to_lds16(arsrc, base + i * 256 * 16, voff + i * vstep, soff);
 #pragma unroll
     for (int i = 0; i < C::B_LD; ++i)
-      rb[i] = __builtin_amdgcn_raw_buffer_load_b128(brsrc, voff + i * vstep, soff, 0);
+      buffer_to_lds16(brsrc, base + (C::A_SLOTS + i * 256) * 16, voff + i * vstep, soff);
   };
-  auto lstore = [&](int buf) {
-    v4i* base = reinterpret_cast<v4i*>(lds + buf * C::STAGE_SLOTS);
+  // this lane's fragment slots for chunk column 2h + jj; fragments f are 32
+  // rows apart, which keeps the swizzle
+  const uint4* a_frag0 = ring + (wm * 128 + fr) * C::NC + swz<C::NC>(fr, 2 * h);
+  const uint4* a_frag1 = ring + (wm * 128 + fr) * C::NC + swz<C::NC>(fr, 2 * h + 1);
+  const uint4* b_frag0 = ring + C::A_SLOTS + (wn * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h);
+  const uint4* b_frag1 = ring + C::A_SLOTS + (wn * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h + 1);
+  auto fread = [&](auto JC, int jj, uint4* pa, uint4* pb) __attribute__((always_inline)) {
+    constexpr int J = decltype(JC)::value;
+    const uint4* As = (jj ? a_frag1 : a_frag0) + J * C::STAGE_SLOTS;
+    const uint4* Bs = (jj ? b_frag1 : b_frag0) + J * C::STAGE_SLOTS;
 #pragma unroll
-    for (int i = 0; i < C::A_LD; ++i) base[tid + 256 * i] = ra[i];
+    for (int f = 0; f < 4; ++f) pa[f] = As[f * 32 * C::NC];
 #pragma unroll
-    for (int i = 0; i < C::B_LD; ++i) base[C::A_SLOTS + tid + 256 * i] = rb[i];
-  };
-  auto fread = [&](int buf, int jj, uint4* pa, uint4* pb) {
-    const uint4* As = lds + buf * C::STAGE_SLOTS;
-    const uint4* Bs = As + C::A_SLOTS;
-    const int c = 2 * h + jj;
-#pragma unroll
-    for (int f = 0; f < 4; ++f) {
-      const int r = wm * 128 + f * 32 + fr;
-      pa[f] = As[r * C::NC + swz<C::NC>(r, c)];
-    }
-#pragma unroll
-    for (int f = 0; f < 2; ++f) {
-      const int r = wn * 64 + f * 32 + fr;
-      pb[f] = Bs[r * C::NC + swz<C::NC>(r, c)];
-    }
+    for (int f = 0; f < 2; ++f) pb[f] = Bs[f * 32 * C::NC];
   };
 
   v16i acc[4][2];
-  float F[4][2][16];
+  v16f F[4][2];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       acc[a][b] = v16i{};
-#pragma unroll
-      for (int i = 0; i < 16; ++i) F[a][b][i] = 0.0f;
+      F[a][b] = v16f{};
     }
 
   // two k-steps (low and high nibbles of one 16-byte chunk per fragment);
-  // FRESH: the low-nibble MFMAs start the accumulators from zero
-  auto mma2 = [&](const uint4* pa, const uint4* pb, auto FC) {
+  // FRESH: the low-nibble MFMAs start the accumulators from zero.  Operands
+  // are unpacked just before use to keep the live registers down.
+  auto mma2 = [&](const uint4* pa, const uint4* pb, auto FC) __attribute__((always_inline)) {
     constexpr bool FRESH = decltype(FC)::value;
-    v4i ua[4], ub[2];
+    const v4i ub0 = wgt_lo16(pb[0]), ub1 = wgt_lo16(pb[1]);
 #pragma unroll
-    for (int f = 0; f < 4; ++f) ua[f] = act_lo(pa[f]);
-#pragma unroll
-    for (int f = 0; f < 2; ++f) ub[f] = wgt_lo16(pb[f]);
-    v4i na[4], nb[2];
-#pragma unroll
-    for (int f = 0; f < 4; ++f) na[f] = act_hi(pa[f]);
-#pragma unroll
-    for (int f = 0; f < 2; ++f) nb[f] = wgt_hi16(pb[f]);
-#pragma unroll
-    for (int fm = 0; fm < 4; ++fm)
-#pragma unroll
-      for (int fn = 0; fn < 2; ++fn)
-        acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub[fn], ua[fm],
-                                                            FRESH ? v16i{} : acc[fm][fn], 0, 0, 0);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+    for (int fm = 0; fm < 4; ++fm) {
+      const v4i ua = act_lo(pa[fm]);
+      acc[fm][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub0, ua, FRESH ? v16i{} : acc[fm][0], 0, 0, 0);
+      acc[fm][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub1, ua, FRESH ? v16i{} : acc[fm][1], 0, 0, 0);
     }
+    const v4i nb0 = wgt_hi16(pb[0]), nb1 = wgt_hi16(pb[1]);
 #pragma unroll
-    for (int fm = 0; fm < 4; ++fm)
-#pragma unroll
-      for (int fn = 0; fn < 2; ++fn)
-        acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(nb[fn], na[fm], acc[fm][fn], 0, 0, 0);
+    for (int fm = 0; fm < 4; ++fm) {
+      const v4i na = act_hi(pa[fm]);
+      acc[fm][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(nb0, na, acc[fm][0], 0, 0, 0);
+      acc[fm][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(nb1, na, acc[fm][1], 0, 0, 0);
+    }
   };
 
   // Lane column fr of fragment fm is token row wm*128 + fm*32 + fr; register
-  // i of fragment (fn) is output channel wn*64 + fn*32 + 8*(i/4) + 4*h + i%4.
-  auto fold = [&](int b) {
-    float2 rp[4];
+  // i of fragment (fm, fn) is output channel wn*64 + fn*32 + 8*(i/4) + 4*h + i%4.
+  // F += (s / 16) * acc  (s / 16 undoes the 16x widening of the weight codes)
+  auto fold = [&](int b) __attribute__((always_inline)) {
 #pragma unroll
-    for (int fm = 0; fm < 4; ++fm) rp[fm] = sRP[b & 1][wm * 128 + fm * 32 + fr];
+    for (int fm = 0; fm < 4; ++fm) {
+      const float rs = sRS[b][wm * 128 + fm * 32 + fr];
 #pragma unroll
-    for (int fn = 0; fn < 2; ++fn)
+      for (int fn = 0; fn < 2; ++fn)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 c4 =
-            *reinterpret_cast<const float4*>(&sCS[b & 1][wn * 64 + fn * 32 + q * 8 + h * 4]);
-        const float cs[4] = {c4.x, c4.y, c4.z, c4.w};
-#pragma unroll
-        for (int fm = 0; fm < 4; ++fm)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            float& f = F[fm][fn][q * 4 + e];
-            f = __builtin_fmaf(rp[fm].x, (float)acc[fm][fn][q * 4 + e], f);
-            f = __builtin_fmaf(rp[fm].y, cs[e], f);
-          }
-      }
+        for (int i = 0; i < 16; ++i)
+          F[fm][fn][i] = __builtin_fmaf(rs, (float)acc[fm][fn][i], F[fm][fn][i]);
+    }
   };
-  auto dump = [&](int b) {  // debug: the raw accumulators of group b
+  auto dump = [&](int b) __attribute__((always_inline)) {  // debug: raw accumulators of group b
 #pragma unroll
     for (int fm = 0; fm < 4; ++fm) {
       const int row = tm + wm * 128 + fm * 32 + fr;
@@ -221,53 +215,163 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
     }
   };
 
-  // prologue: parameters of group 0, stages 0 and 1 into the ring, stage 2
-  // into registers
-  param_load(0);
-  param_store(0);
-  gload(0);
-  lstore(0);
-  if (nst > 1) {
-    gload(1);
-    lstore(1);
-  }
-  if (nst > 2) gload(2);
-  lds_barrier();
-  uint4 pc_a[4], pc_b[2];
-  fread(0, 0, pc_a, pc_b);
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
 
-  for (int st = 0; st < nst; ++st) {
-    const int buf = st % C::NBUF;
-    const int b = st >> (log2g - 7);
-    const bool first = (st & (spg - 1)) == 0;
-    const bool last = (st & (spg - 1)) == spg - 1;
-    if (st + 2 < nst) lstore((st + 2) % C::NBUF);
-    // the next group's parameters: loaded before the stage prefetch so that
-    // writing them to LDS does not wait for it
-    const bool stage_next = first && b + 1 < G;
-    if (stage_next) param_load(b + 1);
-    if (st + 3 < nst) gload(st + 3);
+  // prologue: stages 0, 1, 2 in flight to the ring; the group parameters of
+  // the tile into LDS meanwhile
+  dma(0, 0);
+  if (nst > 1) dma(1, 1);
+  if (nst > 2) dma(2, 2);
+  {
+    // Row parameters of the tile: a contiguous block of 256 * G entries of the
+    // [M, G] arrays, read coalesced (entry e = tid + 256 p is row e / G, group
+    // e % G); column sums: group b, column c = colsum[b * N + tn + c].  All
+    // loads are issued before the first LDS write.
+    const float inv_g = 1.0f / (float)G;
+    const int64_t base = (int64_t)tm * G;
+    const int nrow_e = min(C::BM, M - tm) * G;  // valid entries of the block
+    uint16_t sv[C::GMAX];
+    int16_t zv[C::GMAX];
+#pragma unroll
+    for (int p = 0; p < C::GMAX; ++p) {
+      const int e = tid + 256 * p;
+      const bool ok = p < G && e < nrow_e;
+      sv[p] = ok ? a_scale[base + e] : (uint16_t)0;
+      zv[p] = ok ? a_zero[base + e] : (int16_t)0;
+    }
+    float cv[C::GMAX / 2];
+#pragma unroll
+    for (int p = 0; p < C::GMAX / 2; ++p) {
+      const int b = 2 * p + (tid >> 7), c = tid & 127;
+      cv[p] = (b < G && tn + c < N) ? (float)w_colsum[(int64_t)b * N + tn + c] : 0.0f;
+    }
+#pragma unroll
+    for (int p = 0; p < C::GMAX; ++p) {
+      if (p < G) {
+        // exact: e < 2^13, and (e + 1/2) / G stays 1/(2G) away from integers
+        const int e = tid + 256 * p;
+        const int r = (int)(((float)e + 0.5f) * inv_g);
+        const int b = e - r * G;
+        sRS[b][r] = fp16_bits_to_f32(sv[p]) * 0.0625f;
+        sZ[b][r] = zv[p];
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < C::GMAX / 2; ++p) {
+      const int b = 2 * p + (tid >> 7);
+      if (b < G) sCS[b][tid & 127] = cv[p];
+    }
+  }
+  // stages 0 and 1 landed (stage 2 may still be in flight)
+  if (nst > 2) wait_vmcnt<C::A_LD + C::B_LD>();
+  else wait_vmcnt<0>();
+  ring_barrier();
+  uint4 pc_a[4], pc_b[2];
+  fread(I0{}, 0, pc_a, pc_b);
+
+  // One stage st on ring buffer J = st % 4; FRESH marks the first stage of a
+  // group, whose last stage folds the accumulators.
+  auto body = [&](auto JC, auto FC, int st) __attribute__((always_inline)) {
+    constexpr int J = decltype(JC)::value;
+    using NEXT = std::integral_constant<int, (J + 1) % 4>;
+    const bool ahead = st + 3 < nst;
+    if (ahead) dma((J + 3) % 4, st + 3);
     uint4 p1_a[4], p1_b[2];
-    fread(buf, 1, p1_a, p1_b);
-    if (first) mma2(pc_a, pc_b, std::true_type{});
-    else mma2(pc_a, pc_b, std::false_type{});
-    if (st + 1 < nst) fread((st + 1) % C::NBUF, 0, pc_a, pc_b);
+    fread(JC, 1, p1_a, p1_b);
+    mma2(pc_a, pc_b, FC);
+    // At a group's end the next fragments are read after the fold, which
+    // then runs with few other registers live.  (Past the last stage the
+    // read is stale and unused.)
+    const bool last = (st & (spg - 1)) == spg - 1;
+    if (!last) fread(NEXT{}, 0, pc_a, pc_b);
     mma2(p1_a, p1_b, std::false_type{});
-    if (stage_next) param_store(b + 1);
     if (last) {
+      const int b = st >> (log2g - 7);
       if constexpr (DBG) dump(b);
       else fold(b);
+      fread(NEXT{}, 0, pc_a, pc_b);
     }
-    lds_barrier();
+    // stage st + 2 has landed; stage st + 3 may still be in flight
+    if (ahead) wait_vmcnt<C::A_LD + C::B_LD>();
+    else wait_vmcnt<0>();
+    ring_barrier();
+  };
+
+  using T = std::true_type;
+  using Fl = std::false_type;
+  int st = 0;
+  if constexpr (MODE == 1) {  // every stage starts a group
+    for (; st + 4 <= nst; st += 4) {
+      body(I0{}, T{}, st);
+      body(I1{}, T{}, st + 1);
+      body(I2{}, T{}, st + 2);
+      body(I3{}, T{}, st + 3);
+    }
+    if (st < nst) body(I0{}, T{}, st);
+    if (st + 1 < nst) body(I1{}, T{}, st + 1);
+    if (st + 2 < nst) body(I2{}, T{}, st + 2);
+  } else if constexpr (MODE == 2) {  // groups of two stages
+    for (; st + 4 <= nst; st += 4) {
+      body(I0{}, T{}, st);
+      body(I1{}, Fl{}, st + 1);
+      body(I2{}, T{}, st + 2);
+      body(I3{}, Fl{}, st + 3);
+    }
+    if (st < nst) {
+      body(I0{}, T{}, st);
+      body(I1{}, Fl{}, st + 1);
+    }
+  } else if constexpr (MODE == 4) {  // groups of four stages
+    for (; st < nst; st += 4) {
+      body(I0{}, T{}, st);
+      body(I1{}, Fl{}, st + 1);
+      body(I2{}, Fl{}, st + 2);
+      body(I3{}, Fl{}, st + 3);
+    }
+  } else {  // groups of 8k stages
+    for (; st < nst; st += 8) {
+      if ((st & (spg - 1)) == 0) body(I0{}, T{}, st);
+      else body(I0{}, Fl{}, st);
+      body(I1{}, Fl{}, st + 1);
+      body(I2{}, Fl{}, st + 2);
+      body(I3{}, Fl{}, st + 3);
+      body(I0{}, Fl{}, st + 4);
+      body(I1{}, Fl{}, st + 5);
+      body(I2{}, Fl{}, st + 6);
+      body(I3{}, Fl{}, st + 7);
+    }
   }
   if constexpr (DBG) return;
+
+  // ---- zero-point correction: F += sum_b (-s z)[m, b] * colsum[b, n] ------
+  // fp32 MFMAs with k = group: lane half h supplies group 2 kk + h
+  for (int kk = 0; kk < (G + 1) / 2; ++kk) {
+    const int b = 2 * kk + h;
+    const bool ok = b < G;
+    float csv[2], szv[4];
+#pragma unroll
+    for (int fn = 0; fn < 2; ++fn) csv[fn] = ok ? sCS[b][wn * 64 + fn * 32 + fr] : 0.0f;
+#pragma unroll
+    for (int fm = 0; fm < 4; ++fm) {
+      const int r = wm * 128 + fm * 32 + fr;
+      szv[fm] = ok ? -16.0f * sRS[b][r] * (float)sZ[b][r] : 0.0f;
+    }
+#pragma unroll
+    for (int fm = 0; fm < 4; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < 2; ++fn)
+        F[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(csv[fn], szv[fm], F[fm][fn], 0, 0, 0);
+  }
 
   // ---- epilogue: Y = sw * F -> bf16 ---------------------------------------
   // Each wave writes its 128 x 64 bf16 tile to a private 16 KB LDS area (rows
   // of 16 8-byte units, unit u of row r stored at u ^ (r & 15)), then reads
   // 16-byte pieces back row by row: each store instruction covers 8 rows of
   // 128 contiguous bytes.
-  uint32_t* ot = reinterpret_cast<uint32_t*>(lds) + wave * (128 * 32);
+  uint32_t* ot = reinterpret_cast<uint32_t*>(ring) + wave * (128 * 32);
   const bool vec = (tm + C::BM <= M) && (tn + C::BN <= N) && (ldy % 8 == 0) &&
                    ((reinterpret_cast<uintptr_t>(Y) & 15) == 0);
 #pragma unroll
@@ -282,9 +386,10 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
 #pragma unroll
       for (int fm = 0; fm < 4; ++fm) {
         const int r = fm * 32 + fr;
-        const float* f = &F[fm][fn][q * 4];
+        const v16f& f = F[fm][fn];
         *reinterpret_cast<uint2*>(ot + r * 32 + ((u ^ (r & 15)) * 2)) =
-            make_uint2(bf16x2_rne(sw[0] * f[0], sw[1] * f[1]), bf16x2_rne(sw[2] * f[2], sw[3] * f[3]));
+            make_uint2(bf16x2_rne(sw[0] * f[q * 4 + 0], sw[1] * f[q * 4 + 1]),
+                       bf16x2_rne(sw[2] * f[q * 4 + 2], sw[3] * f[q * 4 + 3]));
       }
     }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
@@ -314,9 +419,10 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
 }  // namespace
 
 bool gemm_grouped_supported(int64_t M, int64_t N, int64_t K, int log2g) {
-  // stages of 128 k never straddle a group; buffer offsets are 32-bit
-  return log2g >= 7 && K % 128 == 0 && M * (K / 2) < (int64_t(1) << 31) &&
-         N * (K / 2) < (int64_t(1) << 31);
+  // stages of 128 k never straddle a group; the group parameters of a tile
+  // fit in LDS; buffer offsets are 32-bit
+  return log2g >= 7 && K % 128 == 0 && (K >> log2g) <= GCfg::GMAX &&
+         M * (K / 2) < (int64_t(1) << 31) && N * (K / 2) < (int64_t(1) << 31);
 }
 
 hipError_t launch_w4a4_gemm_grouped(const uint8_t* a_codes, const uint16_t* a_scale,
@@ -327,13 +433,17 @@ hipError_t launch_w4a4_gemm_grouped(const uint8_t* a_codes, const uint16_t* a_sc
   using C = GCfg;
   const int64_t tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
   const dim3 grid((unsigned)tiles), block(256);
-#define OFFQ_GG(D)                                                                            \
-  hipLaunchKernelGGL((w4a4_gemm_grouped_kernel<D>), grid, block, 0, stream, a_codes, a_scale, \
-                     a_zero, w_codes, w_scale, w_colsum, (int)M, (int)N, (int)K, log2g, y, ldy, \
-                     acc_debug)
+#define OFFQ_GG(D, MD)                                                                        \
+  hipLaunchKernelGGL((w4a4_gemm_grouped_kernel<D, MD>), grid, block, 0, stream, a_codes,      \
+                     a_scale, a_zero, w_codes, w_scale, w_colsum, (int)M, (int)N, (int)K, log2g, \
+                     y, ldy, acc_debug)
+#define OFFQ_GG_M(D) \
+  if (log2g == 7) OFFQ_GG(D, 1); else if (log2g == 8) OFFQ_GG(D, 2);                \
+  else if (log2g == 9) OFFQ_GG(D, 4); else OFFQ_GG(D, 8);
   // A debug request runs an accumulator-only pass, then the regular kernel.
-  if (acc_debug) OFFQ_GG(true);
-  OFFQ_GG(false);
+  if (acc_debug) { OFFQ_GG_M(true) }
+  OFFQ_GG_M(false)
+#undef OFFQ_GG_M
 #undef OFFQ_GG
   return hipGetLastError();
 }
