@@ -9,22 +9,23 @@
 // group; the z * colsum terms carry the absorbed offsets).
 //
 // Organisation
-// * 4 waves per workgroup in a 2 x 2 arrangement, each owning 128 tokens x 64
-//   output channels (4 x 2 MFMA tiles of 32 x 32): 128 int32 accumulators for
-//   the current group and 128 fp32 running sums F; workgroup tile 256 x 128.
+// * 8 waves per workgroup (two per SIMD) in a 4 x 2 arrangement, each owning
+//   64 tokens x 64 output channels (2 x 2 MFMA tiles of 32 x 32): 64 int32
+//   accumulators for the current group and 64 fp32 running sums F; workgroup
+//   tile 256 x 128.  While one wave of a SIMD folds, the other multiplies.
 // * Stages of 128 k go from global memory straight into a 4-deep LDS ring
 //   (buffer loads with the LDS destination, 3 stages ahead; rows past the end
 //   read as zero), so no registers hold staged data.  One barrier per stage,
 //   preceded by a wait for the stage two ahead only.  The stage loop is
-//   unrolled by the ring depth so that every LDS access names its ring buffer
-//   at compile time.
+//   unrolled by the ring depth, which makes the ring offsets of every LDS
+//   access compile-time constants.
 // * Fragment reads, unpacking and the transposed MFMA are those of the
 //   one-group kernel.
 // * At the end of each group (g / 128 stages) the accumulators are folded
 //   into the running sums, F += (s / 16) * acc in fp32 (s / 16 undoes the 16x
 //   widening of the weight codes), and the first MFMA of the next group starts
-//   from a zero accumulator.  The row scales of a group are staged in LDS one
-//   group ahead.
+//   from a zero accumulator.  The row scales, zero-points and column sums of
+//   the tile's groups are loaded into LDS once, in the prologue.
 // * After the last group the zero-point terms are added with one fp32 MFMA
 //   per pair of groups: F += sum_b (-s z)[m, b] * colsum[b, n].
 // * Epilogue: Y = sw * F -> bf16 through LDS for 16-byte coalesced stores.
@@ -46,8 +47,9 @@ struct GCfg {
   static constexpr int A_SLOTS = BM * NC;
   static constexpr int B_SLOTS = BN * NC;
   static constexpr int STAGE_SLOTS = A_SLOTS + B_SLOTS;
-  static constexpr int A_LD = A_SLOTS / 256;       // loads per thread and stage
-  static constexpr int B_LD = B_SLOTS / 256;
+  static constexpr int THREADS = 512;              // 8 waves, 2 per SIMD
+  static constexpr int A_LD = A_SLOTS / THREADS;   // loads per thread and stage
+  static constexpr int B_LD = B_SLOTS / THREADS;
   static constexpr int KSTAGE = 128;               // k per stage
   static constexpr int NBUF = 4;                   // LDS ring depth
   static constexpr int GMAX = 28;                  // groups whose parameters fit in LDS
@@ -85,7 +87,7 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 
 // MODE: stages per group: 1, 2, 4, or a multiple of 8 (MODE 8).
 template <bool DBG, int MODE>
-__global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
+__global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     const uint8_t* __restrict__ A, const uint16_t* __restrict__ a_scale,
     const int16_t* __restrict__ a_zero, const uint8_t* __restrict__ W,
     const uint16_t* __restrict__ w_scale, const int32_t* __restrict__ w_colsum, int M, int N,
@@ -101,7 +103,7 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int h = lane >> 5, fr = lane & 31;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave & 3, wn = wave >> 2;
 
   const int tiles_m = (M + C::BM - 1) / C::BM;
   const int tiles_n = (N + C::BN - 1) / C::BN;
@@ -113,7 +115,7 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
   const int G = K >> log2g;
   const int spg = 1 << (log2g - 7);  // stages per group
 
-  constexpr int RSTEP = 256 / C::NC;
+  constexpr int RSTEP = C::THREADS / C::NC;
   const int row0 = tid / C::NC;
   const int chunk = swz<C::NC>(row0, tid % C::NC);
   const __amdgpu_buffer_rsrc_t arsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -124,22 +126,22 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
   const int vstep = RSTEP * (int)ldk;
   const uint32_t ring_lds = lds_addr(ring) + wave * 64 * 16;
 
-  // stage st into ring buffer J: this thread's slots tid + 256 i, written by
+  // stage st into ring buffer J: this thread's slots tid + 512 i, written by
   // each wave as 64 consecutive 16-byte slots per load
   auto dma = [&](int J, int st) __attribute__((always_inline)) {
     const uint32_t base = ring_lds + J * (C::STAGE_SLOTS * 16);
     const int soff = st * (C::KSTAGE / 2);
 #pragma unroll
     for (int i = 0; i < C::A_LD; ++i)
-      buffer_to_lds16(arsrc, base + i * 256 * 16, voff + i * vstep, soff);
+      buffer_to_lds16(arsrc, base + i * C::THREADS * 16, voff + i * vstep, soff);
 #pragma unroll
     for (int i = 0; i < C::B_LD; ++i)
-      buffer_to_lds16(brsrc, base + (C::A_SLOTS + i * 256) * 16, voff + i * vstep, soff);
+      buffer_to_lds16(brsrc, base + (C::A_SLOTS + i * C::THREADS) * 16, voff + i * vstep, soff);
   };
   // this lane's fragment slots for chunk column 2h + jj; fragments f are 32
   // rows apart, which keeps the swizzle
-  const uint4* a_frag0 = ring + (wm * 128 + fr) * C::NC + swz<C::NC>(fr, 2 * h);
-  const uint4* a_frag1 = ring + (wm * 128 + fr) * C::NC + swz<C::NC>(fr, 2 * h + 1);
+  const uint4* a_frag0 = ring + (wm * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h);
+  const uint4* a_frag1 = ring + (wm * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h + 1);
   const uint4* b_frag0 = ring + C::A_SLOTS + (wn * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h);
   const uint4* b_frag1 = ring + C::A_SLOTS + (wn * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h + 1);
   auto fread = [&](auto JC, int jj, uint4* pa, uint4* pb) __attribute__((always_inline)) {
@@ -147,21 +149,37 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
     const uint4* As = (jj ? a_frag1 : a_frag0) + J * C::STAGE_SLOTS;
     const uint4* Bs = (jj ? b_frag1 : b_frag0) + J * C::STAGE_SLOTS;
 #pragma unroll
-    for (int f = 0; f < 4; ++f) pa[f] = As[f * 32 * C::NC];
+    for (int f = 0; f < 2; ++f) pa[f] = As[f * 32 * C::NC];
 #pragma unroll
     for (int f = 0; f < 2; ++f) pb[f] = Bs[f * 32 * C::NC];
   };
 
-  v16i acc[4][2];
-  v16f F[4][2];
+  v16i acc[2][2];
+  v16f F[2][2];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       acc[a][b] = v16i{};
       F[a][b] = v16f{};
     }
 
+  // Lane column fr of fragment fm is token row wm*64 + fm*32 + fr; register
+  // i of fragment (fm, fn) is output channel wn*64 + fn*32 + 8*(i/4) + 4*h + i%4.
+  // F += (s / 16) * acc for fragment row fm (s / 16 undoes the 16x widening
+  // of the weight codes), with rs[fm] = s / 16 of the finished group.
+  float rs[2] = {0.0f, 0.0f};
+  auto read_rs = [&](int b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int fm = 0; fm < 2; ++fm) rs[fm] = sRS[b][wm * 64 + fm * 32 + fr];
+  };
+  auto fold_row = [&](int fm) __attribute__((always_inline)) {
+#pragma unroll
+    for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        F[fm][fn][i] = __builtin_fmaf(rs[fm], (float)acc[fm][fn][i], F[fm][fn][i]);
+  };
   // two k-steps (low and high nibbles of one 16-byte chunk per fragment);
   // FRESH: the low-nibble MFMAs start the accumulators from zero.  Operands
   // are unpacked just before use to keep the live registers down.
@@ -169,38 +187,24 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
     constexpr bool FRESH = decltype(FC)::value;
     const v4i ub0 = wgt_lo16(pb[0]), ub1 = wgt_lo16(pb[1]);
 #pragma unroll
-    for (int fm = 0; fm < 4; ++fm) {
+    for (int fm = 0; fm < 2; ++fm) {
       const v4i ua = act_lo(pa[fm]);
       acc[fm][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub0, ua, FRESH ? v16i{} : acc[fm][0], 0, 0, 0);
       acc[fm][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub1, ua, FRESH ? v16i{} : acc[fm][1], 0, 0, 0);
     }
     const v4i nb0 = wgt_hi16(pb[0]), nb1 = wgt_hi16(pb[1]);
 #pragma unroll
-    for (int fm = 0; fm < 4; ++fm) {
+    for (int fm = 0; fm < 2; ++fm) {
       const v4i na = act_hi(pa[fm]);
       acc[fm][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(nb0, na, acc[fm][0], 0, 0, 0);
       acc[fm][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(nb1, na, acc[fm][1], 0, 0, 0);
     }
   };
 
-  // Lane column fr of fragment fm is token row wm*128 + fm*32 + fr; register
-  // i of fragment (fm, fn) is output channel wn*64 + fn*32 + 8*(i/4) + 4*h + i%4.
-  // F += (s / 16) * acc  (s / 16 undoes the 16x widening of the weight codes)
-  auto fold = [&](int b) __attribute__((always_inline)) {
-#pragma unroll
-    for (int fm = 0; fm < 4; ++fm) {
-      const float rs = sRS[b][wm * 128 + fm * 32 + fr];
-#pragma unroll
-      for (int fn = 0; fn < 2; ++fn)
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          F[fm][fn][i] = __builtin_fmaf(rs, (float)acc[fm][fn][i], F[fm][fn][i]);
-    }
-  };
   auto dump = [&](int b) __attribute__((always_inline)) {  // debug: raw accumulators of group b
 #pragma unroll
-    for (int fm = 0; fm < 4; ++fm) {
-      const int row = tm + wm * 128 + fm * 32 + fr;
+    for (int fm = 0; fm < 2; ++fm) {
+      const int row = tm + wm * 64 + fm * 32 + fr;
       if (row >= M) continue;
 #pragma unroll
       for (int fn = 0; fn < 2; ++fn)
@@ -227,32 +231,34 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
   if (nst > 2) dma(2, 2);
   {
     // Row parameters of the tile: a contiguous block of 256 * G entries of the
-    // [M, G] arrays, read coalesced (entry e = tid + 256 p is row e / G, group
+    // [M, G] arrays, read coalesced (entry e = tid + 512 p is row e / G, group
     // e % G); column sums: group b, column c = colsum[b * N + tn + c].  All
     // loads are issued before the first LDS write.
     const float inv_g = 1.0f / (float)G;
     const int64_t base = (int64_t)tm * G;
     const int nrow_e = min(C::BM, M - tm) * G;  // valid entries of the block
-    uint16_t sv[C::GMAX];
-    int16_t zv[C::GMAX];
+    constexpr int PE = C::GMAX * C::BM / C::THREADS;  // row entries per thread
+    constexpr int PC = C::GMAX * C::BN / C::THREADS;  // column entries per thread
+    uint16_t sv[PE];
+    int16_t zv[PE];
 #pragma unroll
-    for (int p = 0; p < C::GMAX; ++p) {
-      const int e = tid + 256 * p;
-      const bool ok = p < G && e < nrow_e;
+    for (int p = 0; p < PE; ++p) {
+      const int e = tid + C::THREADS * p;
+      const bool ok = e < C::BM * G && e < nrow_e;
       sv[p] = ok ? a_scale[base + e] : (uint16_t)0;
       zv[p] = ok ? a_zero[base + e] : (int16_t)0;
     }
-    float cv[C::GMAX / 2];
+    float cv[PC];
 #pragma unroll
-    for (int p = 0; p < C::GMAX / 2; ++p) {
-      const int b = 2 * p + (tid >> 7), c = tid & 127;
+    for (int p = 0; p < PC; ++p) {
+      const int b = (C::THREADS / C::BN) * p + tid / C::BN, c = tid % C::BN;
       cv[p] = (b < G && tn + c < N) ? (float)w_colsum[(int64_t)b * N + tn + c] : 0.0f;
     }
 #pragma unroll
-    for (int p = 0; p < C::GMAX; ++p) {
-      if (p < G) {
+    for (int p = 0; p < PE; ++p) {
+      const int e = tid + C::THREADS * p;
+      if (e < C::BM * G) {
         // exact: e < 2^13, and (e + 1/2) / G stays 1/(2G) away from integers
-        const int e = tid + 256 * p;
         const int r = (int)(((float)e + 0.5f) * inv_g);
         const int b = e - r * G;
         sRS[b][r] = fp16_bits_to_f32(sv[p]) * 0.0625f;
@@ -260,9 +266,9 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
       }
     }
 #pragma unroll
-    for (int p = 0; p < C::GMAX / 2; ++p) {
-      const int b = 2 * p + (tid >> 7);
-      if (b < G) sCS[b][tid & 127] = cv[p];
+    for (int p = 0; p < PC; ++p) {
+      const int b = (C::THREADS / C::BN) * p + tid / C::BN;
+      if (b < G) sCS[b][tid % C::BN] = cv[p];
     }
   }
   // stages 0 and 1 landed (stage 2 may still be in flight)
@@ -282,17 +288,17 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
     uint4 p1_a[4], p1_b[2];
     fread(JC, 1, p1_a, p1_b);
     mma2(pc_a, pc_b, FC);
-    // At a group's end the next fragments are read after the fold, which
-    // then runs with few other registers live.  (Past the last stage the
-    // read is stale and unused.)
-    const bool last = (st & (spg - 1)) == spg - 1;
-    if (!last) fread(NEXT{}, 0, pc_a, pc_b);
+    fread(NEXT{}, 0, pc_a, pc_b);  // past the last stage: stale, unused
     mma2(p1_a, p1_b, std::false_type{});
-    if (last) {
+    if ((st & (spg - 1)) == spg - 1) {  // the group's last stage
       const int b = st >> (log2g - 7);
-      if constexpr (DBG) dump(b);
-      else fold(b);
-      fread(NEXT{}, 0, pc_a, pc_b);
+      if constexpr (DBG) {
+        dump(b);
+      } else {
+        read_rs(b);
+        fold_row(0);
+        fold_row(1);
+      }
     }
     // stage st + 2 has landed; stage st + 3 may still be in flight
     if (ahead) wait_vmcnt<C::A_LD + C::B_LD>();
@@ -351,27 +357,27 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
   for (int kk = 0; kk < (G + 1) / 2; ++kk) {
     const int b = 2 * kk + h;
     const bool ok = b < G;
-    float csv[2], szv[4];
+    float csv[2], szv[2];
 #pragma unroll
     for (int fn = 0; fn < 2; ++fn) csv[fn] = ok ? sCS[b][wn * 64 + fn * 32 + fr] : 0.0f;
 #pragma unroll
-    for (int fm = 0; fm < 4; ++fm) {
-      const int r = wm * 128 + fm * 32 + fr;
+    for (int fm = 0; fm < 2; ++fm) {
+      const int r = wm * 64 + fm * 32 + fr;
       szv[fm] = ok ? -16.0f * sRS[b][r] * (float)sZ[b][r] : 0.0f;
     }
 #pragma unroll
-    for (int fm = 0; fm < 4; ++fm)
+    for (int fm = 0; fm < 2; ++fm)
 #pragma unroll
       for (int fn = 0; fn < 2; ++fn)
         F[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(csv[fn], szv[fm], F[fm][fn], 0, 0, 0);
   }
 
   // ---- epilogue: Y = sw * F -> bf16 ---------------------------------------
-  // Each wave writes its 128 x 64 bf16 tile to a private 16 KB LDS area (rows
+  // Each wave writes its 64 x 64 bf16 tile to a private 8 KB LDS area (rows
   // of 16 8-byte units, unit u of row r stored at u ^ (r & 15)), then reads
   // 16-byte pieces back row by row: each store instruction covers 8 rows of
   // 128 contiguous bytes.
-  uint32_t* ot = reinterpret_cast<uint32_t*>(ring) + wave * (128 * 32);
+  uint32_t* ot = reinterpret_cast<uint32_t*>(ring) + wave * (64 * 32);
   const bool vec = (tm + C::BM <= M) && (tn + C::BN <= N) && (ldy % 8 == 0) &&
                    ((reinterpret_cast<uintptr_t>(Y) & 15) == 0);
 #pragma unroll
@@ -384,7 +390,7 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
       for (int e = 0; e < 4; ++e) sw[e] = lc + e < N ? fp16_bits_to_f32(w_scale[lc + e]) : 0.0f;
       const int u = fn * 8 + q * 2 + h;
 #pragma unroll
-      for (int fm = 0; fm < 4; ++fm) {
+      for (int fm = 0; fm < 2; ++fm) {
         const int r = fm * 32 + fr;
         const v16f& f = F[fm][fn];
         *reinterpret_cast<uint2*>(ot + r * 32 + ((u ^ (r & 15)) * 2)) =
@@ -397,13 +403,13 @@ __global__ __launch_bounds__(256) void w4a4_gemm_grouped_kernel(
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
   // lane l of pass p: row 8p + l/8, 16-byte piece l%8 (units 2k, 2k+1)
 #pragma unroll 4
-  for (int p = 0; p < 16; ++p) {
+  for (int p = 0; p < 8; ++p) {
     const int r = 8 * p + (lane >> 3);
     const int k = lane & 7;
     const int pu = (2 * k) ^ (r & 15);
     uint4 d = *reinterpret_cast<const uint4*>(ot + r * 32 + (pu & ~1) * 2);
     if (pu & 1) d = make_uint4(d.z, d.w, d.x, d.y);
-    const int row = tm + wm * 128 + r;
+    const int row = tm + wm * 64 + r;
     const int col = tn + wn * 64 + 8 * k;
     if (vec) {
       *reinterpret_cast<uint4*>(Y + (int64_t)row * ldy + col) = d;
@@ -432,7 +438,7 @@ hipError_t launch_w4a4_gemm_grouped(const uint8_t* a_codes, const uint16_t* a_sc
                                     int32_t* acc_debug, hipStream_t stream) {
   using C = GCfg;
   const int64_t tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
-  const dim3 grid((unsigned)tiles), block(256);
+  const dim3 grid((unsigned)tiles), block(C::THREADS);
 #define OFFQ_GG(D, MD)                                                                        \
   hipLaunchKernelGGL((w4a4_gemm_grouped_kernel<D, MD>), grid, block, 0, stream, a_codes,      \
                      a_scale, a_zero, w_codes, w_scale, w_colsum, (int)M, (int)N, (int)K, log2g, \

@@ -34,6 +34,9 @@ def _layer(M, N, K, g, seed, layout="concentrated", n_out=4):
 @pytest.mark.parametrize("M,N,K,g", [
     (17, 8, 256, 256), (128, 128, 512, 512), (130, 136, 1024, 256), (200, 250, 256, 64),
     (257, 384, 2048, 512), (64, 512, 4096, 4096), (40, 96, 8192, 8192), (33, 64, 512, 128),
+    # groups of 8 and 16 stages of 128 k; more groups than the grouped kernel
+    # keeps in LDS (G = 32); g = 512 over a ragged 2-tile-row x 3-tile-column grid
+    (100, 136, 4096, 1024), (77, 64, 8192, 2048), (40, 64, 4096, 128), (300, 260, 3584, 512),
 ])
 def test_gemm_shapes(M, N, K, g):
     _layer(M, N, K, g, seed=M * 7 + N)
