@@ -40,19 +40,26 @@ namespace {
 
 using namespace gemm;
 
+// FM: 32-row MFMA tiles per wave along the tokens.  FM = 2: 8 waves of
+// 64 x 64 in a 4 x 2 arrangement (workgroup tile 256 x 128), any number of
+// groups up to GMAX; FM = 4: 8 waves of 128 x 64 in a 2 x 4 arrangement
+// (256 x 256), one group per row only (no registers for running sums).
+template <int FM>
 struct GCfg {
-  static constexpr int BM = 256;
-  static constexpr int BN = 128;
+  static constexpr int THREADS = 512;              // 8 waves, 2 per SIMD
+  static constexpr int WAVES_M = FM == 2 ? 4 : 2;
+  static constexpr int WROWS = 32 * FM;            // token rows per wave
+  static constexpr int BM = WAVES_M * WROWS;       // 256
+  static constexpr int BN = (8 / WAVES_M) * 64;    // 128 or 256
   static constexpr int NC = 4;                     // 16-byte chunks per row and stage
   static constexpr int A_SLOTS = BM * NC;
   static constexpr int B_SLOTS = BN * NC;
   static constexpr int STAGE_SLOTS = A_SLOTS + B_SLOTS;
-  static constexpr int THREADS = 512;              // 8 waves, 2 per SIMD
   static constexpr int A_LD = A_SLOTS / THREADS;   // loads per thread and stage
   static constexpr int B_LD = B_SLOTS / THREADS;
   static constexpr int KSTAGE = 128;               // k per stage
   static constexpr int NBUF = 4;                   // LDS ring depth
-  static constexpr int GMAX = 28;                  // groups whose parameters fit in LDS
+  static constexpr int GMAX = FM == 2 ? 28 : 1;    // groups whose parameters fit in LDS
 };
 
 // s_waitcnt with only the vector-memory counter bounded (gfx9 encoding)
@@ -86,13 +93,13 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 // MODE: stages per group: 1, 2, 4, or a multiple of 8 (MODE 8).
-template <bool DBG, int MODE>
+template <bool DBG, int MODE, int FM>
 __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     const uint8_t* __restrict__ A, const uint16_t* __restrict__ a_scale,
     const int16_t* __restrict__ a_zero, const uint8_t* __restrict__ W,
     const uint16_t* __restrict__ w_scale, const int32_t* __restrict__ w_colsum, int M, int N,
     int K, int log2g, uint16_t* __restrict__ Y, int64_t ldy, int32_t* __restrict__ acc_dbg) {
-  using C = GCfg;
+  using C = GCfg<FM>;
   __shared__ uint4 ring[C::NBUF * C::STAGE_SLOTS];
   // per group b: s / 16 and z of the tile's rows, colsum of its columns
   __shared__ float sRS[C::GMAX][C::BM];
@@ -103,7 +110,7 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int h = lane >> 5, fr = lane & 31;
-  const int wm = wave & 3, wn = wave >> 2;
+  const int wm = wave % C::WAVES_M, wn = wave / C::WAVES_M;
 
   const int tiles_m = (M + C::BM - 1) / C::BM;
   const int tiles_n = (N + C::BN - 1) / C::BN;
@@ -140,8 +147,8 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   };
   // this lane's fragment slots for chunk column 2h + jj; fragments f are 32
   // rows apart, which keeps the swizzle
-  const uint4* a_frag0 = ring + (wm * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h);
-  const uint4* a_frag1 = ring + (wm * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h + 1);
+  const uint4* a_frag0 = ring + (wm * C::WROWS + fr) * C::NC + swz<C::NC>(fr, 2 * h);
+  const uint4* a_frag1 = ring + (wm * C::WROWS + fr) * C::NC + swz<C::NC>(fr, 2 * h + 1);
   const uint4* b_frag0 = ring + C::A_SLOTS + (wn * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h);
   const uint4* b_frag1 = ring + C::A_SLOTS + (wn * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h + 1);
   auto fread = [&](auto JC, int jj, uint4* pa, uint4* pb) __attribute__((always_inline)) {
@@ -149,36 +156,40 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     const uint4* As = (jj ? a_frag1 : a_frag0) + J * C::STAGE_SLOTS;
     const uint4* Bs = (jj ? b_frag1 : b_frag0) + J * C::STAGE_SLOTS;
 #pragma unroll
-    for (int f = 0; f < 2; ++f) pa[f] = As[f * 32 * C::NC];
+    for (int f = 0; f < FM; ++f) pa[f] = As[f * 32 * C::NC];
 #pragma unroll
     for (int f = 0; f < 2; ++f) pb[f] = Bs[f * 32 * C::NC];
   };
 
-  v16i acc[2][2];
-  v16f F[2][2];
+  // With one group per row (the only case of FM = 4) F is first written by
+  // the single fold after the loop, so it takes no registers during it.
+  constexpr bool SINGLE = C::GMAX == 1;
+  v16i acc[FM][2];
+  v16f F[FM][2];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < FM; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       acc[a][b] = v16i{};
-      F[a][b] = v16f{};
+      if constexpr (!SINGLE) F[a][b] = v16f{};
     }
 
   // Lane column fr of fragment fm is token row wm*64 + fm*32 + fr; register
   // i of fragment (fm, fn) is output channel wn*64 + fn*32 + 8*(i/4) + 4*h + i%4.
   // F += (s / 16) * acc for fragment row fm (s / 16 undoes the 16x widening
   // of the weight codes), with rs[fm] = s / 16 of the finished group.
-  float rs[2] = {0.0f, 0.0f};
+  float rs[FM] = {};
   auto read_rs = [&](int b) __attribute__((always_inline)) {
 #pragma unroll
-    for (int fm = 0; fm < 2; ++fm) rs[fm] = sRS[b][wm * 64 + fm * 32 + fr];
+    for (int fm = 0; fm < FM; ++fm) rs[fm] = sRS[b][wm * C::WROWS + fm * 32 + fr];
   };
   auto fold_row = [&](int fm) __attribute__((always_inline)) {
 #pragma unroll
     for (int fn = 0; fn < 2; ++fn)
 #pragma unroll
       for (int i = 0; i < 16; ++i)
-        F[fm][fn][i] = __builtin_fmaf(rs[fm], (float)acc[fm][fn][i], F[fm][fn][i]);
+        F[fm][fn][i] = SINGLE ? rs[fm] * (float)acc[fm][fn][i]
+                              : __builtin_fmaf(rs[fm], (float)acc[fm][fn][i], F[fm][fn][i]);
   };
   // two k-steps (low and high nibbles of one 16-byte chunk per fragment);
   // FRESH: the low-nibble MFMAs start the accumulators from zero.  Operands
@@ -187,24 +198,32 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     constexpr bool FRESH = decltype(FC)::value;
     const v4i ub0 = wgt_lo16(pb[0]), ub1 = wgt_lo16(pb[1]);
 #pragma unroll
-    for (int fm = 0; fm < 2; ++fm) {
+    for (int fm = 0; fm < FM; ++fm) {
       const v4i ua = act_lo(pa[fm]);
       acc[fm][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub0, ua, FRESH ? v16i{} : acc[fm][0], 0, 0, 0);
       acc[fm][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub1, ua, FRESH ? v16i{} : acc[fm][1], 0, 0, 0);
     }
     const v4i nb0 = wgt_hi16(pb[0]), nb1 = wgt_hi16(pb[1]);
 #pragma unroll
-    for (int fm = 0; fm < 2; ++fm) {
+    for (int fm = 0; fm < FM; ++fm) {
       const v4i na = act_hi(pa[fm]);
       acc[fm][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(nb0, na, acc[fm][0], 0, 0, 0);
       acc[fm][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(nb1, na, acc[fm][1], 0, 0, 0);
+    }
+    if constexpr (FM == 4) {
+      // keep the 128 accumulators in accumulation registers (an empty asm
+      // with AGPR operands), leaving the vector registers to the pipeline
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < 2; ++fn) asm volatile("" : "+a"(acc[fm][fn]));
     }
   };
 
   auto dump = [&](int b) __attribute__((always_inline)) {  // debug: raw accumulators of group b
 #pragma unroll
-    for (int fm = 0; fm < 2; ++fm) {
-      const int row = tm + wm * 64 + fm * 32 + fr;
+    for (int fm = 0; fm < FM; ++fm) {
+      const int row = tm + wm * C::WROWS + fm * 32 + fr;
       if (row >= M) continue;
 #pragma unroll
       for (int fn = 0; fn < 2; ++fn)
@@ -237,8 +256,8 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     const float inv_g = 1.0f / (float)G;
     const int64_t base = (int64_t)tm * G;
     const int nrow_e = min(C::BM, M - tm) * G;  // valid entries of the block
-    constexpr int PE = C::GMAX * C::BM / C::THREADS;  // row entries per thread
-    constexpr int PC = C::GMAX * C::BN / C::THREADS;  // column entries per thread
+    constexpr int PE = (C::GMAX * C::BM + C::THREADS - 1) / C::THREADS;  // row entries per thread
+    constexpr int PC = (C::GMAX * C::BN + C::THREADS - 1) / C::THREADS;  // column entries per thread
     uint16_t sv[PE];
     int16_t zv[PE];
 #pragma unroll
@@ -252,7 +271,7 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
 #pragma unroll
     for (int p = 0; p < PC; ++p) {
       const int b = (C::THREADS / C::BN) * p + tid / C::BN, c = tid % C::BN;
-      cv[p] = (b < G && tn + c < N) ? (float)w_colsum[(int64_t)b * N + tn + c] : 0.0f;
+      cv[p] = (b < G && b < C::GMAX && tn + c < N) ? (float)w_colsum[(int64_t)b * N + tn + c] : 0.0f;
     }
 #pragma unroll
     for (int p = 0; p < PE; ++p) {
@@ -268,7 +287,7 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
 #pragma unroll
     for (int p = 0; p < PC; ++p) {
       const int b = (C::THREADS / C::BN) * p + tid / C::BN;
-      if (b < G) sCS[b][tid % C::BN] = cv[p];
+      if (b < G && b < C::GMAX) sCS[b][tid % C::BN] = cv[p];
     }
   }
   // stages 0 and 1 landed (stage 2 may still be in flight)
@@ -296,8 +315,10 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
         dump(b);
       } else {
         read_rs(b);
-        fold_row(0);
-        fold_row(1);
+        if constexpr (!SINGLE) {
+#pragma unroll
+          for (int fm = 0; fm < FM; ++fm) fold_row(fm);
+        }
       }
     }
     // stage st + 2 has landed; stage st + 3 may still be in flight
@@ -352,64 +373,62 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   }
   if constexpr (DBG) return;
 
-  // ---- zero-point correction: F += sum_b (-s z)[m, b] * colsum[b, n] ------
-  // fp32 MFMAs with k = group: lane half h supplies group 2 kk + h
-  for (int kk = 0; kk < (G + 1) / 2; ++kk) {
-    const int b = 2 * kk + h;
-    const bool ok = b < G;
-    float csv[2], szv[2];
-#pragma unroll
-    for (int fn = 0; fn < 2; ++fn) csv[fn] = ok ? sCS[b][wn * 64 + fn * 32 + fr] : 0.0f;
-#pragma unroll
-    for (int fm = 0; fm < 2; ++fm) {
-      const int r = wm * 64 + fm * 32 + fr;
-      szv[fm] = ok ? -16.0f * sRS[b][r] * (float)sZ[b][r] : 0.0f;
-    }
-#pragma unroll
-    for (int fm = 0; fm < 2; ++fm)
-#pragma unroll
-      for (int fn = 0; fn < 2; ++fn)
-        F[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(csv[fn], szv[fm], F[fm][fn], 0, 0, 0);
-  }
-
-  // ---- epilogue: Y = sw * F -> bf16 ---------------------------------------
-  // Each wave writes its 64 x 64 bf16 tile to a private 8 KB LDS area (rows
-  // of 16 8-byte units, unit u of row r stored at u ^ (r & 15)), then reads
-  // 16-byte pieces back row by row: each store instruction covers 8 rows of
-  // 128 contiguous bytes.
-  uint32_t* ot = reinterpret_cast<uint32_t*>(ring) + wave * (64 * 32);
+  // ---- finish one fragment row at a time ----------------------------------
+  // zero-point correction F += sum_b (-s z)[m, b] * colsum[b, n] (fp32 MFMAs
+  // with k = group: lane half h supplies group 2 kk + h), then Y = sw * F as
+  // bf16 into a private LDS area per wave: rows of 16 8-byte units, unit u of
+  // row r stored at u ^ (r & 15).  (With one group the fold happens here.)
+  uint32_t* ot = reinterpret_cast<uint32_t*>(ring) + wave * (C::WROWS * 32);
   const bool vec = (tm + C::BM <= M) && (tn + C::BN <= N) && (ldy % 8 == 0) &&
                    ((reinterpret_cast<uintptr_t>(Y) & 15) == 0);
+  float sw[2][4][4];
 #pragma unroll
   for (int fn = 0; fn < 2; ++fn)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int lc = tn + wn * 64 + fn * 32 + q * 8 + h * 4;
-      float sw[4];
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sw[e] = lc + e < N ? fp16_bits_to_f32(w_scale[lc + e]) : 0.0f;
-      const int u = fn * 8 + q * 2 + h;
+      for (int e = 0; e < 4; ++e) {
+        const int c = tn + wn * 64 + fn * 32 + q * 8 + h * 4 + e;
+        sw[fn][q][e] = c < N ? fp16_bits_to_f32(w_scale[c]) : 0.0f;
+      }
 #pragma unroll
-      for (int fm = 0; fm < 2; ++fm) {
-        const int r = fm * 32 + fr;
-        const v16f& f = F[fm][fn];
-        *reinterpret_cast<uint2*>(ot + r * 32 + ((u ^ (r & 15)) * 2)) =
-            make_uint2(bf16x2_rne(sw[0] * f[q * 4 + 0], sw[1] * f[q * 4 + 1]),
-                       bf16x2_rne(sw[2] * f[q * 4 + 2], sw[3] * f[q * 4 + 3]));
+  for (int fm = 0; fm < FM; ++fm) {
+    if constexpr (SINGLE) fold_row(fm);
+    const int r = wm * C::WROWS + fm * 32 + fr;
+    for (int kk = 0; kk < (G + 1) / 2; ++kk) {
+      const int b = 2 * kk + h;
+      const bool ok = b < G;
+      const float szv = ok ? -16.0f * sRS[b][r] * (float)sZ[b][r] : 0.0f;
+#pragma unroll
+      for (int fn = 0; fn < 2; ++fn) {
+        const float csv = ok ? sCS[b][wn * 64 + fn * 32 + fr] : 0.0f;
+        F[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(csv, szv, F[fm][fn], 0, 0, 0);
       }
     }
+    const int lr = fm * 32 + fr;  // row within the wave's tile
+#pragma unroll
+    for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int u = fn * 8 + q * 2 + h;
+        const v16f& f = F[fm][fn];
+        *reinterpret_cast<uint2*>(ot + lr * 32 + ((u ^ (lr & 15)) * 2)) =
+            make_uint2(bf16x2_rne(sw[fn][q][0] * f[q * 4 + 0], sw[fn][q][1] * f[q * 4 + 1]),
+                       bf16x2_rne(sw[fn][q][2] * f[q * 4 + 2], sw[fn][q][3] * f[q * 4 + 3]));
+      }
+  }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
   // lane l of pass p: row 8p + l/8, 16-byte piece l%8 (units 2k, 2k+1)
 #pragma unroll 4
-  for (int p = 0; p < 8; ++p) {
+  for (int p = 0; p < C::WROWS / 8; ++p) {
     const int r = 8 * p + (lane >> 3);
     const int k = lane & 7;
     const int pu = (2 * k) ^ (r & 15);
     uint4 d = *reinterpret_cast<const uint4*>(ot + r * 32 + (pu & ~1) * 2);
     if (pu & 1) d = make_uint4(d.z, d.w, d.x, d.y);
-    const int row = tm + wm * 64 + r;
+    const int row = tm + wm * C::WROWS + r;
     const int col = tn + wn * 64 + 8 * k;
     if (vec) {
       *reinterpret_cast<uint4*>(Y + (int64_t)row * ldy + col) = d;
@@ -427,23 +446,23 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
 bool gemm_grouped_supported(int64_t M, int64_t N, int64_t K, int log2g) {
   // stages of 128 k never straddle a group; the group parameters of a tile
   // fit in LDS; buffer offsets are 32-bit
-  return log2g >= 7 && K % 128 == 0 && (K >> log2g) <= GCfg::GMAX &&
+  return log2g >= 7 && K % 128 == 0 && (K >> log2g) <= GCfg<2>::GMAX &&
          M * (K / 2) < (int64_t(1) << 31) && N * (K / 2) < (int64_t(1) << 31);
 }
 
-hipError_t launch_w4a4_gemm_grouped(const uint8_t* a_codes, const uint16_t* a_scale,
-                                    const int16_t* a_zero, const uint8_t* w_codes,
-                                    const uint16_t* w_scale, const int32_t* w_colsum, int64_t M,
-                                    int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
-                                    int32_t* acc_debug, hipStream_t stream) {
-  using C = GCfg;
+template <int FM>
+hipError_t launch_g(const uint8_t* a_codes, const uint16_t* a_scale, const int16_t* a_zero,
+                    const uint8_t* w_codes, const uint16_t* w_scale, const int32_t* w_colsum,
+                    int64_t M, int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
+                    int32_t* acc_debug, hipStream_t stream) {
+  using C = GCfg<FM>;
   const int64_t tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
   const dim3 grid((unsigned)tiles), block(C::THREADS);
 #define OFFQ_GG(D, MD)                                                                        \
-  hipLaunchKernelGGL((w4a4_gemm_grouped_kernel<D, MD>), grid, block, 0, stream, a_codes,      \
+  hipLaunchKernelGGL((w4a4_gemm_grouped_kernel<D, MD, FM>), grid, block, 0, stream, a_codes,  \
                      a_scale, a_zero, w_codes, w_scale, w_colsum, (int)M, (int)N, (int)K, log2g, \
                      y, ldy, acc_debug)
-#define OFFQ_GG_M(D) \
+#define OFFQ_GG_M(D)                                                                 \
   if (log2g == 7) OFFQ_GG(D, 1); else if (log2g == 8) OFFQ_GG(D, 2);                \
   else if (log2g == 9) OFFQ_GG(D, 4); else OFFQ_GG(D, 8);
   // A debug request runs an accumulator-only pass, then the regular kernel.
@@ -452,6 +471,21 @@ hipError_t launch_w4a4_gemm_grouped(const uint8_t* a_codes, const uint16_t* a_sc
 #undef OFFQ_GG_M
 #undef OFFQ_GG
   return hipGetLastError();
+}
+
+hipError_t launch_w4a4_gemm_grouped(const uint8_t* a_codes, const uint16_t* a_scale,
+                                    const int16_t* a_zero, const uint8_t* w_codes,
+                                    const uint16_t* w_scale, const int32_t* w_colsum, int64_t M,
+                                    int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
+                                    int32_t* acc_debug, hipStream_t stream) {
+  // one group per row and enough 256 x 256 tiles to fill the chip: the wider
+  // wave tiles
+  const bool wide = (K >> log2g) == 1 && ((M + 255) / 256) * ((N + 255) / 256) >= 384;
+  if (wide)
+    return launch_g<4>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, y,
+                       ldy, acc_debug, stream);
+  return launch_g<2>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, y,
+                     ldy, acc_debug, stream);
 }
 
 }  // namespace offq
