@@ -37,6 +37,14 @@ hipError_t launch_w4a4_gemm_grouped(const uint8_t* a_codes, const uint16_t* a_sc
                                     int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
                                     int32_t* acc_debug, hipStream_t stream);
 
+// Decode (M <= 16) on MFMA: 16-channel row tiles, K split over 4 waves.
+bool gemv_mfma_supported(int64_t M, int64_t N, int64_t K, int log2g);
+hipError_t launch_w4a4_gemv_mfma(const uint8_t* a_codes, const uint16_t* a_scale,
+                                 const int16_t* a_zero, const uint8_t* w_codes,
+                                 const uint16_t* w_scale, const int32_t* w_colsum, int64_t M,
+                                 int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
+                                 int32_t* acc_debug, hipStream_t stream);
+
 hipError_t launch_w4a4_gemv(const uint8_t* a_codes, const uint16_t* a_scale,
                             const int16_t* a_zero, const uint8_t* w_codes,
                             const uint16_t* w_scale, const int32_t* w_colsum,

@@ -150,7 +150,10 @@ int offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale, const int16_
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (codes: 16 B)");
   if (int s = check_device()) return s;
   hipError_t e;
-  if (M <= 16)
+  if (M <= 16 && offq::gemv_mfma_supported(M, N, K, lg))
+    e = offq::launch_w4a4_gemv_mfma(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N,
+                                    K, lg, y, ldy, acc_debug, (hipStream_t)stream);
+  else if (M <= 16)
     e = offq::launch_w4a4_gemv(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, lg,
                                y, ldy, acc_debug, (hipStream_t)stream);
   else

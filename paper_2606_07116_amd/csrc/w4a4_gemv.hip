@@ -1,0 +1,247 @@
+// W4A4 decode GEMV (M <= 16 tokens), gfx950, v_mfma_i32_16x16x64_i8.
+//
+//   acc_b[m,n] = sum_{k in group b} q_a[m,k] q_w[n,k]                 (int32)
+//   Y[m,n]     = sw[n] * sum_b s[m,b] * (acc_b[m,n] - z[m,b] * colsum[b,n])
+//
+// (the dequantised product of Eq. 1; the z * colsum terms carry the absorbed
+// offsets).  The int4 weights are streamed once from HBM; the few token rows
+// are padded to the MFMA's 16 columns, which costs MFMA slots that are idle
+// anyway in a memory-bound kernel.
+//
+// Organisation
+// * A workgroup of P waves owns T row tiles of 16 output channels; the P
+//   waves split K and their fp32 partial sums are added through LDS at the
+//   end.
+// * Per step of 128 k every lane loads 16 packed bytes of one weight row per
+//   tile (lane l: row l % 16, k-block l / 16; 64-byte row segments) and the
+//   same 16 bytes of its token row l % 16 (rows >= M read as zero through the
+//   buffer descriptor), and runs two MFMAs per tile (low and high nibbles, the
+//   same k-permutation on both operands).  Weight nibbles are widened to 16 q.
+//   Steps go in batches of 4; the next batch's loads are issued before the
+//   current batch is multiplied.  One activation load serves T weight loads:
+//   the activation rows are re-read by every row tile, so with T = 1 they
+//   would double the load traffic of M = 16.
+// * Accumulators are folded per group: F += (s / 16) * acc - s z colsum (the
+//   zero-point term added by the wave that holds the group's first k), with
+//   the group parameters of the workgroup preloaded into LDS.
+#include "common.h"
+#include "gemm_common.h"
+#include "internal.h"
+
+namespace offq {
+namespace {
+
+using namespace gemm;
+
+constexpr int KSTEP = 128;  // k per step (64 packed bytes per row)
+constexpr int GMAX = 256;   // groups whose parameters fit in LDS
+
+// T: 16-channel row tiles per wave (one activation load serves T weight
+// loads); P: waves per workgroup, each taking 1/P of K.
+template <int T, int P>
+struct GvCfg {
+  static constexpr int BATCH = 4;  // steps per batch
+  static constexpr int THREADS = 64 * P;
+};
+
+template <int T, int P, bool DBG>
+__global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
+    const uint8_t* __restrict__ A, const uint16_t* __restrict__ a_scale,
+    const int16_t* __restrict__ a_zero, const uint8_t* __restrict__ W,
+    const uint16_t* __restrict__ w_scale, const int32_t* __restrict__ w_colsum, int M, int N,
+    int K, int log2g, uint16_t* __restrict__ Y, int64_t ldy, int32_t* __restrict__ acc_dbg) {
+  constexpr int BATCH = GvCfg<T, P>::BATCH;
+  constexpr int NT = GvCfg<T, P>::THREADS;
+  __shared__ float red[P][64][T * 4];
+  // per group: s / 16 and -s z of the 16 token rows, colsum of the tile's channels
+  extern __shared__ float gpar[];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r16 = lane & 15, kb = lane >> 4;
+  const int n0 = (int)blockIdx.x * (16 * T);
+  const int ldk = K >> 1;
+  const int G = K >> log2g;
+  const int kq = K / P;                  // k per wave
+  const int k0 = wave * kq;
+  const int nb = kq / (KSTEP * BATCH);   // batches per wave
+  float* const sS = gpar;                // [G][16]
+  float* const sSZ = gpar + G * 16;      // [G][16]
+  float* const sCS = gpar + G * 32;      // [G][16 T]
+
+  // group parameters of the workgroup into LDS
+  for (int i = tid; i < G * 16; i += NT) {
+    const int b = i >> 4, m = i & 15;
+    const bool ok = m < M;
+    const float s = ok ? fp16_bits_to_f32(a_scale[(int64_t)m * G + b]) : 0.0f;
+    sS[i] = s * 0.0625f;  // undoes the 16x widening of the weight codes
+    sSZ[i] = ok ? -(s * (float)a_zero[(int64_t)m * G + b]) : 0.0f;
+  }
+  for (int i = tid; i < G * 16 * T; i += NT) {
+    const int b = i / (16 * T), c = i % (16 * T);
+    sCS[i] = n0 + c < N ? (float)w_colsum[(int64_t)b * N + n0 + c] : 0.0f;
+  }
+  __syncthreads();
+
+  // rows past N (weights) and past M (tokens) read as zero
+  const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(W + (int64_t)n0 * ldk), 0, (int)((int64_t)min(16 * T, N - n0) * ldk), 0x00020000);
+  const __amdgpu_buffer_rsrc_t arsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void*)A, 0, M * ldk, 0x00020000);
+  const int a_off = r16 * ldk + (k0 >> 1) + 16 * kb;
+  int w_off[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) w_off[t] = (16 * t + r16) * ldk + (k0 >> 1) + 16 * kb;
+
+  v4i acc[T];
+  float F[T][4];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    acc[t] = v4i{};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) F[t][i] = 0.0f;
+  }
+
+  // Register i of tile t is output channel n0 + 16 t + 4 kb + i, token row
+  // r16 (the lane's column).  The zero-point term of a group is added by the
+  // wave that holds the group's first k.
+  auto fold = [&](int b) __attribute__((always_inline)) {
+    if constexpr (DBG) {
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int n = n0 + 16 * t + 4 * kb + i;
+          if (r16 < M && n < N)
+            atomicAdd(&acc_dbg[((int64_t)b * M + r16) * N + n], acc[t][i] >> 4);
+        }
+    } else {
+      const float s = sS[b * 16 + r16];
+      const float sz = (b << log2g) >= k0 ? sSZ[b * 16 + r16] : 0.0f;
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        const float4 c4 = *reinterpret_cast<const float4*>(&sCS[b * 16 * T + 16 * t + 4 * kb]);
+        const float cs[4] = {c4.x, c4.y, c4.z, c4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          F[t][i] = __builtin_fmaf(s, (float)acc[t][i], F[t][i]);
+          F[t][i] = __builtin_fmaf(sz, cs[i], F[t][i]);
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < T; ++t) acc[t] = v4i{};
+  };
+
+  uint4 wa0[BATCH][T], aa0[BATCH], wa1[BATCH][T], aa1[BATCH];
+  auto load = [&](int bt, uint4 (&wa)[BATCH][T], uint4 (&aa)[BATCH]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const int so = (bt * BATCH + u) * (KSTEP / 2);
+      aa[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(arsrc, a_off, so, 0));
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+        wa[u][t] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wrsrc, w_off[t], so, 0));
+    }
+  };
+  const int gmask = (1 << (log2g - 7)) - 1;  // steps per group - 1
+  auto compute = [&](int bt, const uint4 (&wa)[BATCH][T], const uint4 (&aa)[BATCH]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const v4i alo = act_lo(aa[u]), ahi = act_hi(aa[u]);
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wgt_lo16(wa[u][t]), alo, acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wgt_hi16(wa[u][t]), ahi, acc[t], 0, 0, 0);
+      }
+      // the step ends a group, or the wave's part of it
+      const int sabs = (k0 >> 7) + bt * BATCH + u;
+      if ((sabs & gmask) == gmask || bt * BATCH + u == nb * BATCH - 1) fold(sabs >> (log2g - 7));
+    }
+  };
+
+  load(0, wa0, aa0);
+  int bt = 0;
+  for (; bt + 2 <= nb; bt += 2) {
+    load(bt + 1, wa1, aa1);
+    compute(bt, wa0, aa0);
+    if (bt + 2 < nb) load(bt + 2, wa0, aa0);
+    compute(bt + 1, wa1, aa1);
+  }
+  if (bt < nb) compute(bt, wa0, aa0);
+  if constexpr (DBG) return;
+
+  // ---- sum the P parts of K and store ---------------------------------------
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wave][lane][t * 4 + i] = F[t][i];
+  __syncthreads();
+  if (wave == 0 && r16 < M) {
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int n = n0 + 16 * t + 4 * kb + i;
+        if (n < N) {
+          float f = 0.0f;
+#pragma unroll
+          for (int w = 0; w < P; ++w) f += red[w][lane][t * 4 + i];
+          Y[(int64_t)r16 * ldy + n] = f32_to_bf16_rne(fp16_bits_to_f32(w_scale[n]) * f);
+        }
+      }
+  }
+}
+
+}  // namespace
+
+bool gemv_mfma_supported(int64_t M, int64_t N, int64_t K, int log2g) {
+  // the parts of K (eighths at most) are whole batches; no step straddles a
+  // group; the group parameters fit in LDS; 32-bit buffer offsets
+  return M <= 16 && log2g >= 7 && K % 4096 == 0 && (K >> log2g) <= GMAX &&
+         32 * (K / 2) < (int64_t(1) << 31) && M * (K / 2) < (int64_t(1) << 31);
+}
+
+template <int T, int P>
+hipError_t launch_gv(const uint8_t* a_codes, const uint16_t* a_scale, const int16_t* a_zero,
+                     const uint8_t* w_codes, const uint16_t* w_scale, const int32_t* w_colsum,
+                     int64_t M, int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
+                     int32_t* acc_debug, hipStream_t stream) {
+  const int rows = 16 * T;
+  const dim3 grid((unsigned)((N + rows - 1) / rows)), block(64 * P);
+  const size_t lds = (size_t)(K >> log2g) * (32 + rows) * sizeof(float);
+  // A debug request runs an accumulator-only pass (partial sums added
+  // atomically into the zeroed buffer), then the regular kernel.
+  if (acc_debug) {
+    hipError_t e = hipMemsetAsync(acc_debug, 0, (size_t)(K >> log2g) * M * N * sizeof(int32_t),
+                                  stream);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((w4a4_gemv_kernel<T, P, true>), grid, block, lds, stream, a_codes,
+                       a_scale, a_zero, w_codes, w_scale, w_colsum, (int)M, (int)N, (int)K, log2g,
+                       y, ldy, acc_debug);
+  }
+  hipLaunchKernelGGL((w4a4_gemv_kernel<T, P, false>), grid, block, lds, stream, a_codes, a_scale,
+                     a_zero, w_codes, w_scale, w_colsum, (int)M, (int)N, (int)K, log2g, y, ldy,
+                     acc_debug);
+  return hipGetLastError();
+}
+
+hipError_t launch_w4a4_gemv_mfma(const uint8_t* a_codes, const uint16_t* a_scale,
+                                 const int16_t* a_zero, const uint8_t* w_codes,
+                                 const uint16_t* w_scale, const int32_t* w_colsum, int64_t M,
+                                 int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
+                                 int32_t* acc_debug, hipStream_t stream) {
+  // Two row tiles per wave (one activation load serves two weight loads) and
+  // K in quarters, measured best for 8192 and 28672 channels in either
+  // dimension; narrow layers take one tile per wave and K in eighths, for
+  // more waves in flight.
+#define OFFQ_GV(T, P)                                                                         \
+  return launch_gv<T, P>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, \
+                         y, ldy, acc_debug, stream)
+  if (N >= 32 * 128) OFFQ_GV(2, 4);
+  OFFQ_GV(1, 8);
+#undef OFFQ_GV
+}
+
+}  // namespace offq

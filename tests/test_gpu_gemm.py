@@ -43,9 +43,16 @@ def test_gemm_shapes(M, N, K, g):
 
 
 @pytest.mark.parametrize("M", [1, 2, 4, 5, 16])
-@pytest.mark.parametrize("K,g", [(256, 256), (2048, 512), (8192, 8192), (1024, 64)])
+@pytest.mark.parametrize("K,g", [(256, 256), (2048, 512), (8192, 8192), (1024, 64),
+                                 (4096, 128), (1536, 512), (2048, 1024)])
 def test_gemv_shapes(M, K, g):
     _layer(M, 200, K, g, seed=M + K)
+
+
+@pytest.mark.parametrize("N", [16, 33, 1030, 5000, 9000])
+def test_gemv_channel_counts(N):
+    """Single and ragged 16-channel tiles; one, two and four tiles per wave."""
+    _layer(3, N, 4096, 512, seed=N)
 
 
 def test_raw_layout_and_spikes():
