@@ -154,8 +154,8 @@ def cpu_baseline(M, K, N, g, spec, seed):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
-              "multi-GPU sharding is described in DESIGN.md but not built", file=sys.stderr)
+        print(f"bench.py: one GPU only (asked for --gpus {args.gpus}); the kernels run on one "
+              "GPU's share of a layer and no multi-GPU path exists", file=sys.stderr)
         sys.exit(2)
     import torch
 
@@ -296,8 +296,6 @@ def main():
         comp[name]["TOPS"] = round(ops / (comp[name]["us"] * 1e-6) / 1e12, 1)
         comp[name]["frac_int8_peak"] = round(comp[name]["TOPS"] / PEAK_INT8_TOPS, 4)
 
-    gemm_src = ["paper_2606_07116_amd/csrc/w4a4_gemm.hip", "paper_2606_07116_amd/csrc/common.h"]
-    rq_src = ["paper_2606_07116_amd/csrc/rotate_quantize.hip", "paper_2606_07116_amd/csrc/common.h"]
     if wl in ("attn_proj_prefill", "kv_chain"):
         ann_rq("rotate_quantize", M, K, g)
         ann_mm("w4a4_gemm", M, N, K)
@@ -342,7 +340,7 @@ def main():
         "metric": METRIC, "value": round(value, 2), "unit": unit, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "int4 codes on i8 MFMA (i32 accumulate), fp32 rotation",
+        "dtype": "int8",
         "data": "synthetic (seeded Llama-shaped activations with structured outliers; random weights)",
         "config": config, "roofline": roof, "components": comp,
     }
