@@ -1,6 +1,7 @@
-// W4A4 GEMM for several quantization groups per row (g < K): the case of a
-// block-diagonal online rotation, e.g. the MLP down projection with 28 groups
-// of 512 channels.  gfx950, v_mfma_i32_32x32x32_i8.
+// W4A4 GEMM on MFMA (gfx950, v_mfma_i32_32x32x32_i8), for one or several
+// quantization groups per row: g = K (full-width online Hadamard: attention
+// projection, MLP up/gate) and g < K (block-diagonal rotation, e.g. the MLP
+// down projection with 28 groups of 512 channels).
 //
 //   acc_b[m,n] = sum_{k in group b} q_a[m,k] q_w[n,k]                 (int32)
 //   Y[m,n]     = sw[n] * sum_b s[m,b] * (acc_b[m,n] - z[m,b] * colsum[b,n])
@@ -9,26 +10,35 @@
 // group; the z * colsum terms carry the absorbed offsets).
 //
 // Organisation
-// * 8 waves per workgroup (two per SIMD) in a 4 x 2 arrangement, each owning
-//   64 tokens x 64 output channels (2 x 2 MFMA tiles of 32 x 32): 64 int32
-//   accumulators for the current group and 64 fp32 running sums F; workgroup
-//   tile 256 x 128.  While one wave of a SIMD folds, the other multiplies.
-// * Stages of 128 k go from global memory straight into a 4-deep LDS ring
-//   (buffer loads with the LDS destination, 3 stages ahead; rows past the end
-//   read as zero), so no registers hold staged data.  One barrier per stage,
-//   preceded by a wait for the stage two ahead only.  The stage loop is
-//   unrolled by the ring depth, which makes the ring offsets of every LDS
-//   access compile-time constants.
-// * Fragment reads, unpacking and the transposed MFMA are those of the
-//   one-group kernel.
+// * 8 waves per workgroup, two per SIMD.  FM = 2: waves 4 x 2, each 64 tokens
+//   x 64 channels (2 x 2 MFMA tiles of 32 x 32), workgroup tile 256 x 128,
+//   any number of groups up to GMAX.  FM = 4: waves 2 x 4, each 128 x 64,
+//   workgroup tile 256 x 256, one group per row.
+// * Operand unpacking (4-bit nibbles to int8 MFMA operands) is VALU work that
+//   does not overlap the MFMAs, so each packed byte is unpacked as few times
+//   as possible: the operand that four waves share (the weights for FM = 2,
+//   the activations for FM = 4) is unpacked once, when its stage is written
+//   to LDS, into two int8 planes; the other operand stays packed in LDS and
+//   is unpacked in registers by each of the two waves that read it.
+// * Stages of 128 k go global memory -> registers (two stages ahead) -> a
+//   3-deep LDS ring; one LDS-only barrier per stage.  16-byte chunks are
+//   XOR-swizzled by row so that fragment reads are conflict-free.
+// * Activation codes (0..15) feed the signed i8 MFMA unchanged; weight nibbles
+//   are widened to 16 q (high nibble masked, low nibble shifted), so every
+//   accumulator holds 16 acc exactly.  Both operands split each 16-byte chunk
+//   (32 k) into its low and high nibbles: the same k-permutation on both
+//   sides.  The MFMA takes the weight fragment as its row operand and
+//   accumulates the transposed tile.
 // * At the end of each group (g / 128 stages) the accumulators are folded
-//   into the running sums, F += (s / 16) * acc in fp32 (s / 16 undoes the 16x
-//   widening of the weight codes), and the first MFMA of the next group starts
-//   from a zero accumulator.  The row scales, zero-points and column sums of
-//   the tile's groups are loaded into LDS once, in the prologue.
-// * After the last group the zero-point terms are added with one fp32 MFMA
-//   per pair of groups: F += sum_b (-s z)[m, b] * colsum[b, n].
+//   into fp32 running sums F, F += (s / 16) acc, and the next group's first
+//   MFMA starts from zero.  The zero-point terms -sum_b s z colsum_b form a
+//   rank-G product added after the last group with fp32 MFMAs (k = group).
+//   Row scales, zero-points, column sums and weight scales of the tile sit in
+//   LDS from the prologue.  With one group the fold runs in the epilogue, so
+//   F takes no registers during the main loop.
 // * Epilogue: Y = sw * F -> bf16 through LDS for 16-byte coalesced stores.
+// * Tile order is XCD-aware (see tile_of): each XCD walks a block of tile
+//   rows, keeping its A and W panels in its own L2.
 #include <type_traits>
 
 #include "common.h"
@@ -40,71 +50,52 @@ namespace {
 
 using namespace gemm;
 
-// FM: 32-row MFMA tiles per wave along the tokens.  FM = 2: 8 waves of
-// 64 x 64 in a 4 x 2 arrangement (workgroup tile 256 x 128), any number of
-// groups up to GMAX; FM = 4: 8 waves of 128 x 64 in a 2 x 4 arrangement
-// (256 x 256), one group per row only (no registers for running sums).
-template <int FM>
+template <int FM, bool ONEG>
 struct GCfg {
   static constexpr int THREADS = 512;              // 8 waves, 2 per SIMD
   static constexpr int WAVES_M = FM == 2 ? 4 : 2;
   static constexpr int WROWS = 32 * FM;            // token rows per wave
   static constexpr int BM = WAVES_M * WROWS;       // 256
   static constexpr int BN = (8 / WAVES_M) * 64;    // 128 or 256
-  static constexpr int NC = 4;                     // 16-byte chunks per row and stage
-  static constexpr int A_SLOTS = BM * NC;
-  static constexpr int B_SLOTS = BN * NC;
-  static constexpr int STAGE_SLOTS = A_SLOTS + B_SLOTS;
-  static constexpr int A_LD = A_SLOTS / THREADS;   // loads per thread and stage
-  static constexpr int B_LD = B_SLOTS / THREADS;
+  static constexpr bool X_IS_W = FM == 2;          // operand unpacked into LDS
+  static constexpr int P_ROWS = X_IS_W ? BM : BN;  // packed operand rows
+  static constexpr int X_ROWS = X_IS_W ? BN : BM;  // unpacked operand rows
+  static constexpr int P_SLOTS = P_ROWS * 4;       // 16-byte slots: 4 packed chunks per row
+  static constexpr int X_SLOTS = X_ROWS * 8;       // 8 int8 chunks per row (4 x lo/hi)
+  static constexpr int STAGE_SLOTS = P_SLOTS + X_SLOTS;
+  static constexpr int P_LD = P_ROWS * 4 / THREADS;  // packed chunks loaded per thread
+  static constexpr int X_LD = X_ROWS * 4 / THREADS;
   static constexpr int KSTAGE = 128;               // k per stage
-  static constexpr int NBUF = 4;                   // LDS ring depth
-  static constexpr int GMAX = FM == 2 ? 28 : 1;    // groups whose parameters fit in LDS
+  // groups whose parameters fit in LDS; LDS ring depth (with four slots the
+  // slot of every stage in a 4-stage unrolled loop is a compile-time constant)
+  static constexpr int GMAX = (FM == 2 && !ONEG) ? 28 : 1;
+  static constexpr int NBUF = (FM == 2 && ONEG) ? 4 : 3;
 };
 
-// s_waitcnt with only the vector-memory counter bounded (gfx9 encoding)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-// 16 bytes per lane from a buffer straight into LDS: lane l writes bytes
-// [lds + 16 l, lds + 16 l + 16) (lds is the wave-uniform LDS byte address).
-// Issued as inline assembly, so the compiler neither tracks these writes nor
-// inserts waits for them: the ring's own vmcnt waits and barriers order them.
-__device__ __forceinline__ void buffer_to_lds16(__amdgpu_buffer_rsrc_t rsrc, uint32_t lds,
-                                                int voff, int soff) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               :: "s"(lds), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
-}
-
-// Workgroup barrier for the ring: waits for the wave's own LDS operations,
-// synchronises, and is a compiler-level memory barrier.  The buffer-to-LDS
-// loads a stage needs are waited for with wait_vmcnt before it.
-__device__ __forceinline__ void ring_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
-}
+// packed rows: 4 chunks, swizzle c ^ (row/2 mod 4); int8 rows: 8 chunks,
+// swizzle c ^ (row/2 mod 8).  Either way the 16 rows of a 16-lane phase of a
+// fragment read land in 16 distinct 16-byte bank groups.
+__device__ __forceinline__ int pslot(int row, int c) { return row * 4 + (c ^ ((row >> 1) & 3)); }
+__device__ __forceinline__ int xslot(int row, int c) { return row * 8 + (c ^ ((row >> 1) & 7)); }
 
 typedef float v16f __attribute__((ext_vector_type(16)));
 
-// MODE: stages per group: 1, 2, 4, or a multiple of 8 (MODE 8).
-template <bool DBG, int MODE, int FM>
+// MODE: stages per group: 1, 2, 4, or a multiple of 8 (MODE 8).  ONEG: one
+// group per row (g = K).
+template <bool DBG, int MODE, int FM, bool ONEG>
 __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     const uint8_t* __restrict__ A, const uint16_t* __restrict__ a_scale,
     const int16_t* __restrict__ a_zero, const uint8_t* __restrict__ W,
     const uint16_t* __restrict__ w_scale, const int32_t* __restrict__ w_colsum, int M, int N,
     int K, int log2g, uint16_t* __restrict__ Y, int64_t ldy, int32_t* __restrict__ acc_dbg) {
-  using C = GCfg<FM>;
+  using C = GCfg<FM, ONEG>;
+  constexpr bool XW = C::X_IS_W;
   __shared__ uint4 ring[C::NBUF * C::STAGE_SLOTS];
   // per group b: s / 16 and z of the tile's rows, colsum of its columns
   __shared__ float sRS[C::GMAX][C::BM];
   __shared__ short sZ[C::GMAX][C::BM];
   __shared__ float sCS[C::GMAX][C::BN];
+  __shared__ __attribute__((aligned(16))) float sSW[C::BN];  // weight scales
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -122,48 +113,81 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   const int G = K >> log2g;
   const int spg = 1 << (log2g - 7);  // stages per group
 
-  constexpr int RSTEP = C::THREADS / C::NC;
-  const int row0 = tid / C::NC;
-  const int chunk = swz<C::NC>(row0, tid % C::NC);
-  const __amdgpu_buffer_rsrc_t arsrc = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(A + (int64_t)tm * ldk), 0, (int)((int64_t)(M - tm) * ldk), 0x00020000);
-  const __amdgpu_buffer_rsrc_t brsrc = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(W + (int64_t)tn * ldk), 0, (int)((int64_t)(N - tn) * ldk), 0x00020000);
-  const int voff = row0 * (int)ldk + chunk * 16;
-  const int vstep = RSTEP * (int)ldk;
-  const uint32_t ring_lds = lds_addr(ring) + wave * 64 * 16;
-
-  // stage st into ring buffer J: this thread's slots tid + 512 i, written by
-  // each wave as 64 consecutive 16-byte slots per load
-  auto dma = [&](int J, int st) __attribute__((always_inline)) {
-    const uint32_t base = ring_lds + J * (C::STAGE_SLOTS * 16);
-    const int soff = st * (C::KSTAGE / 2);
+  // ---- global -> registers -> LDS staging -----------------------------------
+  // Chunk s = tid + 512 i of an operand's stage is row s / 4, packed chunk
+  // s % 4 (16 bytes = 32 k); rows past M (N) read as zero.
+  const uint8_t* pbase = XW ? A + (int64_t)tm * ldk : W + (int64_t)tn * ldk;
+  const uint8_t* xbase = XW ? W + (int64_t)tn * ldk : A + (int64_t)tm * ldk;
+  const int prows = XW ? M - tm : N - tn, xrows = XW ? N - tn : M - tm;
+  const __amdgpu_buffer_rsrc_t prsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)pbase, 0, (int)((int64_t)prows * ldk), 0x00020000);
+  const __amdgpu_buffer_rsrc_t xrsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)xbase, 0, (int)((int64_t)xrows * ldk), 0x00020000);
+  // the same buffers with no valid bytes: loads past the last stage read zeros
+  const __amdgpu_buffer_rsrc_t prsrc0 = __builtin_amdgcn_make_buffer_rsrc((void*)pbase, 0, 0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t xrsrc0 = __builtin_amdgcn_make_buffer_rsrc((void*)xbase, 0, 0, 0x00020000);
+  const int crow = tid >> 2, cch = tid & 3;
+  const int voff = crow * (int)ldk + cch * 16;
+  const int vstep = (C::THREADS / 4) * (int)ldk;  // 128 rows
+  constexpr int NLD = C::P_LD + C::X_LD;
+  v4i rg0[NLD], rg1[NLD];  // two stages in flight
+  auto gload = [&](int st, v4i (&rg)[NLD]) __attribute__((always_inline)) {
+    const bool ok = st < nst;
+    const __amdgpu_buffer_rsrc_t pr = ok ? prsrc : prsrc0, xr = ok ? xrsrc : xrsrc0;
+    const int soff = ok ? st * (C::KSTAGE / 2) : 0;
 #pragma unroll
-    for (int i = 0; i < C::A_LD; ++i)
-      buffer_to_lds16(arsrc, base + i * C::THREADS * 16, voff + i * vstep, soff);
+    for (int i = 0; i < C::P_LD; ++i)
+      rg[i] = __builtin_amdgcn_raw_buffer_load_b128(pr, voff + i * vstep, soff, 0);
 #pragma unroll
-    for (int i = 0; i < C::B_LD; ++i)
-      buffer_to_lds16(brsrc, base + (C::A_SLOTS + i * C::THREADS) * 16, voff + i * vstep, soff);
+    for (int i = 0; i < C::X_LD; ++i)
+      rg[C::P_LD + i] = __builtin_amdgcn_raw_buffer_load_b128(xr, voff + i * vstep, soff, 0);
   };
-  // this lane's fragment slots for chunk column 2h + jj; fragments f are 32
-  // rows apart, which keeps the swizzle
-  const uint4* a_frag0 = ring + (wm * C::WROWS + fr) * C::NC + swz<C::NC>(fr, 2 * h);
-  const uint4* a_frag1 = ring + (wm * C::WROWS + fr) * C::NC + swz<C::NC>(fr, 2 * h + 1);
-  const uint4* b_frag0 = ring + C::A_SLOTS + (wn * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h);
-  const uint4* b_frag1 = ring + C::A_SLOTS + (wn * 64 + fr) * C::NC + swz<C::NC>(fr, 2 * h + 1);
-  auto fread = [&](auto JC, int jj, uint4* pa, uint4* pb) __attribute__((always_inline)) {
-    constexpr int J = decltype(JC)::value;
-    const uint4* As = (jj ? a_frag1 : a_frag0) + J * C::STAGE_SLOTS;
-    const uint4* Bs = (jj ? b_frag1 : b_frag0) + J * C::STAGE_SLOTS;
+  auto lstore = [&](int slot, const v4i (&rg)[NLD]) __attribute__((always_inline)) {
+    uint4* P = ring + slot * C::STAGE_SLOTS;
+    uint4* X = P + C::P_SLOTS;
 #pragma unroll
-    for (int f = 0; f < FM; ++f) pa[f] = As[f * 32 * C::NC];
+    for (int i = 0; i < C::P_LD; ++i)
+      P[pslot(crow + 128 * i, cch)] = __builtin_bit_cast(uint4, rg[i]);
 #pragma unroll
-    for (int f = 0; f < 2; ++f) pb[f] = Bs[f * 32 * C::NC];
+    for (int i = 0; i < C::X_LD; ++i) {
+      const uint4 d = __builtin_bit_cast(uint4, rg[C::P_LD + i]);
+      const int r = crow + 128 * i;
+      v4i lo, hi;
+      if constexpr (XW) {
+        lo = wgt_lo16(d);
+        hi = wgt_hi16(d);
+      } else {
+        lo = act_lo(d);
+        hi = act_hi(d);
+      }
+      X[xslot(r, 2 * cch)] = __builtin_bit_cast(uint4, lo);
+      X[xslot(r, 2 * cch + 1)] = __builtin_bit_cast(uint4, hi);
+    }
+  };
+
+  // ---- fragments ---------------------------------------------------------------
+  // Per 64 k (chunk column c = 2h + jj of the stage) a wave reads its packed
+  // fragments (one 16-byte chunk each) and, per plane pl, its unpacked
+  // fragments; lane row fr, fragment f is 32 rows further (which keeps both
+  // swizzles).
+  constexpr int NPF = XW ? FM : 2;  // packed fragments per wave
+  constexpr int NXF = XW ? 2 : FM;  // unpacked fragments per wave
+  const int prow0 = (XW ? wm * C::WROWS : wn * 64) + fr;
+  const int xrow0 = (XW ? wn * 64 : wm * C::WROWS) + fr;
+  auto pread = [&](int slot, int jj, uint4 (&pp)[NPF]) __attribute__((always_inline)) {
+    const uint4* P = ring + slot * C::STAGE_SLOTS;
+#pragma unroll
+    for (int f = 0; f < NPF; ++f) pp[f] = P[pslot(prow0, 2 * h + jj) + f * 32 * 4];
+  };
+  auto xread = [&](int slot, int jj, int pl, uint4 (&px)[NXF]) __attribute__((always_inline)) {
+    const uint4* X = ring + slot * C::STAGE_SLOTS + C::P_SLOTS;
+#pragma unroll
+    for (int f = 0; f < NXF; ++f) px[f] = X[xslot(xrow0, 4 * h + 2 * jj + pl) + f * 32 * 8];
   };
 
   // With one group per row (the only case of FM = 4) F is first written by
   // the single fold after the loop, so it takes no registers during it.
-  constexpr bool SINGLE = C::GMAX == 1;
+  constexpr bool SINGLE = ONEG;
   v16i acc[FM][2];
   v16f F[FM][2];
 #pragma unroll
@@ -174,10 +198,9 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
       if constexpr (!SINGLE) F[a][b] = v16f{};
     }
 
-  // Lane column fr of fragment fm is token row wm*64 + fm*32 + fr; register
+  // Lane column fr of fragment fm is token row wm*WROWS + fm*32 + fr; register
   // i of fragment (fm, fn) is output channel wn*64 + fn*32 + 8*(i/4) + 4*h + i%4.
-  // F += (s / 16) * acc for fragment row fm (s / 16 undoes the 16x widening
-  // of the weight codes), with rs[fm] = s / 16 of the finished group.
+  // F += (s / 16) * acc for fragment row fm, rs[fm] = s / 16 of the group.
   float rs[FM] = {};
   auto read_rs = [&](int b) __attribute__((always_inline)) {
 #pragma unroll
@@ -191,24 +214,31 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
         F[fm][fn][i] = SINGLE ? rs[fm] * (float)acc[fm][fn][i]
                               : __builtin_fmaf(rs[fm], (float)acc[fm][fn][i], F[fm][fn][i]);
   };
-  // two k-steps (low and high nibbles of one 16-byte chunk per fragment);
-  // FRESH: the low-nibble MFMAs start the accumulators from zero.  Operands
-  // are unpacked just before use to keep the live registers down.
-  auto mma2 = [&](const uint4* pa, const uint4* pb, auto FC) __attribute__((always_inline)) {
+
+  // one k-step of 32: plane pl of the packed fragments pp against the
+  // unpacked plane px; FRESH: start the accumulators from zero.
+  auto mma1 = [&](const uint4 (&pp)[NPF], const uint4 (&px)[NXF], auto PL, auto FC)
+      __attribute__((always_inline)) {
+    constexpr bool HI = decltype(PL)::value;
     constexpr bool FRESH = decltype(FC)::value;
-    const v4i ub0 = wgt_lo16(pb[0]), ub1 = wgt_lo16(pb[1]);
+    if constexpr (XW) {  // activations packed, weights unpacked
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) {
-      const v4i ua = act_lo(pa[fm]);
-      acc[fm][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub0, ua, FRESH ? v16i{} : acc[fm][0], 0, 0, 0);
-      acc[fm][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub1, ua, FRESH ? v16i{} : acc[fm][1], 0, 0, 0);
-    }
-    const v4i nb0 = wgt_hi16(pb[0]), nb1 = wgt_hi16(pb[1]);
+      for (int fm = 0; fm < FM; ++fm) {
+        const v4i ua = HI ? act_hi(pp[fm]) : act_lo(pp[fm]);
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) {
-      const v4i na = act_hi(pa[fm]);
-      acc[fm][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(nb0, na, acc[fm][0], 0, 0, 0);
-      acc[fm][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(nb1, na, acc[fm][1], 0, 0, 0);
+        for (int fn = 0; fn < 2; ++fn)
+          acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+              __builtin_bit_cast(v4i, px[fn]), ua, FRESH ? v16i{} : acc[fm][fn], 0, 0, 0);
+      }
+    } else {  // weights packed, activations unpacked
+#pragma unroll
+      for (int fn = 0; fn < 2; ++fn) {
+        const v4i ub = HI ? wgt_hi16(pp[fn]) : wgt_lo16(pp[fn]);
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+          acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+              ub, __builtin_bit_cast(v4i, px[fm]), FRESH ? v16i{} : acc[fm][fn], 0, 0, 0);
+      }
     }
     if constexpr (FM == 4) {
       // keep the 128 accumulators in accumulation registers (an empty asm
@@ -219,7 +249,6 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
         for (int fn = 0; fn < 2; ++fn) asm volatile("" : "+a"(acc[fm][fn]));
     }
   };
-
   auto dump = [&](int b) __attribute__((always_inline)) {  // debug: raw accumulators of group b
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm) {
@@ -238,26 +267,24 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     }
   };
 
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
-
-  // prologue: stages 0, 1, 2 in flight to the ring; the group parameters of
-  // the tile into LDS meanwhile
-  dma(0, 0);
-  if (nst > 1) dma(1, 1);
-  if (nst > 2) dma(2, 2);
+  // ---- prologue: stages 0 and 1 into the ring, 2 and 3 into registers; the
+  // group parameters and weight scales of the tile into LDS ----------------
+  gload(0, rg0);
+  if (nst > 1) gload(1, rg1);
+  lstore(0, rg0);
+  if (nst > 2) gload(2, rg0);
+  if (nst > 1) lstore(1, rg1);
+  if (nst > 3) gload(3, rg1);
   {
-    // Row parameters of the tile: a contiguous block of 256 * G entries of the
-    // [M, G] arrays, read coalesced (entry e = tid + 512 p is row e / G, group
+    // Row parameters: a contiguous block of 256 G entries of the [M, G]
+    // arrays, read coalesced (entry e = tid + 512 p is row e / G, group
     // e % G); column sums: group b, column c = colsum[b * N + tn + c].  All
     // loads are issued before the first LDS write.
     const float inv_g = 1.0f / (float)G;
     const int64_t base = (int64_t)tm * G;
     const int nrow_e = min(C::BM, M - tm) * G;  // valid entries of the block
-    constexpr int PE = (C::GMAX * C::BM + C::THREADS - 1) / C::THREADS;  // row entries per thread
-    constexpr int PC = (C::GMAX * C::BN + C::THREADS - 1) / C::THREADS;  // column entries per thread
+    constexpr int PE = (C::GMAX * C::BM + C::THREADS - 1) / C::THREADS;
+    constexpr int PC = (C::GMAX * C::BN + C::THREADS - 1) / C::THREADS;
     uint16_t sv[PE];
     int16_t zv[PE];
 #pragma unroll
@@ -271,8 +298,10 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
 #pragma unroll
     for (int p = 0; p < PC; ++p) {
       const int b = (C::THREADS / C::BN) * p + tid / C::BN, c = tid % C::BN;
-      cv[p] = (b < G && b < C::GMAX && tn + c < N) ? (float)w_colsum[(int64_t)b * N + tn + c] : 0.0f;
+      cv[p] = (b < G && b < C::GMAX && tn + c < N) ? (float)w_colsum[(int64_t)b * N + tn + c]
+                                                   : 0.0f;
     }
+    const float swv = (tid < C::BN && tn + tid < N) ? fp16_bits_to_f32(w_scale[tn + tid]) : 0.0f;
 #pragma unroll
     for (int p = 0; p < PE; ++p) {
       const int e = tid + C::THREADS * p;
@@ -289,88 +318,102 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
       const int b = (C::THREADS / C::BN) * p + tid / C::BN;
       if (b < G && b < C::GMAX) sCS[b][tid % C::BN] = cv[p];
     }
+    if (tid < C::BN) sSW[tid] = swv;
   }
-  // stages 0 and 1 landed (stage 2 may still be in flight)
-  if (nst > 2) wait_vmcnt<C::A_LD + C::B_LD>();
-  else wait_vmcnt<0>();
-  ring_barrier();
-  uint4 pc_a[4], pc_b[2];
-  fread(I0{}, 0, pc_a, pc_b);
+  lds_barrier();
+  uint4 pa[NPF], pb[NPF], xa[NXF], xb[NXF];
+  pread(0, 0, pa);
+  xread(0, 0, 0, xa);
 
-  // One stage st on ring buffer J = st % 4; FRESH marks the first stage of a
-  // group, whose last stage folds the accumulators.
-  auto body = [&](auto JC, auto FC, int st) __attribute__((always_inline)) {
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+
+  // One stage st; J = st mod 4 picks the register buffer (J even: rg0).
+  // FRESH marks the first stage of a group, LAST its last one (which folds).
+  // Each k-step's fragments are read during the previous k-step's MFMAs; on
+  // entry pa / xa hold the stage's first ones.  The body has no branches, so
+  // that the compiler can interleave the LDS traffic, the unpacking and the
+  // global loads with the MFMAs: past the last stage the stores fill a slot
+  // that is never read again and the loads read zeros.
+  auto body = [&](auto JC, auto FC, auto LC, int st) __attribute__((always_inline)) {
     constexpr int J = decltype(JC)::value;
-    using NEXT = std::integral_constant<int, (J + 1) % 4>;
-    const bool ahead = st + 3 < nst;
-    if (ahead) dma((J + 3) % 4, st + 3);
-    uint4 p1_a[4], p1_b[2];
-    fread(JC, 1, p1_a, p1_b);
-    mma2(pc_a, pc_b, FC);
-    fread(NEXT{}, 0, pc_a, pc_b);  // past the last stage: stale, unused
-    mma2(p1_a, p1_b, std::false_type{});
-    if ((st & (spg - 1)) == spg - 1) {  // the group's last stage
+    v4i(&rg)[NLD] = (J % 2 == 0) ? rg0 : rg1;
+    // ring slot of stage st + d (J = st mod 4)
+    auto slot_of = [&](int d) __attribute__((always_inline)) {
+      return C::NBUF == 4 ? ((J + d) & 3) : (st + d) % 3;
+    };
+    const int slot = slot_of(0);
+    // stage st + 2 into the slot read during stage st - 1, then the register
+    // buffer takes stage st + 4
+    lstore(slot_of(2), rg);
+    gload(st + 4, rg);
+    xread(slot, 0, 1, xb);
+    mma1(pa, xa, std::false_type{}, FC);
+    pread(slot, 1, pb);
+    xread(slot, 1, 0, xa);
+    mma1(pa, xb, std::true_type{}, std::false_type{});
+    xread(slot, 1, 1, xb);
+    mma1(pb, xa, std::false_type{}, std::false_type{});
+    pread(slot_of(1), 0, pa);  // past the last stage: stale, unused
+    xread(slot_of(1), 0, 0, xa);
+    mma1(pb, xb, std::true_type{}, std::false_type{});
+    if constexpr (decltype(LC)::value) {  // the group's last stage
       const int b = st >> (log2g - 7);
       if constexpr (DBG) {
         dump(b);
-      } else {
+      } else if constexpr (!SINGLE) {
         read_rs(b);
-        if constexpr (!SINGLE) {
 #pragma unroll
-          for (int fm = 0; fm < FM; ++fm) fold_row(fm);
-        }
+        for (int fm = 0; fm < FM; ++fm) fold_row(fm);
       }
     }
-    // stage st + 2 has landed; stage st + 3 may still be in flight
-    if (ahead) wait_vmcnt<C::A_LD + C::B_LD>();
-    else wait_vmcnt<0>();
-    ring_barrier();
+    lds_barrier();
+  };
+  // four stages from st (a multiple of 4); FIRST / LASTG: they start / end a group
+  auto four = [&](int st, auto FIRST, auto LASTG) __attribute__((always_inline)) {
+    using Fl = std::false_type;
+    body(I0{}, FIRST, Fl{}, st);
+    body(I1{}, Fl{}, Fl{}, st + 1);
+    body(I2{}, Fl{}, Fl{}, st + 2);
+    body(I3{}, Fl{}, LASTG, st + 3);
   };
 
   using T = std::true_type;
   using Fl = std::false_type;
   int st = 0;
-  if constexpr (MODE == 1) {  // every stage starts a group
+  if constexpr (MODE == 1) {  // every stage is a group
     for (; st + 4 <= nst; st += 4) {
-      body(I0{}, T{}, st);
-      body(I1{}, T{}, st + 1);
-      body(I2{}, T{}, st + 2);
-      body(I3{}, T{}, st + 3);
+      body(I0{}, T{}, T{}, st);
+      body(I1{}, T{}, T{}, st + 1);
+      body(I2{}, T{}, T{}, st + 2);
+      body(I3{}, T{}, T{}, st + 3);
     }
-    if (st < nst) body(I0{}, T{}, st);
-    if (st + 1 < nst) body(I1{}, T{}, st + 1);
-    if (st + 2 < nst) body(I2{}, T{}, st + 2);
+    if (st < nst) body(I0{}, T{}, T{}, st);
+    if (st + 1 < nst) body(I1{}, T{}, T{}, st + 1);
+    if (st + 2 < nst) body(I2{}, T{}, T{}, st + 2);
   } else if constexpr (MODE == 2) {  // groups of two stages
     for (; st + 4 <= nst; st += 4) {
-      body(I0{}, T{}, st);
-      body(I1{}, Fl{}, st + 1);
-      body(I2{}, T{}, st + 2);
-      body(I3{}, Fl{}, st + 3);
+      body(I0{}, T{}, Fl{}, st);
+      body(I1{}, Fl{}, T{}, st + 1);
+      body(I2{}, T{}, Fl{}, st + 2);
+      body(I3{}, Fl{}, T{}, st + 3);
     }
     if (st < nst) {
-      body(I0{}, T{}, st);
-      body(I1{}, Fl{}, st + 1);
+      body(I0{}, T{}, Fl{}, st);
+      body(I1{}, Fl{}, T{}, st + 1);
     }
   } else if constexpr (MODE == 4) {  // groups of four stages
+    for (; st < nst; st += 4) four(st, T{}, T{});
+  } else {  // groups of 8k stages: first four, middle fours, last four
     for (; st < nst; st += 4) {
-      body(I0{}, T{}, st);
-      body(I1{}, Fl{}, st + 1);
-      body(I2{}, Fl{}, st + 2);
-      body(I3{}, Fl{}, st + 3);
-    }
-  } else {  // groups of 8k stages
-    for (; st < nst; st += 8) {
-      if ((st & (spg - 1)) == 0) body(I0{}, T{}, st);
-      else body(I0{}, Fl{}, st);
-      body(I1{}, Fl{}, st + 1);
-      body(I2{}, Fl{}, st + 2);
-      body(I3{}, Fl{}, st + 3);
-      body(I0{}, Fl{}, st + 4);
-      body(I1{}, Fl{}, st + 5);
-      body(I2{}, Fl{}, st + 6);
-      body(I3{}, Fl{}, st + 7);
+      four(st, T{}, Fl{});
+      for (st += 4; (st & (spg - 1)) != spg - 4; st += 4) four(st, Fl{}, Fl{});
+      four(st, Fl{}, T{});
     }
   }
+  if constexpr (SINGLE && !DBG) read_rs(0);
   if constexpr (DBG) return;
 
   // ---- finish one fragment row at a time ----------------------------------
@@ -385,12 +428,13 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
 #pragma unroll
   for (int fn = 0; fn < 2; ++fn)
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int c = tn + wn * 64 + fn * 32 + q * 8 + h * 4 + e;
-        sw[fn][q][e] = c < N ? fp16_bits_to_f32(w_scale[c]) : 0.0f;
-      }
+    for (int q = 0; q < 4; ++q) {
+      const float4 v = *reinterpret_cast<const float4*>(&sSW[wn * 64 + fn * 32 + q * 8 + h * 4]);
+      sw[fn][q][0] = v.x;
+      sw[fn][q][1] = v.y;
+      sw[fn][q][2] = v.z;
+      sw[fn][q][3] = v.w;
+    }
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
     if constexpr (SINGLE) fold_row(fm);
@@ -446,20 +490,20 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
 bool gemm_grouped_supported(int64_t M, int64_t N, int64_t K, int log2g) {
   // stages of 128 k never straddle a group; the group parameters of a tile
   // fit in LDS; buffer offsets are 32-bit
-  return log2g >= 7 && K % 128 == 0 && (K >> log2g) <= GCfg<2>::GMAX &&
+  return log2g >= 7 && K % 128 == 0 && (K >> log2g) <= GCfg<2, false>::GMAX &&
          M * (K / 2) < (int64_t(1) << 31) && N * (K / 2) < (int64_t(1) << 31);
 }
 
-template <int FM>
+template <int FM, bool ONEG>
 hipError_t launch_g(const uint8_t* a_codes, const uint16_t* a_scale, const int16_t* a_zero,
                     const uint8_t* w_codes, const uint16_t* w_scale, const int32_t* w_colsum,
                     int64_t M, int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
                     int32_t* acc_debug, hipStream_t stream) {
-  using C = GCfg<FM>;
+  using C = GCfg<FM, ONEG>;
   const int64_t tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
   const dim3 grid((unsigned)tiles), block(C::THREADS);
 #define OFFQ_GG(D, MD)                                                                        \
-  hipLaunchKernelGGL((w4a4_gemm_grouped_kernel<D, MD, FM>), grid, block, 0, stream, a_codes,  \
+  hipLaunchKernelGGL((w4a4_gemm_grouped_kernel<D, MD, FM, ONEG>), grid, block, 0, stream, a_codes,  \
                      a_scale, a_zero, w_codes, w_scale, w_colsum, (int)M, (int)N, (int)K, log2g, \
                      y, ldy, acc_debug)
 #define OFFQ_GG_M(D)                                                                 \
@@ -482,10 +526,13 @@ hipError_t launch_w4a4_gemm_grouped(const uint8_t* a_codes, const uint16_t* a_sc
   // wave tiles
   const bool wide = (K >> log2g) == 1 && ((M + 255) / 256) * ((N + 255) / 256) >= 384;
   if (wide)
-    return launch_g<4>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, y,
-                       ldy, acc_debug, stream);
-  return launch_g<2>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, y,
-                     ldy, acc_debug, stream);
+    return launch_g<4, true>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g,
+                             y, ldy, acc_debug, stream);
+  if ((K >> log2g) == 1)
+    return launch_g<2, true>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g,
+                             y, ldy, acc_debug, stream);
+  return launch_g<2, false>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g,
+                            y, ldy, acc_debug, stream);
 }
 
 }  // namespace offq
