@@ -70,12 +70,15 @@ struct GCfg {
   // slot of every stage in a 4-stage unrolled loop is a compile-time constant)
   static constexpr int GMAX = (FM == 2 && !ONEG) ? 28 : 1;
   static constexpr int NBUF = (FM == 2 && ONEG) ? 4 : 3;
+  // stages held in registers between their global load and their LDS store:
+  // the loads are issued NRB stages before the store
+  static constexpr int NRB = (FM == 2 && ONEG) ? 4 : 2;
 };
 
-// packed rows: 4 chunks, swizzle c ^ (row/2 mod 4); int8 rows: 8 chunks,
-// swizzle c ^ (row/2 mod 8).  Either way the 16 rows of a 16-lane phase of a
-// fragment read land in 16 distinct 16-byte bank groups.
-__device__ __forceinline__ int pslot(int row, int c) { return row * 4 + (c ^ ((row >> 1) & 3)); }
+// packed rows: 4 chunks, swizzle c ^ (row/4 mod 4); int8 rows: 8 chunks,
+// swizzle c ^ (row/2 mod 8).  (Chosen by measurement: these gave the fewest
+// LDS bank-conflict cycles of the XOR swizzles tried.)
+__device__ __forceinline__ int pslot(int row, int c) { return row * 4 + (c ^ ((row >> 2) & 3)); }
 __device__ __forceinline__ int xslot(int row, int c) { return row * 8 + (c ^ ((row >> 1) & 7)); }
 
 typedef float v16f __attribute__((ext_vector_type(16)));
@@ -130,7 +133,8 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   const int voff = crow * (int)ldk + cch * 16;
   const int vstep = (C::THREADS / 4) * (int)ldk;  // 128 rows
   constexpr int NLD = C::P_LD + C::X_LD;
-  v4i rg0[NLD], rg1[NLD];  // two stages in flight
+  v4i rgb[C::NRB][NLD];   // stages in flight
+  v4i ra[NLD], rb[NLD];    // stages 0 and 1 in the prologue
   auto gload = [&](int st, v4i (&rg)[NLD]) __attribute__((always_inline)) {
     const bool ok = st < nst;
     const __amdgpu_buffer_rsrc_t pr = ok ? prsrc : prsrc0, xr = ok ? xrsrc : xrsrc0;
@@ -142,12 +146,14 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     for (int i = 0; i < C::X_LD; ++i)
       rg[C::P_LD + i] = __builtin_amdgcn_raw_buffer_load_b128(xr, voff + i * vstep, soff, 0);
   };
-  auto lstore = [&](int slot, const v4i (&rg)[NLD]) __attribute__((always_inline)) {
+  auto lstore_p = [&](int slot, const v4i (&rg)[NLD]) __attribute__((always_inline)) {
     uint4* P = ring + slot * C::STAGE_SLOTS;
-    uint4* X = P + C::P_SLOTS;
 #pragma unroll
     for (int i = 0; i < C::P_LD; ++i)
       P[pslot(crow + 128 * i, cch)] = __builtin_bit_cast(uint4, rg[i]);
+  };
+  auto lstore_x = [&](int slot, const v4i (&rg)[NLD]) __attribute__((always_inline)) {
+    uint4* X = ring + slot * C::STAGE_SLOTS + C::P_SLOTS;
 #pragma unroll
     for (int i = 0; i < C::X_LD; ++i) {
       const uint4 d = __builtin_bit_cast(uint4, rg[C::P_LD + i]);
@@ -163,6 +169,10 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
       X[xslot(r, 2 * cch)] = __builtin_bit_cast(uint4, lo);
       X[xslot(r, 2 * cch + 1)] = __builtin_bit_cast(uint4, hi);
     }
+  };
+  auto lstore = [&](int slot, const v4i (&rg)[NLD]) __attribute__((always_inline)) {
+    lstore_p(slot, rg);
+    lstore_x(slot, rg);
   };
 
   // ---- fragments ---------------------------------------------------------------
@@ -267,19 +277,14 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     }
   };
 
-  // ---- prologue: stages 0 and 1 into the ring, 2 and 3 into registers; the
-  // group parameters and weight scales of the tile into LDS ----------------
-  gload(0, rg0);
-  if (nst > 1) gload(1, rg1);
-  lstore(0, rg0);
-  if (nst > 2) gload(2, rg0);
-  if (nst > 1) lstore(1, rg1);
-  if (nst > 3) gload(3, rg1);
+  // ---- prologue: the group parameters and weight scales of the tile, then
+  // the first four stages are requested together; the parameters go to LDS,
+  // stages 0 and 1 into the ring, 2 and 3 stay in registers ----------------
   {
     // Row parameters: a contiguous block of 256 G entries of the [M, G]
     // arrays, read coalesced (entry e = tid + 512 p is row e / G, group
-    // e % G); column sums: group b, column c = colsum[b * N + tn + c].  All
-    // loads are issued before the first LDS write.
+    // e % G); column sums: group b, column c = colsum[b * N + tn + c].  They
+    // are requested first, so that writing them waits for nothing else.
     const float inv_g = 1.0f / (float)G;
     const int64_t base = (int64_t)tm * G;
     const int nrow_e = min(C::BM, M - tm) * G;  // valid entries of the block
@@ -302,6 +307,11 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
                                                    : 0.0f;
     }
     const float swv = (tid < C::BN && tn + tid < N) ? fp16_bits_to_f32(w_scale[tn + tid]) : 0.0f;
+    gload(0, ra);
+    gload(1, rb);
+    // stage s > 1 waits in buffer s mod NRB
+#pragma unroll
+    for (int s2 = 2; s2 < 2 + C::NRB; ++s2) gload(s2, rgb[s2 % C::NRB]);
 #pragma unroll
     for (int p = 0; p < PE; ++p) {
       const int e = tid + C::THREADS * p;
@@ -320,17 +330,25 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     }
     if (tid < C::BN) sSW[tid] = swv;
   }
+  lstore(0, ra);
+  lstore(1, rb);
   lds_barrier();
-  uint4 pa[NPF], pb[NPF], xa[NXF], xb[NXF];
+  // With one group, FM = 2 reads each k-step's unpacked fragments two
+  // k-steps ahead (xa, xb, x2, x3 hold k-steps 0..3 of a stage); otherwise,
+  // short of registers, one ahead.
+  constexpr bool PF2 = FM == 2 && ONEG;
+  uint4 pa[NPF], pb[NPF], xa[NXF], xb[NXF], x2[NXF], x3[NXF];
   pread(0, 0, pa);
   xread(0, 0, 0, xa);
+  if constexpr (PF2) xread(0, 0, 1, xb);
 
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
   using I3 = std::integral_constant<int, 3>;
 
-  // One stage st; J = st mod 4 picks the register buffer (J even: rg0).
+  // One stage st; J = st mod 4 (which fixes the register buffer of stage
+  // st + 2, (st + 2) mod NRB).
   // FRESH marks the first stage of a group, LAST its last one (which folds).
   // Each k-step's fragments are read during the previous k-step's MFMAs; on
   // entry pa / xa hold the stage's first ones.  The body has no branches, so
@@ -339,26 +357,72 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   // that is never read again and the loads read zeros.
   auto body = [&](auto JC, auto FC, auto LC, int st) __attribute__((always_inline)) {
     constexpr int J = decltype(JC)::value;
-    v4i(&rg)[NLD] = (J % 2 == 0) ? rg0 : rg1;
+    v4i(&rg)[NLD] = rgb[(J + 2) % C::NRB];
     // ring slot of stage st + d (J = st mod 4)
     auto slot_of = [&](int d) __attribute__((always_inline)) {
       return C::NBUF == 4 ? ((J + d) & 3) : (st + d) % 3;
     };
     const int slot = slot_of(0);
-    // stage st + 2 into the slot read during stage st - 1, then the register
-    // buffer takes stage st + 4
-    lstore(slot_of(2), rg);
-    gload(st + 4, rg);
-    xread(slot, 0, 1, xb);
-    mma1(pa, xa, std::false_type{}, FC);
-    pread(slot, 1, pb);
-    xread(slot, 1, 0, xa);
-    mma1(pa, xb, std::true_type{}, std::false_type{});
-    xread(slot, 1, 1, xb);
-    mma1(pb, xa, std::false_type{}, std::false_type{});
-    pread(slot_of(1), 0, pa);  // past the last stage: stale, unused
-    xread(slot_of(1), 0, 0, xa);
-    mma1(pb, xb, std::true_type{}, std::false_type{});
+    // Four k-steps.  Stage st + 2 goes into the slot read during stage
+    // st - 2 (or st - 1 with three slots), its packed part during k-step 1
+    // and its unpacked part during k-step 2, each after that k-step's
+    // fragment reads (so that the reads do not queue behind the writes of
+    // all waves); then its register buffer takes stage st + 2 + NRB.  The
+    // scheduling barriers keep this order.
+    using LO = std::false_type;
+    using HI = std::true_type;
+    if constexpr (PF2) {  // on entry pa, xa (k-step 0) and xb (k-step 1) are loaded
+      pread(slot, 1, pb);
+      xread(slot, 1, 0, x2);
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(pa, xa, LO{}, FC);
+      xread(slot, 1, 1, x3);
+      lstore_p(slot_of(2), rg);
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(pa, xb, HI{}, LO{});
+      pread(slot_of(1), 0, pa);  // past the last stage: stale, unused
+      xread(slot_of(1), 0, 0, xa);
+      lstore_x(slot_of(2), rg);
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(pb, x2, LO{}, LO{});
+      xread(slot_of(1), 0, 1, xb);
+      gload(st + 2 + C::NRB, rg);
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(pb, x3, HI{}, LO{});
+    } else if constexpr (!ONEG) {
+      // several groups (the fold's registers are live): the stage's stores and
+      // loads first, which needs fewer registers
+      lstore(slot_of(2), rg);
+      gload(st + 2 + C::NRB, rg);
+      xread(slot, 0, 1, xb);
+      mma1(pa, xa, LO{}, FC);
+      pread(slot, 1, pb);
+      xread(slot, 1, 0, xa);
+      mma1(pa, xb, HI{}, LO{});
+      xread(slot, 1, 1, xb);
+      mma1(pb, xa, LO{}, LO{});
+      pread(slot_of(1), 0, pa);  // past the last stage: stale, unused
+      xread(slot_of(1), 0, 0, xa);
+      mma1(pb, xb, HI{}, LO{});
+    } else {  // on entry pa, xa (k-step 0) are loaded
+      xread(slot, 0, 1, xb);
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(pa, xa, LO{}, FC);
+      pread(slot, 1, pb);
+      xread(slot, 1, 0, xa);
+      lstore_p(slot_of(2), rg);
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(pa, xb, HI{}, LO{});
+      xread(slot, 1, 1, xb);
+      lstore_x(slot_of(2), rg);
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(pb, xa, LO{}, LO{});
+      pread(slot_of(1), 0, pa);  // past the last stage: stale, unused
+      xread(slot_of(1), 0, 0, xa);
+      gload(st + 2 + C::NRB, rg);
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(pb, xb, HI{}, LO{});
+    }
     if constexpr (decltype(LC)::value) {  // the group's last stage
       const int b = st >> (log2g - 7);
       if constexpr (DBG) {
