@@ -15,6 +15,12 @@ last-level cache are cycled so that every step reads from HBM.
 Prints ONE JSON line: the step throughput (integer TOP/s of the GEMM work per
 step time), per-kernel times from HIP events recorded on the launch stream,
 the roofline of the dominant kernel, and the CPU oracle timed on the host.
+
+Timed region: the K steps run kernel by kernel -- the first kernel of the
+step for steps 1..K, then the second for steps 1..K, and so on (step i's
+kernels still run in their order on step i's buffers) -- with one HIP event
+between these phases, so that each kernel's average duration is its phase
+time / K with no event between two launches of it.
 """
 
 import argparse
@@ -171,8 +177,6 @@ def main():
         if st != 0:
             raise RuntimeError(f"{what}: {_lib.status_name(st)}: {_lib.last_error()}")
 
-    kernels = {}   # name -> list of (start_event, end_event)
-    steps = []     # list of callables producing one step (each records its own events)
 
     if wl in ("attn_proj_prefill", "kv_chain"):
         cfg = inputs.WORKLOADS["attn_proj_prefill" if wl == "attn_proj_prefill" else "kv_chain_proj"]
@@ -236,53 +240,39 @@ def main():
 
     torch.cuda.synchronize()
 
-    def record(name, fn):
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        check(fn(), name)
-        b.record(stream)
-        kernels.setdefault(name, []).append((a, b))
-
-    def one_step(i, timed):
-        if wl == "kv_chain":
-            for j in range(2):
-                fn = (lambda j=j: _lib.offq_kv_quantize_raw(kv[j].data_ptr(), R, Dh, Dh, 1,
-                                                            kvo[j]["codes"].data_ptr(),
-                                                            kvo[j]["scale"].data_ptr(),
-                                                            kvo[j]["zero"].data_ptr(), None, sp))
-                if timed:
-                    record("kv_quantize", fn)
-                else:
-                    check(fn(), "kv_quantize")
-        for rq_name, mm_name, sets_ in layers:
-            s = sets_[i]
-            if timed:
-                record(rq_name, lambda: run_rq(_lib, s, sp))
-                record(mm_name, lambda: run_gemm(_lib, s, sp))
-            else:
-                check(run_rq(_lib, s, sp), rq_name)
-                check(run_gemm(_lib, s, sp), mm_name)
+    # the step's launches in order: (kernel name, launch of step i)
+    phases = []
+    if wl == "kv_chain":
+        for j in range(2):
+            phases.append(("kv_quantize", lambda i, j=j: _lib.offq_kv_quantize_raw(
+                kv[j].data_ptr(), R, Dh, Dh, 1, kvo[j]["codes"].data_ptr(), kvo[j]["scale"].data_ptr(),
+                kvo[j]["zero"].data_ptr(), None, sp)))
+    for rq_name, mm_name, sets_ in layers:
+        phases.append((rq_name, lambda i, s_=sets_: run_rq(_lib, s_[i], sp)))
+        phases.append((mm_name, lambda i, s_=sets_: run_gemm(_lib, s_[i], sp)))
 
     for i in range(args.warmup):
-        one_step(i, False)
+        for name, fn in phases:
+            check(fn(i), name)
     torch.cuda.synchronize()
-    kernels.clear()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record(stream)
-    for i in range(args.steps):
-        one_step(args.warmup + i, True)
-    t_end.record(stream)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)]
+    evs[0].record(stream)
+    for p, (name, fn) in enumerate(phases):
+        for i in range(args.steps):
+            check(fn(args.warmup + i), name)
+        evs[p + 1].record(stream)
     torch.cuda.synchronize()
-    ms = t_start.elapsed_time(t_end) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
 
     comp = {}
-    for name, evs in kernels.items():
-        times = sorted(a.elapsed_time(b) for a, b in evs)
-        us = 1000.0 * sum(times) / len(times)
-        comp[name] = {"us": round(us, 3), "us_p10": round(1000 * times[len(times) // 10], 3),
-                      "us_p90": round(1000 * times[(9 * len(times)) // 10], 3)}
+    for p, (name, fn) in enumerate(phases):
+        us = 1000.0 * evs[p].elapsed_time(evs[p + 1]) / args.steps
+        if name in comp:  # a kernel launched twice per step (K and V): per launch
+            comp[name]["us"] = round((comp[name]["us"] * comp[name]["launches"] + us) /
+                                     (comp[name]["launches"] + 1), 3)
+            comp[name]["launches"] += 1
+        else:
+            comp[name] = {"us": round(us, 3), "launches": 1}
 
     def ann_rq(name, M, K, g, n=1):
         b = rq_bytes(M, K, g) * n
