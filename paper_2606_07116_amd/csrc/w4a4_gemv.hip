@@ -40,7 +40,7 @@ constexpr int GMAX = 256;   // groups whose parameters fit in LDS
 // loads); P: waves per workgroup, each taking 1/P of K.
 template <int T, int P>
 struct GvCfg {
-  static constexpr int BATCH = 4;  // steps per batch
+  static constexpr int BATCH = T >= 4 ? 2 : 4;  // steps per batch (registers)
   static constexpr int THREADS = 64 * P;
 };
 
@@ -70,19 +70,6 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
   float* const sSZ = gpar + G * 16;      // [G][16]
   float* const sCS = gpar + G * 32;      // [G][16 T]
 
-  // group parameters of the workgroup into LDS
-  for (int i = tid; i < G * 16; i += NT) {
-    const int b = i >> 4, m = i & 15;
-    const bool ok = m < M;
-    const float s = ok ? fp16_bits_to_f32(a_scale[(int64_t)m * G + b]) : 0.0f;
-    sS[i] = s * 0.0625f;  // undoes the 16x widening of the weight codes
-    sSZ[i] = ok ? -(s * (float)a_zero[(int64_t)m * G + b]) : 0.0f;
-  }
-  for (int i = tid; i < G * 16 * T; i += NT) {
-    const int b = i / (16 * T), c = i % (16 * T);
-    sCS[i] = n0 + c < N ? (float)w_colsum[(int64_t)b * N + n0 + c] : 0.0f;
-  }
-  __syncthreads();
 
   // rows past N (weights) and past M (tokens) read as zero
   const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -161,13 +148,49 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
     }
   };
 
+  // Group parameters of the workgroup into LDS: the first PRE entries per
+  // thread are requested before the first two batches and written after
+  // them (so that the weight stream starts at once and the writes wait for
+  // the parameters only); the rest, if any, after.
+  constexpr int PRE = 4;
+  auto par_s = [&](int i, float& s, float& sz) __attribute__((always_inline)) {
+    const int b = i >> 4, m = i & 15;
+    const bool ok = m < M;
+    s = ok ? fp16_bits_to_f32(a_scale[(int64_t)m * G + b]) : 0.0f;
+    sz = ok ? -(s * (float)a_zero[(int64_t)m * G + b]) : 0.0f;
+    s *= 0.0625f;  // undoes the 16x widening of the weight codes
+  };
+  auto par_c = [&](int i) __attribute__((always_inline)) {
+    const int b = i / (16 * T), c = i % (16 * T);
+    return n0 + c < N ? (float)w_colsum[(int64_t)b * N + n0 + c] : 0.0f;
+  };
+  float ps[PRE], pz[PRE], pc[PRE];
+#pragma unroll
+  for (int p = 0; p < PRE; ++p) {
+    const int i = tid + p * NT;
+    if (i < G * 16) par_s(i, ps[p], pz[p]);
+    if (i < G * 16 * T) pc[p] = par_c(i);
+  }
   load(0, wa0, aa0);
+  if (nb > 1) load(1, wa1, aa1);
+#pragma unroll
+  for (int p = 0; p < PRE; ++p) {
+    const int i = tid + p * NT;
+    if (i < G * 16) {
+      sS[i] = ps[p];
+      sSZ[i] = pz[p];
+    }
+    if (i < G * 16 * T) sCS[i] = pc[p];
+  }
+  for (int i = tid + PRE * NT; i < G * 16; i += NT) par_s(i, sS[i], sSZ[i]);
+  for (int i = tid + PRE * NT; i < G * 16 * T; i += NT) sCS[i] = par_c(i);
+  __syncthreads();
   int bt = 0;
   for (; bt + 2 <= nb; bt += 2) {
-    load(bt + 1, wa1, aa1);
     compute(bt, wa0, aa0);
     if (bt + 2 < nb) load(bt + 2, wa0, aa0);
     compute(bt + 1, wa1, aa1);
+    if (bt + 3 < nb) load(bt + 3, wa1, aa1);
   }
   if (bt < nb) compute(bt, wa0, aa0);
   if constexpr (DBG) return;
@@ -232,13 +255,14 @@ hipError_t launch_w4a4_gemv_mfma(const uint8_t* a_codes, const uint16_t* a_scale
                                  const uint16_t* w_scale, const int32_t* w_colsum, int64_t M,
                                  int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
                                  int32_t* acc_debug, hipStream_t stream) {
-  // Two row tiles per wave (one activation load serves two weight loads) and
-  // K in quarters, measured best for 8192 and 28672 channels in either
-  // dimension; narrow layers take one tile per wave and K in eighths, for
-  // more waves in flight.
+  // K in quarters with four row tiles per wave (one activation load serves
+  // four weight loads) for wide layers (28672 channels: 448 workgroups), two
+  // for medium ones (8192 channels: 256 workgroups), as measured; narrow
+  // layers take one tile per wave and K in eighths, for more waves in flight.
 #define OFFQ_GV(T, P)                                                                         \
   return launch_gv<T, P>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, \
                          y, ldy, acc_debug, stream)
+  if (N >= 16384) OFFQ_GV(4, 4);
   if (N >= 32 * 128) OFFQ_GV(2, 4);
   OFFQ_GV(1, 8);
 #undef OFFQ_GV

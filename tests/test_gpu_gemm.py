@@ -49,9 +49,10 @@ def test_gemv_shapes(M, K, g):
     _layer(M, 200, K, g, seed=M + K)
 
 
-@pytest.mark.parametrize("N", [16, 33, 1030, 5000, 9000])
+@pytest.mark.parametrize("N", [16, 33, 1030, 5000, 9000, 16400])
 def test_gemv_channel_counts(N):
-    """Single and ragged 16-channel tiles; one, two and four tiles per wave."""
+    """Single and ragged 16-channel tiles; one, two and four tiles per wave
+    (the last with a ragged final workgroup)."""
     _layer(3, N, 4096, 512, seed=N)
 
 
