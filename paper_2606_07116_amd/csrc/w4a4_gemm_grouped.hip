@@ -20,9 +20,9 @@
 //   the activations for FM = 4) is unpacked once, when its stage is written
 //   to LDS, into two int8 planes; the other operand stays packed in LDS and
 //   is unpacked in registers by each of the two waves that read it.
-// * Stages of 128 k go global memory -> registers (two stages ahead) -> a
-//   3-deep LDS ring; one LDS-only barrier per stage.  16-byte chunks are
-//   XOR-swizzled by row so that fragment reads are conflict-free.
+// * Stages of 128 k go global memory -> registers (two or four stages ahead)
+//   -> an LDS ring of three or four slots; one LDS-only barrier per stage.
+//   16-byte chunks are XOR-swizzled by row to spread the LDS banks.
 // * Activation codes (0..15) feed the signed i8 MFMA unchanged; weight nibbles
 //   are widened to 16 q (high nibble masked, low nibble shifted), so every
 //   accumulator holds 16 acc exactly.  Both operands split each 16-byte chunk
