@@ -214,8 +214,10 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
   __shared__ __attribute__((aligned(16))) float lds[Gm::WORDS];
   __shared__ uint32_t s_lo[STATS_B ? GPT : 1];
 
-  const int lane = threadIdx.x;
-  const int64_t gbase = (int64_t)blockIdx.x * GPT;
+  // (the id builtins directly: this file's NaN/IEEE flags keep the device
+  // library's id functions from being inlined)
+  const int lane = (int)__builtin_amdgcn_workitem_id_x();
+  const int64_t gbase = (int64_t)__builtin_amdgcn_workgroup_id_x() * GPT;
   const bool full = gbase + GPT <= n_groups;
   float* const la = lds + Gm::a_base(lane);
   float* const lb = lds + Gm::b_base(lane);
@@ -224,26 +226,24 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
   // elements this lane holds in layout A.  For g >= 512 the chunk's group is
   // the same for every lane (scalar arithmetic).  Groups past the end are
   // clamped to the last one: read, never stored.
+  // With one group per row and g < 512 the tile is GPT whole rows: offsets
+  // are taken from the tile's first row (a wave-uniform base) in 32 bits
+  // (the launcher checks that GPT rows fit).
+  constexpr bool ROWS = LOGG < 9 && G1;
+  const uint16_t* const xt = ROWS ? x + gbase * ldx : x;
+  uint8_t* const ct = ROWS ? codes + gbase * ldc : codes;
   int64_t xoff[NCH], coff[NCH];
-  if constexpr (LOGG < 9 && G1) {
-    // group (= row) gbase + (ch << (9 - log2 g)) + (lane >> (log2 g - 3))
+  if constexpr (ROWS) {
+    // row gbase + (ch << (9 - log2 g)) + (lane >> (log2 g - 3)), clamped
     const int lr = lane >> (LOGG - 3);
     const int c = 8 * (lane & ((1 << (LOGG - 3)) - 1));
-    if (full) {
-      const int64_t x0 = (gbase + lr) * ldx + c, c0 = (gbase + lr) * ldc + (c >> 1);
+    const int last = (int)min<int64_t>(n_groups - 1 - gbase, GPT - 1);
 #pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        xoff[ch] = x0 + (int64_t)(ch << (9 - LOGG)) * ldx;
-        coff[ch] = c0 + (int64_t)(ch << (9 - LOGG)) * ldc;
-      }
-    } else {
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        int64_t q = gbase + (ch << (9 - LOGG)) + lr;
-        if (q >= n_groups) q = n_groups - 1;
-        xoff[ch] = q * ldx + c;
-        coff[ch] = q * ldc + (c >> 1);
-      }
+    for (int ch = 0; ch < NCH; ++ch) {
+      int r = (ch << (9 - LOGG)) + lr;
+      if (!full) r = min(r, last);
+      xoff[ch] = (uint32_t)(r * (int)ldx + c);
+      coff[ch] = (uint32_t)(r * (int)ldc + (c >> 1));
     }
   } else {
 #pragma unroll
@@ -277,7 +277,7 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
   // for the sum and the difference.
 #pragma unroll
   for (int ch = 0; ch < NCH; ++ch) {
-    uint4 d = *reinterpret_cast<const uint4*>(x + xoff[ch]);
+    uint4 d = *reinterpret_cast<const uint4*>(xt + xoff[ch]);
     const uint32_t w[4] = {d.x, d.y, d.z, d.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -316,8 +316,9 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
       if (stored(ch)) {
-        const int64_t row = xoff[ch] / ldx;
-        float* yp = ydbg + row * ldy + (xoff[ch] - row * ldx);
+        const int64_t xo = (xt - x) + xoff[ch];
+        const int64_t row = xo / ldx;
+        float* yp = ydbg + row * ldy + (xo - row * ldx);
         *reinterpret_cast<float4*>(yp) = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
         *reinterpret_cast<float4*>(yp + 4) =
             *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
@@ -417,7 +418,7 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
 #pragma unroll
     for (int j = 0; j < 8; ++j) w += __float_as_uint(v[ch * 8 + j]) << (4 * j);
     w -= corr[ch];
-    if (stored(ch)) *reinterpret_cast<uint32_t*>(codes + coff[ch]) = w;
+    if (stored(ch)) *reinterpret_cast<uint32_t*>(ct + coff[ch]) = w;
   }
 }
 
@@ -438,8 +439,11 @@ hipError_t launch_t(const uint16_t* x, int64_t n_groups, int G, int64_t ldx, boo
   hipLaunchKernelGGL((rotate_quantize_kernel<LOGG, HD, DB, G1>), grid, block, 0, stream, x, \
                      n_groups, G, dm, dsh, ldx, codes, ldc, scale, zero, ydbg, ldy,         \
                      HD ? cnorm : 1.0f)
+  // one group per row: the fast addressing when GPT rows fit in 32-bit offsets
+  const bool g1 = G == 1 && (LOGG >= 9 || (GPT * ldx < (int64_t(1) << 31) &&
+                                           GPT * ldc < (int64_t(1) << 31)));
 #define OFFQ_RQ_G(HD, DB) \
-  if (G == 1) OFFQ_RQ(HD, DB, true); else OFFQ_RQ(HD, DB, false);
+  if (g1) OFFQ_RQ(HD, DB, true); else OFFQ_RQ(HD, DB, false);
   if (had) {
     if (ydbg) { OFFQ_RQ_G(true, true) } else { OFFQ_RQ_G(true, false) }
   } else {
