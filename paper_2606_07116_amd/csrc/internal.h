@@ -21,14 +21,6 @@ hipError_t launch_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale,
                             uint16_t* y, int64_t ldy, int32_t* acc_debug,
                             hipStream_t stream);
 
-// One group per row (g == K): MFMA GEMM with 128 x 128 wave tiles.
-bool gemm_1g_supported(int64_t M, int64_t N, int64_t K);
-hipError_t launch_w4a4_gemm_1g(const uint8_t* a_codes, const uint16_t* a_scale,
-                               const int16_t* a_zero, const uint8_t* w_codes,
-                               const uint16_t* w_scale, const int32_t* w_colsum, int64_t M,
-                               int64_t N, int64_t K, uint16_t* y, int64_t ldy,
-                               int32_t* acc_debug, hipStream_t stream);
-
 // Several groups per row (g < K, g >= 128): MFMA GEMM with per-group fold.
 bool gemm_grouped_supported(int64_t M, int64_t N, int64_t K, int log2g);
 hipError_t launch_w4a4_gemm_grouped(const uint8_t* a_codes, const uint16_t* a_scale,

@@ -289,9 +289,6 @@ hipError_t launch_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale,
   if (gemm_grouped_supported(M, N, K, log2g))
     return launch_w4a4_gemm_grouped(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N,
                                     K, log2g, y, ldy, acc_debug, stream);
-  if ((K >> log2g) == 1 && gemm_1g_supported(M, N, K))
-    return launch_w4a4_gemm_1g(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, y,
-                               ldy, acc_debug, stream);
   const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   const dim3 grid((unsigned)tiles), block(256);
   const bool wide = log2g >= 13;
