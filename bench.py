@@ -48,6 +48,9 @@ def parse():
                    choices=["attn_proj_prefill", "mlp_prefill", "decode", "kv_chain"])
     p.add_argument("--decode-m", type=int, default=16)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--group-size", type=int, default=0,
+                   help="quantization group (= Hadamard block) size for every layer of the "
+                        "workload, e.g. 128 (the paper's default); 0 keeps the workload's own")
     return p.parse_args()
 
 
@@ -173,13 +176,24 @@ def main():
     sp = stream.cuda_stream
     wl = args.workload
 
+    def regroup(cfg):
+        """The workload's layer with --group-size applied (outliers then sit at
+        the first channel of each group of that size)."""
+        if not args.group_size:
+            return cfg
+        g = args.group_size
+        if g & (g - 1) or g < 64 or cfg["K"] % g:
+            raise SystemExit(f"bench.py: --group-size {g} must be a power of two >= 64 dividing K")
+        return dict(cfg, g=g)
+
     def check(st, what):
         if st != 0:
             raise RuntimeError(f"{what}: {_lib.status_name(st)}: {_lib.last_error()}")
 
 
     if wl in ("attn_proj_prefill", "kv_chain"):
-        cfg = inputs.WORKLOADS["attn_proj_prefill" if wl == "attn_proj_prefill" else "kv_chain_proj"]
+        cfg = regroup(inputs.WORKLOADS["attn_proj_prefill" if wl == "attn_proj_prefill"
+                                       else "kv_chain_proj"])
         M, K, N, g = cfg["M"], cfg["K"], cfg["N"], cfg["g"]
         spec = dict(n_outliers=cfg["n_outliers"], lo=cfg["lo"], hi=cfg["hi"])
         per_set = M * K * 2 + N * K // 2 + M * K // 2 + M * N * 2
@@ -202,8 +216,8 @@ def main():
             config.update({"kv_shape": [B, H, S, Dh], "step": "kv_quantize(K) + kv_quantize(V) + "
                            "rotate_quantize + w4a4_gemm"})
     elif wl == "mlp_prefill":
-        up = inputs.WORKLOADS["mlp_up_gate_prefill"]
-        dn = inputs.WORKLOADS["mlp_down_prefill"]
+        up = regroup(inputs.WORKLOADS["mlp_up_gate_prefill"])
+        dn = regroup(inputs.WORKLOADS["mlp_down_prefill"])
         spec_u = dict(n_outliers=up["n_outliers"], lo=up["lo"], hi=up["hi"],
                       spike_frac=up["spike_frac"], spike_mult=up["spike_mult"])
         spec_d = dict(n_outliers=dn["n_outliers"], lo=dn["lo"], hi=dn["hi"],
@@ -222,8 +236,8 @@ def main():
                   "step": "rotate_quantize + gemm(up|gate, N=28672) + rotate_quantize(g=512) + gemm(down)",
                   "input_sets": [su.n, sd.n]}
     else:  # decode
-        up = inputs.WORKLOADS["decode_up"]
-        dn = inputs.WORKLOADS["decode_down"]
+        up = regroup(inputs.WORKLOADS["decode_up"])
+        dn = regroup(inputs.WORKLOADS["decode_down"])
         Md = args.decode_m
         spec = dict(n_outliers=up["n_outliers"], lo=up["lo"], hi=up["hi"])
         per = up["N"] * up["K"] // 2 * 2

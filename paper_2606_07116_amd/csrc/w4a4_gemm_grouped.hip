@@ -50,7 +50,7 @@ namespace {
 
 using namespace gemm;
 
-template <int FM, bool ONEG>
+template <int FM, bool ONEG, bool STREAM = false>
 struct GCfg {
   static constexpr int THREADS = 512;              // 8 waves, 2 per SIMD
   static constexpr int WAVES_M = FM == 2 ? 4 : 2;
@@ -68,8 +68,11 @@ struct GCfg {
   static constexpr int KSTAGE = 128;               // k per stage
   // groups whose parameters fit in LDS; LDS ring depth (with four slots the
   // slot of every stage in a 4-stage unrolled loop is a compile-time constant)
-  static constexpr int GMAX = (FM == 2 && !ONEG) ? 28 : 1;
-  static constexpr int NBUF = (FM == 2 && ONEG) ? 4 : 3;
+  // (STREAM: any number of groups, their parameters staged with the stages
+  // through a ring of GR entries)
+  static constexpr int GMAX = (FM == 2 && !ONEG && !STREAM) ? 28 : 1;
+  static constexpr int NBUF = (FM == 2 && (ONEG || STREAM)) ? 4 : 3;
+  static constexpr int GR = STREAM ? 4 : 1;
   // stages held in registers between their global load and their LDS store:
   // the loads are issued NRB stages before the store
   static constexpr int NRB = (FM == 2 && ONEG) ? 4 : 2;
@@ -84,20 +87,28 @@ __device__ __forceinline__ int xslot(int row, int c) { return row * 8 + (c ^ ((r
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 // MODE: stages per group: 1, 2, 4, or a multiple of 8 (MODE 8).  ONEG: one
-// group per row (g = K).
-template <bool DBG, int MODE, int FM, bool ONEG>
+// group per row (g = K).  STREAM: several groups, any number of them: each
+// group's parameters travel with its stages (row scales and zero-points of
+// the tile's rows, column sums of its columns) through a small LDS ring, and
+// its zero-point term is applied right after its fold, in pairs of groups.
+template <bool DBG, int MODE, int FM, bool ONEG, bool STREAM>
 __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     const uint8_t* __restrict__ A, const uint16_t* __restrict__ a_scale,
     const int16_t* __restrict__ a_zero, const uint8_t* __restrict__ W,
     const uint16_t* __restrict__ w_scale, const int32_t* __restrict__ w_colsum, int M, int N,
     int K, int log2g, uint16_t* __restrict__ Y, int64_t ldy, int32_t* __restrict__ acc_dbg) {
-  using C = GCfg<FM, ONEG>;
+  using C = GCfg<FM, ONEG, STREAM>;
   constexpr bool XW = C::X_IS_W;
   __shared__ uint4 ring[C::NBUF * C::STAGE_SLOTS];
   // per group b: s / 16 and z of the tile's rows, colsum of its columns
   __shared__ float sRS[C::GMAX][C::BM];
   __shared__ short sZ[C::GMAX][C::BM];
   __shared__ float sCS[C::GMAX][C::BN];
+  // STREAM: per group b (entry b mod GR): s / 16 and -s z of the rows,
+  // colsum of the columns
+  __shared__ float gRS[C::GR][C::BM];
+  __shared__ float gSZ[C::GR][C::BM];
+  __shared__ float gCS[C::GR][C::BN];
   __shared__ __attribute__((aligned(16))) float sSW[C::BN];  // weight scales
 
   const int tid = threadIdx.x;
@@ -135,6 +146,7 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   constexpr int NLD = C::P_LD + C::X_LD;
   v4i rgb[C::NRB][NLD];   // stages in flight
   v4i ra[NLD], rb[NLD];    // stages 0 and 1 in the prologue
+  uint32_t gqb[C::NRB][2] = {}, gqa0[2] = {}, gqa1[2] = {};  // STREAM: their group parameters
   auto gload = [&](int st, v4i (&rg)[NLD]) __attribute__((always_inline)) {
     const bool ok = st < nst;
     const __amdgpu_buffer_rsrc_t pr = ok ? prsrc : prsrc0, xr = ok ? xrsrc : xrsrc0;
@@ -173,6 +185,45 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   auto lstore = [&](int slot, const v4i (&rg)[NLD]) __attribute__((always_inline)) {
     lstore_p(slot, rg);
     lstore_x(slot, rg);
+  };
+
+  // STREAM: the parameters of stage st's group, loaded with the stage's data
+  // (thread t < BM: scale and zero-point of row tm + t; BM <= t < BM + BN:
+  // colsum of column tn + t - BM) and stored with it.  Rows past M and
+  // columns past N read as zero.
+  const int lgs = log2g - 7;  // log2(stages per group)
+  const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a_scale + (int64_t)tm * G), 0, STREAM ? (int)((int64_t)min(C::BM, M - tm) * G * 2) : 0,
+      0x00020000);
+  const __amdgpu_buffer_rsrc_t zrsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a_zero + (int64_t)tm * G), 0, STREAM ? (int)((int64_t)min(C::BM, M - tm) * G * 2) : 0,
+      0x00020000);
+  const __amdgpu_buffer_rsrc_t crsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(w_colsum + tn), 0, STREAM ? (int)(((int64_t)G * N - tn) * 4) : 0, 0x00020000);
+  const int gt_c = tid - C::BM;  // column of a colsum thread
+  const bool g_row = tid < C::BM, g_col = gt_c >= 0 && gt_c < C::BN && tn + gt_c < N;
+  auto gload_g = [&](int st, uint32_t (&gq)[2]) __attribute__((always_inline)) {
+    if constexpr (STREAM) {
+      const int b = min(st, nst - 1) >> lgs;
+      if (g_row) {
+        gq[0] = __builtin_amdgcn_raw_buffer_load_b16(srsrc, (tid * G + b) * 2, 0, 0);
+        gq[1] = __builtin_amdgcn_raw_buffer_load_b16(zrsrc, (tid * G + b) * 2, 0, 0);
+      } else if (g_col) {
+        gq[0] = __builtin_amdgcn_raw_buffer_load_b32(crsrc, (b * N + gt_c) * 4, 0, 0);
+      }
+    }
+  };
+  auto lstore_g = [&](int st, const uint32_t (&gq)[2]) __attribute__((always_inline)) {
+    if constexpr (STREAM) {
+      const int e = (min(st, nst - 1) >> lgs) & (C::GR - 1);
+      if (g_row) {
+        const float sc = fp16_bits_to_f32((uint16_t)gq[0]);
+        gRS[e][tid] = sc * 0.0625f;
+        gSZ[e][tid] = -(sc * (float)(int16_t)gq[1]);
+      } else if (g_col) {
+        gCS[e][gt_c] = (float)(int32_t)gq[0];
+      }
+    }
   };
 
   // ---- fragments ---------------------------------------------------------------
@@ -214,7 +265,26 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   float rs[FM] = {};
   auto read_rs = [&](int b) __attribute__((always_inline)) {
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) rs[fm] = sRS[b][wm * C::WROWS + fm * 32 + fr];
+    for (int fm = 0; fm < FM; ++fm) {
+      const int r = wm * C::WROWS + fm * 32 + fr;
+      rs[fm] = STREAM ? gRS[b & (C::GR - 1)][r] : sRS[b][r];
+    }
+  };
+  // STREAM: zero-point terms of groups b0 and b0 + 1 (b0 even; a group past
+  // the last adds nothing), F += sum (-s z)[m] colsum[n], with the fp32 MFMA
+  // over k = group: lane half h supplies group b0 + h.
+  auto zp_pair = [&](int b0) __attribute__((always_inline)) {
+    const int e = b0 + h;
+    const bool ok = e < G;
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const float szv = ok ? gSZ[e & (C::GR - 1)][wm * C::WROWS + fm * 32 + fr] : 0.0f;
+#pragma unroll
+      for (int fn = 0; fn < 2; ++fn) {
+        const float csv = ok ? gCS[e & (C::GR - 1)][wn * 64 + fn * 32 + fr] : 0.0f;
+        F[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(csv, szv, F[fm][fn], 0, 0, 0);
+      }
+    }
   };
   auto fold_row = [&](int fm) __attribute__((always_inline)) {
 #pragma unroll
@@ -285,7 +355,7 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     // arrays, read coalesced (entry e = tid + 512 p is row e / G, group
     // e % G); column sums: group b, column c = colsum[b * N + tn + c].  They
     // are requested first, so that writing them waits for nothing else.
-    const float inv_g = 1.0f / (float)G;
+    const float inv_g = STREAM ? 0.0f : 1.0f / (float)G;
     const int64_t base = (int64_t)tm * G;
     const int nrow_e = min(C::BM, M - tm) * G;  // valid entries of the block
     constexpr int PE = (C::GMAX * C::BM + C::THREADS - 1) / C::THREADS;
@@ -295,7 +365,7 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
 #pragma unroll
     for (int p = 0; p < PE; ++p) {
       const int e = tid + C::THREADS * p;
-      const bool ok = e < C::BM * G && e < nrow_e;
+      const bool ok = !STREAM && e < C::BM * G && e < nrow_e;
       sv[p] = ok ? a_scale[base + e] : (uint16_t)0;
       zv[p] = ok ? a_zero[base + e] : (int16_t)0;
     }
@@ -303,19 +373,25 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
 #pragma unroll
     for (int p = 0; p < PC; ++p) {
       const int b = (C::THREADS / C::BN) * p + tid / C::BN, c = tid % C::BN;
-      cv[p] = (b < G && b < C::GMAX && tn + c < N) ? (float)w_colsum[(int64_t)b * N + tn + c]
-                                                   : 0.0f;
+      cv[p] = (!STREAM && b < G && b < C::GMAX && tn + c < N)
+                  ? (float)w_colsum[(int64_t)b * N + tn + c]
+                  : 0.0f;
     }
     const float swv = (tid < C::BN && tn + tid < N) ? fp16_bits_to_f32(w_scale[tn + tid]) : 0.0f;
     gload(0, ra);
+    gload_g(0, gqa0);
     gload(1, rb);
+    gload_g(1, gqa1);
     // stage s > 1 waits in buffer s mod NRB
 #pragma unroll
-    for (int s2 = 2; s2 < 2 + C::NRB; ++s2) gload(s2, rgb[s2 % C::NRB]);
+    for (int s2 = 2; s2 < 2 + C::NRB; ++s2) {
+      gload(s2, rgb[s2 % C::NRB]);
+      gload_g(s2, gqb[s2 % C::NRB]);
+    }
 #pragma unroll
     for (int p = 0; p < PE; ++p) {
       const int e = tid + C::THREADS * p;
-      if (e < C::BM * G) {
+      if (!STREAM && e < C::BM * G) {
         // exact: e < 2^13, and (e + 1/2) / G stays 1/(2G) away from integers
         const int r = (int)(((float)e + 0.5f) * inv_g);
         const int b = e - r * G;
@@ -326,12 +402,14 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
 #pragma unroll
     for (int p = 0; p < PC; ++p) {
       const int b = (C::THREADS / C::BN) * p + tid / C::BN;
-      if (b < G && b < C::GMAX) sCS[b][tid % C::BN] = cv[p];
+      if (!STREAM && b < G && b < C::GMAX) sCS[b][tid % C::BN] = cv[p];
     }
     if (tid < C::BN) sSW[tid] = swv;
   }
   lstore(0, ra);
+  lstore_g(0, gqa0);
   lstore(1, rb);
+  lstore_g(1, gqa1);
   lds_barrier();
   // With one group, FM = 2 reads each k-step's unpacked fragments two
   // k-steps ahead (xa, xb, x2, x3 hold k-steps 0..3 of a stage); otherwise,
@@ -358,6 +436,7 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   auto body = [&](auto JC, auto FC, auto LC, int st) __attribute__((always_inline)) {
     constexpr int J = decltype(JC)::value;
     v4i(&rg)[NLD] = rgb[(J + 2) % C::NRB];
+    uint32_t(&gq)[2] = gqb[(J + 2) % C::NRB];
     // ring slot of stage st + d (J = st mod 4)
     auto slot_of = [&](int d) __attribute__((always_inline)) {
       return C::NBUF == 4 ? ((J + d) & 3) : (st + d) % 3;
@@ -393,7 +472,9 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
       // several groups (the fold's registers are live): the stage's stores and
       // loads first, which needs fewer registers
       lstore(slot_of(2), rg);
+      lstore_g(st + 2, gq);
       gload(st + 2 + C::NRB, rg);
+      gload_g(st + 2 + C::NRB, gq);
       xread(slot, 0, 1, xb);
       mma1(pa, xa, LO{}, FC);
       pread(slot, 1, pb);
@@ -431,6 +512,9 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
         read_rs(b);
 #pragma unroll
         for (int fm = 0; fm < FM; ++fm) fold_row(fm);
+        if constexpr (STREAM) {
+          if ((b & 1) || b == G - 1) zp_pair(b & ~1);
+        }
       }
     }
     lds_barrier();
@@ -503,7 +587,7 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   for (int fm = 0; fm < FM; ++fm) {
     if constexpr (SINGLE) fold_row(fm);
     const int r = wm * C::WROWS + fm * 32 + fr;
-    for (int kk = 0; kk < (G + 1) / 2; ++kk) {
+    for (int kk = 0; kk < (STREAM ? 0 : (G + 1) / 2); ++kk) {  // (STREAM: applied per pair)
       const int b = 2 * kk + h;
       const bool ok = b < G;
       const float szv = ok ? -16.0f * sRS[b][r] * (float)sZ[b][r] : 0.0f;
@@ -552,22 +636,24 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
 }  // namespace
 
 bool gemm_grouped_supported(int64_t M, int64_t N, int64_t K, int log2g) {
-  // stages of 128 k never straddle a group; the group parameters of a tile
-  // fit in LDS; buffer offsets are 32-bit
-  return log2g >= 7 && K % 128 == 0 && (K >> log2g) <= GCfg<2, false>::GMAX &&
-         M * (K / 2) < (int64_t(1) << 31) && N * (K / 2) < (int64_t(1) << 31);
+  // stages of 128 k never straddle a group; buffer offsets (codes, and the
+  // streamed group parameters) are 32-bit
+  const int64_t G = K >> log2g;
+  return log2g >= 7 && K % 128 == 0 && M * (K / 2) < (int64_t(1) << 31) &&
+         N * (K / 2) < (int64_t(1) << 31) && G * N * 4 < (int64_t(1) << 31) &&
+         256 * G * 2 < (int64_t(1) << 31);
 }
 
-template <int FM, bool ONEG>
+template <int FM, bool ONEG, bool STREAM = false>
 hipError_t launch_g(const uint8_t* a_codes, const uint16_t* a_scale, const int16_t* a_zero,
                     const uint8_t* w_codes, const uint16_t* w_scale, const int32_t* w_colsum,
                     int64_t M, int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
                     int32_t* acc_debug, hipStream_t stream) {
-  using C = GCfg<FM, ONEG>;
+  using C = GCfg<FM, ONEG, STREAM>;
   const int64_t tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
   const dim3 grid((unsigned)tiles), block(C::THREADS);
 #define OFFQ_GG(D, MD)                                                                        \
-  hipLaunchKernelGGL((w4a4_gemm_grouped_kernel<D, MD, FM, ONEG>), grid, block, 0, stream, a_codes,  \
+  hipLaunchKernelGGL((w4a4_gemm_grouped_kernel<D, MD, FM, ONEG, STREAM>), grid, block, 0, stream, a_codes,  \
                      a_scale, a_zero, w_codes, w_scale, w_colsum, (int)M, (int)N, (int)K, log2g, \
                      y, ldy, acc_debug)
 #define OFFQ_GG_M(D)                                                                 \
@@ -595,6 +681,11 @@ hipError_t launch_w4a4_gemm_grouped(const uint8_t* a_codes, const uint16_t* a_sc
   if ((K >> log2g) == 1)
     return launch_g<2, true>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g,
                              y, ldy, acc_debug, stream);
+  // several groups: the parameters of up to 28 groups sit in LDS for the whole
+  // tile; more groups stream theirs with the stages
+  if ((K >> log2g) > GCfg<2, false>::GMAX)
+    return launch_g<2, false, true>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K,
+                                    log2g, y, ldy, acc_debug, stream);
   return launch_g<2, false>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g,
                             y, ldy, acc_debug, stream);
 }

@@ -37,6 +37,10 @@ def _layer(M, N, K, g, seed, layout="concentrated", n_out=4):
     # groups of 8 and 16 stages of 128 k; more groups than the grouped kernel
     # keeps in LDS (G = 32); g = 512 over a ragged 2-tile-row x 3-tile-column grid
     (100, 136, 4096, 1024), (77, 64, 8192, 2048), (40, 64, 4096, 128), (300, 260, 3584, 512),
+    # more groups than fit in LDS (parameters streamed with the stages): one,
+    # two, four and sixteen stages per group, an odd number of groups
+    (257, 200, 14336, 128), (300, 136, 8192, 256), (100, 520, 16384, 512),
+    (33, 130, 3712, 128), (64, 96, 65536, 2048),
 ])
 def test_gemm_shapes(M, N, K, g):
     _layer(M, N, K, g, seed=M * 7 + N)
