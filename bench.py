@@ -270,6 +270,11 @@ def main():
             check(fn(i), name)
     torch.cuda.synchronize()
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)]
+    # The GPU first spins (about 50 us per launch to come) while the host
+    # enqueues the whole timed region, so that no kernel waits for its launch
+    # call (a launch from Python takes longer than the shortest kernels here).
+    if hasattr(torch.cuda, "_sleep"):
+        torch.cuda._sleep(100_000 * len(phases) * args.steps)
     evs[0].record(stream)
     for p, (name, fn) in enumerate(phases):
         for i in range(args.steps):
