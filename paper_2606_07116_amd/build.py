@@ -69,7 +69,27 @@ def build(verbose=False):
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
+    _build_checks()
     return LIB
+
+
+CHECKS = os.path.join(ROOT, "tests", "gpu_checks")
+
+
+def _build_checks():
+    """Stand-alone GPU checks under tests/gpu_checks (one executable per
+    source, next to it), run by the GPU tests."""
+    if not os.path.isdir(CHECKS):
+        return
+    for f in sorted(os.listdir(CHECKS)):
+        if not f.endswith(".hip"):
+            continue
+        src = os.path.join(CHECKS, f)
+        exe = src[:-4]
+        cmd = [hipcc()] + [x for x in FLAGS if x != "-fPIC"] + [src, "-o", exe]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
 
 
 if __name__ == "__main__":

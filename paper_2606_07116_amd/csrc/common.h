@@ -49,18 +49,43 @@ struct QParams {
 // because every float in [2^23, 2^24) is an integer and MAGIC is even.
 #define OFFQ_MAGIC 12582912.0f
 
+// fl32(d / 15) without a division: q0 = fl(d * fl(1/15)), then one
+// correction with the exact remainder fma(-q0, 15, d) (Markstein's method for
+// a known divisor).  Equal to the IEEE quotient for every d with d / 15 in
+// [2^-25, 2^17] (checked exhaustively on the GPU by
+// tests/gpu_checks/fast_division.hip); outside that range both lie on the same
+// side of the clamp to [2^-24, 65504] in quant_params (for finite d), so the
+// clamped scale is the same.
+__device__ __forceinline__ float div15_rn(float d) {
+  const float R = 1.0f / 15.0f;
+  const float q0 = d * R;
+  const float rem = __builtin_fmaf(-q0, 15.0f, d);
+  return __builtin_fmaf(rem, R, q0);
+}
+
+// fl32(1 / s) for s an fp16 value: the hardware reciprocal refined by one
+// Newton step with fma.  Equal to the IEEE quotient for every positive finite
+// fp16 value (checked exhaustively by the same GPU test).
+__device__ __forceinline__ float rcp_fp16_rn(float s) {
+  const float r0 = __builtin_amdgcn_rcpf(s);
+  const float e = __builtin_fmaf(-s, r0, 1.0f);
+  return __builtin_fmaf(e, r0, r0);
+}
+
 __device__ __forceinline__ QParams quant_params(float mx, float mn) {
 #pragma clang fp contract(off)
   float s;
   if (mx > mn) {
-    s = (mx - mn) / 15.0f;             // IEEE fp32 division
+    // (an overflowed range is taken as the largest float: the scale clamps
+    // to 65504 either way)
+    s = div15_rn(fminf(mx - mn, 0x1.fffffep127f));
   } else {
     s = (mn != 0.0f) ? fabsf(mn) : 1.0f;
   }
   s = fminf(fmaxf(s, 0x1p-24f), 65504.0f);
   _Float16 h = (_Float16)s;            // round to nearest even
   float sq = (float)h;
-  float r = 1.0f / sq;                 // IEEE fp32 division
+  float r = rcp_fp16_rn(sq);           // = the IEEE fp32 quotient 1 / sq
   double zd = __builtin_rint(-(double)mn * (double)r);  // exact product, RNE
   zd = fmin(fmax(zd, -32768.0), 32767.0);
   int z = (int)zd;
