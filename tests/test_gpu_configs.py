@@ -111,3 +111,25 @@ def test_kv_cache_and_projection_chain():
         torch.cuda.empty_cache()
     p = W["kv_chain_proj"]
     _layer_full(p["M"], p["K"], p["N"], p["g"], p["seed"], _spec(p), sample_rows=128, acc_rows=256)
+
+
+# The paper's default group of 128 channels on every layer (32, 112 and 224
+# groups per row): full-size parity of the attention projection, the MLP down
+# projection and the decode down GEMV.
+def test_attn_proj_prefill_g128():
+    c = dict(W["attn_proj_prefill"], g=128)
+    _layer_full(c["M"], c["K"], c["N"], c["g"], c["seed"], _spec(c, "concentrated"),
+                sample_rows=256, acc_rows=130)
+
+
+def test_mlp_down_prefill_g128():
+    c = dict(W["mlp_down_prefill"], g=128)
+    _layer_full(c["M"], c["K"], c["N"], c["g"], c["seed"], _spec(c, "concentrated"),
+                sample_rows=96, acc_rows=66)
+
+
+def test_decode_down_g128():
+    c = dict(W["decode_down"], g=128)
+    wts = _weights(c["N"], c["K"], c["g"], c["seed"])
+    for M in (1, 16):
+        _layer_full(M, c["K"], c["N"], c["g"], c["seed"] + M, _spec(c), acc_rows=M, wts=wts)
