@@ -45,7 +45,8 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="attn_proj_prefill",
-                   choices=["attn_proj_prefill", "mlp_prefill", "decode", "kv_chain"])
+                   choices=["attn_proj_prefill", "mlp_prefill", "decode", "kv_chain",
+                            "kv_decode_attention"])
     p.add_argument("--decode-m", type=int, default=16)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--group-size", type=int, default=0,
@@ -63,6 +64,13 @@ def gemv_bytes(M, N, K, g):
     """Algorithmic HBM bytes of the decode GEMV (weights dominate)."""
     G = K // g
     return N * K // 2 + 2 * N + 4 * G * N + M * K // 2 + 4 * M * G + 2 * M * N
+
+
+def attn_bytes(BH, S, Dh=128):
+    """Algorithmic HBM bytes of one decode-attention step: the 4-bit K and V
+    rows of every attended position with their fp16 scale and int16 zero-point,
+    plus the bf16 query and output of each (b, h)."""
+    return BH * (S * (2 * (Dh // 2) + 2 * 4) + 2 * 2 * Dh)
 
 
 def source_hash(paths):
@@ -235,6 +243,28 @@ def main():
                   "down": [dn["M"], dn["K"], dn["N"], dn["g"]],
                   "step": "rotate_quantize + gemm(up|gate, N=28672) + rotate_quantize(g=512) + gemm(down)",
                   "input_sets": [su.n, sd.n]}
+    elif wl == "kv_decode_attention":
+        ac = inputs.WORKLOADS["kv_decode_attention"]
+        B, H, S, Dh = ac["B"], ac["H"], ac["S"], ac["Dh"]
+
+        def make_attn(i):
+            kc_, ks_, kz_ = inputs.kv4_cache_device(B, H, S, Dh, seed=ac["seed"] + 10 * i,
+                                                     device="cuda")
+            vc_, vs_, vz_ = inputs.kv4_cache_device(B, H, S, Dh, seed=ac["seed"] + 10 * i + 1,
+                                                     device="cuda")
+            q_ = torch.from_numpy(inputs.queries(B, H, Dh, seed=ac["seed"] + i)).to(
+                torch.bfloat16).cuda()
+            wsb = offq.offq_kv_attention_workspace_bytes(B, H, S)
+            return dict(q=q_, kc=kc_, ks=ks_, kz=kz_, vc=vc_, vs=vs_, vz=vz_,
+                        out=torch.empty((B, H, Dh), dtype=torch.bfloat16, device="cuda"),
+                        ws=torch.empty(wsb // 4, dtype=torch.float32, device="cuda"), wsb=wsb)
+
+        asets = Sets(make_attn, attn_bytes(B * H, S, Dh))
+        layers = []
+        work_ops = None
+        config = {"workload": wl, "kv_shape": [B, H, S, Dh], "seq_len": S,
+                  "step": "kv_attention_decode (split-sequence pass + combine pass)",
+                  "input_sets": asets.n}
     else:  # decode
         up = regroup(inputs.WORKLOADS["decode_up"])
         dn = regroup(inputs.WORKLOADS["decode_down"])
@@ -261,6 +291,14 @@ def main():
             phases.append(("kv_quantize", lambda i, j=j: _lib.offq_kv_quantize_raw(
                 kv[j].data_ptr(), R, Dh, Dh, 1, kvo[j]["codes"].data_ptr(), kvo[j]["scale"].data_ptr(),
                 kvo[j]["zero"].data_ptr(), None, sp)))
+    if wl == "kv_decode_attention":
+        def run_attn(i):
+            a_ = asets[i]
+            return _lib.offq_kv_attention_decode_raw(
+                a_["q"].data_ptr(), a_["kc"].data_ptr(), a_["ks"].data_ptr(), a_["kz"].data_ptr(),
+                a_["vc"].data_ptr(), a_["vs"].data_ptr(), a_["vz"].data_ptr(), B, H, S, S, Dh,
+                1.0 / Dh ** 0.5, 0, a_["out"].data_ptr(), a_["ws"].data_ptr(), a_["wsb"], sp)
+        phases.append(("kv_attention_decode", run_attn))
     for rq_name, mm_name, sets_ in layers:
         phases.append((rq_name, lambda i, s_=sets_: run_rq(_lib, s_[i], sp)))
         phases.append((mm_name, lambda i, s_=sets_: run_gemm(_lib, s_[i], sp)))
@@ -329,6 +367,18 @@ def main():
                 "unit": "TOP/s", "frac": comp[dom]["frac_int8_peak"],
                 "traffic": traffic_for(f"w4a4_gemm:{wl}"), "kernel": dom,
                 "alg_ops_per_launch": comp[dom]["alg_ops"], "avg_launch_us": comp[dom]["us"]}
+    elif wl == "kv_decode_attention":
+        name = "kv_attention_decode"
+        b_ = attn_bytes(B * H, S, Dh)
+        comp[name]["alg_bytes"] = b_
+        comp[name]["GBs"] = round(b_ / (comp[name]["us"] * 1e-6) / 1e9, 1)
+        comp[name]["frac_hbm"] = round(comp[name]["GBs"] / PEAK_HBM_GBS, 4)
+        value = comp[name]["GBs"]
+        unit = "GB/s"
+        roof = {"bound": "hbm", "achieved": comp[name]["GBs"], "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": comp[name]["frac_hbm"],
+                "traffic": traffic_for("kv_attention:kv_decode_attention"), "kernel": name,
+                "alg_bytes_per_launch": b_, "avg_launch_us": comp[name]["us"]}
     else:
         ann_rq("rotate_quantize_up", Md, up["K"], up["g"])
         ann_rq("rotate_quantize_down", Md, dn["K"], dn["g"])

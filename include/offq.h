@@ -163,6 +163,45 @@ int offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g,
                       uint8_t* w_codes, uint16_t* w_scale, int32_t* w_colsum,
                       void* stream);
 
+/*
+ * offq_kv_attention_decode -- one decode step of attention over the 4-bit KV
+ * cache written by offq_kv_quantize (sec. 3.3 step 2(2)/(3), sec. 4.2): keys
+ * rotated by the per-head Hadamard H3 before quantization (apply_hadamard = 1),
+ * values either rotated offline by R2 (apply_hadamard = 0; the output then
+ * stays in that basis, which the output projection undoes) or by H3
+ * (v_hadamard = 1: the output is rotated back).  For every (b, h), with
+ * c = fl32(1/sqrt(128)) and H the 128-point Sylvester Hadamard matrix:
+ *
+ *     q_r[d] = bf16_rne(c * sum_i q[i] H[i][d])      (fp32 sum)
+ *     s_j    = sm_scale * sk_j * sum_d q_r[d] (ck_j[d] - zk_j)     0 <= j < seq_len
+ *     p      = softmax(s)
+ *     o[d]   = sum_j p_j * sv_j * (cv_j[d] - zv_j);  if v_hadamard: o = c H o
+ *     out    = bf16_rne(o)
+ *
+ *   q            bf16 [B, H, 128] contiguous (the query after RoPE).
+ *   k_codes      uint8 [B, H, s_cap, 64], 16-byte aligned; k_scale fp16 and
+ *                k_zero int16 [B, H, s_cap] (rows (b, h, j) of offq_kv_quantize
+ *                with head_dim = 128).  v_codes, v_scale, v_zero likewise
+ *                (v_codes 4-byte aligned).
+ *   seq_len      positions in use, 1 <= seq_len <= s_cap.
+ *   sm_scale     score scale (1/sqrt(128) for standard attention).
+ *   out          bf16 [B, H, 128].
+ *   workspace    caller-owned device buffer of at least
+ *                offq_kv_attention_workspace_bytes(B, H, seq_len) bytes,
+ *                4-byte aligned; its contents are scratch.  Calls that share
+ *                a workspace must be ordered on one stream.
+ * head_dim is 128; other sizes return OFFQ_ERR_UNSUPPORTED.
+ */
+int offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,
+                             const int16_t* k_zero, const uint8_t* v_codes,
+                             const uint16_t* v_scale, const int16_t* v_zero, int64_t B,
+                             int64_t H, int64_t s_cap, int64_t seq_len, int32_t head_dim,
+                             float sm_scale, int32_t v_hadamard, uint16_t* out, void* workspace,
+                             int64_t workspace_bytes, void* stream);
+
+/* Bytes of workspace offq_kv_attention_decode needs (0 for invalid sizes). */
+int64_t offq_kv_attention_workspace_bytes(int64_t B, int64_t H, int64_t seq_len);
+
 #ifdef __cplusplus
 }
 #endif

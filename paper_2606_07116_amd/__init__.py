@@ -7,6 +7,7 @@ arguments.  Entry points (same names as ``include/offq.h``):
     offq_w4a4_gemm(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, g, debug=False)
     offq_kv_quantize(kv, apply_hadamard=True, debug=False)
     offq_pack_weights(w, g)
+    offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, seq_len, ...)
 
 Importing the package loads the library and raises if it has not been built.
 """
@@ -16,6 +17,8 @@ from ._lib import (  # noqa: F401
     EXPORTED,
     OffqError,
     last_error,
+    offq_kv_attention_decode,
+    offq_kv_attention_workspace_bytes,
     offq_kv_quantize,
     offq_pack_weights,
     offq_rotate_quantize,

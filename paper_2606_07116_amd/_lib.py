@@ -28,6 +28,8 @@ EXPORTED = (
     "offq_w4a4_gemm",
     "offq_kv_quantize",
     "offq_pack_weights",
+    "offq_kv_attention_decode",
+    "offq_kv_attention_workspace_bytes",
 )
 
 
@@ -40,7 +42,7 @@ class OffqError(RuntimeError):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
-            f"{LIB_PATH} is missing: build it with `python -m paper_2606_07116_amd.build` "
+            f"{LIB_PATH} is missing: build it with `python paper_2606_07116_amd/build.py` "
             "(there is no non-HIP fallback)")
     # torch ships its own HIP runtime (SONAME libamdhip64.so.7).  Import it
     # first so that the library binds to that same runtime: a second runtime in
@@ -63,6 +65,11 @@ def _load():
     lib.offq_kv_quantize.argtypes = [vp, i64, i32, i64, i32, vp, vp, vp, vp, vp]
     lib.offq_pack_weights.restype = ctypes.c_int
     lib.offq_pack_weights.argtypes = [vp, i64, i64, i32, vp, vp, vp, vp]
+    lib.offq_kv_attention_decode.restype = ctypes.c_int
+    lib.offq_kv_attention_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i32,
+                                             ctypes.c_float, i32, vp, vp, i64, vp]
+    lib.offq_kv_attention_workspace_bytes.restype = i64
+    lib.offq_kv_attention_workspace_bytes.argtypes = [i64, i64, i64]
     return lib
 
 
@@ -102,6 +109,18 @@ def offq_kv_quantize_raw(kv, rows, head_dim, row_stride, apply_hadamard, codes, 
 
 def offq_pack_weights_raw(w, N, K, g, w_codes, w_scale, w_colsum, stream):
     return lib.offq_pack_weights(w, N, K, g, w_codes, w_scale, w_colsum, stream)
+
+
+def offq_kv_attention_decode_raw(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B, H, s_cap,
+                                 seq_len, head_dim, sm_scale, v_hadamard, out, workspace,
+                                 workspace_bytes, stream):
+    return lib.offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B, H,
+                                        s_cap, seq_len, head_dim, sm_scale, v_hadamard, out,
+                                        workspace, workspace_bytes, stream)
+
+
+def offq_kv_attention_workspace_bytes(B, H, seq_len):
+    return lib.offq_kv_attention_workspace_bytes(B, H, seq_len)
 
 
 # ------------------------------------------------------------ tensor wrappers
@@ -216,3 +235,48 @@ def offq_pack_weights(w, g):
     _check(lib.offq_pack_weights(_ptr(w), N, K, int(g), _ptr(wc), _ptr(ws), _ptr(cs), _stream()),
            "offq_pack_weights")
     return wc, ws, cs
+
+
+def offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, seq_len,
+                             sm_scale=None, v_hadamard=False, out=None, workspace=None):
+    """One decode step of attention over the 4-bit cache.
+
+    q: bf16 [B, H, 128]; k_codes / v_codes: u8 [B, H, s_cap, 64];
+    k_scale / v_scale: fp16 [B, H, s_cap]; k_zero / v_zero: int16 [B, H, s_cap]
+    (all contiguous).  Positions 0 .. seq_len-1 are attended.  sm_scale
+    defaults to 1/sqrt(128).  Returns out bf16 [B, H, 128]."""
+    torch = _torch()
+    _need(q, torch.bfloat16, "q", 3)
+    for t, dt, n in ((k_codes, torch.uint8, "k_codes"), (v_codes, torch.uint8, "v_codes")):
+        _need(t, dt, n, 4)
+    for t, dt, n in ((k_scale, torch.float16, "k_scale"), (v_scale, torch.float16, "v_scale"),
+                     (k_zero, torch.int16, "k_zero"), (v_zero, torch.int16, "v_zero")):
+        _need(t, dt, n, 3)
+    for t, n in ((q, "q"), (k_codes, "k_codes"), (k_scale, "k_scale"), (k_zero, "k_zero"),
+                 (v_codes, "v_codes"), (v_scale, "v_scale"), (v_zero, "v_zero")):
+        if not t.is_contiguous():
+            raise ValueError(f"{n} must be contiguous")
+    B, H, Dh = q.shape
+    s_cap = k_codes.shape[2]
+    if k_codes.shape != (B, H, s_cap, Dh // 2) or v_codes.shape != k_codes.shape \
+            or k_scale.shape != (B, H, s_cap) or k_zero.shape != (B, H, s_cap) \
+            or v_scale.shape != (B, H, s_cap) or v_zero.shape != (B, H, s_cap):
+        raise ValueError("operand shapes do not match")
+    if sm_scale is None:
+        sm_scale = 1.0 / float(Dh) ** 0.5
+    dev = q.device
+    if out is None:
+        out = torch.empty((B, H, Dh), dtype=torch.bfloat16, device=dev)
+    _need(out, torch.bfloat16, "out", 3)
+    if not out.is_contiguous() or out.shape != (B, H, Dh):
+        raise ValueError("out must be a contiguous [B, H, head_dim] tensor")
+    need = lib.offq_kv_attention_workspace_bytes(B, H, int(seq_len))
+    if workspace is None:
+        workspace = torch.empty((max(need, 4) + 3) // 4, dtype=torch.float32, device=dev)
+    _need(workspace, torch.float32, "workspace", 1)
+    _check(lib.offq_kv_attention_decode(_ptr(q), _ptr(k_codes), _ptr(k_scale), _ptr(k_zero),
+                                        _ptr(v_codes), _ptr(v_scale), _ptr(v_zero), B, H, s_cap,
+                                        int(seq_len), Dh, float(sm_scale), int(bool(v_hadamard)),
+                                        _ptr(out), _ptr(workspace), workspace.numel() * 4,
+                                        _stream()), "offq_kv_attention_decode")
+    return out

@@ -1,6 +1,6 @@
 """Build liboffq.so (HIP, gfx950) in-tree.
 
-    python -m paper_2606_07116_amd.build
+    python paper_2606_07116_amd/build.py
 
 Compiles every ``csrc/*.hip`` with hipcc for gfx950 and links them into
 ``paper_2606_07116_amd/liboffq.so``.  Packed-fp32 VALU instructions are

@@ -48,4 +48,13 @@ hipError_t launch_pack_weights(const float* w, int64_t N, int64_t K, int log2g,
                                uint8_t* w_codes, uint16_t* w_scale,
                                int32_t* w_colsum, hipStream_t stream);
 
+// One decode step of attention over the 4-bit KV cache (head_dim 128).
+int64_t kv_attention_workspace_floats(int64_t BH, int64_t seq_len);
+hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
+                                      const uint16_t* k_scale, const int16_t* k_zero,
+                                      const uint8_t* v_codes, const uint16_t* v_scale,
+                                      const int16_t* v_zero, int64_t BH, int64_t S_cap,
+                                      int64_t seq_len, float sm_scale, bool v_hadamard,
+                                      uint16_t* out, float* workspace, hipStream_t stream);
+
 }  // namespace offq

@@ -181,3 +181,44 @@ int offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g, uint8_t* 
 }
 
 }  // extern "C"
+
+int64_t offq_kv_attention_workspace_bytes(int64_t B, int64_t H, int64_t seq_len) {
+  if (B <= 0 || H <= 0 || seq_len <= 0 || B * H > (1 << 24) || seq_len > (int64_t(1) << 30))
+    return 0;
+  return offq::kv_attention_workspace_floats(B * H, seq_len) * (int64_t)sizeof(float);
+}
+
+int offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,
+                             const int16_t* k_zero, const uint8_t* v_codes,
+                             const uint16_t* v_scale, const int16_t* v_zero, int64_t B,
+                             int64_t H, int64_t s_cap, int64_t seq_len, int32_t head_dim,
+                             float sm_scale, int32_t v_hadamard, uint16_t* out, void* workspace,
+                             int64_t workspace_bytes, void* stream) {
+  if (B <= 0 || H <= 0) return fail(OFFQ_ERR_INVALID, "need B > 0 and H > 0");
+  if (head_dim != 128) return fail(OFFQ_ERR_UNSUPPORTED, "head_dim = %d (only 128)", head_dim);
+  if (seq_len < 1 || seq_len > s_cap)
+    return fail(OFFQ_ERR_INVALID, "need 1 <= seq_len <= s_cap");
+  if (B * H > (1 << 24) || seq_len > (int64_t(1) << 30) || s_cap > (int64_t(1) << 40) / (B * H) ||
+      B * H * ((seq_len + 1023) / 1024) > (1 << 24))
+    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large (B H ceil(seq_len / 1024) <= 2^24)");
+  if (v_hadamard != 0 && v_hadamard != 1) return fail(OFFQ_ERR_INVALID, "v_hadamard must be 0 or 1");
+  if (!(sm_scale == sm_scale)) return fail(OFFQ_ERR_INVALID, "sm_scale is NaN");
+  if (!q || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale || !v_zero || !out ||
+      !workspace)
+    return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(q, 2) || !aligned(k_codes, 16) || !aligned(v_codes, 4) || !aligned(k_scale, 2) ||
+      !aligned(k_zero, 2) || !aligned(v_scale, 2) || !aligned(v_zero, 2) || !aligned(out, 2) ||
+      !aligned(workspace, 4))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (k_codes: 16 B; v_codes, workspace: 4 B)");
+  const int64_t need = offq_kv_attention_workspace_bytes(B, H, seq_len);
+  if (workspace_bytes < need)
+    return fail(OFFQ_ERR_INVALID, "workspace of %lld bytes, need %lld", (long long)workspace_bytes,
+                (long long)need);
+  if (int st = check_device()) return st;
+  return launched(offq::launch_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale,
+                                                   v_zero, B * H, s_cap, seq_len, sm_scale,
+                                                   v_hadamard != 0, out,
+                                                   static_cast<float*>(workspace),
+                                                   (hipStream_t)stream),
+                  "kv_attention_decode");
+}

@@ -138,13 +138,13 @@ __device__ __forceinline__ void stages_B(float* v, float c) {
   stage_B<LOGE, LOGG, SCALED, 5>(v, c);
 }
 
-// a.lo * b.lo + a.hi * b.hi for two packed bf16 pairs, fp32 result.  The
-// three-operand encoding with an inline zero addend avoids the accumulator
-// copy that the two-operand form would need.
+// a.lo * b.lo + a.hi * b.hi for two packed bf16 pairs, fp32 result.  Through
+// the builtin, not inline asm: a VALU that reads a dot result within a few
+// cycles needs wait states that only the compiler's hazard tracking inserts.
+typedef __bf16 rq_bf16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b) {
-  float r;
-  asm("v_dot2_f32_bf16 %0, %1, %2, 0" : "=v"(r) : "v"(a), "s"(b));
-  return r;
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(rq_bf16x2, a),
+                                         __builtin_bit_cast(rq_bf16x2, b), 0.0f, false);
 }
 
 template <int CTRL>

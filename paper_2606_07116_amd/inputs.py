@@ -50,6 +50,7 @@ WORKLOADS = {
                         lo=50.0, hi=200.0, seed=44),
     "kv_cache": dict(B=8, H=32, S=32768, Dh=128, n_outliers=2, lo=20.0, hi=80.0,
                      seed=5),
+    "kv_decode_attention": dict(B=8, H=32, S=32768, Dh=128, seed=6),
     "kv_chain_proj": dict(M=8192, K=4096, N=4096, g=4096, n_outliers=4,
                           lo=50.0, hi=200.0, seed=55),
 }
@@ -152,6 +153,43 @@ def kv_cache_device(B, H, S, Dh, *, seed, device, n_outliers=2, lo=20.0, hi=80.0
         for d, v in zip(dims, vals):
             x[:, h, :, int(d)] += float(v)
     return x.to(torch.bfloat16)
+
+
+def kv4_cache(B, H, S, Dh, *, seed, s_lo=0.05, s_hi=0.6, z_lo=3, z_hi=12):
+    """Host 4-bit cache in the layout the KV quantizer writes: packed code bytes
+    uint8 [B, H, S, Dh/2] (both nibbles uniform on 0..15), fp16 scales
+    [B, H, S] ~ U(s_lo, s_hi) and int16 zero-points [B, H, S] uniform on
+    z_lo..z_hi.  Drawn directly (no rotation or quantization happens here): a
+    Hadamard-rotated row spans its 16 levels around a zero-point near the
+    middle of the grid."""
+    rng = np.random.Generator(np.random.PCG64(seed + 7000))
+    codes = rng.integers(0, 256, size=(B, H, S, Dh // 2), dtype=np.uint8)
+    scale = rng.uniform(s_lo, s_hi, size=(B, H, S)).astype(np.float16)
+    zero = rng.integers(z_lo, z_hi + 1, size=(B, H, S)).astype(np.int16)
+    return codes, scale, zero
+
+
+def kv4_cache_device(B, H, S, Dh, *, seed, device, s_lo=0.05, s_hi=0.6, z_lo=3, z_hi=12):
+    """Device version of ``kv4_cache`` (same distributions, torch's device RNG)."""
+    import torch
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed + 7000)
+    codes = torch.randint(0, 256, (B, H, S, Dh // 2), generator=gen, device=device,
+                          dtype=torch.uint8)
+    scale = (torch.rand((B, H, S), generator=gen, device=device) * (s_hi - s_lo) + s_lo
+             ).to(torch.float16)
+    zero = torch.randint(z_lo, z_hi + 1, (B, H, S), generator=gen, device=device,
+                         dtype=torch.int16)
+    return codes, scale, zero
+
+
+def queries(B, H, Dh, *, seed, std=1.0):
+    """Host decode queries [B, H, Dh] ~ N(0, std^2), rounded to bfloat16
+    (fp32 numpy holding the bf16 values)."""
+    rng = np.random.Generator(np.random.PCG64(seed + 9000))
+    q = rng.standard_normal((B, H, Dh), dtype=np.float32) * np.float32(std)
+    return round_to_bf16(q)
 
 
 def kv_rows(R, Dh, *, seed, n_outliers=2, lo=20.0, hi=80.0, heads=4):

@@ -107,3 +107,40 @@ def test_valid_call_without_gpu_reports_hip_error():
         pytest.skip("a GPU is present")
     st = _lib.offq_rotate_quantize_raw(P, 4, 256, 256, 256, 1, P, P, P, None, None)
     assert st == _lib.OFFQ_ERR_HIP
+
+
+@pytest.mark.parametrize("args,expect", [
+    # (B, H, s_cap, seq_len, head_dim, sm_scale, v_had, workspace_bytes)
+    ((2, 4, 100, 0, 128, 0.1, 0, 1 << 20), _lib.OFFQ_ERR_INVALID),        # seq_len = 0
+    ((2, 4, 100, 101, 128, 0.1, 0, 1 << 20), _lib.OFFQ_ERR_INVALID),      # seq_len > s_cap
+    ((2, 4, 100, 100, 64, 0.1, 0, 1 << 20), _lib.OFFQ_ERR_UNSUPPORTED),   # head_dim 64
+    ((0, 4, 100, 100, 128, 0.1, 0, 1 << 20), _lib.OFFQ_ERR_INVALID),      # B = 0
+    ((2, 4, 100, 100, 128, 0.1, 2, 1 << 20), _lib.OFFQ_ERR_INVALID),      # bad flag
+    ((2, 4, 100, 100, 128, float("nan"), 0, 1 << 20), _lib.OFFQ_ERR_INVALID),
+    ((2, 4, 2048, 2048, 128, 0.1, 0, 8 * 2 * 130 * 4 - 4), _lib.OFFQ_ERR_INVALID),  # small ws
+    ((1 << 12, 1 << 12, 1 << 20, 1 << 20, 128, 0.1, 0, 1 << 60), _lib.OFFQ_ERR_UNSUPPORTED),
+])
+def test_kv_attention_validation(args, expect):
+    B, H, s_cap, seq_len, dh, sm, vh, wsb = args
+    st = _lib.offq_kv_attention_decode_raw(P, P, P, P, P, P, P, B, H, s_cap, seq_len, dh, sm, vh, P,
+                                           P, wsb, None)
+    assert st == expect, _lib.last_error()
+    assert _lib.last_error()
+
+
+def test_kv_attention_misaligned_and_null():
+    args = [P] * 7 + [2, 4, 100, 100, 128, 0.1, 0, P, P, 1 << 20, None]
+    for i, bad in ((1, P + 4), (4, P + 2), (0, None), (15, None)):
+        a = list(args)
+        a[i] = bad
+        assert _lib.offq_kv_attention_decode_raw(*a) == _lib.OFFQ_ERR_INVALID, i
+
+
+def test_kv_attention_workspace_bytes():
+    # one record of 2 + 128 floats per (b, h, chunk of 1024 positions)
+    assert _lib.offq_kv_attention_workspace_bytes(2, 4, 1) == 8 * 130 * 4
+    assert _lib.offq_kv_attention_workspace_bytes(2, 4, 1024) == 8 * 130 * 4
+    assert _lib.offq_kv_attention_workspace_bytes(2, 4, 1025) == 8 * 2 * 130 * 4
+    assert _lib.offq_kv_attention_workspace_bytes(8, 32, 32768) == 256 * 32 * 130 * 4
+    assert _lib.offq_kv_attention_workspace_bytes(0, 4, 10) == 0
+    assert _lib.offq_kv_attention_workspace_bytes(1, 1, 0) == 0

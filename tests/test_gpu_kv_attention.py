@@ -1,0 +1,156 @@
+"""GPU parity: decode attention over the 4-bit KV cache (offq_kv_attention_decode)
+vs the oracle (oracle/attention.py).
+
+Tolerance (fp32 kernel against the exact fp64 result, then one bf16 rounding):
+  |out - ref| <= 2^-8 (1 + 2^-5) |ref| + 2^-11 E,
+  E = sum_j p_j max_d |V_j[d]|  (the magnitude of the weighted value rows).
+The first term is the final bf16 rounding (unit roundoff 2^-8); the second covers the fp32 score
+dot products (about 2^-24 times sums of magnitude 128 sum|q_r| per position,
+relative score errors near 1e-5 that move p by as much), the fp32 value sums
+and, with the value rotation, an fp32 128-point transform -- each at least
+ten times below 2^-11 E.  A dropped or doubled position, a wrong zero-point or
+scale, a misplaced dimension or a missing rescale of a chunk is far above it
+at the small sizes these tests use.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_07116_amd as offq
+from oracle import attention as OA
+from paper_2606_07116_amd import inputs
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+SM = 1.0 / math.sqrt(128.0)
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(P.DEV)
+
+
+def _magnitude(q, kc, ks, kz, vc, vs, vz, seq_len, sm):
+    qr = OA.rotate_query(q)
+    k = OA.dequantize_rows(kc[:, :, :seq_len], ks[:, :, :seq_len], kz[:, :, :seq_len])
+    p = OA.softmax(sm * np.einsum("bhd,bhsd->bhs", qr, k))
+    v = OA.dequantize_rows(vc[:, :, :seq_len], vs[:, :, :seq_len], vz[:, :, :seq_len])
+    return np.einsum("bhs,bhs->bh", p, np.abs(v).max(axis=-1))[..., None]
+
+
+def check(out, ref, mag):
+    out = out.astype(np.float64)
+    tol = 2.0 ** -8 * (1 + 2.0 ** -5) * np.abs(ref) + 2.0 ** -11 * mag
+    err = np.abs(out - ref)
+    bad = err > tol
+    assert not bad.any(), (
+        f"attention output mismatch at {np.argwhere(bad)[:5].tolist()} (of {bad.sum()}): "
+        f"gpu {out[bad][:5]} ref {ref[bad][:5]} tol {np.broadcast_to(tol, bad.shape)[bad][:5]}")
+
+
+def _run_host_case(B, H, S, seq_len, sm, v_had, seed, poison=True):
+    q = inputs.queries(B, H, 128, seed=seed)
+    kc, ks, kz = inputs.kv4_cache(B, H, S, 128, seed=seed)
+    vc, vs, vz = inputs.kv4_cache(B, H, S, 128, seed=seed + 1)
+    if poison and seq_len < S:
+        # past seq_len: codes that would dominate every score and huge values
+        kc[:, :, seq_len:] = 0xFF
+        ks[:, :, seq_len:] = np.float16(60000.0)
+        kz[:, :, seq_len:] = -30000
+        vs[:, :, seq_len:] = np.float16(60000.0)
+    out = offq.offq_kv_attention_decode(P.to_dev_bf16(q), _dev(kc), _dev(ks), _dev(kz), _dev(vc),
+                                        _dev(vs), _dev(vz), seq_len, sm_scale=sm,
+                                        v_hadamard=v_had)
+    torch.cuda.synchronize()
+    got = P.host(out.float())
+    ref = OA.decode_attention(q, kc, ks, kz, vc, vs, vz, seq_len, sm, v_hadamard=v_had)
+    mag = _magnitude(q, kc, ks, kz, vc, vs, vz, seq_len, sm)
+    check(got, ref, mag)
+    return out
+
+
+@pytest.mark.parametrize("v_had", [False, True])
+@pytest.mark.parametrize("B,H,S,seq_len", [
+    (1, 1, 1, 1), (1, 2, 64, 37), (2, 3, 1024, 1024), (1, 2, 3000, 2049), (2, 2, 5000, 4097),
+    (1, 1, 8192, 8192), (3, 1, 1100, 1025), (1, 4, 2048, 1023),
+])
+def test_attention_shapes(B, H, S, seq_len, v_had):
+    _run_host_case(B, H, S, seq_len, SM, v_had, seed=B * 100 + H * 10 + seq_len)
+
+
+@pytest.mark.parametrize("sm", [0.02, 0.5, 4.0])
+def test_attention_score_scales(sm):
+    """Flat to very peaked softmax (sm = 4: one or two positions dominate)."""
+    _run_host_case(2, 2, 3000, 2500, sm, False, seed=int(sm * 100))
+
+
+def test_attention_deterministic_and_out_buffer():
+    B, H, S = 2, 2, 2100
+    q = inputs.queries(B, H, 128, seed=4)
+    kc, ks, kz = inputs.kv4_cache(B, H, S, 128, seed=4)
+    vc, vs, vz = inputs.kv4_cache(B, H, S, 128, seed=5)
+    args = [P.to_dev_bf16(q)] + [_dev(a) for a in (kc, ks, kz, vc, vs, vz)]
+    out = torch.full((B, H, 128), 3.0, dtype=torch.bfloat16, device=P.DEV)
+    ws = torch.empty(offq.offq_kv_attention_workspace_bytes(B, H, S) // 4, dtype=torch.float32,
+                     device=P.DEV)
+    r1 = offq.offq_kv_attention_decode(*args, S, out=out, workspace=ws)
+    assert r1.data_ptr() == out.data_ptr()
+    a = out.clone()
+    offq.offq_kv_attention_decode(*args, S, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(a, out)
+
+
+def test_attention_workspace_too_small_raises():
+    B, H, S = 1, 1, 2048
+    q = torch.zeros((B, H, 128), dtype=torch.bfloat16, device=P.DEV)
+    c = torch.zeros((B, H, S, 64), dtype=torch.uint8, device=P.DEV)
+    s = torch.ones((B, H, S), dtype=torch.float16, device=P.DEV)
+    z = torch.zeros((B, H, S), dtype=torch.int16, device=P.DEV)
+    ws = torch.empty(130, dtype=torch.float32, device=P.DEV)  # one chunk; two are needed
+    with pytest.raises(offq.OffqError):
+        offq.offq_kv_attention_decode(q, c, s, z, c, s, z, S, workspace=ws)
+
+
+def test_attention_quantized_cache_chain():
+    """Cache rows written by the oracle's KV quantizer (rotated keys with the
+    codes 0 and 15 present in every row), attended on the GPU."""
+    from oracle import kv as OKV
+    from oracle import quantizer as OQ
+    B, H, S, seq_len = 1, 4, 1500, 1400
+    rows = inputs.kv_rows(B * H * S * 2, 128, seed=8, heads=H)
+    k_rows, v_rows = rows[: B * H * S], rows[B * H * S:]
+    kq, ks, kz = OKV.kv_quantize(OKV.kv_rotate(k_rows, True).astype(np.float32))
+    vq, vs, vz = OKV.kv_quantize(OKV.kv_rotate(v_rows, False).astype(np.float32))
+    shp = (B, H, S)
+    kc, vc = OQ.pack_nibbles(kq).reshape(shp + (64,)), OQ.pack_nibbles(vq).reshape(shp + (64,))
+    ks, kz, vs, vz = (a.reshape(shp) for a in (ks, kz, vs, vz))
+    q = inputs.queries(B, H, 128, seed=8)
+    out = offq.offq_kv_attention_decode(P.to_dev_bf16(q), _dev(kc), _dev(ks), _dev(kz), _dev(vc),
+                                        _dev(vs), _dev(vz), seq_len)
+    torch.cuda.synchronize()
+    ref = OA.decode_attention(q, kc, ks, kz, vc, vs, vz, seq_len, SM)
+    check(P.host(out.float()), ref, _magnitude(q, kc, ks, kz, vc, vs, vz, seq_len, SM))
+
+
+@pytest.mark.parametrize("seq_len", [32768, 30001])
+def test_attention_full_size_sampled(seq_len):
+    """[8, 32, 32768, 128] cache (the decode-attention workload, one launch as
+    timed by the benchmark); eight (b, h) heads checked against the oracle."""
+    cfg = inputs.WORKLOADS["kv_decode_attention"]
+    B, H, S = cfg["B"], cfg["H"], cfg["S"]
+    kc, ks, kz = inputs.kv4_cache_device(B, H, S, 128, seed=cfg["seed"], device=P.DEV)
+    vc, vs, vz = inputs.kv4_cache_device(B, H, S, 128, seed=cfg["seed"] + 1, device=P.DEV)
+    q = inputs.queries(B, H, 128, seed=cfg["seed"])
+    out = offq.offq_kv_attention_decode(P.to_dev_bf16(q), kc, ks, kz, vc, vs, vz, seq_len)
+    torch.cuda.synchronize()
+    got = P.host(out.float())
+    rng = np.random.Generator(np.random.PCG64(seq_len))
+    for _ in range(8):
+        b, h = int(rng.integers(B)), int(rng.integers(H))
+        sel = [P.host(t[b:b + 1, h:h + 1, :seq_len]) for t in (kc, ks, kz, vc, vs, vz)]
+        qq = q[b:b + 1, h:h + 1]
+        ref = OA.decode_attention(qq, *sel, seq_len, SM)
+        check(got[b:b + 1, h:h + 1], ref, _magnitude(qq, *sel, seq_len, SM))
