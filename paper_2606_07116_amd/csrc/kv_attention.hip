@@ -8,56 +8,73 @@
 // step 2(2)), which the output projection undoes, or, if they were quantized
 // with the online Hadamard as well, the output is rotated back by H3.
 //
-//   q_r  = bf16_rne(c * H q)                         c = fl32(1 / sqrt(128))
+//   q_r  = bf16_rne(fl32(c * fl32(H q)))             c = fl32(1 / sqrt(128))
 //   s_j  = sm_scale * sk_j * sum_d q_r[d] (ck_j[d] - zk_j)
 //   p    = softmax_j(s)
-//   o[d] = sum_j p_j * sv_j * (cv_j[d] - zv_j)       (then c * H o if asked)
+//   o[d] = sum_j w_j (cv_j[d] - zv_j) / sum_j p_j,   w_j = fp16(p_j sv_j)
+//   (then c * H o if asked)
+//
+// The work is HBM-bound (136 bytes per position and head) and unpacking the
+// 4-bit codes is what costs VALU time, so the kernel is built around
+// unpacking with as few instructions as possible:
+// * a 4-bit code c masked in place inside a 16-bit half is the fp16
+//   subnormal c 2^-24 (or 16 c 2^-24 for the high nibble of a byte); its
+//   products with fp16 operands are exact in fp32, so v_dot2_f32_f16 takes
+//   two codes per instruction straight from one AND of the code word, with
+//   no offset and no conversion;
+// * scores: the rotated query, scaled by a power of two into the fp16 range
+//   (exact), is laid out as fp16 pairs (dims 8i + j, 8i + j + 4) matching
+//   the nibbles j, j + 4 of code word i, divided by 16 for odd j;
+// * values: a lane takes two positions at once; v_perm_b32 interleaves their
+//   code bytes so that every AND yields (code of A, code of B) for one
+//   dimension, dotted with the fp16 pair of their weights p sv.
 //
 // Organisation (split over the sequence, as in flash decoding)
-// * Pass 1: one workgroup of 4 waves per (b, h, chunk of CH positions).
-//   Scores: a lane owns whole positions; it reads the position's 64 code bytes
-//   and forms the dot product with v_dot2_f32_bf16 against pairs of query
-//   values: a pair of codes (c, c') becomes the bf16 pair (128 + c, 128 + c')
-//   with one and-or, so sum q (128 + c) - 128 sum q = sum q c.  Softmax
-//   statistics of the chunk through DPP and LDS; the weights p_j sv_j go to
-//   LDS.  Values: a lane owns 8 dimensions (one code dword of a row) and a
-//   quarter of the positions of its wave; codes are widened with
-//   v_cvt_f32_ubyte and accumulated in fp32.  The chunk's maximum, sum and
-//   unnormalised output go to the workspace.
+// * Pass 1: one workgroup of 4 waves per (b, h, chunk of 1024 positions);
+//   a wave owns 256 consecutive positions, in 8 blocks of 32.  A lane
+//   (quarter qd = lane & 3, row group rg = lane >> 2) takes the 16-byte
+//   quarter qd of the code rows rg and rg + 16 of a block, so each load
+//   instruction of a wave reads 1 KB of contiguous codes.  Partial dot
+//   products meet through two DPP adds in the quad; the chunk's maximum goes
+//   through LDS; the weights stay in registers for the value pass.  The
+//   chunk's maximum (log2 domain), its sum of p and its unnormalised output
+//   go to the workspace.
 // * Pass 2: one workgroup per (b, h) merges the chunks (rescaled by
-//   exp(m_i - m)), divides by the sum, optionally rotates back, and stores
-//   bf16.
+//   2^(m_i - m)), divides by the sum, optionally rotates back, stores bf16.
 #include "common.h"
 #include "internal.h"
 
 namespace offq {
 namespace {
 
-constexpr int DH = 128;       // head dimension
-constexpr int CH = 1024;      // positions per chunk (pass 1 workgroup)
-constexpr int THREADS = 256;  // 4 waves
-constexpr int PPL = CH / THREADS;  // positions per lane in the score phase
+constexpr int DH = 128;            // head dimension
+constexpr int CH = 1024;           // positions per pass-1 workgroup
+constexpr int THREADS = 256;       // 4 waves
+constexpr int WAVES = THREADS / 64;
+constexpr int WROWS = CH / WAVES;  // 256 positions per wave
+constexpr int NIT = WROWS / 32;    // blocks of 32 positions per wave
 constexpr float LOG2E = 1.4426950408889634f;
+constexpr int WS_FLOATS = 2 + DH;  // per (b, h, chunk): m, l, o[128]
 
-// acc + a.lo * b.lo + a.hi * b.hi for two packed bf16 pairs (fp32 result).
-// Through the builtin, not inline asm: a dot result read by another VALU
-// within a few cycles needs wait states that only the compiler's hazard
-// tracking inserts.
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ float dot2_bf16_acc(uint32_t a, uint32_t b, float acc) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
-                                         __builtin_bit_cast(bf16x2_t, b), acc, false);
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+
+// acc + a.lo * b.lo + a.hi * b.hi for two packed fp16 pairs (fp32 result;
+// fp16 subnormal operands are kept).  The builtin, not inline asm, so that
+// the compiler's hazard tracking sees the dot instruction.
+__device__ __forceinline__ float dot2_f16(uint32_t a, uint32_t b, float acc) {
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2_t, a), __builtin_bit_cast(f16x2_t, b),
+                                acc, false);
 }
 
-// byte K of w as a float (v_cvt_f32_ubyteK)
-template <int K>
-__device__ __forceinline__ float ubyte(uint32_t w) {
-  return (float)((w >> (8 * K)) & 0xFFu);
+__device__ __forceinline__ uint32_t pack_f16(float a, float b) {
+  const f16x2_t h = {(_Float16)a, (_Float16)b};
+  return __builtin_bit_cast(uint32_t, h);
 }
 
-// (-1)^popcount(i & j): entry (i, j) of the Sylvester Hadamard matrix
-__device__ __forceinline__ float had_sign(int i, int j) {
-  return (__builtin_popcount(i & j) & 1) ? -1.0f : 1.0f;
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xf, 0xf, true));
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -71,201 +88,301 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// Workspace per (b, h, chunk): m, l, then o[128] (fp32).
-constexpr int WS_FLOATS = 2 + DH;
+struct ChunkSmem {
+  float qf[DH];                 // rotated query, scaled into the fp16 range
+  uint32_t qp[DH / 2];          // query as fp16 pairs, see the header
+  float qsum, qexp;             // sum of q_r; the power-of-two exponent
+  float2 kab[CH];               // per position: score (log2 domain) = a * dot + b
+  float2 vsz[CH];               // per position: (sv, zv)
+  float red[3][WAVES];          // per wave: max, sum p, sum w zv
+  float o[WAVES][4][DH];        // per wave and DPP row: partial outputs
+};
+
+template <bool FULL>
+__device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __restrict__ q,
+                                                const uint8_t* __restrict__ kc,
+                                                const uint16_t* __restrict__ ks,
+                                                const int16_t* __restrict__ kz,
+                                                const uint8_t* __restrict__ vc,
+                                                const uint16_t* __restrict__ vs,
+                                                const int16_t* __restrict__ vz, int64_t row0,
+                                                int64_t bh, int n, float sm2, float cnorm,
+                                                float* __restrict__ rec) {
+  const int tid = (int)__builtin_amdgcn_workitem_id_x();
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qd = lane & 3, rg = lane >> 2;
+
+  // row of block it, half h (chunk-relative): wave * 256 + it * 32 + h * 16 + rg
+  auto row = [&](int it, int h) {
+    const int r = wave * WROWS + it * 32 + h * 16 + rg;
+    return FULL ? r : min(r, n - 1);
+  };
+
+  // ---- key codes of the wave's 256 positions, issued first ---------------
+  const uint8_t* kbase = kc + row0 * (DH / 2);
+  uint4 kd[NIT][2];
+#pragma unroll
+  for (int it = 0; it < NIT; ++it)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      kd[it][h] = *reinterpret_cast<const uint4*>(kbase + (uint32_t)(row(it, h) * (DH / 2) + qd * 16));
+
+  // ---- query: FWHT across the lanes of wave 0 (lane holds dims 2l, 2l+1) --
+  if (wave == 0) {
+    const float a = bf16_lo(q[bh * DH + 2 * lane]), b = bf16_lo(q[bh * DH + 2 * lane + 1]);
+    float x0 = a + b, x1 = a - b;
+#pragma unroll
+    for (int s = 0; s < 6; ++s) {
+      const float y0 = __shfl_xor(x0, 1 << s), y1 = __shfl_xor(x1, 1 << s);
+      const bool up = (lane >> s) & 1;
+      x0 = up ? y0 - x0 : x0 + y0;
+      x1 = up ? y1 - x1 : x1 + y1;
+    }
+    const float r0 = bf16_lo(f32_to_bf16_rne(cnorm * x0));
+    const float r1 = bf16_lo(f32_to_bf16_rne(cnorm * x1));
+    const float qsum = wave_sum(r0 + r1);
+    const float qmax = wave_max(fmaxf(fabsf(r0), fabsf(r1)));
+    // scale so that max |q| lies in [2^14, 2^15): fp16 holds every value
+    const int e = __builtin_amdgcn_frexp_expf(qmax);
+    S.qf[2 * lane] = __builtin_amdgcn_ldexpf(r0, 15 - e);
+    S.qf[2 * lane + 1] = __builtin_amdgcn_ldexpf(r1, 15 - e);
+    if (lane == 0) {
+      S.qsum = qsum;
+      S.qexp = (float)e;
+    }
+  }
+  __syncthreads();
+
+  // ---- query pairs; per-position score and value parameters -------------
+  if (tid < DH / 2) {
+    // pair p = 4 i + j: dims 8 i + j and 8 i + j + 4, divided by 16 for odd j
+    const int i = tid >> 2, j = tid & 3;
+    const float f = (j & 1) ? 0.0625f : 1.0f;
+    S.qp[tid] = pack_f16(S.qf[8 * i + j] * f, S.qf[8 * i + j + 4] * f);
+  }
+  {
+    const float qsum = S.qsum;
+    const int e = (int)S.qexp;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int r = tid * 4 + t;
+      const bool valid = FULL || r < n;
+      const int64_t rr = row0 + (FULL ? r : min(r, n - 1));
+      const float skm = sm2 * fp16_bits_to_f32(ks[rr]);
+      const float a = __builtin_amdgcn_ldexpf(skm, 9 + e);  // dot = 2^-24 sum q' c
+      const float b = -skm * (float)kz[rr] * qsum;
+      S.kab[r] = valid ? make_float2(a, b) : make_float2(0.0f, -__builtin_inff());
+      S.vsz[r] = valid ? make_float2(fp16_bits_to_f32(vs[rr]), (float)vz[rr])
+                       : make_float2(0.0f, 0.0f);
+    }
+  }
+  __syncthreads();
+
+  uint32_t qp[4][4];  // [word u][nibble j] of code words 4 qd + u
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) qp[u][j] = S.qp[16 * qd + 4 * u + j];
+
+  const uint8_t* vbase = vc + row0 * (DH / 2);
+  uint4 vd[NIT][2];
+
+  // ---- scores (log2 domain); value codes issued after the first blocks ----
+  float sc[NIT][2];
+  float mloc = -__builtin_inff();
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t w4[4] = {kd[it][h].x, kd[it][h].y, kd[it][h].z, kd[it][h].w};
+      float d = 0.0f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t w = w4[u], w8 = w >> 8;
+        d = dot2_f16(qp[u][0], w & 0x000F000Fu, d);
+        d = dot2_f16(qp[u][1], w & 0x00F000F0u, d);
+        d = dot2_f16(qp[u][2], w8 & 0x000F000Fu, d);
+        d = dot2_f16(qp[u][3], w8 & 0x00F000F0u, d);
+      }
+      d += dpp<0xB1>(d);  // quad_perm [1, 0, 3, 2]
+      d += dpp<0x4E>(d);  // quad_perm [2, 3, 0, 1]
+      const float2 ab = S.kab[wave * WROWS + it * 32 + h * 16 + rg];
+      sc[it][h] = __builtin_fmaf(ab.x, d, ab.y);
+      mloc = fmaxf(mloc, sc[it][h]);
+    }
+    if (it == 1) {
+#pragma unroll
+      for (int jt = 0; jt < NIT; ++jt)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          vd[jt][h] =
+              *reinterpret_cast<const uint4*>(vbase + (uint32_t)(row(jt, h) * (DH / 2) + qd * 16));
+    }
+  }
+  mloc = wave_max(mloc);
+  if (lane == 0) S.red[0][wave] = mloc;
+  __syncthreads();
+  const float m = fmaxf(fmaxf(S.red[0][0], S.red[0][1]), fmaxf(S.red[0][2], S.red[0][3]));
+
+  // ---- weights p sv as fp16 pairs (rows rg, rg + 16 of each block) --------
+  uint32_t wp[NIT];
+  float lsum = 0.0f, zsum = 0.0f;
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    float wf[2], zv[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float p = __builtin_amdgcn_exp2f(sc[it][h] - m);
+      const float2 sz = S.vsz[wave * WROWS + it * 32 + h * 16 + rg];
+      wf[h] = p * sz.x;
+      zv[h] = sz.y;
+      lsum += p;
+    }
+    wp[it] = pack_f16(wf[0], wf[1]);
+    const f16x2_t wh = __builtin_bit_cast(f16x2_t, wp[it]);
+    zsum = __builtin_fmaf((float)wh.x, zv[0], zsum);
+    zsum = __builtin_fmaf((float)wh.y, zv[1], zsum);
+  }
+
+  // ---- values: acc[8 u + k] is dimension 32 qd + 8 u + k ------------------
+  float acc[32];
+#pragma unroll
+  for (int k = 0; k < 32; ++k) acc[k] = 0.0f;
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const uint32_t a4[4] = {vd[it][0].x, vd[it][0].y, vd[it][0].z, vd[it][0].w};
+    const uint32_t b4[4] = {vd[it][1].x, vd[it][1].y, vd[it][1].z, vd[it][1].w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      // bytes (A.b0, A.b1, B.b0, B.b1) and (A.b2, A.b3, B.b2, B.b3)
+      const uint32_t x0 = __builtin_amdgcn_perm(b4[u], a4[u], 0x05040100u);
+      const uint32_t x1 = __builtin_amdgcn_perm(b4[u], a4[u], 0x07060302u);
+      const uint32_t x08 = x0 >> 8, x18 = x1 >> 8;
+      acc[8 * u + 0] = dot2_f16(wp[it], x0 & 0x000F000Fu, acc[8 * u + 0]);
+      acc[8 * u + 1] = dot2_f16(wp[it], x0 & 0x00F000F0u, acc[8 * u + 1]);
+      acc[8 * u + 2] = dot2_f16(wp[it], x08 & 0x000F000Fu, acc[8 * u + 2]);
+      acc[8 * u + 3] = dot2_f16(wp[it], x08 & 0x00F000F0u, acc[8 * u + 3]);
+      acc[8 * u + 4] = dot2_f16(wp[it], x1 & 0x000F000Fu, acc[8 * u + 4]);
+      acc[8 * u + 5] = dot2_f16(wp[it], x1 & 0x00F000F0u, acc[8 * u + 5]);
+      acc[8 * u + 6] = dot2_f16(wp[it], x18 & 0x000F000Fu, acc[8 * u + 6]);
+      acc[8 * u + 7] = dot2_f16(wp[it], x18 & 0x00F000F0u, acc[8 * u + 7]);
+    }
+  }
+
+  // ---- reductions: the 4 row groups of a DPP row, then rows and waves -----
+#pragma unroll
+  for (int k = 0; k < 32; ++k) {
+    acc[k] += dpp<0x124>(acc[k]);  // row_ror:4
+    acc[k] += dpp<0x128>(acc[k]);  // row_ror:8
+  }
+  if ((lane & 12) == 0) {
+    float* dst = &S.o[wave][lane >> 4][32 * qd];
+#pragma unroll
+    for (int k = 0; k < 32; k += 4)
+      *reinterpret_cast<float4*>(dst + k) = make_float4(acc[k], acc[k + 1], acc[k + 2], acc[k + 3]);
+  }
+  // the 4 lanes of a quad counted the same positions
+  lsum = 0.25f * wave_sum(lsum);
+  zsum = 0.25f * wave_sum(zsum);
+  if (lane == 0) {
+    S.red[1][wave] = lsum;
+    S.red[2][wave] = zsum;
+  }
+  __syncthreads();
+  if (tid < DH) {
+    float o = 0.0f;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) o += S.o[w][r][tid];
+    // codes entered as c 2^-24 (even dims) or 16 c 2^-24 (odd dims)
+    o *= (tid & 1) ? 0x1p20f : 0x1p24f;
+    const float zw = S.red[2][0] + S.red[2][1] + S.red[2][2] + S.red[2][3];
+    rec[2 + tid] = o - zw;
+  }
+  if (tid == 0) {
+    rec[0] = m;
+    rec[1] = S.red[1][0] + S.red[1][1] + S.red[1][2] + S.red[1][3];
+  }
+}
 
 __global__ __launch_bounds__(THREADS) void kv_attention_chunk_kernel(
     const uint16_t* __restrict__ q, const uint8_t* __restrict__ kc, const uint16_t* __restrict__ ks,
     const int16_t* __restrict__ kz, const uint8_t* __restrict__ vc, const uint16_t* __restrict__ vs,
-    const int16_t* __restrict__ vz, int64_t S_cap, int seq_len, int nchunk, float sm_scale,
+    const int16_t* __restrict__ vz, int64_t S_cap, int seq_len, int nchunk, float sm2,
     float cnorm, float* __restrict__ ws) {
-  __shared__ float s_q[DH];                     // query (fp32)
-  __shared__ float s_qr[DH];                    // H q (fp32)
-  __shared__ uint32_t s_qp[DH / 2];             // rotated query as bf16 pairs
-  __shared__ float s_qsum;                      // sum of the bf16 query values
-  __shared__ float s_red[2][THREADS / 64];      // per-wave max / sum
-  __shared__ float s_w[CH];                     // p_j * sv_j of the chunk
-  __shared__ float s_o[THREADS / 64][DH];       // per-wave partial outputs
-  __shared__ float s_zw[THREADS / 64];          // per-wave sum of p_j sv_j zv_j
-
-  const int tid = (int)__builtin_amdgcn_workitem_id_x();
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  __shared__ ChunkSmem S;
   const int blk = (int)__builtin_amdgcn_workgroup_id_x();
   const int bh = blk / nchunk, chunk = blk - bh * nchunk;
   const int j0 = chunk * CH;
-  const int n = min(CH, seq_len - j0);          // positions of this chunk (>= 1)
+  const int n = min(CH, seq_len - j0);  // positions of this chunk (>= 1)
   const int64_t row0 = (int64_t)bh * S_cap + j0;
-
-  // ---- query: q_r = bf16(c H q), as pairs (d, d + 4) of each group of 8 ----
-  if (tid < DH) s_q[tid] = bf16_lo(q[(int64_t)bh * DH + tid]);
-  __syncthreads();
-  if (tid < DH) {
-    float acc = 0.0f;
-    for (int i = 0; i < DH; ++i) acc = __builtin_fmaf(s_q[i], had_sign(i, tid), acc);
-    s_qr[tid] = acc;
-  }
-  __syncthreads();
-  if (tid < DH / 2) {
-    // pair p = 4 i + j (i = 0..15, j = 0..3): dimensions 8 i + j and 8 i + j + 4
-    const int i = tid >> 2, j = tid & 3;
-    const float a = s_qr[8 * i + j] * cnorm, b = s_qr[8 * i + j + 4] * cnorm;
-    s_qp[tid] = bf16x2_rne(a, b);
-  }
-  __syncthreads();
-  if (tid == 0) {
-    float t = 0.0f;
-    for (int p = 0; p < DH / 2; ++p) t += bf16_lo(s_qp[p]) + bf16_hi(s_qp[p]);
-    s_qsum = t;
-  }
-  __syncthreads();
-
-  // ---- scores: lane owns positions wave*256 + it*64 + lane -----------------
-  uint32_t qp[DH / 2];
-#pragma unroll
-  for (int p = 0; p < DH / 2; ++p) qp[p] = s_qp[p];
-  const float qsum = s_qsum;
-  float sc[PPL];
-  float mloc = -__builtin_inff();
-  {
-    uint4 kr[PPL][4];
-    float ksc[PPL];
-    int kzz[PPL];
-#pragma unroll
-    for (int it = 0; it < PPL; ++it) {
-      const int jl = wave * (CH / 4) + it * 64 + lane;
-      const int jj = min(jl, n - 1);  // past the chunk: a valid row, result unused
-      const uint4* src = reinterpret_cast<const uint4*>(kc + (row0 + jj) * (DH / 2));
-#pragma unroll
-      for (int c = 0; c < 4; ++c) kr[it][c] = src[c];
-      ksc[it] = fp16_bits_to_f32(ks[row0 + jj]);
-      kzz[it] = kz[row0 + jj];
-    }
-#pragma unroll
-    for (int it = 0; it < PPL; ++it) {
-      float dot = 0.0f;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const uint32_t w4[4] = {kr[it][c].x, kr[it][c].y, kr[it][c].z, kr[it][c].w};
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int i = 4 * c + u;  // dims 8 i .. 8 i + 7
-          const uint32_t w = w4[u];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const uint32_t pr = ((w >> (4 * j)) & 0x000F000Fu) | 0x43004300u;  // (128 + c, 128 + c')
-            dot = dot2_bf16_acc(qp[4 * i + j], pr, dot);
-          }
-        }
-      }
-      const int jl = wave * (CH / 4) + it * 64 + lane;
-      const float s = sm_scale * ksc[it] * (dot - (128.0f + (float)kzz[it]) * qsum);
-      sc[it] = jl < n ? s : -__builtin_inff();
-      mloc = fmaxf(mloc, sc[it]);
-    }
-  }
-  mloc = wave_max(mloc);
-  if (lane == 0) s_red[0][wave] = mloc;
-  __syncthreads();
-  const float m = fmaxf(fmaxf(s_red[0][0], s_red[0][1]), fmaxf(s_red[0][2], s_red[0][3]));
-
-  // ---- probabilities and value weights -------------------------------------
-  float lsum = 0.0f, zsum = 0.0f;
-#pragma unroll
-  for (int it = 0; it < PPL; ++it) {
-    const int jl = wave * (CH / 4) + it * 64 + lane;
-    const int jj = min(jl, n - 1);
-    const float p = jl < n ? __builtin_amdgcn_exp2f((sc[it] - m) * LOG2E) : 0.0f;
-    const float w = p * fp16_bits_to_f32(vs[row0 + jj]);
-    lsum += p;
-    zsum = __builtin_fmaf(w, (float)vz[row0 + jj], zsum);
-    s_w[jl] = w;
-  }
-  lsum = wave_sum(lsum);
-  zsum = wave_sum(zsum);
-  if (lane == 0) {
-    s_red[1][wave] = lsum;
-    s_zw[wave] = zsum;
-  }
-  __syncthreads();
-
-  // ---- values: lane (dg, pg) owns dims 8 dg .. 8 dg + 7 and the positions
-  // jl = wave * 256 + 4 t + pg of its wave's quarter ---------------------------
-  const int dg = lane & 15, pg = lane >> 4;
-  float acc[8] = {};
-  {
-    const uint32_t* vrow = reinterpret_cast<const uint32_t*>(vc + row0 * (DH / 2)) + dg;
-    constexpr int NT = CH / 4 / 4;  // positions per lane (64)
-    constexpr int BT = 16;          // loads in flight
-#pragma unroll 1
-    for (int t0 = 0; t0 < NT; t0 += BT) {
-      uint32_t cw[BT];
-#pragma unroll
-      for (int t = 0; t < BT; ++t) {
-        const int jl = wave * (CH / 4) + 4 * (t0 + t) + pg;
-        cw[t] = vrow[(int64_t)min(jl, n - 1) * (DH / 8)];
-      }
-#pragma unroll
-      for (int t = 0; t < BT; ++t) {
-        const int jl = wave * (CH / 4) + 4 * (t0 + t) + pg;
-        const float w = jl < n ? s_w[jl] : 0.0f;
-        const uint32_t lo = cw[t] & 0x0F0F0F0Fu, hi = (cw[t] >> 4) & 0x0F0F0F0Fu;
-        // byte k of lo: dim 8 dg + 2 k; byte k of hi: dim 8 dg + 2 k + 1
-        acc[0] = __builtin_fmaf(w, ubyte<0>(lo), acc[0]);
-        acc[1] = __builtin_fmaf(w, ubyte<0>(hi), acc[1]);
-        acc[2] = __builtin_fmaf(w, ubyte<1>(lo), acc[2]);
-        acc[3] = __builtin_fmaf(w, ubyte<1>(hi), acc[3]);
-        acc[4] = __builtin_fmaf(w, ubyte<2>(lo), acc[4]);
-        acc[5] = __builtin_fmaf(w, ubyte<2>(hi), acc[5]);
-        acc[6] = __builtin_fmaf(w, ubyte<3>(lo), acc[6]);
-        acc[7] = __builtin_fmaf(w, ubyte<3>(hi), acc[7]);
-      }
-    }
-  }
-  // sum over the four position groups of the wave, then over the waves
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    acc[k] += __shfl_xor(acc[k], 16);
-    acc[k] += __shfl_xor(acc[k], 32);
-  }
-  if (pg == 0) {
-#pragma unroll
-    for (int k = 0; k < 8; ++k) s_o[wave][8 * dg + k] = acc[k];
-  }
-  __syncthreads();
-  float* const out = ws + (int64_t)blk * WS_FLOATS;
-  if (tid < DH) {
-    const float zw = s_zw[0] + s_zw[1] + s_zw[2] + s_zw[3];
-    out[2 + tid] = s_o[0][tid] + s_o[1][tid] + s_o[2][tid] + s_o[3][tid] - zw;
-  }
-  if (tid == 0) {
-    out[0] = m;
-    out[1] = s_red[1][0] + s_red[1][1] + s_red[1][2] + s_red[1][3];
-  }
+  float* rec = ws + (int64_t)blk * WS_FLOATS;
+  if (n == CH)
+    attention_chunk<true>(S, q, kc, ks, kz, vc, vs, vz, row0, bh, n, sm2, cnorm, rec);
+  else
+    attention_chunk<false>(S, q, kc, ks, kz, vc, vs, vz, row0, bh, n, sm2, cnorm, rec);
 }
+
+// Pass 2: merge the chunk records of one (b, h).  The chunk maxima are read
+// by all lanes at once (a chain of dependent loads over the chunks would cost
+// far more than the data), the factors 2^(m_i - m) go through LDS, and every
+// thread then sums its dimension over the chunks with independent loads.
+constexpr int CT = 1024;  // chunk factors held in LDS per round
 
 __global__ __launch_bounds__(DH) void kv_attention_combine_kernel(const float* __restrict__ ws,
                                                                   int nchunk, int v_had,
                                                                   float cnorm,
                                                                   uint16_t* __restrict__ out) {
+  __shared__ float s_e[CT];
+  __shared__ float s_red[2][DH / 64];
   __shared__ float s_o[DH];
   const int d = (int)__builtin_amdgcn_workitem_id_x();
+  const int lane = d & 63, wave = d >> 6;
   const int bh = (int)__builtin_amdgcn_workgroup_id_x();
   const float* w = ws + (int64_t)bh * nchunk * WS_FLOATS;
+
   float m = -__builtin_inff();
-  for (int i = 0; i < nchunk; ++i) m = fmaxf(m, w[i * WS_FLOATS]);
+  for (int i = d; i < nchunk; i += DH) m = fmaxf(m, w[(int64_t)i * WS_FLOATS]);
+  m = wave_max(m);
+  if (lane == 0) s_red[0][wave] = m;
+  __syncthreads();
+  m = fmaxf(s_red[0][0], s_red[0][1]);
+
   float l = 0.0f, o = 0.0f;
-  for (int i = 0; i < nchunk; ++i) {
-    const float e = __builtin_amdgcn_exp2f((w[i * WS_FLOATS] - m) * LOG2E);
-    l = __builtin_fmaf(e, w[i * WS_FLOATS + 1], l);
-    o = __builtin_fmaf(e, w[i * WS_FLOATS + 2 + d], o);
+  for (int i0 = 0; i0 < nchunk; i0 += CT) {
+    const int nt = min(CT, nchunk - i0);
+    __syncthreads();  // the previous round's factors are consumed
+    for (int i = d; i < nt; i += DH) {
+      const float* r = w + (int64_t)(i0 + i) * WS_FLOATS;
+      const float e = __builtin_amdgcn_exp2f(r[0] - m);
+      s_e[i] = e;
+      l = __builtin_fmaf(e, r[1], l);
+    }
+    __syncthreads();
+    const float* od = w + (int64_t)i0 * WS_FLOATS + 2 + d;
+    int i = 0;
+    for (; i + 8 <= nt; i += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = od[(int64_t)(i + u) * WS_FLOATS];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) o = __builtin_fmaf(s_e[i + u], v[u], o);
+    }
+    for (; i < nt; ++i) o = __builtin_fmaf(s_e[i], od[(int64_t)i * WS_FLOATS], o);
   }
+  l = wave_sum(l);
+  if (lane == 0) s_red[1][wave] = l;
+  __syncthreads();
+  l = s_red[1][0] + s_red[1][1];
   o = o / l;
   if (v_had) {
     s_o[d] = o;
     __syncthreads();
     float a = 0.0f;
-    for (int i = 0; i < DH; ++i) a = __builtin_fmaf(s_o[i], had_sign(i, d), a);
+    for (int i = 0; i < DH; ++i)
+      a = __builtin_fmaf(s_o[i], (__builtin_popcount(i & d) & 1) ? -1.0f : 1.0f, a);
     o = a * cnorm;
   }
   out[(int64_t)bh * DH + d] = f32_to_bf16_rne(o);
@@ -287,7 +404,7 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
   const float cnorm = (float)(1.0 / __builtin_sqrt((double)DH));
   hipLaunchKernelGGL(kv_attention_chunk_kernel, dim3((unsigned)(BH * nchunk)), dim3(THREADS), 0,
                      stream, q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, S_cap,
-                     (int)seq_len, nchunk, sm_scale, cnorm, workspace);
+                     (int)seq_len, nchunk, sm_scale * LOG2E, cnorm, workspace);
   hipLaunchKernelGGL(kv_attention_combine_kernel, dim3((unsigned)BH), dim3(DH), 0, stream,
                      workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out);
   return hipGetLastError();

@@ -4,11 +4,12 @@ vs the oracle (oracle/attention.py).
 Tolerance (fp32 kernel against the exact fp64 result, then one bf16 rounding):
   |out - ref| <= 2^-8 (1 + 2^-5) |ref| + 2^-11 E,
   E = sum_j p_j max_d |V_j[d]|  (the magnitude of the weighted value rows).
-The first term is the final bf16 rounding (unit roundoff 2^-8); the second covers the fp32 score
-dot products (about 2^-24 times sums of magnitude 128 sum|q_r| per position,
-relative score errors near 1e-5 that move p by as much), the fp32 value sums
-and, with the value rotation, an fp32 128-point transform -- each at least
-ten times below 2^-11 E.  A dropped or doubled position, a wrong zero-point or
+The first term is the final bf16 rounding (unit roundoff 2^-8).  The second
+covers the kernel's own roundings: the weights p_j sv_j enter the value sum
+as fp16 (relative error <= 2^-12 each, so at most 2^-12 E in the output), and
+the fp32 score dot products (exact products of fp16 operands, sums of
+magnitude sum|q_r c| with relative errors near 1e-6), the fp32 value sums
+and, with the value rotation, an fp32 128-point transform add far less.  A dropped or doubled position, a wrong zero-point or
 scale, a misplaced dimension or a missing rescale of a chunk is far above it
 at the small sizes these tests use.
 """
