@@ -46,7 +46,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="attn_proj_prefill",
                    choices=["attn_proj_prefill", "mlp_prefill", "decode", "kv_chain",
-                            "kv_decode_attention"])
+                            "kv_decode_attention", "decode_layer"])
     p.add_argument("--decode-m", type=int, default=16)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--group-size", type=int, default=0,
@@ -71,6 +71,11 @@ def attn_bytes(BH, S, Dh=128):
     rows of every attended position with their fp16 scale and int16 zero-point,
     plus the bf16 query and output of each (b, h)."""
     return BH * (S * (2 * (Dh // 2) + 2 * 4) + 2 * 2 * Dh)
+
+
+def weight_bytes(N, K, g):
+    """Packed int4 weights with fp16 scales and int32 per-group column sums."""
+    return N * K // 2 + 2 * N + 4 * (K // g) * N
 
 
 def source_hash(paths):
@@ -265,6 +270,46 @@ def main():
         config = {"workload": wl, "kv_shape": [B, H, S, Dh], "seq_len": S,
                   "step": "kv_attention_decode (split-sequence pass + combine pass)",
                   "input_sets": asets.n}
+    elif wl == "decode_layer":
+        lc = inputs.WORKLOADS["decode_layer"]
+        M, D, Hq, Hkv, F, g = lc["M"], lc["D"], lc["Hq"], lc["Hkv"], lc["F"], lc["g"]
+        ctx = lc["ctx"]
+        s_cap, seq_len = ctx + 1, ctx + 1
+        NQKV = (Hq + 2 * Hkv) * 128
+        lshapes = {"qkv": (NQKV, D), "o": (D, Hq * 128), "ug": (2 * F, D), "down": (D, F)}
+        bf, u8, f16, i16 = torch.bfloat16, torch.uint8, torch.float16, torch.int16
+
+        def make_layer(i):
+            sd = lc["seed"] + 100 * i
+            st = {"x": torch.from_numpy(inputs.queries(1, M, D, seed=sd)[0]).to(bf).cuda()}
+            for j, (k, (n_, k_)) in enumerate(lshapes.items()):
+                w = inputs.weights_device(n_, k_, seed=sd + j, device="cuda", std=1.0 / k_ ** 0.5)
+                st["w_" + k] = offq.offq_pack_weights(w, g)
+                del w
+            kc_, ks_, kz_ = inputs.kv4_cache_device(M, Hkv, s_cap, 128, seed=sd, device="cuda")
+            vc_, vs_, vz_ = inputs.kv4_cache_device(M, Hkv, s_cap, 128, seed=sd + 1, device="cuda")
+            st.update(kc=kc_, ks=ks_, kz=kz_, vc=vc_, vs=vs_, vz=vz_,
+                      pos=torch.full((M,), ctx, dtype=torch.int32, device="cuda"))
+            e = lambda *sh, dt=bf: torch.empty(sh, dtype=dt, device="cuda")
+            st.update(y0=e(M, D), qkv=e(M, NQKV), q=e(M, Hq, 128), o=e(M, Hq, 128),
+                      ao=e(M, D), h1=e(M, D), y1=e(M, D), gu=e(M, 2 * F), a=e(M, F),
+                      dn=e(M, D), out=e(M, D))
+            for name, K_ in (("c_in", D), ("c_o", Hq * 128), ("c_d", F)):
+                st[name] = (e(M, K_ // 2, dt=u8), e(M, K_ // g, dt=f16), e(M, K_ // g, dt=i16))
+            st["wsb"] = offq.offq_kv_attention_workspace_bytes(M, Hq, seq_len)
+            st["ws"] = e(st["wsb"] // 4, dt=torch.float32)
+            return st
+
+        lbytes = sum(weight_bytes(n_, k_, g) for n_, k_ in lshapes.values())
+        kvbytes = M * Hkv * seq_len * 136
+        step_bytes = lbytes + kvbytes + M * (D * 2 * 4 + NQKV * 2 + F * 6)
+        lsets = Sets(make_layer, lbytes + kvbytes)
+        layers = []
+        work_ops = None
+        config = {"workload": wl, "M": M, "D": D, "heads": [Hq, Hkv], "mlp": F, "g": g,
+                  "context": ctx, "step": "add+RMSNorm, quantize, QKV GEMV, RoPE + H3 + KV4 append, "
+                  "GQA decode attention, quantize, O GEMV, add+RMSNorm, quantize, up/gate GEMV, "
+                  "SwiGLU, H4 + quantize, down GEMV, add", "input_sets": lsets.n}
     else:  # decode
         up = regroup(inputs.WORKLOADS["decode_up"])
         dn = regroup(inputs.WORKLOADS["decode_down"])
@@ -291,6 +336,41 @@ def main():
             phases.append(("kv_quantize", lambda i, j=j: _lib.offq_kv_quantize_raw(
                 kv[j].data_ptr(), R, Dh, Dh, 1, kvo[j]["codes"].data_ptr(), kvo[j]["scale"].data_ptr(),
                 kvo[j]["zero"].data_ptr(), None, sp)))
+    if wl == "decode_layer":
+        eps, base, sm = 1e-5, 500000.0, 1.0 / 128 ** 0.5
+        P_ = lambda t: t.data_ptr()
+
+        def lin(st, cname, src, K_, N_, wname, dst, had):
+            c_, s_, z_ = st[cname]
+            check(_lib.offq_rotate_quantize_raw(P_(src), M, K_, K_, g, had, P_(c_), P_(s_), P_(z_),
+                                                None, sp), "rotate_quantize")
+            wc_, ws_, wcs_ = st[wname]
+            return _lib.offq_w4a4_gemm_raw(P_(c_), P_(s_), P_(z_), P_(wc_), P_(ws_), P_(wcs_), M,
+                                           N_, K_, g, P_(dst), N_, None, sp)
+
+        def step_layer(i):
+            st = lsets[i]
+            check(_lib.offq_add_rmsnorm_raw(P_(st["x"]), D, None, 0, M, D, eps, None, 0,
+                                            P_(st["y0"]), D, sp), "add_rmsnorm")
+            check(lin(st, "c_in", st["y0"], D, NQKV, "w_qkv", st["qkv"], 0), "gemv qkv")
+            check(_lib.offq_rope_kv_append_raw(
+                P_(st["qkv"]), NQKV, M, Hq, Hkv, 128, P_(st["pos"]), base, 1, 0, P_(st["q"]),
+                P_(st["kc"]), P_(st["ks"]), P_(st["kz"]), P_(st["vc"]), P_(st["vs"]), P_(st["vz"]),
+                s_cap, None, None, sp), "rope_kv_append")
+            check(_lib.offq_kv_attention_decode_gqa_raw(
+                P_(st["q"]), P_(st["kc"]), P_(st["ks"]), P_(st["kz"]), P_(st["vc"]), P_(st["vs"]),
+                P_(st["vz"]), M, Hq, Hkv, s_cap, seq_len, 128, sm, 0, P_(st["o"]), P_(st["ws"]),
+                st["wsb"], sp), "attention")
+            check(lin(st, "c_o", st["o"], Hq * 128, D, "w_o", st["ao"], 0), "gemv o")
+            check(_lib.offq_add_rmsnorm_raw(P_(st["x"]), D, P_(st["ao"]), D, M, D, eps,
+                                            P_(st["h1"]), D, P_(st["y1"]), D, sp), "add_rmsnorm")
+            check(lin(st, "c_in", st["y1"], D, 2 * F, "w_ug", st["gu"], 0), "gemv up/gate")
+            check(_lib.offq_swiglu_raw(P_(st["gu"]), 2 * F, M, F, P_(st["a"]), F, sp), "swiglu")
+            check(lin(st, "c_d", st["a"], F, D, "w_down", st["dn"], 1), "gemv down")
+            return _lib.offq_add_rmsnorm_raw(P_(st["h1"]), D, P_(st["dn"]), D, M, D, eps,
+                                             P_(st["out"]), D, None, 0, sp)
+        # the whole layer is one phase: its kernels depend on each other
+        phases.append(("decode_layer", step_layer))
     if wl == "kv_decode_attention":
         def run_attn(i):
             a_ = asets[i]
@@ -303,6 +383,8 @@ def main():
         phases.append((rq_name, lambda i, s_=sets_: run_rq(_lib, s_[i], sp)))
         phases.append((mm_name, lambda i, s_=sets_: run_gemm(_lib, s_[i], sp)))
 
+    # library launches per step (the spin below covers the host's enqueue time)
+    launches_per_step = 15 if wl == "decode_layer" else len(phases)
     for i in range(args.warmup):
         for name, fn in phases:
             check(fn(i), name)
@@ -312,7 +394,7 @@ def main():
     # enqueues the whole timed region, so that no kernel waits for its launch
     # call (a launch from Python takes longer than the shortest kernels here).
     if hasattr(torch.cuda, "_sleep"):
-        torch.cuda._sleep(100_000 * len(phases) * args.steps)
+        torch.cuda._sleep(100_000 * launches_per_step * args.steps)
     evs[0].record(stream)
     for p, (name, fn) in enumerate(phases):
         for i in range(args.steps):
@@ -367,6 +449,17 @@ def main():
                 "unit": "TOP/s", "frac": comp[dom]["frac_int8_peak"],
                 "traffic": traffic_for(f"w4a4_gemm:{wl}"), "kernel": dom,
                 "alg_ops_per_launch": comp[dom]["alg_ops"], "avg_launch_us": comp[dom]["us"]}
+    elif wl == "decode_layer":
+        name = "decode_layer"
+        comp[name]["alg_bytes"] = step_bytes
+        comp[name]["GBs"] = round(step_bytes / (comp[name]["us"] * 1e-6) / 1e9, 1)
+        comp[name]["frac_hbm"] = round(comp[name]["GBs"] / PEAK_HBM_GBS, 4)
+        comp[name]["tokens_per_s"] = round(M / (comp[name]["us"] * 1e-6), 1)
+        value = comp[name]["GBs"]
+        unit = "GB/s"
+        roof = {"bound": "hbm", "achieved": comp[name]["GBs"], "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": comp[name]["frac_hbm"], "traffic": None, "kernel": name,
+                "alg_bytes_per_launch": step_bytes, "avg_launch_us": comp[name]["us"]}
     elif wl == "kv_decode_attention":
         name = "kv_attention_decode"
         b_ = attn_bytes(B * H, S, Dh)

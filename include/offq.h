@@ -181,8 +181,8 @@ int offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g,
  *   q            bf16 [B, H, 128] contiguous (the query after RoPE).
  *   k_codes      uint8 [B, H, s_cap, 64], 16-byte aligned; k_scale fp16 and
  *                k_zero int16 [B, H, s_cap] (rows (b, h, j) of offq_kv_quantize
- *                with head_dim = 128).  v_codes, v_scale, v_zero likewise
- *                (v_codes 4-byte aligned).
+ *                with head_dim = 128).  v_codes (16-byte aligned), v_scale,
+ *                v_zero likewise.
  *   seq_len      positions in use, 1 <= seq_len <= s_cap.
  *   sm_scale     score scale (1/sqrt(128) for standard attention).
  *   out          bf16 [B, H, 128].
@@ -199,8 +199,86 @@ int offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const ui
                              float sm_scale, int32_t v_hadamard, uint16_t* out, void* workspace,
                              int64_t workspace_bytes, void* stream);
 
-/* Bytes of workspace offq_kv_attention_decode needs (0 for invalid sizes). */
+/* Bytes of workspace offq_kv_attention_decode needs (0 for invalid sizes);
+ * H is the number of query heads. */
 int64_t offq_kv_attention_workspace_bytes(int64_t B, int64_t H, int64_t seq_len);
+
+/*
+ * offq_kv_attention_decode_gqa -- the same step with grouped-query attention
+ * (the key/value heads of Llama 3 style models): Hq query heads share Hkv
+ * key/value heads, query head h of batch b reading the cache rows of
+ * key/value head h / (Hq / Hkv).  q and out are [B, Hq, 128]; the cache
+ * arrays are [B, Hkv, s_cap, ...]; the workspace is sized by
+ * offq_kv_attention_workspace_bytes(B, Hq, seq_len).  Hq must be a multiple
+ * of Hkv (OFFQ_ERR_INVALID otherwise).  offq_kv_attention_decode is this call
+ * with Hkv = Hq.
+ */
+int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
+                                 const uint16_t* k_scale, const int16_t* k_zero,
+                                 const uint8_t* v_codes, const uint16_t* v_scale,
+                                 const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv,
+                                 int64_t s_cap, int64_t seq_len, int32_t head_dim, float sm_scale,
+                                 int32_t v_hadamard, uint16_t* out, void* workspace,
+                                 int64_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Decoder-layer steps around the quantized linear layers (one decode step,
+ * one new token per sequence), following the pipeline of sec. 3.3 / Fig. 2.
+ * All tensors are bf16 unless stated; rows are contiguous in their last
+ * dimension with the given row strides (in elements).
+ * ------------------------------------------------------------------------- */
+
+/*
+ * offq_add_rmsnorm -- the residual stream and its RMSNorm (the norm's scale is
+ * fused into the next weights offline, so none is applied here):
+ *     h = bf16(fl32(x + res))          (h = x when res is NULL)
+ *     y = bf16(h * fl32(1 / sqrt(mean_k h^2 + eps)))
+ *   x [M, D] (ldx), res [M, D] (ldr) or NULL, h_out [M, D] (ldh) or NULL,
+ *   y_out [M, D] (ldy) or NULL (at least one output).  D a multiple of 8,
+ *   strides multiples of 8, pointers 16-byte aligned.  M = 0 is a no-op.
+ */
+int offq_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr, int64_t M,
+                     int64_t D, float eps, uint16_t* h_out, int64_t ldh, uint16_t* y_out,
+                     int64_t ldy, void* stream);
+
+/*
+ * offq_swiglu -- out[m, f] = bf16(fl32(silu(g) * u)), silu(g) = g / (1 + e^-g)
+ * in fp32, with g = gu[m, f] and u = gu[m, F + f]: the up/gate projection
+ * writes gate in columns [0, F) and up in [F, 2F) (the grouping permutation
+ * P4 of sec. 3.3 step 2(4) is fused into those weights offline).
+ *   gu [M, 2F] (ldg >= 2F), out [M, F] (ldo >= F); F, ldg, ldo multiples of
+ *   8; pointers 16-byte aligned.
+ */
+int offq_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t* out, int64_t ldo,
+                void* stream);
+
+/*
+ * offq_rope_kv_append -- RoPE on the new token's query and key heads, the
+ * per-head online Hadamard H3 on the key (sec. 3.3 step 2(3)) and the KV4
+ * quantizer (as offq_kv_quantize, group = head dim) writing position
+ * positions[m] of sequence m into the cache:
+ *   qkv [M, (Hq + 2 Hkv) * 128] (ldq >= that, even): query heads, then key
+ *     heads, then value heads of the QKV projection of token m;
+ *   positions int32 [M] (device): the position of token m in its sequence;
+ *     a position outside [0, s_cap) writes nothing to the cache;
+ *   rope_base: RoPE's base (theta); dims (i, i + 64) rotate by angle
+ *     fl32(pos * fl32(base^(-2i/128))), computed in fp32;
+ *   k_hadamard / v_hadamard (0 or 1): c H on the key (after RoPE and a bf16
+ *     rounding) / on the value before quantization (paper: 1 / 0);
+ *   q_out [M, Hq, 128]: the query after RoPE;
+ *   k_codes, v_codes uint8 [M, Hkv, s_cap, 64]; k_scale, v_scale fp16 and
+ *     k_zero, v_zero int16 [M, Hkv, s_cap] (the layout the decode attention
+ *     reads);
+ *   k_y_debug, v_y_debug fp32 [M, Hkv, 128] or NULL: the rows that were
+ *     quantized.
+ * head_dim must be 128.
+ */
+int offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq, int64_t Hkv,
+                        int32_t head_dim, const int32_t* positions, double rope_base,
+                        int32_t k_hadamard, int32_t v_hadamard, uint16_t* q_out,
+                        uint8_t* k_codes, uint16_t* k_scale, int16_t* k_zero, uint8_t* v_codes,
+                        uint16_t* v_scale, int16_t* v_zero, int64_t s_cap, float* k_y_debug,
+                        float* v_y_debug, void* stream);
 
 #ifdef __cplusplus
 }

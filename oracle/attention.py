@@ -58,8 +58,9 @@ def decode_attention(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, seq_
                      v_hadamard=False):
     """One decode step for every (b, h).
 
-    q: [B, H, Dh] bf16 values; k_codes, v_codes: uint8 [B, H, S_cap, Dh/2];
-    k_scale, v_scale: fp16 [B, H, S_cap]; k_zero, v_zero: int16 [B, H, S_cap].
+    q: [B, Hq, Dh] bf16 values; k_codes, v_codes: uint8 [B, Hkv, S_cap, Dh/2];
+    k_scale, v_scale: fp16 [B, Hkv, S_cap]; k_zero, v_zero: int16 [B, Hkv, S_cap],
+    Hq a multiple of Hkv (query head h reads key/value head h // (Hq / Hkv)).
     Returns fp64 [B, H, Dh]:  softmax_j(sm_scale * q_r . K_j) @ V  over the
     positions j < seq_len, followed by the inverse rotation of V if
     ``v_hadamard``.
@@ -67,6 +68,11 @@ def decode_attention(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, seq_
     qr = rotate_query(q)
     k = dequantize_rows(k_codes[:, :, :seq_len], k_scale[:, :, :seq_len], k_zero[:, :, :seq_len])
     v = dequantize_rows(v_codes[:, :, :seq_len], v_scale[:, :, :seq_len], v_zero[:, :, :seq_len])
+    group = qr.shape[1] // k.shape[1]
+    if group > 1:
+        # grouped-query attention: query head h reads key/value head h // group
+        k = np.repeat(k, group, axis=1)
+        v = np.repeat(v, group, axis=1)
     scores = np.float64(sm_scale) * np.einsum("bhd,bhsd->bhs", qr, k)
     p = softmax(scores)
     o = np.einsum("bhs,bhsd->bhd", p, v)

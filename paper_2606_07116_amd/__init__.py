@@ -8,6 +8,9 @@ arguments.  Entry points (same names as ``include/offq.h``):
     offq_kv_quantize(kv, apply_hadamard=True, debug=False)
     offq_pack_weights(w, g)
     offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, seq_len, ...)
+    offq_add_rmsnorm(x, res=None, eps=1e-5)
+    offq_swiglu(gu)
+    offq_rope_kv_append(qkv, Hq, Hkv, positions, cache, rope_base=500000.0, ...)
 
 Importing the package loads the library and raises if it has not been built.
 """
@@ -17,6 +20,9 @@ from ._lib import (  # noqa: F401
     EXPORTED,
     OffqError,
     last_error,
+    offq_add_rmsnorm,
+    offq_rope_kv_append,
+    offq_swiglu,
     offq_kv_attention_decode,
     offq_kv_attention_workspace_bytes,
     offq_kv_quantize,

@@ -30,6 +30,10 @@ EXPORTED = (
     "offq_pack_weights",
     "offq_kv_attention_decode",
     "offq_kv_attention_workspace_bytes",
+    "offq_kv_attention_decode_gqa",
+    "offq_add_rmsnorm",
+    "offq_swiglu",
+    "offq_rope_kv_append",
 )
 
 
@@ -70,6 +74,17 @@ def _load():
                                              ctypes.c_float, i32, vp, vp, i64, vp]
     lib.offq_kv_attention_workspace_bytes.restype = i64
     lib.offq_kv_attention_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.offq_kv_attention_decode_gqa.restype = ctypes.c_int
+    lib.offq_kv_attention_decode_gqa.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64,
+                                                 i32, ctypes.c_float, i32, vp, vp, i64, vp]
+    lib.offq_add_rmsnorm.restype = ctypes.c_int
+    lib.offq_add_rmsnorm.argtypes = [vp, i64, vp, i64, i64, i64, ctypes.c_float, vp, i64, vp, i64,
+                                     vp]
+    lib.offq_swiglu.restype = ctypes.c_int
+    lib.offq_swiglu.argtypes = [vp, i64, i64, i64, vp, i64, vp]
+    lib.offq_rope_kv_append.restype = ctypes.c_int
+    lib.offq_rope_kv_append.argtypes = [vp, i64, i64, i64, i64, i32, vp, ctypes.c_double, i32, i32,
+                                        vp, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp]
     return lib
 
 
@@ -121,6 +136,30 @@ def offq_kv_attention_decode_raw(q, k_codes, k_scale, k_zero, v_codes, v_scale, 
 
 def offq_kv_attention_workspace_bytes(B, H, seq_len):
     return lib.offq_kv_attention_workspace_bytes(B, H, seq_len)
+
+
+def offq_kv_attention_decode_gqa_raw(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B, Hq,
+                                     Hkv, s_cap, seq_len, head_dim, sm_scale, v_hadamard, out,
+                                     workspace, workspace_bytes, stream):
+    return lib.offq_kv_attention_decode_gqa(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B,
+                                            Hq, Hkv, s_cap, seq_len, head_dim, sm_scale, v_hadamard,
+                                            out, workspace, workspace_bytes, stream)
+
+
+def offq_add_rmsnorm_raw(x, ldx, res, ldr, M, D, eps, h_out, ldh, y_out, ldy, stream):
+    return lib.offq_add_rmsnorm(x, ldx, res, ldr, M, D, eps, h_out, ldh, y_out, ldy, stream)
+
+
+def offq_swiglu_raw(gu, ldg, M, F, out, ldo, stream):
+    return lib.offq_swiglu(gu, ldg, M, F, out, ldo, stream)
+
+
+def offq_rope_kv_append_raw(qkv, ldq, M, Hq, Hkv, head_dim, positions, rope_base, k_hadamard,
+                            v_hadamard, q_out, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero,
+                            s_cap, k_y_debug, v_y_debug, stream):
+    return lib.offq_rope_kv_append(qkv, ldq, M, Hq, Hkv, head_dim, positions, rope_base, k_hadamard,
+                                   v_hadamard, q_out, k_codes, k_scale, k_zero, v_codes, v_scale,
+                                   v_zero, s_cap, k_y_debug, v_y_debug, stream)
 
 
 # ------------------------------------------------------------ tensor wrappers
@@ -257,10 +296,10 @@ def offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_ze
         if not t.is_contiguous():
             raise ValueError(f"{n} must be contiguous")
     B, H, Dh = q.shape
-    s_cap = k_codes.shape[2]
-    if k_codes.shape != (B, H, s_cap, Dh // 2) or v_codes.shape != k_codes.shape \
-            or k_scale.shape != (B, H, s_cap) or k_zero.shape != (B, H, s_cap) \
-            or v_scale.shape != (B, H, s_cap) or v_zero.shape != (B, H, s_cap):
+    Hkv, s_cap = k_codes.shape[1], k_codes.shape[2]
+    if k_codes.shape != (B, Hkv, s_cap, Dh // 2) or v_codes.shape != k_codes.shape \
+            or k_scale.shape != (B, Hkv, s_cap) or k_zero.shape != (B, Hkv, s_cap) \
+            or v_scale.shape != (B, Hkv, s_cap) or v_zero.shape != (B, Hkv, s_cap):
         raise ValueError("operand shapes do not match")
     if sm_scale is None:
         sm_scale = 1.0 / float(Dh) ** 0.5
@@ -274,9 +313,81 @@ def offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_ze
     if workspace is None:
         workspace = torch.empty((max(need, 4) + 3) // 4, dtype=torch.float32, device=dev)
     _need(workspace, torch.float32, "workspace", 1)
-    _check(lib.offq_kv_attention_decode(_ptr(q), _ptr(k_codes), _ptr(k_scale), _ptr(k_zero),
-                                        _ptr(v_codes), _ptr(v_scale), _ptr(v_zero), B, H, s_cap,
-                                        int(seq_len), Dh, float(sm_scale), int(bool(v_hadamard)),
-                                        _ptr(out), _ptr(workspace), workspace.numel() * 4,
-                                        _stream()), "offq_kv_attention_decode")
+    _check(lib.offq_kv_attention_decode_gqa(_ptr(q), _ptr(k_codes), _ptr(k_scale), _ptr(k_zero),
+                                            _ptr(v_codes), _ptr(v_scale), _ptr(v_zero), B, H, Hkv,
+                                            s_cap, int(seq_len), Dh, float(sm_scale),
+                                            int(bool(v_hadamard)), _ptr(out), _ptr(workspace),
+                                            workspace.numel() * 4, _stream()),
+           "offq_kv_attention_decode")
     return out
+
+
+def _rows(t, name):
+    """2-D view facts of a bf16 tensor with a contiguous last dimension."""
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError(f"{name} must be 2-D with a contiguous last dimension")
+    return t.stride(0)
+
+
+def offq_add_rmsnorm(x, res=None, eps=1e-5, want_h=True, want_y=True):
+    """x, res: bf16 [M, D].  Returns (h, y): h = bf16(x + res) (x if res is None),
+    y = bf16(rmsnorm(h)); either may be None if not wanted."""
+    torch = _torch()
+    _need(x, torch.bfloat16, "x", 2)
+    if res is not None:
+        _need(res, torch.bfloat16, "res", 2)
+        if res.shape != x.shape:
+            raise ValueError("res must match x")
+    M, D = x.shape
+    h = torch.empty((M, D), dtype=torch.bfloat16, device=x.device) if want_h else None
+    y = torch.empty((M, D), dtype=torch.bfloat16, device=x.device) if want_y else None
+    _check(lib.offq_add_rmsnorm(_ptr(x), _rows(x, "x"), _ptr(res),
+                                _rows(res, "res") if res is not None else 0, M, D, float(eps),
+                                _ptr(h), D, _ptr(y), D, _stream()), "offq_add_rmsnorm")
+    return h, y
+
+
+def offq_swiglu(gu):
+    """gu: bf16 [M, 2F] (gate | up).  Returns bf16 [M, F]."""
+    torch = _torch()
+    _need(gu, torch.bfloat16, "gu", 2)
+    M, F2 = gu.shape
+    F = F2 // 2
+    out = torch.empty((M, F), dtype=torch.bfloat16, device=gu.device)
+    _check(lib.offq_swiglu(_ptr(gu), _rows(gu, "gu"), M, F, _ptr(out), F, _stream()), "offq_swiglu")
+    return out
+
+
+def offq_rope_kv_append(qkv, Hq, Hkv, positions, cache, rope_base=500000.0, k_hadamard=True,
+                        v_hadamard=False, debug=False):
+    """qkv: bf16 [M, (Hq + 2 Hkv) * 128]; positions: int32 [M] (device);
+    cache: dict with k_codes/v_codes u8 [M, Hkv, s_cap, 64] and k_scale/v_scale
+    fp16, k_zero/v_zero int16 [M, Hkv, s_cap] (written in place).  Returns
+    (q bf16 [M, Hq, 128], k_y fp32 [M, Hkv, 128] or None, v_y or None)."""
+    torch = _torch()
+    _need(qkv, torch.bfloat16, "qkv", 2)
+    _need(positions, torch.int32, "positions", 1)
+    M = qkv.shape[0]
+    s_cap = cache["k_codes"].shape[2]
+    for n in ("k_codes", "v_codes"):
+        _need(cache[n], torch.uint8, n, 4)
+        if cache[n].shape != (M, Hkv, s_cap, 64) or not cache[n].is_contiguous():
+            raise ValueError(f"{n} must be a contiguous [M, Hkv, s_cap, 64] tensor")
+    for n, dt in (("k_scale", torch.float16), ("v_scale", torch.float16), ("k_zero", torch.int16),
+                  ("v_zero", torch.int16)):
+        _need(cache[n], dt, n, 3)
+        if cache[n].shape != (M, Hkv, s_cap) or not cache[n].is_contiguous():
+            raise ValueError(f"{n} must be a contiguous [M, Hkv, s_cap] tensor")
+    if positions.shape != (M,):
+        raise ValueError("positions must be [M]")
+    dev = qkv.device
+    q = torch.empty((M, Hq, 128), dtype=torch.bfloat16, device=dev)
+    ky = torch.empty((M, Hkv, 128), dtype=torch.float32, device=dev) if debug else None
+    vy = torch.empty((M, Hkv, 128), dtype=torch.float32, device=dev) if debug else None
+    _check(lib.offq_rope_kv_append(_ptr(qkv), _rows(qkv, "qkv"), M, Hq, Hkv, 128, _ptr(positions),
+                                   float(rope_base), int(bool(k_hadamard)), int(bool(v_hadamard)),
+                                   _ptr(q), _ptr(cache["k_codes"]), _ptr(cache["k_scale"]),
+                                   _ptr(cache["k_zero"]), _ptr(cache["v_codes"]),
+                                   _ptr(cache["v_scale"]), _ptr(cache["v_zero"]), s_cap, _ptr(ky),
+                                   _ptr(vy), _stream()), "offq_rope_kv_append")
+    return q, ky, vy

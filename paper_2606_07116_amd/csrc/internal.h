@@ -53,8 +53,22 @@ int64_t kv_attention_workspace_floats(int64_t BH, int64_t seq_len);
 hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
                                       const uint16_t* k_scale, const int16_t* k_zero,
                                       const uint8_t* v_codes, const uint16_t* v_scale,
-                                      const int16_t* v_zero, int64_t BH, int64_t S_cap,
-                                      int64_t seq_len, float sm_scale, bool v_hadamard,
-                                      uint16_t* out, float* workspace, hipStream_t stream);
+                                      const int16_t* v_zero, int64_t BH, int64_t group,
+                                      int64_t S_cap, int64_t seq_len, float sm_scale,
+                                      bool v_hadamard, uint16_t* out, float* workspace,
+                                      hipStream_t stream);
+
+// decoder-layer kernels (layer_ops.hip)
+hipError_t launch_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr,
+                              int64_t M, int64_t D, float eps, uint16_t* h_out, int64_t ldh,
+                              uint16_t* y_out, int64_t ldy, hipStream_t stream);
+hipError_t launch_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t* out,
+                         int64_t ldo, hipStream_t stream);
+hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq,
+                                 int64_t Hkv, const int32_t* positions, double rope_base,
+                                 bool k_had, bool v_had, uint16_t* q_out, uint8_t* kc,
+                                 uint16_t* ks, int16_t* kz, uint8_t* vc, uint16_t* vs,
+                                 int16_t* vz, int64_t s_cap, float* k_dbg, float* v_dbg,
+                                 hipStream_t stream);
 
 }  // namespace offq

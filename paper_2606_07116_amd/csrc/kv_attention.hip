@@ -29,6 +29,9 @@
 //   code bytes so that every AND yields (code of A, code of B) for one
 //   dimension, dotted with the fp16 pair of their weights p sv.
 //
+// Grouped-query attention: query head h of batch b reads the cache of
+// key/value head h / group (group = Hq / Hkv; 1 for plain multi-head).
+//
 // Organisation (split over the sequence, as in flash decoding)
 // * Pass 1: one workgroup of 4 waves per (b, h, chunk of 1024 positions);
 //   a wave owns 256 consecutive positions, in 8 blocks of 32.  A lane
@@ -310,14 +313,15 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
 __global__ __launch_bounds__(THREADS) void kv_attention_chunk_kernel(
     const uint16_t* __restrict__ q, const uint8_t* __restrict__ kc, const uint16_t* __restrict__ ks,
     const int16_t* __restrict__ kz, const uint8_t* __restrict__ vc, const uint16_t* __restrict__ vs,
-    const int16_t* __restrict__ vz, int64_t S_cap, int seq_len, int nchunk, float sm2,
+    const int16_t* __restrict__ vz, int64_t S_cap, int seq_len, int nchunk, int group, float sm2,
     float cnorm, float* __restrict__ ws) {
   __shared__ ChunkSmem S;
   const int blk = (int)__builtin_amdgcn_workgroup_id_x();
-  const int bh = blk / nchunk, chunk = blk - bh * nchunk;
+  const int bh = blk / nchunk, chunk = blk - bh * nchunk;  // bh: query head b * Hq + h
   const int j0 = chunk * CH;
   const int n = min(CH, seq_len - j0);  // positions of this chunk (>= 1)
-  const int64_t row0 = (int64_t)bh * S_cap + j0;
+  // key/value head b * Hkv + h / group, with Hq = group * Hkv
+  const int64_t row0 = (int64_t)(bh / group) * S_cap + j0;
   float* rec = ws + (int64_t)blk * WS_FLOATS;
   if (n == CH)
     attention_chunk<true>(S, q, kc, ks, kz, vc, vs, vz, row0, bh, n, sm2, cnorm, rec);
@@ -397,14 +401,15 @@ int64_t kv_attention_workspace_floats(int64_t BH, int64_t seq_len) {
 hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
                                       const uint16_t* k_scale, const int16_t* k_zero,
                                       const uint8_t* v_codes, const uint16_t* v_scale,
-                                      const int16_t* v_zero, int64_t BH, int64_t S_cap,
-                                      int64_t seq_len, float sm_scale, bool v_hadamard,
-                                      uint16_t* out, float* workspace, hipStream_t stream) {
+                                      const int16_t* v_zero, int64_t BH, int64_t group,
+                                      int64_t S_cap, int64_t seq_len, float sm_scale,
+                                      bool v_hadamard, uint16_t* out, float* workspace,
+                                      hipStream_t stream) {
   const int nchunk = (int)((seq_len + CH - 1) / CH);
   const float cnorm = (float)(1.0 / __builtin_sqrt((double)DH));
   hipLaunchKernelGGL(kv_attention_chunk_kernel, dim3((unsigned)(BH * nchunk)), dim3(THREADS), 0,
                      stream, q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, S_cap,
-                     (int)seq_len, nchunk, sm_scale * LOG2E, cnorm, workspace);
+                     (int)seq_len, nchunk, (int)group, sm_scale * LOG2E, cnorm, workspace);
   hipLaunchKernelGGL(kv_attention_combine_kernel, dim3((unsigned)BH), dim3(DH), 0, stream,
                      workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out);
   return hipGetLastError();

@@ -1,0 +1,242 @@
+// Decoder-layer kernels around the quantized linear layers, for one decode
+// step (one new token per sequence):
+// * add + RMSNorm of the residual stream (RMSNorm's scale is fused into the
+//   following weights offline, sec. 3.1 "Why the L-infinity norm", so the
+//   kernel only normalises);
+// * RoPE on the query and key heads, the per-head online Hadamard H3 on the
+//   key (sec. 3.3 step 2(3)) and the KV4 quantizer (Eq. 1, group = head
+//   dimension, sec. 4.2) writing the new position into the cache;
+// * SwiGLU between the up/gate and down projections (the grouping
+//   permutation P4 is fused into the up/gate weights offline, sec. 3.3
+//   step 2(4), so the kernel is elementwise).
+#include "common.h"
+#include "internal.h"
+
+namespace offq {
+namespace {
+
+__device__ __forceinline__ float wsum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wmax(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wmin(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fminf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// ---------------------------------------------------------------- add + RMSNorm
+constexpr int RN_THREADS = 256;
+
+// h = bf16(fl32(x + res)) (h = x without res); y = bf16(h * fl32(1 / sqrt(mean(h^2) + eps))).
+// One workgroup per row, 8 elements per 16-byte load.
+__global__ __launch_bounds__(RN_THREADS) void add_rmsnorm_kernel(
+    const uint16_t* __restrict__ x, int64_t ldx, const uint16_t* __restrict__ res, int64_t ldr,
+    int D, float eps, uint16_t* __restrict__ h_out, int64_t ldh, uint16_t* __restrict__ y_out,
+    int64_t ldy) {
+  __shared__ float s_red[RN_THREADS / 64];
+  const int tid = (int)__builtin_amdgcn_workitem_id_x();
+  const int64_t row = __builtin_amdgcn_workgroup_id_x();
+  const uint4* xr = reinterpret_cast<const uint4*>(x + row * ldx);
+  const uint4* rr = res ? reinterpret_cast<const uint4*>(res + row * ldr) : nullptr;
+  const int nc = D / 8;
+  auto h8 = [&](int c, float* h) {
+    const uint4 a = xr[c];
+    const uint32_t aw[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      h[2 * k] = bf16_lo(aw[k]);
+      h[2 * k + 1] = bf16_hi(aw[k]);
+    }
+    if (rr) {
+      const uint4 b = rr[c];
+      const uint32_t bw[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        h[2 * k] = bf16_lo(f32_to_bf16_rne(h[2 * k] + bf16_lo(bw[k])));
+        h[2 * k + 1] = bf16_lo(f32_to_bf16_rne(h[2 * k + 1] + bf16_hi(bw[k])));
+      }
+    }
+  };
+  float ss = 0.0f;
+  for (int c = tid; c < nc; c += RN_THREADS) {
+    float h[8];
+    h8(c, h);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) ss = __builtin_fmaf(h[k], h[k], ss);
+    if (h_out) {
+      uint4 o;
+      o.x = bf16x2_rne(h[0], h[1]);
+      o.y = bf16x2_rne(h[2], h[3]);
+      o.z = bf16x2_rne(h[4], h[5]);
+      o.w = bf16x2_rne(h[6], h[7]);
+      reinterpret_cast<uint4*>(h_out + row * ldh)[c] = o;
+    }
+  }
+  if (!y_out) return;
+  ss = wsum(ss);
+  if ((tid & 63) == 0) s_red[tid >> 6] = ss;
+  __syncthreads();
+  ss = s_red[0] + s_red[1] + s_red[2] + s_red[3];
+  const float inv = 1.0f / __builtin_sqrtf(ss / (float)D + eps);
+  for (int c = tid; c < nc; c += RN_THREADS) {
+    float h[8];
+    h8(c, h);
+    uint4 o;
+    o.x = bf16x2_rne(h[0] * inv, h[1] * inv);
+    o.y = bf16x2_rne(h[2] * inv, h[3] * inv);
+    o.z = bf16x2_rne(h[4] * inv, h[5] * inv);
+    o.w = bf16x2_rne(h[6] * inv, h[7] * inv);
+    reinterpret_cast<uint4*>(y_out + row * ldy)[c] = o;
+  }
+}
+
+// ---------------------------------------------------------------- SwiGLU
+// out[m, f] = bf16(fl32(silu(g) * u)), silu(g) = g / (1 + exp(-g)) in fp32,
+// g = gu[m, f], u = gu[m, F + f].  8 outputs per thread.
+__global__ __launch_bounds__(256) void swiglu_kernel(const uint16_t* __restrict__ gu, int64_t ldg,
+                                                     int F, uint16_t* __restrict__ out,
+                                                     int64_t ldo, int64_t total8) {
+  const int64_t i = (int64_t)__builtin_amdgcn_workgroup_id_x() * 256 +
+                    (int)__builtin_amdgcn_workitem_id_x();
+  if (i >= total8) return;
+  const int per_row = F / 8;
+  const int64_t m = i / per_row;
+  const int c = (int)(i - m * per_row);
+  const uint4 g = reinterpret_cast<const uint4*>(gu + m * ldg)[c];
+  const uint4 u = reinterpret_cast<const uint4*>(gu + m * ldg + F)[c];
+  const uint32_t gw[4] = {g.x, g.y, g.z, g.w}, uw[4] = {u.x, u.y, u.z, u.w};
+  uint32_t ow[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float g0 = bf16_lo(gw[k]), g1 = bf16_hi(gw[k]);
+    const float a0 = g0 / (1.0f + expf(-g0)), a1 = g1 / (1.0f + expf(-g1));
+    ow[k] = bf16x2_rne(a0 * bf16_lo(uw[k]), a1 * bf16_hi(uw[k]));
+  }
+  reinterpret_cast<uint4*>(out + m * ldo)[c] = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+}
+
+// ---------------------------------------------------------------- RoPE + KV append
+constexpr int HD = 128;  // head dimension
+
+struct RopeTable {
+  float inv_freq[HD / 2];  // fl32(base^(-2i/128)), computed on the host in double
+};
+
+// One wave per (token m, head slot j): j < Hq query heads, then Hkv key heads,
+// then Hkv value heads of the projection row qkv[m].  Lane l holds dims 2l,
+// 2l + 1.  RoPE pairs dims (i, i + 64) (rotation of the two halves):
+//   x'[i] = x[i] cos(a_i) - x[i + 64] sin(a_i),  x'[i + 64] = x[i + 64] cos(a_i) + x[i] sin(a_i)
+// with a_i = fl32(pos * inv_freq[i]).  Queries are stored as bf16; keys are
+// rounded to bf16, rotated by c H (optional) and quantized; values are
+// quantized (optionally after c H).  The cache row of token m, kv head h is
+// (m * Hkv + h) * s_cap + pos[m]; positions outside [0, s_cap) write nothing.
+__global__ __launch_bounds__(256) void rope_kv_append_kernel(
+    const uint16_t* __restrict__ qkv, int64_t ldq, int M, int Hq, int Hkv,
+    const int32_t* __restrict__ positions, RopeTable tab, int k_had, int v_had,
+    uint16_t* __restrict__ q_out, uint8_t* __restrict__ kc, uint16_t* __restrict__ ks,
+    int16_t* __restrict__ kz, uint8_t* __restrict__ vc, uint16_t* __restrict__ vs,
+    int16_t* __restrict__ vz, int64_t s_cap, float* __restrict__ k_dbg,
+    float* __restrict__ v_dbg) {
+  const int lane = (int)__builtin_amdgcn_workitem_id_x() & 63;
+  const int64_t wid = (int64_t)__builtin_amdgcn_workgroup_id_x() * 4 +
+                      ((int)__builtin_amdgcn_workitem_id_x() >> 6);
+  const int slots = Hq + 2 * Hkv;
+  if (wid >= (int64_t)M * slots) return;
+  const int m = (int)(wid / slots), j = (int)(wid - (int64_t)m * slots);
+  const uint32_t w = reinterpret_cast<const uint32_t*>(qkv + (int64_t)m * ldq + (int64_t)j * HD)[lane];
+  float x0 = bf16_lo(w), x1 = bf16_hi(w);
+  const int pos = positions[m];
+  const bool is_v = j >= Hq + Hkv;
+  if (!is_v) {
+    const float p0 = __shfl_xor(x0, 32), p1 = __shfl_xor(x1, 32);
+    const int i0 = (2 * lane) & 63;
+    float s0, c0, s1, c1;
+    sincosf((float)pos * tab.inv_freq[i0], &s0, &c0);
+    sincosf((float)pos * tab.inv_freq[i0 + 1], &s1, &c1);
+    if (lane < 32) {
+      x0 = x0 * c0 - p0 * s0;
+      x1 = x1 * c1 - p1 * s1;
+    } else {
+      x0 = x0 * c0 + p0 * s0;
+      x1 = x1 * c1 + p1 * s1;
+    }
+    if (j < Hq) {
+      reinterpret_cast<uint32_t*>(q_out + ((int64_t)m * Hq + j) * HD)[lane] = bf16x2_rne(x0, x1);
+      return;
+    }
+    // the key after RoPE is a bf16 activation
+    x0 = bf16_lo(f32_to_bf16_rne(x0));
+    x1 = bf16_lo(f32_to_bf16_rne(x1));
+  }
+  const int h = is_v ? j - Hq - Hkv : j - Hq;
+  if (is_v ? v_had : k_had) {
+    // 128-point FWHT: dim bit 0 inside the lane, bits 1..6 across lanes
+    float a = x0 + x1, b = x0 - x1;
+#pragma unroll
+    for (int s = 0; s < 6; ++s) {
+      const float ya = __shfl_xor(a, 1 << s), yb = __shfl_xor(b, 1 << s);
+      const bool up = (lane >> s) & 1;
+      a = up ? ya - a : a + ya;
+      b = up ? yb - b : b + yb;
+    }
+    const float c = 0.08838834764831845f;  // fl32(1 / sqrt(128))
+    x0 = a * c;
+    x1 = b * c;
+  }
+  float* dbg = is_v ? v_dbg : k_dbg;
+  if (dbg) reinterpret_cast<float2*>(dbg + ((int64_t)m * Hkv + h) * HD)[lane] = make_float2(x0, x1);
+  const float mx = wmax(fmaxf(x0, x1)), mn = wmin(fminf(x0, x1));
+  const QParams p = quant_params(mx, mn);
+  const uint32_t lo = __float_as_uint(p.lo);
+  const uint32_t code = (quant_bits(x0, p) - lo) | ((quant_bits(x1, p) - lo) << 4);
+  if (pos < 0 || (int64_t)pos >= s_cap) return;
+  const int64_t row = ((int64_t)m * Hkv + h) * s_cap + pos;
+  (is_v ? vc : kc)[row * (HD / 2) + lane] = (uint8_t)code;
+  if (lane == 0) {
+    (is_v ? vs : ks)[row] = p.s16;
+    (is_v ? vz : kz)[row] = p.z;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr,
+                              int64_t M, int64_t D, float eps, uint16_t* h_out, int64_t ldh,
+                              uint16_t* y_out, int64_t ldy, hipStream_t stream) {
+  hipLaunchKernelGGL(add_rmsnorm_kernel, dim3((unsigned)M), dim3(RN_THREADS), 0, stream, x, ldx,
+                     res, ldr, (int)D, eps, h_out, ldh, y_out, ldy);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t* out,
+                         int64_t ldo, hipStream_t stream) {
+  const int64_t total8 = M * (F / 8);
+  hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)((total8 + 255) / 256)), dim3(256), 0, stream,
+                     gu, ldg, (int)F, out, ldo, total8);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq,
+                                 int64_t Hkv, const int32_t* positions, double rope_base,
+                                 bool k_had, bool v_had, uint16_t* q_out, uint8_t* kc,
+                                 uint16_t* ks, int16_t* kz, uint8_t* vc, uint16_t* vs,
+                                 int16_t* vz, int64_t s_cap, float* k_dbg, float* v_dbg,
+                                 hipStream_t stream) {
+  RopeTable tab;
+  for (int i = 0; i < HD / 2; ++i)
+    tab.inv_freq[i] = (float)__builtin_pow(rope_base, -2.0 * i / (double)HD);
+  const int64_t waves = M * (Hq + 2 * Hkv);
+  hipLaunchKernelGGL(rope_kv_append_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0,
+                     stream, qkv, ldq, (int)M, (int)Hq, (int)Hkv, positions, tab, k_had ? 1 : 0,
+                     v_had ? 1 : 0, q_out, kc, ks, kz, vc, vs, vz, s_cap, k_dbg, v_dbg);
+  return hipGetLastError();
+}
+
+}  // namespace offq

@@ -180,12 +180,49 @@ int offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g, uint8_t* 
                   "pack_weights");
 }
 
-}  // extern "C"
 
 int64_t offq_kv_attention_workspace_bytes(int64_t B, int64_t H, int64_t seq_len) {
   if (B <= 0 || H <= 0 || seq_len <= 0 || B * H > (1 << 24) || seq_len > (int64_t(1) << 30))
     return 0;
   return offq::kv_attention_workspace_floats(B * H, seq_len) * (int64_t)sizeof(float);
+}
+
+int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
+                                 const uint16_t* k_scale, const int16_t* k_zero,
+                                 const uint8_t* v_codes, const uint16_t* v_scale,
+                                 const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv,
+                                 int64_t s_cap, int64_t seq_len, int32_t head_dim, float sm_scale,
+                                 int32_t v_hadamard, uint16_t* out, void* workspace,
+                                 int64_t workspace_bytes, void* stream) {
+  if (B <= 0 || Hq <= 0 || Hkv <= 0) return fail(OFFQ_ERR_INVALID, "need B, Hq, Hkv > 0");
+  if (Hq % Hkv) return fail(OFFQ_ERR_INVALID, "Hq = %lld is not a multiple of Hkv = %lld",
+                            (long long)Hq, (long long)Hkv);
+  if (head_dim != 128) return fail(OFFQ_ERR_UNSUPPORTED, "head_dim = %d (only 128)", head_dim);
+  if (seq_len < 1 || seq_len > s_cap)
+    return fail(OFFQ_ERR_INVALID, "need 1 <= seq_len <= s_cap");
+  if (B * Hq > (1 << 24) || seq_len > (int64_t(1) << 30) ||
+      s_cap > (int64_t(1) << 40) / (B * Hkv) || B * Hq * ((seq_len + 1023) / 1024) > (1 << 24))
+    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large (B Hq ceil(seq_len / 1024) <= 2^24)");
+  if (v_hadamard != 0 && v_hadamard != 1) return fail(OFFQ_ERR_INVALID, "v_hadamard must be 0 or 1");
+  if (!(sm_scale == sm_scale)) return fail(OFFQ_ERR_INVALID, "sm_scale is NaN");
+  if (!q || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale || !v_zero || !out ||
+      !workspace)
+    return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(q, 2) || !aligned(k_codes, 16) || !aligned(v_codes, 16) || !aligned(k_scale, 2) ||
+      !aligned(k_zero, 2) || !aligned(v_scale, 2) || !aligned(v_zero, 2) || !aligned(out, 2) ||
+      !aligned(workspace, 4))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (codes: 16 B; workspace: 4 B)");
+  const int64_t need = offq_kv_attention_workspace_bytes(B, Hq, seq_len);
+  if (workspace_bytes < need)
+    return fail(OFFQ_ERR_INVALID, "workspace of %lld bytes, need %lld", (long long)workspace_bytes,
+                (long long)need);
+  if (int st = check_device()) return st;
+  return launched(offq::launch_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale,
+                                                   v_zero, B * Hq, Hq / Hkv, s_cap, seq_len,
+                                                   sm_scale, v_hadamard != 0, out,
+                                                   static_cast<float*>(workspace),
+                                                   (hipStream_t)stream),
+                  "kv_attention_decode");
 }
 
 int offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,
@@ -194,31 +231,81 @@ int offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const ui
                              int64_t H, int64_t s_cap, int64_t seq_len, int32_t head_dim,
                              float sm_scale, int32_t v_hadamard, uint16_t* out, void* workspace,
                              int64_t workspace_bytes, void* stream) {
-  if (B <= 0 || H <= 0) return fail(OFFQ_ERR_INVALID, "need B > 0 and H > 0");
-  if (head_dim != 128) return fail(OFFQ_ERR_UNSUPPORTED, "head_dim = %d (only 128)", head_dim);
-  if (seq_len < 1 || seq_len > s_cap)
-    return fail(OFFQ_ERR_INVALID, "need 1 <= seq_len <= s_cap");
-  if (B * H > (1 << 24) || seq_len > (int64_t(1) << 30) || s_cap > (int64_t(1) << 40) / (B * H) ||
-      B * H * ((seq_len + 1023) / 1024) > (1 << 24))
-    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large (B H ceil(seq_len / 1024) <= 2^24)");
-  if (v_hadamard != 0 && v_hadamard != 1) return fail(OFFQ_ERR_INVALID, "v_hadamard must be 0 or 1");
-  if (!(sm_scale == sm_scale)) return fail(OFFQ_ERR_INVALID, "sm_scale is NaN");
-  if (!q || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale || !v_zero || !out ||
-      !workspace)
-    return fail(OFFQ_ERR_INVALID, "null pointer argument");
-  if (!aligned(q, 2) || !aligned(k_codes, 16) || !aligned(v_codes, 4) || !aligned(k_scale, 2) ||
-      !aligned(k_zero, 2) || !aligned(v_scale, 2) || !aligned(v_zero, 2) || !aligned(out, 2) ||
-      !aligned(workspace, 4))
-    return fail(OFFQ_ERR_INVALID, "misaligned pointer (k_codes: 16 B; v_codes, workspace: 4 B)");
-  const int64_t need = offq_kv_attention_workspace_bytes(B, H, seq_len);
-  if (workspace_bytes < need)
-    return fail(OFFQ_ERR_INVALID, "workspace of %lld bytes, need %lld", (long long)workspace_bytes,
-                (long long)need);
-  if (int st = check_device()) return st;
-  return launched(offq::launch_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale,
-                                                   v_zero, B * H, s_cap, seq_len, sm_scale,
-                                                   v_hadamard != 0, out,
-                                                   static_cast<float*>(workspace),
-                                                   (hipStream_t)stream),
-                  "kv_attention_decode");
+  return offq_kv_attention_decode_gqa(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B, H,
+                                      H, s_cap, seq_len, head_dim, sm_scale, v_hadamard, out,
+                                      workspace, workspace_bytes, stream);
 }
+
+int offq_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr, int64_t M,
+                     int64_t D, float eps, uint16_t* h_out, int64_t ldh, uint16_t* y_out,
+                     int64_t ldy, void* stream) {
+  if (M < 0) return fail(OFFQ_ERR_INVALID, "M < 0");
+  if (D < 8 || D % 8) return fail(OFFQ_ERR_INVALID, "D = %lld must be a positive multiple of 8",
+                                  (long long)D);
+  if (D > (1 << 20) || M > (int64_t(1) << 31) - 1)
+    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
+  if (!(eps >= 0.0f) || eps > 1e30f) return fail(OFFQ_ERR_INVALID, "eps must be finite and >= 0");
+  if (!x || (!h_out && !y_out)) return fail(OFFQ_ERR_INVALID, "need x and at least one output");
+  if (ldx < D || ldx % 8 || (res && (ldr < D || ldr % 8)) || (h_out && (ldh < D || ldh % 8)) ||
+      (y_out && (ldy < D || ldy % 8)))
+    return fail(OFFQ_ERR_INVALID, "row strides must be >= D and multiples of 8");
+  if (!aligned(x, 16) || (res && !aligned(res, 16)) || (h_out && !aligned(h_out, 16)) ||
+      (y_out && !aligned(y_out, 16)))
+    return fail(OFFQ_ERR_INVALID, "pointers must be 16-byte aligned");
+  if (M == 0) return ok();
+  if (int st = check_device()) return st;
+  return launched(offq::launch_add_rmsnorm(x, ldx, res, ldr, M, D, eps, h_out, ldh, y_out, ldy,
+                                           (hipStream_t)stream),
+                  "add_rmsnorm");
+}
+
+int offq_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t* out, int64_t ldo,
+                void* stream) {
+  if (M < 0) return fail(OFFQ_ERR_INVALID, "M < 0");
+  if (F < 8 || F % 8) return fail(OFFQ_ERR_INVALID, "F must be a positive multiple of 8");
+  if (ldg < 2 * F || ldg % 8 || ldo < F || ldo % 8)
+    return fail(OFFQ_ERR_INVALID, "need ldg >= 2F, ldo >= F, both multiples of 8");
+  if (F > (1 << 24) || M * (F / 8) > (int64_t(1) << 38))
+    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
+  if (!gu || !out) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(gu, 16) || !aligned(out, 16))
+    return fail(OFFQ_ERR_INVALID, "pointers must be 16-byte aligned");
+  if (M == 0) return ok();
+  if (int st = check_device()) return st;
+  return launched(offq::launch_swiglu(gu, ldg, M, F, out, ldo, (hipStream_t)stream), "swiglu");
+}
+
+int offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq, int64_t Hkv,
+                        int32_t head_dim, const int32_t* positions, double rope_base,
+                        int32_t k_hadamard, int32_t v_hadamard, uint16_t* q_out,
+                        uint8_t* k_codes, uint16_t* k_scale, int16_t* k_zero, uint8_t* v_codes,
+                        uint16_t* v_scale, int16_t* v_zero, int64_t s_cap, float* k_y_debug,
+                        float* v_y_debug, void* stream) {
+  if (M < 0 || Hq <= 0 || Hkv <= 0) return fail(OFFQ_ERR_INVALID, "need M >= 0, Hq, Hkv > 0");
+  if (head_dim != 128) return fail(OFFQ_ERR_UNSUPPORTED, "head_dim = %d (only 128)", head_dim);
+  if (ldq < (Hq + 2 * Hkv) * 128 || ldq % 2)
+    return fail(OFFQ_ERR_INVALID, "ldq must be >= (Hq + 2 Hkv) * 128 and even");
+  if (s_cap < 1) return fail(OFFQ_ERR_INVALID, "s_cap must be >= 1");
+  if (!(rope_base > 1.0) || rope_base > 1e30) return fail(OFFQ_ERR_INVALID, "rope_base must be > 1");
+  if ((k_hadamard != 0 && k_hadamard != 1) || (v_hadamard != 0 && v_hadamard != 1))
+    return fail(OFFQ_ERR_INVALID, "k_hadamard / v_hadamard must be 0 or 1");
+  if (M * (Hq + 2 * Hkv) > (int64_t(1) << 32) || Hq + 2 * Hkv > (1 << 20) ||
+      s_cap > (int64_t(1) << 40) / (M > 0 ? M * Hkv : 1))
+    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
+  if (!qkv || !positions || !q_out || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale ||
+      !v_zero)
+    return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(qkv, 4) || !aligned(positions, 4) || !aligned(q_out, 4) || !aligned(k_scale, 2) ||
+      !aligned(k_zero, 2) || !aligned(v_scale, 2) || !aligned(v_zero, 2) ||
+      (k_y_debug && !aligned(k_y_debug, 8)) || (v_y_debug && !aligned(v_y_debug, 8)))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (qkv, q_out, positions: 4 B; debug: 8 B)");
+  if (M == 0) return ok();
+  if (int st = check_device()) return st;
+  return launched(offq::launch_rope_kv_append(qkv, ldq, M, Hq, Hkv, positions, rope_base,
+                                              k_hadamard != 0, v_hadamard != 0, q_out, k_codes,
+                                              k_scale, k_zero, v_codes, v_scale, v_zero, s_cap,
+                                              k_y_debug, v_y_debug, (hipStream_t)stream),
+                  "rope_kv_append");
+}
+
+}  // extern "C"

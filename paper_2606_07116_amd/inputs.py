@@ -51,6 +51,8 @@ WORKLOADS = {
     "kv_cache": dict(B=8, H=32, S=32768, Dh=128, n_outliers=2, lo=20.0, hi=80.0,
                      seed=5),
     "kv_decode_attention": dict(B=8, H=32, S=32768, Dh=128, seed=6),
+    # one decode step of a Llama-3-8B-shaped layer: 16 sequences at context 4096
+    "decode_layer": dict(M=16, D=4096, Hq=32, Hkv=8, F=14336, g=128, ctx=4096, seed=7),
     "kv_chain_proj": dict(M=8192, K=4096, N=4096, g=4096, n_outliers=4,
                           lo=50.0, hi=200.0, seed=55),
 }

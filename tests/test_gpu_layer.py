@@ -1,0 +1,265 @@
+"""GPU parity: the decoder-layer steps (offq_add_rmsnorm, offq_swiglu,
+offq_rope_kv_append, grouped-query offq_kv_attention_decode) against
+oracle/layer.py, and one whole decode step of a Llama-3-8B-shaped layer
+(D 4096, 32 query / 8 key-value heads, MLP 14336, g = 128) against the oracle
+chain.
+
+Bars: the residual sum h = bf16(fl32(x + r)) is bit-exact; bf16 outputs of
+fp32 arithmetic (RMSNorm, SwiGLU, RoPE) are within one bf16 ulp of the
+oracle's exact value plus a tiny absolute term; the quantized key/value rows
+meet the rotation bound of the KV tests and their codes, scales and
+zero-points are bit-exact against the oracle quantizer fed the same rows.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_07116_amd as offq
+from oracle import attention as OA
+from oracle import gemm as OG
+from oracle import kv as OKV
+from oracle import layer as OL
+from oracle import quantizer as OQ
+from paper_2606_07116_amd import inputs
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def _bf16_dev(a):
+    return P.to_dev_bf16(np.ascontiguousarray(a, dtype=np.float32))
+
+
+def _within_ulp(got, ref, atol=0.0):
+    got = np.asarray(got, np.float64)
+    tol = OG.bf16_ulp(ref) * (1 + 1e-9) + atol
+    bad = np.abs(got - ref) > tol
+    assert not bad.any(), (f"{bad.sum()} values off by more than 1 bf16 ulp, e.g. "
+                           f"gpu {got[bad][:4]} ref {ref[bad][:4]}")
+
+
+def _rand_bf16(shape, seed, scale=1.0):
+    return inputs.round_to_bf16(
+        np.random.default_rng(seed).standard_normal(shape).astype(np.float32) * np.float32(scale))
+
+
+@pytest.mark.parametrize("M,D,with_res", [(1, 8, False), (16, 4096, True), (5, 14336, True),
+                                          (3, 8000, False), (7, 4096, False)])
+def test_add_rmsnorm(M, D, with_res):
+    x = _rand_bf16((M, D), M + D, 3.0)
+    r = _rand_bf16((M, D), M + D + 1) if with_res else None
+    h, y = offq.offq_add_rmsnorm(_bf16_dev(x), _bf16_dev(r) if with_res else None, eps=1e-5)
+    torch.cuda.synchronize()
+    h_ref, y_ref = OL.add_rmsnorm(x, r, 1e-5)
+    assert np.array_equal(P.host(h.float()), h_ref)
+    _within_ulp(P.host(y.float()), y_ref)
+
+
+def test_add_rmsnorm_outputs_alone():
+    x = _rand_bf16((4, 64), 9)
+    r = _rand_bf16((4, 64), 10)
+    h, y = offq.offq_add_rmsnorm(_bf16_dev(x), _bf16_dev(r), want_y=False)
+    assert y is None
+    h2, y2 = offq.offq_add_rmsnorm(_bf16_dev(x), _bf16_dev(r), want_h=False)
+    torch.cuda.synchronize()
+    assert h2 is None
+    h_ref, y_ref = OL.add_rmsnorm(x, r, 1e-5)
+    assert np.array_equal(P.host(h.float()), h_ref)
+    _within_ulp(P.host(y2.float()), y_ref)
+
+
+@pytest.mark.parametrize("M,F", [(1, 8), (16, 14336), (3, 1000)])
+def test_swiglu(M, F):
+    gu = _rand_bf16((M, 2 * F), F, 4.0)
+    out = offq.offq_swiglu(_bf16_dev(gu))
+    torch.cuda.synchronize()
+    ref = OL.swiglu(gu)
+    # exp in fp32 is accurate to a few ulp: the exact value rounds to one of
+    # the two bf16 neighbours, plus a floor for products that underflow
+    _within_ulp(P.host(out.float()), ref, atol=1e-30)
+
+
+def _cache(M, Hkv, s_cap, fill):
+    z = lambda *s, dt: torch.full(s, fill, dtype=dt, device=P.DEV)
+    return dict(k_codes=z(M, Hkv, s_cap, 64, dt=torch.uint8), v_codes=z(M, Hkv, s_cap, 64, dt=torch.uint8),
+                k_scale=z(M, Hkv, s_cap, dt=torch.float16), v_scale=z(M, Hkv, s_cap, dt=torch.float16),
+                k_zero=z(M, Hkv, s_cap, dt=torch.int16), v_zero=z(M, Hkv, s_cap, dt=torch.int16))
+
+
+@pytest.mark.parametrize("M,Hq,Hkv,s_cap,v_had", [(16, 32, 8, 300, False), (3, 4, 4, 17, True),
+                                                  (1, 8, 1, 5000, False)])
+def test_rope_kv_append(M, Hq, Hkv, s_cap, v_had):
+    qkv = _rand_bf16((M, (Hq + 2 * Hkv) * 128), M * Hq, 2.0)
+    rng = np.random.default_rng(s_cap)
+    pos = rng.integers(0, s_cap, size=M).astype(np.int32)
+    cache = _cache(M, Hkv, s_cap, 7)
+    q, ky, vy = offq.offq_rope_kv_append(_bf16_dev(qkv), Hq, Hkv, torch.from_numpy(pos).to(P.DEV),
+                                         cache, rope_base=500000.0, v_hadamard=v_had, debug=True)
+    torch.cuda.synchronize()
+    q_ref, ky_ref, vy_ref = OL.kv_rows(qkv, Hq, Hkv, pos, 500000.0, True, v_had)
+    _within_ulp(P.host(q.float()), OL.bf16(q_ref), atol=1e-6 * np.abs(q_ref).max())
+    ky, vy = P.host(ky), P.host(vy)
+    # rotation rows: fp32 RoPE + a bf16 rounding of the key before H3 (a
+    # neighbouring bf16 in a few dims moves the rotated row by up to one bf16
+    # ulp of those inputs / sqrt(128)), then the 7-stage fp32 butterfly
+    k_in = OL.bf16(OL.rope(qkv.reshape(M, Hq + 2 * Hkv, 128)[:, Hq:Hq + Hkv], pos[:, None], 500000.0))
+    kb = (7 + 2) * 2.0 ** -24 * np.abs(k_in).sum(-1, keepdims=True) / math.sqrt(128) + \
+        OG.bf16_ulp(k_in).sum(-1, keepdims=True) / math.sqrt(128) + 1e-5 * np.abs(k_in).max(-1, keepdims=True)
+    assert np.all(np.abs(ky - ky_ref) <= kb)
+    v_in = qkv.reshape(M, Hq + 2 * Hkv, 128)[:, Hq + Hkv:].astype(np.float64)
+    vb = (7 + 2) * 2.0 ** -24 * np.abs(v_in).sum(-1, keepdims=True) / math.sqrt(128)
+    assert np.all(np.abs(vy - vy_ref) <= (vb if v_had else 0.0))
+    # the cache: the written row is the oracle quantizer of the GPU's row; every other row untouched
+    for name, rows in (("k", ky), ("v", vy)):
+        codes, s, z = OKV.kv_quantize(rows.reshape(-1, 128))
+        packed = OQ.pack_nibbles(codes).reshape(M, Hkv, 64)
+        c = P.host(cache[name + "_codes"])
+        sc = P.fp16_bits(P.host(cache[name + "_scale"]))
+        zz = P.host(cache[name + "_zero"])
+        for m in range(M):
+            assert np.array_equal(c[m, :, pos[m]], packed[m])
+            assert np.array_equal(sc[m, :, pos[m]], P.fp16_bits(s.reshape(M, Hkv)[m]))
+            assert np.array_equal(zz[m, :, pos[m]], z.reshape(M, Hkv)[m])
+            others = np.delete(np.arange(s_cap), pos[m])
+            assert np.all(c[m][:, others] == 7)
+            assert np.all(zz[m][:, others] == 7)
+
+
+def test_rope_kv_append_position_outside_cache_writes_nothing():
+    M, Hq, Hkv, s_cap = 2, 2, 1, 8
+    qkv = _rand_bf16((M, 4 * 128), 3)
+    cache = _cache(M, Hkv, s_cap, 7)
+    pos = torch.tensor([-1, 8], dtype=torch.int32, device=P.DEV)
+    q, _, _ = offq.offq_rope_kv_append(_bf16_dev(qkv), Hq, Hkv, pos, cache)
+    torch.cuda.synchronize()
+    for t in cache.values():
+        assert torch.all(t == 7)
+    assert q.shape == (M, Hq, 128)
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,S,seq_len", [(2, 32, 8, 2100, 2100), (1, 8, 2, 1500, 1025),
+                                                (3, 4, 1, 64, 50)])
+def test_gqa_attention(B, Hq, Hkv, S, seq_len):
+    q = inputs.queries(B, Hq, 128, seed=S)
+    kc, ks, kz = inputs.kv4_cache(B, Hkv, S, 128, seed=S)
+    vc, vs, vz = inputs.kv4_cache(B, Hkv, S, 128, seed=S + 1)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(P.DEV)
+    out = offq.offq_kv_attention_decode(P.to_dev_bf16(q), dev(kc), dev(ks), dev(kz), dev(vc),
+                                        dev(vs), dev(vz), seq_len)
+    torch.cuda.synchronize()
+    ref = OA.decode_attention(q, kc, ks, kz, vc, vs, vz, seq_len, 1 / math.sqrt(128))
+    got = P.host(out.float()).astype(np.float64)
+    g = Hq // Hkv
+    v = OA.dequantize_rows(vc[:, :, :seq_len], vs[:, :, :seq_len], vz[:, :, :seq_len])
+    mag = np.repeat(np.abs(v).max(axis=(2, 3)), g, axis=1)[..., None]
+    assert np.all(np.abs(got - ref) <= 2.0 ** -8 * (1 + 2.0 ** -5) * np.abs(ref) + 2.0 ** -11 * mag)
+
+
+def _llama_layer(M, ctx, seed=0, D=4096, Hq=32, Hkv=8, F=14336, g=128):
+    """Seeded weights, activations and a filled 4-bit cache for one decode step."""
+    rng = np.random.default_rng(seed)
+    x = inputs.round_to_bf16(rng.standard_normal((M, D)).astype(np.float32))
+    shapes = {"qkv": ((Hq + 2 * Hkv) * 128, D), "o": (D, Hq * 128), "ug": (2 * F, D), "down": (D, F)}
+    wf = {k: inputs.weights(*s, seed=seed + i, std=1.0 / math.sqrt(s[1]))
+          for i, (k, s) in enumerate(shapes.items())}
+    s_cap = ctx + 1
+    kc, ks, kz = inputs.kv4_cache(M, Hkv, s_cap, 128, seed=seed)
+    vc, vs, vz = inputs.kv4_cache(M, Hkv, s_cap, 128, seed=seed + 1)
+    cache = dict(k_codes=kc, k_scale=ks, k_zero=kz, v_codes=vc, v_scale=vs, v_zero=vz)
+    cfg = dict(Hq=Hq, Hkv=Hkv, g=g, eps=1e-5, rope_base=500000.0)
+    return x, wf, cache, np.full(M, ctx, np.int32), ctx + 1, cfg
+
+
+def run_gpu_layer(x, wpk, cache, pos, seq_len, cfg, debug=False):
+    """One decode step through the C ABI: the sequence of library calls a
+    serving loop makes for a layer.  With debug, also the fp32 rows the
+    quantizers saw (the rotated MLP down input and the new K/V rows)."""
+    Hq, Hkv, g, eps = cfg["Hq"], cfg["Hkv"], cfg["g"], cfg["eps"]
+    M = x.shape[0]
+    _, y0 = offq.offq_add_rmsnorm(x, None, eps, want_h=False)
+    c, s, z, _ = offq.offq_rotate_quantize(y0, g, apply_hadamard=False)
+    qkv, _ = offq.offq_w4a4_gemm(c, s, z, *wpk["qkv"], g)
+    q, ky, vy = offq.offq_rope_kv_append(qkv, Hq, Hkv, pos, cache, rope_base=cfg["rope_base"],
+                                         debug=debug)
+    o = offq.offq_kv_attention_decode(q, cache["k_codes"], cache["k_scale"], cache["k_zero"],
+                                      cache["v_codes"], cache["v_scale"], cache["v_zero"], seq_len)
+    c, s, z, _ = offq.offq_rotate_quantize(o.reshape(M, Hq * 128), g, apply_hadamard=False)
+    attn_out, _ = offq.offq_w4a4_gemm(c, s, z, *wpk["o"], g)
+    h1, y1 = offq.offq_add_rmsnorm(x, attn_out, eps)
+    c, s, z, _ = offq.offq_rotate_quantize(y1, g, apply_hadamard=False)
+    gu, _ = offq.offq_w4a4_gemm(c, s, z, *wpk["ug"], g)
+    a = offq.offq_swiglu(gu)
+    c, s, z, ya = offq.offq_rotate_quantize(a, g, apply_hadamard=True, debug=debug)
+    down, _ = offq.offq_w4a4_gemm(c, s, z, *wpk["down"], g)
+    out, _ = offq.offq_add_rmsnorm(h1, down, eps, want_y=False)
+    return out, dict(y0=y0, qkv=qkv, q=q, k_y=ky, v_y=vy, o=o, attn_out=attn_out, h1=h1, y1=y1,
+                     gu=gu, a=a, a_rot=ya, down=down)
+
+
+def _gemm_bar(got, y_in, weights, g, y_rot=None):
+    """The W4A4 GEMM bar of the GEMM tests for the oracle layer fed the same
+    bf16 input (or, with an online rotation, the same fp32 rotated rows, so
+    that both sides take the 4-bit decisions on identical values)."""
+    q_w, sw = weights
+    yq = np.asarray(y_rot if y_rot is not None else y_in, np.float32)
+    q, s, z = OQ.quantize_groups(yq, g)
+    P.check_output(np.asarray(got, np.float64), OG.int_gemm_groups(q, q_w, g), s, z, sw,
+                   OQ.colsum(q_w, g))
+
+
+@pytest.mark.parametrize("M,ctx", [(4, 300), (16, 2048)])
+def test_decode_layer_chain(M, ctx):
+    """Stage by stage, each GPU step meets its bar against the oracle step fed
+    the previous GPU step's output (the steps end in 4-bit decisions, which
+    both sides then take on the same values); end to end, the GPU step stays
+    close to the oracle chain run from the same seeded inputs."""
+    x, wf, cache, pos, seq_len, cfg = _llama_layer(M, ctx)
+    g, eps = cfg["g"], cfg["eps"]
+    weights = {k: OQ.quantize_weights(w) for k, w in wf.items()}
+    wpk = {k: offq.offq_pack_weights(torch.from_numpy(w).to(P.DEV), g) for k, w in wf.items()}
+    dcache = {k: torch.from_numpy(np.ascontiguousarray(v)).to(P.DEV) for k, v in cache.items()}
+    out, it = run_gpu_layer(_bf16_dev(x), wpk, dcache, torch.from_numpy(pos).to(P.DEV), seq_len,
+                            cfg, debug=True)
+    torch.cuda.synchronize()
+    H = {k: (P.host(v.float()) if v.dtype == torch.bfloat16 else P.host(v)) for k, v in it.items()}
+    Hq, Hkv = cfg["Hq"], cfg["Hkv"]
+    # norm and residual steps
+    _within_ulp(H["y0"], OL.add_rmsnorm(x, None, eps)[1])
+    h1_ref, y1_ref = OL.add_rmsnorm(x, H["attn_out"], eps)
+    assert np.array_equal(H["h1"], h1_ref)
+    _within_ulp(H["y1"], y1_ref)
+    assert np.array_equal(P.host(out.float()), OL.add_rmsnorm(H["h1"], H["down"], eps)[0])
+    # the four quantized linear layers
+    _gemm_bar(H["qkv"], H["y0"], weights["qkv"], g)
+    _gemm_bar(H["attn_out"], H["o"].reshape(M, -1), weights["o"], g)
+    _gemm_bar(H["gu"], H["y1"], weights["ug"], g)
+    from oracle import hadamard as OH
+    assert np.all(np.abs(H["a_rot"] - OH.rotate(H["a"], g)) <=
+                  9 * 2.0 ** -24 * np.abs(H["a"]).reshape(M, -1, g).sum(-1).repeat(g, -1) / math.sqrt(g))
+    _gemm_bar(H["down"], H["a"], weights["down"], g, y_rot=H["a_rot"])
+    _within_ulp(H["a"], OL.swiglu(H["gu"]), atol=1e-30)
+    # RoPE + the new cache rows
+    q_ref, ky_ref, vy_ref = OL.kv_rows(H["qkv"], Hq, Hkv, pos, cfg["rope_base"])
+    _within_ulp(H["q"], OL.bf16(q_ref), atol=1e-6 * np.abs(q_ref).max())
+    for name, rows in (("k", H["k_y"]), ("v", H["v_y"])):
+        codes, s_, z_ = OKV.kv_quantize(rows.reshape(-1, 128))
+        got = P.host(dcache[name + "_codes"])[np.arange(M), :, pos]
+        assert np.array_equal(got, OQ.pack_nibbles(codes).reshape(M, Hkv, 64)), name
+    assert np.array_equal(H["v_y"], vy_ref)
+    # attention over the cache the GPU wrote, with the GPU's query
+    hc = {k: P.host(v) for k, v in dcache.items()}
+    o_ref = OA.decode_attention(H["q"], hc["k_codes"], hc["k_scale"], hc["k_zero"], hc["v_codes"],
+                                hc["v_scale"], hc["v_zero"], seq_len, 1 / math.sqrt(128))
+    v = OA.dequantize_rows(hc["v_codes"][:, :, :seq_len], hc["v_scale"][:, :, :seq_len],
+                           hc["v_zero"][:, :, :seq_len])
+    mag = np.repeat(np.abs(v).max(axis=(2, 3)), Hq // Hkv, axis=1)[..., None]
+    assert np.all(np.abs(H["o"] - o_ref) <= 2.0 ** -8 * (1 + 2.0 ** -5) * np.abs(o_ref) + 2.0 ** -11 * mag)
+    # end to end from the seeded inputs: rounding-order differences upstream
+    # flip a few 4-bit codes downstream and each quantized layer amplifies
+    # them (measured: 0.05 % at the attention output, 10 % on the MLP down
+    # output, ~1 % on the residual stream); the bar bounds the residual stream
+    ref, _, _ = OL.decode_layer(x, weights, cache, pos, seq_len, cfg)
+    rel = np.linalg.norm(P.host(out.float()) - ref) / np.linalg.norm(ref)
+    assert rel < 5e-2, rel

@@ -1,0 +1,149 @@
+"""Pins of the decoder-layer oracle (oracle/layer.py): RMSNorm against torch's
+fp64 rms_norm and closed forms, RoPE against a complex-number rotation and its
+relative-position property, SwiGLU against torch's silu, the KV step against
+the KV quantizer, grouped-query attention against repeated heads, and the
+whole quantized layer against the same layer without quantization."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as OA
+from oracle import hadamard as OH
+from oracle import kv as OKV
+from oracle import layer as OL
+from oracle import quantizer as OQ
+from paper_2606_07116_amd import inputs
+
+
+def test_add_rmsnorm_matches_torch_and_closed_form():
+    x = inputs.round_to_bf16(np.random.default_rng(0).standard_normal((5, 64)).astype(np.float32) * 3)
+    r = inputs.round_to_bf16(np.random.default_rng(1).standard_normal((5, 64)).astype(np.float32))
+    h, y = OL.add_rmsnorm(x, r, 1e-5)
+    hs = (torch.from_numpy(x) + torch.from_numpy(r)).to(torch.bfloat16).double()  # fp32 add, bf16
+    assert np.array_equal(h, hs.numpy())
+    ref = torch.nn.functional.rms_norm(hs, (64,), eps=1e-5).numpy()
+    assert np.all(np.abs(y - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-30)
+    # a constant row c normalises to sign(c) / sqrt(1 + eps / c^2)
+    c = np.full((1, 16), -0.75, np.float32)
+    _, yc = OL.add_rmsnorm(c, None, 0.0)
+    assert np.all(yc == -1.0)
+    # scale invariance by powers of two
+    _, y2 = OL.add_rmsnorm(x * 4, None, 0.0)
+    _, y1 = OL.add_rmsnorm(x, None, 0.0)
+    assert np.array_equal(y1, y2)
+
+
+def test_rope_is_a_complex_rotation():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((3, 4, 128))
+    pos = np.array([0, 7, 4095])
+    out = OL.rope(x, pos[:, None], 500000.0)
+    inv = OL.rope_inv_freq(500000.0)
+    z = (x[..., :64] + 1j * x[..., 64:]) * np.exp(
+        1j * (pos[:, None, None].astype(np.float32) * inv).astype(np.float64))
+    assert np.allclose(out[..., :64], z.real, rtol=0, atol=1e-12)
+    assert np.allclose(out[..., 64:], z.imag, rtol=0, atol=1e-12)
+    assert np.array_equal(out[0], x[0])  # position 0: identity
+    # pairs keep their norm
+    n0 = x[..., :64] ** 2 + x[..., 64:] ** 2
+    n1 = out[..., :64] ** 2 + out[..., 64:] ** 2
+    assert np.allclose(n0, n1, rtol=1e-12)
+    # the frequencies: base^(-2i/128), the first one 1
+    assert inv[0] == 1.0 and abs(inv[1] - 500000.0 ** (-2 / 128)) < 1e-7
+
+
+def test_rope_scores_depend_on_relative_position():
+    rng = np.random.default_rng(3)
+    q, k = rng.standard_normal(128), rng.standard_normal(128)
+    # small positions: the fp32 angles are exact products, so the identity is exact up to fp64
+    s1 = OL.rope(q, np.array(9), 10000.0) @ OL.rope(k, np.array(5), 10000.0)
+    s2 = OL.rope(q, np.array(4), 10000.0) @ OL.rope(k, np.array(0), 10000.0)
+    assert abs(s1 - s2) < 1e-5 * (np.abs(q).sum() * np.abs(k).max())
+
+
+def test_swiglu_matches_torch():
+    gu = inputs.round_to_bf16(np.random.default_rng(4).standard_normal((3, 2 * 40)).astype(np.float32) * 4)
+    out = OL.swiglu(gu)
+    g = torch.from_numpy(gu[:, :40]).double()
+    ref = (torch.nn.functional.silu(g) * torch.from_numpy(gu[:, 40:]).double()).numpy()
+    assert np.allclose(out, ref, rtol=1e-14, atol=0)
+    assert np.all(OL.swiglu(np.zeros((1, 8))) == 0)
+
+
+def test_kv_rows_follow_rope_then_hadamard():
+    M, Hq, Hkv = 2, 4, 2
+    qkv = inputs.round_to_bf16(np.random.default_rng(5).standard_normal((M, (Hq + 2 * Hkv) * 128)).astype(np.float32))
+    pos = np.array([3, 100])
+    q, ky, vy = OL.kv_rows(qkv, Hq, Hkv, pos, 500000.0)
+    heads = qkv.reshape(M, Hq + 2 * Hkv, 128).astype(np.float64)
+    assert np.allclose(q[1, 2], OL.rope(heads[1, 2], np.array(100), 500000.0), atol=0)
+    k_bf = OL.bf16(OL.rope(heads[0, Hq + 1], np.array(3), 500000.0))
+    h = OH.sylvester(128).astype(np.float64) / math.sqrt(128)
+    assert np.allclose(ky[0, 1], k_bf @ h, rtol=0, atol=1e-12)
+    assert np.array_equal(vy[1, 0], heads[1, Hq + Hkv])  # no rotation on V
+
+
+def test_gqa_attention_equals_repeated_heads():
+    B, Hq, Hkv, S = 2, 8, 2, 30
+    q = inputs.queries(B, Hq, 128, seed=1)
+    kc, ks, kz = inputs.kv4_cache(B, Hkv, S, 128, seed=1)
+    vc, vs, vz = inputs.kv4_cache(B, Hkv, S, 128, seed=2)
+    o = OA.decode_attention(q, kc, ks, kz, vc, vs, vz, S, 0.1)
+    rep = [np.repeat(a, 4, axis=1) for a in (kc, ks, kz, vc, vs, vz)]
+    assert np.array_equal(o, OA.decode_attention(q, *rep, S, 0.1))
+    # query head 5 reads key/value head 1
+    one = OA.decode_attention(q[:, 5:6], *[a[:, 1:2] for a in (kc, ks, kz, vc, vs, vz)], S, 0.1)
+    assert np.array_equal(o[:, 5:6], one)
+
+
+def _layer_case(M=3, D=256, Hq=2, Hkv=1, F=384, s_cap=40, seq_len=20, g=128, seed=0):
+    rng = np.random.default_rng(seed)
+    cfg = dict(Hq=Hq, Hkv=Hkv, g=g, eps=1e-5, rope_base=500000.0)
+    x = inputs.round_to_bf16(rng.standard_normal((M, D)).astype(np.float32))
+    shapes = {"qkv": ((Hq + 2 * Hkv) * 128, D), "o": (D, Hq * 128), "ug": (2 * F, D), "down": (D, F)}
+    wf = {k: rng.standard_normal(s).astype(np.float32) * np.float32(1 / math.sqrt(s[1]))
+          for k, s in shapes.items()}
+    weights = {k: OQ.quantize_weights(w) for k, w in wf.items()}
+    kc, ks, kz = inputs.kv4_cache(M, Hkv, s_cap, 128, seed=seed)
+    vc, vs, vz = inputs.kv4_cache(M, Hkv, s_cap, 128, seed=seed + 1)
+    cache = dict(k_codes=kc, k_scale=ks, k_zero=kz, v_codes=vc, v_scale=vs, v_zero=vz)
+    pos = np.full(M, seq_len - 1)
+    return x, weights, wf, cache, pos, seq_len, cfg
+
+
+def test_decode_layer_writes_the_cache_and_approximates_the_float_layer():
+    x, weights, wf, cache, pos, seq_len, cfg = _layer_case()
+    out, inter, new = OL.decode_layer(x, weights, cache, pos, seq_len, cfg)
+    assert out.shape == x.shape and np.all(np.isfinite(out))
+    # only position seq_len - 1 of the cache changed
+    for k in cache:
+        diff = np.argwhere(np.any(np.atleast_3d(new[k] != cache[k]).reshape(new[k].shape[:3] + (-1,)), axis=-1))
+        assert set(map(int, diff[:, 2])) <= {seq_len - 1}, k
+    # the same layer in fp64 without activation quantization (weights dequantized)
+    def lin(y, name):
+        q_w, sw = weights[name]
+        return y @ (q_w.astype(np.float64) * sw.astype(np.float64)[:, None]).T
+    _, y0 = OL.add_rmsnorm(x, None, cfg["eps"])
+    qkv = lin(y0, "qkv")
+    q, ky, vy = OL.kv_rows(qkv, cfg["Hq"], cfg["Hkv"], pos, cfg["rope_base"])
+    kf = OA.dequantize_rows(new["k_codes"], new["k_scale"], new["k_zero"])
+    vf = OA.dequantize_rows(new["v_codes"], new["v_scale"], new["v_zero"])
+    kf[:, :, seq_len - 1] = ky
+    vf[:, :, seq_len - 1] = vy
+    qr = q @ (OH.sylvester(128) / math.sqrt(128))
+    s = np.einsum("bhd,bhsd->bhs", qr, kf[:, :, :seq_len]) / math.sqrt(128)
+    o = np.einsum("bhs,bhsd->bhd", OA.softmax(s), vf[:, :, :seq_len]).reshape(x.shape[0], -1)
+    h1 = x + lin(o, "o")
+    _, y1 = OL.add_rmsnorm(h1, None, cfg["eps"])
+    # the down projection's weights act on H4-rotated inputs (H4 fused into them offline)
+    ref = h1 + lin(OH.rotate(OL.swiglu(lin(y1, "ug")), cfg["g"]), "down")
+    # 4-bit activations with per-128 groups add ~10 % relative noise per
+    # linear layer on Gaussian inputs (step ~ range / 15, noise step / sqrt 12);
+    # the chain measures ~13 %.  A sign error in RoPE, a missing H4 or a
+    # gate/up swap each give errors near 100 %.
+    err = np.linalg.norm(out - ref) / np.linalg.norm(ref)
+    assert err < 0.25, err
+    # and the intermediates are consistent with the final output
+    assert np.array_equal(out, OL.add_rmsnorm(inter["h1"], inter["down"], cfg["eps"])[0])
