@@ -280,6 +280,89 @@ int offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq,
                         uint16_t* v_scale, int16_t* v_zero, int64_t s_cap, float* k_y_debug,
                         float* v_y_debug, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Offline calibration (sec. 3.1 top-1 PCA, sec. 3.2 group-wise offsetting,
+ * sec. 3.3 steps 1-2): from calibration activations to the fused, permuted
+ * and rotated fp32 weights that offq_pack_weights then quantizes.  These run
+ * once per model, not in the online path; offq_eigh blocks the calling thread
+ * (it reads the convergence measure back after every sweep).
+ * ------------------------------------------------------------------------- */
+
+/* Bytes of workspace offq_top1_select needs: one float per token. */
+int64_t offq_top1_workspace_bytes(int64_t n_seq, int64_t seq_len);
+
+/*
+ * offq_top1_select -- per calibration sequence, the token whose row has the
+ * largest L-infinity norm (the first such token on ties), copied as fp32:
+ *   x bf16: token t of sequence s at x + s*ld_seq + t*ld_tok, D channels
+ *     (D, ld_tok, ld_seq multiples of 8; x 16-byte aligned);
+ *   idx int32 [n_seq] (the selected token), X fp32 [n_seq, D] (row stride ldX).
+ * Inputs must be finite.
+ */
+int offq_top1_select(const uint16_t* x, int64_t n_seq, int64_t seq_len, int64_t D, int64_t ld_tok,
+                     int64_t ld_seq, int32_t* idx, float* X, int64_t ldX, void* workspace,
+                     int64_t workspace_bytes, void* stream);
+
+/* offq_channel_absmax -- out fp64 [D] = max over rows of |x[r, c]| (bf16 x
+ * [rows, D], row stride ldx): the statistic that picks the outlier channels of
+ * the down-projection input (sec. 3.3 step 2(4)). */
+int offq_channel_absmax(const uint16_t* x, int64_t rows, int64_t D, int64_t ldx, double* out,
+                        void* stream);
+
+/* offq_gram -- C fp64 [D, D] (row stride ldC) = X^T X / N for X fp32 [N, D]
+ * (row stride ldX), accumulated in fp64 (Eq. 2; zero-mean assumed, as there).
+ * C is exactly symmetric. */
+int offq_gram(const float* X, int64_t N, int64_t D, int64_t ldX, double* C, int64_t ldC,
+              void* stream);
+
+/* Bytes of workspace offq_eigh needs (about 32 D^2). */
+int64_t offq_eigh_workspace_bytes(int64_t D);
+
+/*
+ * offq_eigh -- C = U diag(evals) U^T for symmetric C fp64 [D, D] (row stride
+ * ldC; read only), D even, 2 <= D <= 8192: evals fp64 [D] descending, U fp64
+ * [D, D] (row stride ldU) with eigenvector k in column k, its entry of largest
+ * magnitude positive.  Parallel cyclic Jacobi in fp64 until the off-diagonal
+ * Frobenius norm is at most tol times the whole norm, or max_sweeps sweeps;
+ * *sweeps and *rel_off (nullable) report what was reached.  workspace: at least
+ * offq_eigh_workspace_bytes(D), 16-byte aligned.
+ */
+int offq_eigh(const double* C, int64_t D, int64_t ldC, double* evals, double* U, int64_t ldU,
+              void* workspace, int64_t workspace_bytes, int32_t max_sweeps, double tol,
+              int32_t* sweeps, double* rel_off, void* stream);
+
+/*
+ * offq_group_permutation -- the sorted grouping of sec. 3.2 / sec. 4.3 for D
+ * channels in groups of g (D a multiple of g): with G = D / g, the G channels
+ * of largest key lead the groups in descending order (perm[b g] = the b-th
+ * largest), the others fill slots 1..g-1 of the groups in ascending key order
+ * (ties by channel index).  perm int32 [D]: new slot -> original channel.
+ * workspace: D int32.
+ */
+int offq_group_permutation(const double* key, int64_t D, int32_t g, int32_t* perm,
+                           void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * offq_build_rotation -- R fp32 [D, D] (row stride ldR) = U P B, with U fp64
+ * [D, D] (NULL: identity), P the permutation matrix of perm (NULL: identity;
+ * column s of U P is column perm[s] of U) and B = blockdiag(H_g / sqrt(g)) on
+ * consecutive groups of g columns when apply_hadamard (else identity); the
+ * product is formed in fp64.  D <= 8192, D a multiple of g (power of two).
+ */
+int offq_build_rotation(const double* U, int64_t ldU, int64_t D, const int32_t* perm, int32_t g,
+                        int32_t apply_hadamard, float* R, int64_t ldR, void* stream);
+
+/* offq_fuse_weights -- W_out fp32 [N, K] = W R for W fp32 [N, K] and R fp32
+ * [K, K] (the rotation a linear layer's input receives, fused into its
+ * weights: y = x W^T = (x R)(W R)^T). */
+int offq_fuse_weights(const float* W, int64_t ldW, int64_t N, int64_t K, const float* R,
+                      int64_t ldR, float* W_out, int64_t ldo, void* stream);
+
+/* offq_permute_rows -- W_out[s, :] = W[perm[s], :] (fp32 [N, K]): an output-
+ * channel permutation fused into the producing weights (P4 into up/gate). */
+int offq_permute_rows(const float* W, int64_t ldW, int64_t N, int64_t K, const int32_t* perm,
+                      float* W_out, int64_t ldo, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

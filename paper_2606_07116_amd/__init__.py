@@ -12,6 +12,9 @@ arguments.  Entry points (same names as ``include/offq.h``):
     offq_swiglu(gu)
     offq_rope_kv_append(qkv, Hq, Hkv, positions, cache, rope_base=500000.0, ...)
 
+Offline calibration: offq_top1_select, offq_channel_absmax, offq_gram, offq_eigh,
+offq_group_permutation, offq_build_rotation, offq_fuse_weights, offq_permute_rows.
+
 Importing the package loads the library and raises if it has not been built.
 """
 
@@ -20,6 +23,14 @@ from ._lib import (  # noqa: F401
     EXPORTED,
     OffqError,
     last_error,
+    offq_build_rotation,
+    offq_channel_absmax,
+    offq_eigh,
+    offq_fuse_weights,
+    offq_gram,
+    offq_group_permutation,
+    offq_permute_rows,
+    offq_top1_select,
     offq_add_rmsnorm,
     offq_rope_kv_append,
     offq_swiglu,

@@ -34,6 +34,16 @@ EXPORTED = (
     "offq_add_rmsnorm",
     "offq_swiglu",
     "offq_rope_kv_append",
+    "offq_top1_workspace_bytes",
+    "offq_top1_select",
+    "offq_channel_absmax",
+    "offq_gram",
+    "offq_eigh_workspace_bytes",
+    "offq_eigh",
+    "offq_group_permutation",
+    "offq_build_rotation",
+    "offq_fuse_weights",
+    "offq_permute_rows",
 )
 
 
@@ -85,6 +95,24 @@ def _load():
     lib.offq_rope_kv_append.restype = ctypes.c_int
     lib.offq_rope_kv_append.argtypes = [vp, i64, i64, i64, i64, i32, vp, ctypes.c_double, i32, i32,
                                         vp, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp]
+    f64 = ctypes.c_double
+    sigs = {
+        "offq_top1_workspace_bytes": (i64, [i64, i64]),
+        "offq_top1_select": (ctypes.c_int, [vp, i64, i64, i64, i64, i64, vp, vp, i64, vp, i64, vp]),
+        "offq_channel_absmax": (ctypes.c_int, [vp, i64, i64, i64, vp, vp]),
+        "offq_gram": (ctypes.c_int, [vp, i64, i64, i64, vp, i64, vp]),
+        "offq_eigh_workspace_bytes": (i64, [i64]),
+        "offq_eigh": (ctypes.c_int, [vp, i64, i64, vp, vp, i64, vp, i64, i32, f64,
+                                     ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(f64), vp]),
+        "offq_group_permutation": (ctypes.c_int, [vp, i64, i32, vp, vp, i64, vp]),
+        "offq_build_rotation": (ctypes.c_int, [vp, i64, i64, vp, i32, i32, vp, i64, vp]),
+        "offq_fuse_weights": (ctypes.c_int, [vp, i64, i64, i64, vp, i64, vp, i64, vp]),
+        "offq_permute_rows": (ctypes.c_int, [vp, i64, i64, i64, vp, vp, i64, vp]),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
     return lib
 
 
@@ -391,3 +419,116 @@ def offq_rope_kv_append(qkv, Hq, Hkv, positions, cache, rope_base=500000.0, k_ha
                                    _ptr(cache["v_scale"]), _ptr(cache["v_zero"]), s_cap, _ptr(ky),
                                    _ptr(vy), _stream()), "offq_rope_kv_append")
     return q, ky, vy
+
+
+# ------------------------------------------------------- offline calibration
+def offq_top1_select(x):
+    """x: bf16 [n_seq, L, D] (last dim contiguous).  Returns (idx int32 [n_seq],
+    X fp32 [n_seq, D]): per sequence the token of largest L-infinity norm."""
+    torch = _torch()
+    _need(x, torch.bfloat16, "x", 3)
+    if x.stride(2) != 1:
+        raise ValueError("x must have a contiguous last dimension")
+    n, L, D = x.shape
+    dev = x.device
+    idx = torch.empty((n,), dtype=torch.int32, device=dev)
+    X = torch.empty((n, D), dtype=torch.float32, device=dev)
+    wb = lib.offq_top1_workspace_bytes(n, L)
+    ws = torch.empty((max(wb, 4) + 3) // 4, dtype=torch.float32, device=dev)
+    _check(lib.offq_top1_select(_ptr(x), n, L, D, x.stride(1), x.stride(0), _ptr(idx), _ptr(X), D,
+                                _ptr(ws), ws.numel() * 4, _stream()), "offq_top1_select")
+    return idx, X
+
+
+def offq_channel_absmax(x):
+    """x: bf16 [rows, D].  Returns fp64 [D]: max over rows of |x|."""
+    torch = _torch()
+    _need(x, torch.bfloat16, "x", 2)
+    out = torch.empty((x.shape[1],), dtype=torch.float64, device=x.device)
+    _check(lib.offq_channel_absmax(_ptr(x), x.shape[0], x.shape[1], _rows(x, "x"), _ptr(out),
+                                   _stream()), "offq_channel_absmax")
+    return out
+
+
+def offq_gram(X):
+    """X: fp32 [N, D].  Returns C = X^T X / N, fp64 [D, D]."""
+    torch = _torch()
+    _need(X, torch.float32, "X", 2)
+    N, D = X.shape
+    C = torch.empty((D, D), dtype=torch.float64, device=X.device)
+    _check(lib.offq_gram(_ptr(X), N, D, _rows(X, "X"), _ptr(C), D, _stream()), "offq_gram")
+    return C
+
+
+def offq_eigh(C, max_sweeps=30, tol=None):
+    """C: fp64 [D, D] symmetric.  Returns (evals fp64 [D] descending, U fp64
+    [D, D] with eigenvectors in columns, sweeps, relative off-diagonal norm).
+    tol defaults to D * 2^-52 (the level fp64 rotations bottom out at)."""
+    torch = _torch()
+    _need(C, torch.float64, "C", 2)
+    D = C.shape[0]
+    if tol is None:
+        tol = D * 2.0 ** -52
+    if C.shape != (D, D):
+        raise ValueError("C must be square")
+    ev = torch.empty((D,), dtype=torch.float64, device=C.device)
+    U = torch.empty((D, D), dtype=torch.float64, device=C.device)
+    wb = lib.offq_eigh_workspace_bytes(D)
+    ws = torch.empty((max(wb, 8) + 7) // 8, dtype=torch.float64, device=C.device)
+    sw = ctypes.c_int32(0)
+    ro = ctypes.c_double(0.0)
+    _check(lib.offq_eigh(_ptr(C), D, _rows(C, "C"), _ptr(ev), _ptr(U), D, _ptr(ws), ws.numel() * 8,
+                         int(max_sweeps), float(tol), ctypes.byref(sw), ctypes.byref(ro),
+                         _stream()), "offq_eigh")
+    return ev, U, sw.value, ro.value
+
+
+def offq_group_permutation(key, g):
+    """key: fp64 [D].  Returns perm int32 [D] (new slot -> original channel)."""
+    torch = _torch()
+    _need(key, torch.float64, "key", 1)
+    D = key.shape[0]
+    perm = torch.empty((D,), dtype=torch.int32, device=key.device)
+    ws = torch.empty((D,), dtype=torch.int32, device=key.device)
+    _check(lib.offq_group_permutation(_ptr(key), D, int(g), _ptr(perm), _ptr(ws), D * 4, _stream()),
+           "offq_group_permutation")
+    return perm
+
+
+def offq_build_rotation(U, D, perm=None, g=1, apply_hadamard=False, device=None):
+    """Returns R fp32 [D, D] = U P blockdiag(H_g / sqrt g) (U None: identity)."""
+    torch = _torch()
+    dev = U.device if U is not None else perm.device if perm is not None else (device or "cuda")
+    if U is not None:
+        _need(U, torch.float64, "U", 2)
+    if perm is not None:
+        _need(perm, torch.int32, "perm", 1)
+    R = torch.empty((D, D), dtype=torch.float32, device=dev)
+    _check(lib.offq_build_rotation(_ptr(U), _rows(U, "U") if U is not None else D, D, _ptr(perm),
+                                   int(g), int(bool(apply_hadamard)), _ptr(R), D, _stream()),
+           "offq_build_rotation")
+    return R
+
+
+def offq_fuse_weights(W, R):
+    """W: fp32 [N, K], R: fp32 [K, K].  Returns W R (fp32 [N, K])."""
+    torch = _torch()
+    _need(W, torch.float32, "W", 2)
+    _need(R, torch.float32, "R", 2)
+    N, K = W.shape
+    out = torch.empty((N, K), dtype=torch.float32, device=W.device)
+    _check(lib.offq_fuse_weights(_ptr(W), _rows(W, "W"), N, K, _ptr(R), _rows(R, "R"), _ptr(out), K,
+                                 _stream()), "offq_fuse_weights")
+    return out
+
+
+def offq_permute_rows(W, perm):
+    """W: fp32 [N, K]; perm int32 [N].  Returns W[perm] (fp32 [N, K])."""
+    torch = _torch()
+    _need(W, torch.float32, "W", 2)
+    _need(perm, torch.int32, "perm", 1)
+    N, K = W.shape
+    out = torch.empty((N, K), dtype=torch.float32, device=W.device)
+    _check(lib.offq_permute_rows(_ptr(W), _rows(W, "W"), N, K, _ptr(perm), _ptr(out), K, _stream()),
+           "offq_permute_rows")
+    return out

@@ -71,4 +71,25 @@ hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, in
                                  int16_t* vz, int64_t s_cap, float* k_dbg, float* v_dbg,
                                  hipStream_t stream);
 
+// offline calibration (calibration.hip)
+hipError_t launch_top1_select(const uint16_t* x, int64_t n_seq, int64_t L, int64_t D,
+                              int64_t ld_tok, int64_t ld_seq, int32_t* idx, float* X, int64_t ldX,
+                              float* linf, hipStream_t stream);
+hipError_t launch_channel_absmax(const uint16_t* x, int64_t rows, int64_t D, int64_t ldx,
+                                 double* out, hipStream_t stream);
+hipError_t launch_gram(const float* X, int64_t N, int64_t D, int64_t ldX, double* C, int64_t ldC,
+                       hipStream_t stream);
+int64_t eigh_workspace_doubles(int64_t D);
+hipError_t launch_eigh(const double* C, int64_t ldC, int64_t D, double* evals, double* U,
+                       int64_t ldU, double* ws, int max_sweeps, double tol, int* sweeps_done,
+                       double* rel_off, hipStream_t stream);
+hipError_t launch_group_permutation(const double* key, int64_t D, int64_t g, int32_t* perm,
+                                    int32_t* rank, hipStream_t stream);
+hipError_t launch_build_rotation(const double* U, int64_t ldU, int64_t D, const int32_t* perm,
+                                 int log2g, float* R, int64_t ldR, hipStream_t stream);
+hipError_t launch_fuse_weights(const float* W, int64_t ldW, int64_t N, int64_t K, const float* R,
+                               int64_t ldR, float* Wo, int64_t ldo, hipStream_t stream);
+hipError_t launch_permute_rows(const float* W, int64_t ldW, int64_t N, int64_t K,
+                               const int32_t* perm, float* Wo, int64_t ldo, hipStream_t stream);
+
 }  // namespace offq

@@ -313,16 +313,25 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
 __global__ __launch_bounds__(THREADS) void kv_attention_chunk_kernel(
     const uint16_t* __restrict__ q, const uint8_t* __restrict__ kc, const uint16_t* __restrict__ ks,
     const int16_t* __restrict__ kz, const uint8_t* __restrict__ vc, const uint16_t* __restrict__ vs,
-    const int16_t* __restrict__ vz, int64_t S_cap, int seq_len, int nchunk, int group, float sm2,
-    float cnorm, float* __restrict__ ws) {
+    const int16_t* __restrict__ vz, int64_t S_cap, int seq_len, int nchunk, int units, int group,
+    float sm2, float cnorm, float* __restrict__ ws) {
   __shared__ ChunkSmem S;
+  // Workgroups go to the 8 XCDs round-robin by id.  The `group` query heads
+  // that read one key/value chunk get ids 8 apart, i.e. the same XCD at about
+  // the same time, so the chunk comes from HBM once and from that XCD's L2
+  // for the others.  Work unit u = (key/value head, chunk); ids past the
+  // units (padding to a multiple of 8) exit.
   const int blk = (int)__builtin_amdgcn_workgroup_id_x();
-  const int bh = blk / nchunk, chunk = blk - bh * nchunk;  // bh: query head b * Hq + h
+  const int slot = blk >> 3;
+  const int gq = slot % group;
+  const int unit = (slot / group) * 8 + (blk & 7);
+  if (unit >= units) return;
+  const int kvh = unit / nchunk, chunk = unit - kvh * nchunk;  // kvh = b * Hkv + h_kv
+  const int bh = kvh * group + gq;                              // query head b * Hq + h
   const int j0 = chunk * CH;
   const int n = min(CH, seq_len - j0);  // positions of this chunk (>= 1)
-  // key/value head b * Hkv + h / group, with Hq = group * Hkv
-  const int64_t row0 = (int64_t)(bh / group) * S_cap + j0;
-  float* rec = ws + (int64_t)blk * WS_FLOATS;
+  const int64_t row0 = (int64_t)kvh * S_cap + j0;
+  float* rec = ws + ((int64_t)bh * nchunk + chunk) * WS_FLOATS;
   if (n == CH)
     attention_chunk<true>(S, q, kc, ks, kz, vc, vs, vz, row0, bh, n, sm2, cnorm, rec);
   else
@@ -407,9 +416,11 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
                                       hipStream_t stream) {
   const int nchunk = (int)((seq_len + CH - 1) / CH);
   const float cnorm = (float)(1.0 / __builtin_sqrt((double)DH));
-  hipLaunchKernelGGL(kv_attention_chunk_kernel, dim3((unsigned)(BH * nchunk)), dim3(THREADS), 0,
-                     stream, q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, S_cap,
-                     (int)seq_len, nchunk, (int)group, sm_scale * LOG2E, cnorm, workspace);
+  const int64_t units = BH / group * nchunk;  // (key/value head, chunk) pairs
+  const int64_t grid = (units + 7) / 8 * 8 * group;
+  hipLaunchKernelGGL(kv_attention_chunk_kernel, dim3((unsigned)grid), dim3(THREADS), 0, stream, q,
+                     k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, S_cap, (int)seq_len,
+                     nchunk, (int)units, (int)group, sm_scale * LOG2E, cnorm, workspace);
   hipLaunchKernelGGL(kv_attention_combine_kernel, dim3((unsigned)BH), dim3(DH), 0, stream,
                      workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out);
   return hipGetLastError();

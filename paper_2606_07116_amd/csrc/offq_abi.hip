@@ -308,4 +308,139 @@ int offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq,
                   "rope_kv_append");
 }
 
+int64_t offq_top1_workspace_bytes(int64_t n_seq, int64_t seq_len) {
+  if (n_seq <= 0 || seq_len <= 0 || n_seq > (int64_t(1) << 31) / seq_len) return 0;
+  return n_seq * seq_len * (int64_t)sizeof(float);
+}
+
+int offq_top1_select(const uint16_t* x, int64_t n_seq, int64_t seq_len, int64_t D, int64_t ld_tok,
+                     int64_t ld_seq, int32_t* idx, float* X, int64_t ldX, void* workspace,
+                     int64_t workspace_bytes, void* stream) {
+  if (n_seq <= 0 || seq_len <= 0) return fail(OFFQ_ERR_INVALID, "need n_seq, seq_len > 0");
+  if (D < 8 || D % 8 || ld_tok < D || ld_tok % 8 || ld_seq % 8 || ldX < D)
+    return fail(OFFQ_ERR_INVALID, "D, ld_tok, ld_seq must be multiples of 8 with ld_tok >= D, ldX >= D");
+  if (ld_seq < (seq_len - 1) * ld_tok + D && n_seq > 1)
+    return fail(OFFQ_ERR_INVALID, "sequences overlap (ld_seq too small)");
+  if (D > (1 << 20) || n_seq > (1 << 24) || n_seq * seq_len > (int64_t(1) << 31))
+    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
+  if (!x || !idx || !X || !workspace) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(x, 16) || !aligned(idx, 4) || !aligned(X, 4) || !aligned(workspace, 4))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (x: 16 B)");
+  if (workspace_bytes < offq_top1_workspace_bytes(n_seq, seq_len))
+    return fail(OFFQ_ERR_INVALID, "workspace too small");
+  if (int st = check_device()) return st;
+  return launched(offq::launch_top1_select(x, n_seq, seq_len, D, ld_tok, ld_seq, idx, X, ldX,
+                                           static_cast<float*>(workspace), (hipStream_t)stream),
+                  "top1_select");
+}
+
+int offq_channel_absmax(const uint16_t* x, int64_t rows, int64_t D, int64_t ldx, double* out,
+                        void* stream) {
+  if (rows <= 0 || D <= 0 || ldx < D) return fail(OFFQ_ERR_INVALID, "need rows, D > 0, ldx >= D");
+  if (D > (1 << 24)) return fail(OFFQ_ERR_UNSUPPORTED, "D too large");
+  if (!x || !out) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(x, 2) || !aligned(out, 8)) return fail(OFFQ_ERR_INVALID, "misaligned pointer");
+  if (int st = check_device()) return st;
+  return launched(offq::launch_channel_absmax(x, rows, D, ldx, out, (hipStream_t)stream),
+                  "channel_absmax");
+}
+
+int offq_gram(const float* X, int64_t N, int64_t D, int64_t ldX, double* C, int64_t ldC,
+              void* stream) {
+  if (N <= 0 || D <= 0 || ldX < D || ldC < D)
+    return fail(OFFQ_ERR_INVALID, "need N, D > 0, ldX >= D, ldC >= D");
+  if (D > 65536 || N > (int64_t(1) << 30)) return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
+  if (!X || !C) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(X, 4) || !aligned(C, 8)) return fail(OFFQ_ERR_INVALID, "misaligned pointer");
+  if (int st = check_device()) return st;
+  return launched(offq::launch_gram(X, N, D, ldX, C, ldC, (hipStream_t)stream), "gram");
+}
+
+int64_t offq_eigh_workspace_bytes(int64_t D) {
+  if (D < 2 || D > 8192 || D % 2) return 0;
+  return offq::eigh_workspace_doubles(D) * (int64_t)sizeof(double);
+}
+
+int offq_eigh(const double* C, int64_t D, int64_t ldC, double* evals, double* U, int64_t ldU,
+              void* workspace, int64_t workspace_bytes, int32_t max_sweeps, double tol,
+              int32_t* sweeps, double* rel_off, void* stream) {
+  if (D < 2 || D % 2) return fail(OFFQ_ERR_INVALID, "D must be even and >= 2");
+  if (D > 8192) return fail(OFFQ_ERR_UNSUPPORTED, "D = %lld > 8192", (long long)D);
+  if (ldC < D || ldU < D) return fail(OFFQ_ERR_INVALID, "row strides must be >= D");
+  if (max_sweeps < 0 || !(tol >= 0.0)) return fail(OFFQ_ERR_INVALID, "need max_sweeps >= 0, tol >= 0");
+  if (!C || !evals || !U || !workspace) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(C, 8) || !aligned(evals, 8) || !aligned(U, 8) || !aligned(workspace, 16))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (workspace: 16 B)");
+  if (workspace_bytes < offq_eigh_workspace_bytes(D))
+    return fail(OFFQ_ERR_INVALID, "workspace of %lld bytes, need %lld", (long long)workspace_bytes,
+                (long long)offq_eigh_workspace_bytes(D));
+  if (int st = check_device()) return st;
+  int sw = 0;
+  double ro = 0.0;
+  const hipError_t e = offq::launch_eigh(C, ldC, D, evals, U, ldU, static_cast<double*>(workspace),
+                                         max_sweeps, tol, &sw, &ro, (hipStream_t)stream);
+  if (sweeps) *sweeps = sw;
+  if (rel_off) *rel_off = ro;
+  return launched(e, "eigh");
+}
+
+int offq_group_permutation(const double* key, int64_t D, int32_t g, int32_t* perm,
+                           void* workspace, int64_t workspace_bytes, void* stream) {
+  if (D <= 0 || g <= 0 || D % g) return fail(OFFQ_ERR_INVALID, "need D > 0 a multiple of g > 0");
+  if (D > (1 << 20)) return fail(OFFQ_ERR_UNSUPPORTED, "D too large");
+  if (!key || !perm || !workspace) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(key, 8) || !aligned(perm, 4) || !aligned(workspace, 4))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer");
+  if (workspace_bytes < D * 4) return fail(OFFQ_ERR_INVALID, "workspace too small (D int32)");
+  if (int st = check_device()) return st;
+  return launched(offq::launch_group_permutation(key, D, g, perm, static_cast<int32_t*>(workspace),
+                                                 (hipStream_t)stream),
+                  "group_permutation");
+}
+
+int offq_build_rotation(const double* U, int64_t ldU, int64_t D, const int32_t* perm, int32_t g,
+                        int32_t apply_hadamard, float* R, int64_t ldR, void* stream) {
+  if (D <= 0 || D > 8192) return fail(OFFQ_ERR_UNSUPPORTED, "need 0 < D <= 8192");
+  if (apply_hadamard != 0 && apply_hadamard != 1)
+    return fail(OFFQ_ERR_INVALID, "apply_hadamard must be 0 or 1");
+  int lg = 0;
+  if (apply_hadamard) {
+    lg = ilog2_pow2(g);
+    if (lg < 0 || D % g) return fail(OFFQ_ERR_INVALID, "g must be a power of two dividing D");
+  }
+  if ((U && ldU < D) || ldR < D) return fail(OFFQ_ERR_INVALID, "row strides must be >= D");
+  if (!R) return fail(OFFQ_ERR_INVALID, "null output");
+  if ((U && !aligned(U, 8)) || (perm && !aligned(perm, 4)) || !aligned(R, 4))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer");
+  if (int st = check_device()) return st;
+  return launched(offq::launch_build_rotation(U, ldU, D, perm, lg, R, ldR, (hipStream_t)stream),
+                  "build_rotation");
+}
+
+int offq_fuse_weights(const float* W, int64_t ldW, int64_t N, int64_t K, const float* R,
+                      int64_t ldR, float* W_out, int64_t ldo, void* stream) {
+  if (N <= 0 || K <= 0 || ldW < K || ldR < K || ldo < K)
+    return fail(OFFQ_ERR_INVALID, "need N, K > 0 and row strides >= K");
+  if (N > (1 << 24) || K > 65536) return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
+  if (!W || !R || !W_out) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(W, 4) || !aligned(R, 4) || !aligned(W_out, 4))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer");
+  if (int st = check_device()) return st;
+  return launched(offq::launch_fuse_weights(W, ldW, N, K, R, ldR, W_out, ldo, (hipStream_t)stream),
+                  "fuse_weights");
+}
+
+int offq_permute_rows(const float* W, int64_t ldW, int64_t N, int64_t K, const int32_t* perm,
+                      float* W_out, int64_t ldo, void* stream) {
+  if (N <= 0 || K <= 0 || ldW < K || ldo < K)
+    return fail(OFFQ_ERR_INVALID, "need N, K > 0 and row strides >= K");
+  if (N > (int64_t(1) << 31) - 1) return fail(OFFQ_ERR_UNSUPPORTED, "N too large");
+  if (!W || !perm || !W_out) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(W, 4) || !aligned(perm, 4) || !aligned(W_out, 4))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer");
+  if (int st = check_device()) return st;
+  return launched(offq::launch_permute_rows(W, ldW, N, K, perm, W_out, ldo, (hipStream_t)stream),
+                  "permute_rows");
+}
+
 }  // extern "C"

@@ -219,10 +219,30 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
 
 }  // namespace
 
+// Launch shape by layer width: K in quarters with four row tiles per wave
+// (one activation load serves four weight loads) for wide layers (28672
+// channels: 448 workgroups), two for medium ones (8192 channels: 256
+// workgroups), as measured; narrow layers take one tile per wave and K in
+// eighths, for more waves in flight.
+static void gemv_shape(int64_t N, int& T, int& P) {
+  if (N >= 16384) {
+    T = 4, P = 4;
+  } else if (N >= 32 * 128) {
+    T = 2, P = 4;
+  } else {
+    T = 1, P = 8;
+  }
+}
+
 bool gemv_mfma_supported(int64_t M, int64_t N, int64_t K, int log2g) {
-  // the parts of K (eighths at most) are whole batches; no step straddles a
-  // group; the group parameters fit in LDS; 32-bit buffer offsets
-  return M <= 16 && log2g >= 7 && K % 4096 == 0 && (K >> log2g) <= GMAX &&
+  // each wave's part of K is a whole number of batches (a part may end inside
+  // a group: the group's zero-point term is added once, by the wave holding
+  // its first k); no step straddles a group; the group parameters fit in LDS;
+  // 32-bit buffer offsets
+  int T, P;
+  gemv_shape(N, T, P);
+  const int64_t batch = (int64_t)P * KSTEP * (T >= 4 ? 2 : 4);
+  return M <= 16 && log2g >= 7 && K % batch == 0 && (K >> log2g) <= GMAX &&
          32 * (K / 2) < (int64_t(1) << 31) && M * (K / 2) < (int64_t(1) << 31);
 }
 
@@ -255,15 +275,13 @@ hipError_t launch_w4a4_gemv_mfma(const uint8_t* a_codes, const uint16_t* a_scale
                                  const uint16_t* w_scale, const int32_t* w_colsum, int64_t M,
                                  int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
                                  int32_t* acc_debug, hipStream_t stream) {
-  // K in quarters with four row tiles per wave (one activation load serves
-  // four weight loads) for wide layers (28672 channels: 448 workgroups), two
-  // for medium ones (8192 channels: 256 workgroups), as measured; narrow
-  // layers take one tile per wave and K in eighths, for more waves in flight.
+  int T, P;
+  gemv_shape(N, T, P);
 #define OFFQ_GV(T, P)                                                                         \
   return launch_gv<T, P>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, \
                          y, ldy, acc_debug, stream)
-  if (N >= 16384) OFFQ_GV(4, 4);
-  if (N >= 32 * 128) OFFQ_GV(2, 4);
+  if (T == 4) OFFQ_GV(4, 4);
+  if (T == 2) OFFQ_GV(2, 4);
   OFFQ_GV(1, 8);
 #undef OFFQ_GV
 }

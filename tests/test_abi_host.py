@@ -144,3 +144,36 @@ def test_kv_attention_workspace_bytes():
     assert _lib.offq_kv_attention_workspace_bytes(8, 32, 32768) == 256 * 32 * 130 * 4
     assert _lib.offq_kv_attention_workspace_bytes(0, 4, 10) == 0
     assert _lib.offq_kv_attention_workspace_bytes(1, 1, 0) == 0
+
+
+def test_layer_and_calibration_validation():
+    L = _lib
+    # add_rmsnorm: D not a multiple of 8; no output
+    assert L.offq_add_rmsnorm_raw(P, 16, None, 0, 4, 12, 1e-5, P, 16, P, 16, None) == L.OFFQ_ERR_INVALID
+    assert L.offq_add_rmsnorm_raw(P, 16, None, 0, 4, 16, 1e-5, None, 0, None, 0, None) == L.OFFQ_ERR_INVALID
+    assert L.offq_add_rmsnorm_raw(P, 16, None, 0, 0, 16, 1e-5, P, 16, None, 0, None) == L.OFFQ_OK
+    # swiglu: ldg < 2F
+    assert L.offq_swiglu_raw(P, 16, 2, 16, P, 16, None) == L.OFFQ_ERR_INVALID
+    # rope: head_dim 64, bad flag
+    args = [P, 768, 2, 2, 2, 128, P, 500000.0, 1, 0, P, P, P, P, P, P, P, 100, None, None, None]
+    a = list(args); a[5] = 64
+    assert L.offq_rope_kv_append_raw(*a) == L.OFFQ_ERR_UNSUPPORTED
+    a = list(args); a[8] = 3
+    assert L.offq_rope_kv_append_raw(*a) == L.OFFQ_ERR_INVALID
+    a = list(args); a[1] = 700
+    assert L.offq_rope_kv_append_raw(*a) == L.OFFQ_ERR_INVALID
+    # gqa: Hq not a multiple of Hkv
+    assert L.offq_kv_attention_decode_gqa_raw(P, P, P, P, P, P, P, 2, 6, 4, 100, 100, 128, 0.1, 0, P,
+                                              P, 1 << 20, None) == L.OFFQ_ERR_INVALID
+    # eigh: odd D, too large, small workspace
+    f = lambda D, wsb: L.lib.offq_eigh(P, D, D, P, P, D, P, wsb, 30, 1e-14, None, None, None)
+    assert f(7, 1 << 30) == L.OFFQ_ERR_INVALID
+    assert f(16384, 1 << 40) == L.OFFQ_ERR_UNSUPPORTED
+    assert f(64, 100) == L.OFFQ_ERR_INVALID
+    assert L.lib.offq_eigh_workspace_bytes(64) >= 4 * 64 * 64 * 8
+    # grouping: D not a multiple of g
+    assert L.lib.offq_group_permutation(P, 100, 64, P, P, 400, None) == L.OFFQ_ERR_INVALID
+    # rotation: g not a power of two with the Hadamard
+    assert L.lib.offq_build_rotation(None, 0, 96, None, 24, 1, P, 96, None) == L.OFFQ_ERR_INVALID
+    # top-1: D not a multiple of 8
+    assert L.lib.offq_top1_select(P, 2, 3, 12, 16, 48, P, P, 12, P, 1 << 10, None) == L.OFFQ_ERR_INVALID

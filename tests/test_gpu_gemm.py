@@ -60,6 +60,16 @@ def test_gemv_channel_counts(N):
     _layer(3, N, 4096, 512, seed=N)
 
 
+@pytest.mark.parametrize("M,N,K,g", [(4, 4096, 14336, 128), (16, 4096, 14336, 512),
+                                     (1, 20000, 5120, 128), (3, 8192, 6144, 256),
+                                     (5, 8192, 6144, 1024)])
+def test_gemv_parts_of_k(M, N, K, g):
+    """K not a multiple of 4096: each wave's part of K is an odd number of
+    batches, and with g = 1024 a part ends inside a group (the group's
+    zero-point term is added once)."""
+    _layer(M, N, K, g, seed=K + g)
+
+
 def test_raw_layout_and_spikes():
     _layer(150, 192, 1024, 1024, seed=5, layout="raw", n_out=6)
 
