@@ -46,7 +46,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="attn_proj_prefill",
                    choices=["attn_proj_prefill", "mlp_prefill", "decode", "kv_chain",
-                            "kv_decode_attention", "decode_layer"])
+                            "kv_decode_attention", "decode_layer", "calibration"])
     p.add_argument("--decode-m", type=int, default=16)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--group-size", type=int, default=0,
@@ -270,6 +270,23 @@ def main():
         config = {"workload": wl, "kv_shape": [B, H, S, Dh], "seq_len": S,
                   "step": "kv_attention_decode (split-sequence pass + combine pass)",
                   "input_sets": asets.n}
+    elif wl == "calibration":
+        cc = inputs.WORKLOADS["calibration"]
+        n_seq, L, D, g = cc["n_seq"], cc["L"], cc["D"], cc["g"]
+        x_cal = inputs.activations_device(n_seq * L, D, seed=cc["seed"], device="cuda",
+                                          n_outliers=cc["n_outliers"], lo=cc["lo"], hi=cc["hi"],
+                                          spike_frac=cc["spike_frac"],
+                                          spike_mult=cc["spike_mult"]).view(n_seq, L, D)
+        w_in = {name: inputs.weights_device(n_, D, seed=cc["seed"] + j, device="cuda")
+                for j, (name, n_) in enumerate(cc["layers"].items())}
+        cal = {}
+        layers = []
+        work_ops = None
+        args.steps, args.warmup = min(args.steps, 1), 0  # seconds per step
+        config = {"workload": wl, "calibration": [n_seq, L, D], "g": g,
+                  "fused_layers": {k: [v, D] for k, v in cc["layers"].items()},
+                  "step": "top-1 selection, covariance, Jacobi eigendecomposition, sorted "
+                          "grouping, rotation U P H, weight fusion and packing"}
     elif wl == "decode_layer":
         lc = inputs.WORKLOADS["decode_layer"]
         M, D, Hq, Hkv, F, g = lc["M"], lc["D"], lc["Hq"], lc["Hkv"], lc["F"], lc["g"]
@@ -336,6 +353,34 @@ def main():
             phases.append(("kv_quantize", lambda i, j=j: _lib.offq_kv_quantize_raw(
                 kv[j].data_ptr(), R, Dh, Dh, 1, kvo[j]["codes"].data_ptr(), kvo[j]["scale"].data_ptr(),
                 kvo[j]["zero"].data_ptr(), None, sp)))
+    if wl == "calibration":
+        def c_top1(i):
+            cal["idx"], cal["X"] = offq.offq_top1_select(x_cal)
+            return 0
+
+        def c_gram(i):
+            cal["C"] = offq.offq_gram(cal["X"])
+            return 0
+
+        def c_eigh(i):
+            cal["ev"], cal["U"], cal["sweeps"], cal["rel"] = offq.offq_eigh(cal["C"])
+            return 0
+
+        def c_group(i):
+            cal["perm"] = offq.offq_group_permutation(cal["ev"], g)
+            cal["R"] = offq.offq_build_rotation(cal["U"], D, cal["perm"], g, True)
+            return 0
+
+        def c_fuse(i):
+            cal["W"] = {k: offq.offq_fuse_weights(w, cal["R"]) for k, w in w_in.items()}
+            return 0
+
+        def c_pack(i):
+            cal["packed"] = {k: offq.offq_pack_weights(w, g) for k, w in cal["W"].items()}
+            return 0
+        phases += [("top1_select", c_top1), ("gram", c_gram), ("eigh", c_eigh),
+                   ("grouping_rotation", c_group), ("fuse_weights", c_fuse),
+                   ("pack_weights", c_pack)]
     if wl == "decode_layer":
         eps, base, sm = 1e-5, 500000.0, 1.0 / 128 ** 0.5
         P_ = lambda t: t.data_ptr()
@@ -449,6 +494,24 @@ def main():
                 "unit": "TOP/s", "frac": comp[dom]["frac_int8_peak"],
                 "traffic": traffic_for(f"w4a4_gemm:{wl}"), "kernel": dom,
                 "alg_ops_per_launch": comp[dom]["alg_ops"], "avg_launch_us": comp[dom]["us"]}
+    elif wl == "calibration":
+        tb = n_seq * L * D * 2
+        comp["top1_select"]["alg_bytes"] = tb
+        comp["top1_select"]["GBs"] = round(tb / (comp["top1_select"]["us"] * 1e-6) / 1e9, 1)
+        gf = n_seq * D * D  # fp64 multiply-adds of the upper triangle, x2 flops
+        comp["gram"]["fp64_TFLOPs"] = round(2 * gf / (comp["gram"]["us"] * 1e-6) / 1e12, 3)
+        nf = sum(2.0 * n_ * D * D for n_ in cc["layers"].values())
+        comp["fuse_weights"]["fp32_TFLOPs"] = round(nf / (comp["fuse_weights"]["us"] * 1e-6) / 1e12, 2)
+        # every Jacobi step reads and writes A and V once: 32 D^2 bytes
+        eb = 32.0 * D * D * (D - 1) * cal["sweeps"]
+        comp["eigh"].update({"sweeps": cal["sweeps"], "rel_offdiag": cal["rel"], "alg_bytes": eb,
+                             "GBs": round(eb / (comp["eigh"]["us"] * 1e-6) / 1e9, 1)})
+        comp["eigh"]["frac_hbm"] = round(comp["eigh"]["GBs"] / PEAK_HBM_GBS, 4)
+        value = round(ms / 1e3, 3)
+        unit = "s per layer-input calibration"
+        roof = {"bound": "hbm", "achieved": comp["eigh"]["GBs"], "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": comp["eigh"]["frac_hbm"], "traffic": None, "kernel": "eigh",
+                "alg_bytes_per_launch": eb, "avg_launch_us": comp["eigh"]["us"]}
     elif wl == "decode_layer":
         name = "decode_layer"
         comp[name]["alg_bytes"] = step_bytes
@@ -491,7 +554,7 @@ def main():
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": unit, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "higher_is_better": wl != "calibration", "scaling": "weak", "vs_baseline": None,
         "dtype": "int8",
         "data": "synthetic (seeded Llama-shaped activations with structured outliers; random weights)",
         "config": config, "roofline": roof, "components": comp,

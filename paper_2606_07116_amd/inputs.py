@@ -53,6 +53,12 @@ WORKLOADS = {
     "kv_decode_attention": dict(B=8, H=32, S=32768, Dh=128, seed=6),
     # one decode step of a Llama-3-8B-shaped layer: 16 sequences at context 4096
     "decode_layer": dict(M=16, D=4096, Hq=32, Hkv=8, F=14336, g=128, ctx=4096, seed=7),
+    # offline calibration of one 4096-channel layer input (U1 P1 H1): 128
+    # calibration sequences of 2048 tokens; the rotation fused into the QKV
+    # and up/gate weights of a Llama-3-8B-shaped layer
+    "calibration": dict(n_seq=128, L=2048, D=4096, g=128, n_outliers=6, lo=50.0, hi=500.0,
+                        spike_frac=1e-3, spike_mult=20.0, seed=8,
+                        layers={"qkv": 6144, "up_gate": 28672}),
     "kv_chain_proj": dict(M=8192, K=4096, N=4096, g=4096, n_outliers=4,
                           lo=50.0, hi=200.0, seed=55),
 }
