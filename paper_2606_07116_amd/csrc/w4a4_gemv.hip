@@ -219,18 +219,21 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
 
 }  // namespace
 
-// Launch shape by layer width: K in quarters with four row tiles per wave
-// (one activation load serves four weight loads) for wide layers (28672
-// channels: 448 workgroups), two for medium ones (8192 channels: 256
-// workgroups), as measured; narrow layers take one tile per wave and K in
-// eighths, for more waves in flight.
-static void gemv_shape(int64_t N, int& T, int& P) {
+// Launch shape (T row tiles per wave, K in P parts), as measured at M = 16
+// (g = 128 ... 8192): wide layers (>= 16384 channels) take four row tiles per
+// wave (one activation load serves four weight loads) and K in quarters;
+// narrower ones need more waves in flight: K in eighths with two tiles per
+// wave from 6144 channels, one below, where K splits into eighths of whole
+// batches; else one tile per wave and K in quarters (e.g. K = 14336).
+static void gemv_shape(int64_t N, int64_t K, int& T, int& P) {
   if (N >= 16384) {
     T = 4, P = 4;
-  } else if (N >= 32 * 128) {
-    T = 2, P = 4;
+  } else if (K % 4096 == 0) {
+    T = N >= 6144 ? 2 : 1, P = 8;
+  } else if (K % 2048 == 0) {
+    T = 1, P = 4;
   } else {
-    T = 1, P = 8;
+    T = 4, P = 4;
   }
 }
 
@@ -240,9 +243,12 @@ bool gemv_mfma_supported(int64_t M, int64_t N, int64_t K, int log2g) {
   // its first k); no step straddles a group; the group parameters fit in LDS;
   // 32-bit buffer offsets
   int T, P;
-  gemv_shape(N, T, P);
+  gemv_shape(N, K, T, P);
   const int64_t batch = (int64_t)P * KSTEP * (T >= 4 ? 2 : 4);
+  // group parameters (dynamic) + the partial sums of the P waves (static)
+  const int64_t lds = (K >> log2g) * (32 + 16 * T) * 4 + (int64_t)P * 64 * 4 * T * 4;
   return M <= 16 && log2g >= 7 && K % batch == 0 && (K >> log2g) <= GMAX &&
+         lds <= 160 * 1024 &&
          32 * (K / 2) < (int64_t(1) << 31) && M * (K / 2) < (int64_t(1) << 31);
 }
 
@@ -276,13 +282,14 @@ hipError_t launch_w4a4_gemv_mfma(const uint8_t* a_codes, const uint16_t* a_scale
                                  int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
                                  int32_t* acc_debug, hipStream_t stream) {
   int T, P;
-  gemv_shape(N, T, P);
+  gemv_shape(N, K, T, P);
 #define OFFQ_GV(T, P)                                                                         \
   return launch_gv<T, P>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, \
                          y, ldy, acc_debug, stream)
   if (T == 4) OFFQ_GV(4, 4);
-  if (T == 2) OFFQ_GV(2, 4);
-  OFFQ_GV(1, 8);
+  if (T == 2) OFFQ_GV(2, 8);
+  if (P == 8) OFFQ_GV(1, 8);
+  OFFQ_GV(1, 4);
 #undef OFFQ_GV
 }
 
