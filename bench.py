@@ -324,9 +324,9 @@ def main():
         layers = []
         work_ops = None
         config = {"workload": wl, "M": M, "D": D, "heads": [Hq, Hkv], "mlp": F, "g": g,
-                  "context": ctx, "step": "add+RMSNorm, quantize, QKV GEMV, RoPE + H3 + KV4 append, "
-                  "GQA decode attention, quantize, O GEMV, add+RMSNorm, quantize, up/gate GEMV, "
-                  "SwiGLU, H4 + quantize, down GEMV, add", "input_sets": lsets.n}
+                  "context": ctx, "step": "add+RMSNorm+quantize, QKV GEMV, RoPE + H3 + KV4 append, "
+                  "GQA decode attention, quantize, O GEMV, add+RMSNorm+quantize, up/gate GEMV, "
+                  "SwiGLU+H4+quantize, down GEMV, add", "input_sets": lsets.n}
     else:  # decode
         up = regroup(inputs.WORKLOADS["decode_up"])
         dn = regroup(inputs.WORKLOADS["decode_down"])
@@ -385,19 +385,29 @@ def main():
         eps, base, sm = 1e-5, 500000.0, 1.0 / 128 ** 0.5
         P_ = lambda t: t.data_ptr()
 
-        def lin(st, cname, src, K_, N_, wname, dst, had):
+        def gemm(st, cname, K_, N_, wname, dst):
             c_, s_, z_ = st[cname]
-            check(_lib.offq_rotate_quantize_raw(P_(src), M, K_, K_, g, had, P_(c_), P_(s_), P_(z_),
-                                                None, sp), "rotate_quantize")
             wc_, ws_, wcs_ = st[wname]
             return _lib.offq_w4a4_gemm_raw(P_(c_), P_(s_), P_(z_), P_(wc_), P_(ws_), P_(wcs_), M,
                                            N_, K_, g, P_(dst), N_, None, sp)
 
+        def lin(st, cname, src, K_, N_, wname, dst, had):
+            c_, s_, z_ = st[cname]
+            check(_lib.offq_rotate_quantize_raw(P_(src), M, K_, K_, g, had, P_(c_), P_(s_), P_(z_),
+                                                None, sp), "rotate_quantize")
+            return gemm(st, cname, K_, N_, wname, dst)
+
+        def norm_quant(st, res, h_out):
+            c_, s_, z_ = st["c_in"]
+            check(_lib.offq_add_rmsnorm_quantize_raw(
+                P_(st["x"]), D, P_(res) if res is not None else None, D, M, D, eps, g,
+                P_(h_out) if h_out is not None else None, D, P_(c_), P_(s_), P_(z_), None, 0, sp),
+                "add_rmsnorm_quantize")
+
         def step_layer(i):
             st = lsets[i]
-            check(_lib.offq_add_rmsnorm_raw(P_(st["x"]), D, None, 0, M, D, eps, None, 0,
-                                            P_(st["y0"]), D, sp), "add_rmsnorm")
-            check(lin(st, "c_in", st["y0"], D, NQKV, "w_qkv", st["qkv"], 0), "gemv qkv")
+            norm_quant(st, None, None)
+            check(gemm(st, "c_in", D, NQKV, "w_qkv", st["qkv"]), "gemv qkv")
             check(_lib.offq_rope_kv_append_raw(
                 P_(st["qkv"]), NQKV, M, Hq, Hkv, 128, P_(st["pos"]), base, 1, 0, P_(st["q"]),
                 P_(st["kc"]), P_(st["ks"]), P_(st["kz"]), P_(st["vc"]), P_(st["vs"]), P_(st["vz"]),
@@ -407,11 +417,12 @@ def main():
                 P_(st["vz"]), M, Hq, Hkv, s_cap, seq_len, 128, sm, 0, P_(st["o"]), P_(st["ws"]),
                 st["wsb"], sp), "attention")
             check(lin(st, "c_o", st["o"], Hq * 128, D, "w_o", st["ao"], 0), "gemv o")
-            check(_lib.offq_add_rmsnorm_raw(P_(st["x"]), D, P_(st["ao"]), D, M, D, eps,
-                                            P_(st["h1"]), D, P_(st["y1"]), D, sp), "add_rmsnorm")
-            check(lin(st, "c_in", st["y1"], D, 2 * F, "w_ug", st["gu"], 0), "gemv up/gate")
-            check(_lib.offq_swiglu_raw(P_(st["gu"]), 2 * F, M, F, P_(st["a"]), F, sp), "swiglu")
-            check(lin(st, "c_d", st["a"], F, D, "w_down", st["dn"], 1), "gemv down")
+            norm_quant(st, st["ao"], st["h1"])
+            check(gemm(st, "c_in", D, 2 * F, "w_ug", st["gu"]), "gemv up/gate")
+            c_, s_, z_ = st["c_d"]
+            check(_lib.offq_swiglu_rotate_quantize_raw(P_(st["gu"]), 2 * F, M, F, P_(c_), P_(s_),
+                                                       P_(z_), None, sp), "swiglu_rotate_quantize")
+            check(gemm(st, "c_d", F, D, "w_down", st["dn"]), "gemv down")
             return _lib.offq_add_rmsnorm_raw(P_(st["h1"]), D, P_(st["dn"]), D, M, D, eps,
                                              P_(st["out"]), D, None, 0, sp)
         # the whole layer is one phase: its kernels depend on each other
@@ -429,7 +440,7 @@ def main():
         phases.append((mm_name, lambda i, s_=sets_: run_gemm(_lib, s_[i], sp)))
 
     # library launches per step (the spin below covers the host's enqueue time)
-    launches_per_step = 15 if wl == "decode_layer" else len(phases)
+    launches_per_step = 12 if wl == "decode_layer" else len(phases)
     for i in range(args.warmup):
         for name, fn in phases:
             check(fn(i), name)

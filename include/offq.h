@@ -253,6 +253,33 @@ int offq_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t*
                 void* stream);
 
 /*
+ * offq_add_rmsnorm_quantize -- offq_add_rmsnorm followed by the quantizer of
+ * offq_rotate_quantize with apply_hadamard = 0 on y (the QKV and up/gate
+ * inputs, whose rotations are fused into the weights offline), in one pass:
+ * h_out (nullable) as offq_add_rmsnorm; codes uint8 [M, D/2], scale fp16 and
+ * zero int16 [M, D/g] as offq_rotate_quantize; y_debug bf16 [M, D] (row
+ * stride ldy) or NULL: the normalized rows that were quantized.
+ * D / 256 in {8, 16, 32, 64} (D = 2048 ... 16384); g a power of two with
+ * D/256 <= g <= D/4 dividing D.
+ */
+int offq_add_rmsnorm_quantize(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr,
+                              int64_t M, int64_t D, float eps, int32_t g, uint16_t* h_out,
+                              int64_t ldh, uint8_t* codes, uint16_t* scale, int16_t* zero,
+                              uint16_t* y_debug, int64_t ldy, void* stream);
+
+/*
+ * offq_swiglu_rotate_quantize -- offq_swiglu followed by the online
+ * 128-point Hadamard H4 and the quantizer (offq_rotate_quantize with g = 128,
+ * apply_hadamard = 1) on the bf16 SwiGLU output, in one pass (the
+ * down-projection input, sec. 3.3 step 2(4)): codes uint8 [M, F/2], scale fp16
+ * and zero int16 [M, F/128]; y_debug fp32 [M, F] or NULL: the rotated rows
+ * that were quantized.  F a multiple of 128; ldg >= 2F, a multiple of 8.
+ */
+int offq_swiglu_rotate_quantize(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F,
+                                uint8_t* codes, uint16_t* scale, int16_t* zero, float* y_debug,
+                                void* stream);
+
+/*
  * offq_rope_kv_append -- RoPE on the new token's query and key heads, the
  * per-head online Hadamard H3 on the key (sec. 3.3 step 2(3)) and the KV4
  * quantizer (as offq_kv_quantize, group = head dim) writing position

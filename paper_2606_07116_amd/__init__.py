@@ -32,6 +32,8 @@ from ._lib import (  # noqa: F401
     offq_permute_rows,
     offq_top1_select,
     offq_add_rmsnorm,
+    offq_add_rmsnorm_quantize,
+    offq_swiglu_rotate_quantize,
     offq_rope_kv_append,
     offq_swiglu,
     offq_kv_attention_decode,

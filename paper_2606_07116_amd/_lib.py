@@ -34,6 +34,8 @@ EXPORTED = (
     "offq_add_rmsnorm",
     "offq_swiglu",
     "offq_rope_kv_append",
+    "offq_add_rmsnorm_quantize",
+    "offq_swiglu_rotate_quantize",
     "offq_top1_workspace_bytes",
     "offq_top1_select",
     "offq_channel_absmax",
@@ -97,6 +99,9 @@ def _load():
                                         vp, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp]
     f64 = ctypes.c_double
     sigs = {
+        "offq_add_rmsnorm_quantize": (ctypes.c_int, [vp, i64, vp, i64, i64, i64, ctypes.c_float,
+                                                     i32, vp, i64, vp, vp, vp, vp, i64, vp]),
+        "offq_swiglu_rotate_quantize": (ctypes.c_int, [vp, i64, i64, i64, vp, vp, vp, vp, vp]),
         "offq_top1_workspace_bytes": (i64, [i64, i64]),
         "offq_top1_select": (ctypes.c_int, [vp, i64, i64, i64, i64, i64, vp, vp, i64, vp, i64, vp]),
         "offq_channel_absmax": (ctypes.c_int, [vp, i64, i64, i64, vp, vp]),
@@ -180,6 +185,16 @@ def offq_add_rmsnorm_raw(x, ldx, res, ldr, M, D, eps, h_out, ldh, y_out, ldy, st
 
 def offq_swiglu_raw(gu, ldg, M, F, out, ldo, stream):
     return lib.offq_swiglu(gu, ldg, M, F, out, ldo, stream)
+
+
+def offq_add_rmsnorm_quantize_raw(x, ldx, res, ldr, M, D, eps, g, h_out, ldh, codes, scale, zero,
+                                  y_debug, ldy, stream):
+    return lib.offq_add_rmsnorm_quantize(x, ldx, res, ldr, M, D, eps, g, h_out, ldh, codes, scale,
+                                         zero, y_debug, ldy, stream)
+
+
+def offq_swiglu_rotate_quantize_raw(gu, ldg, M, F, codes, scale, zero, y_debug, stream):
+    return lib.offq_swiglu_rotate_quantize(gu, ldg, M, F, codes, scale, zero, y_debug, stream)
 
 
 def offq_rope_kv_append_raw(qkv, ldq, M, Hq, Hkv, head_dim, positions, rope_base, k_hadamard,
@@ -373,6 +388,48 @@ def offq_add_rmsnorm(x, res=None, eps=1e-5, want_h=True, want_y=True):
                                 _rows(res, "res") if res is not None else 0, M, D, float(eps),
                                 _ptr(h), D, _ptr(y), D, _stream()), "offq_add_rmsnorm")
     return h, y
+
+
+def offq_add_rmsnorm_quantize(x, g, res=None, eps=1e-5, want_h=False, debug=False):
+    """Fused add + RMSNorm + quantize (no rotation).  x, res: bf16 [M, D].
+    Returns (codes u8 [M, D/2], scale fp16 [M, D/g], zero int16 [M, D/g],
+    h bf16 [M, D] or None, y bf16 [M, D] or None)."""
+    torch = _torch()
+    _need(x, torch.bfloat16, "x", 2)
+    if res is not None:
+        _need(res, torch.bfloat16, "res", 2)
+    M, D = x.shape
+    dev = x.device
+    codes = torch.empty((M, D // 2), dtype=torch.uint8, device=dev)
+    scale = torch.empty((M, D // g), dtype=torch.float16, device=dev)
+    zero = torch.empty((M, D // g), dtype=torch.int16, device=dev)
+    h = torch.empty((M, D), dtype=torch.bfloat16, device=dev) if want_h else None
+    y = torch.empty((M, D), dtype=torch.bfloat16, device=dev) if debug else None
+    _check(lib.offq_add_rmsnorm_quantize(_ptr(x), _rows(x, "x"), _ptr(res),
+                                         _rows(res, "res") if res is not None else 0, M, D,
+                                         float(eps), int(g), _ptr(h), D, _ptr(codes), _ptr(scale),
+                                         _ptr(zero), _ptr(y), D, _stream()),
+           "offq_add_rmsnorm_quantize")
+    return codes, scale, zero, h, y
+
+
+def offq_swiglu_rotate_quantize(gu, debug=False):
+    """Fused SwiGLU + 128-point Hadamard + quantize.  gu: bf16 [M, 2F].
+    Returns (codes u8 [M, F/2], scale fp16 [M, F/128], zero int16 [M, F/128],
+    y fp32 [M, F] or None)."""
+    torch = _torch()
+    _need(gu, torch.bfloat16, "gu", 2)
+    M, F2 = gu.shape
+    F = F2 // 2
+    dev = gu.device
+    codes = torch.empty((M, F // 2), dtype=torch.uint8, device=dev)
+    scale = torch.empty((M, F // 128), dtype=torch.float16, device=dev)
+    zero = torch.empty((M, F // 128), dtype=torch.int16, device=dev)
+    y = torch.empty((M, F), dtype=torch.float32, device=dev) if debug else None
+    _check(lib.offq_swiglu_rotate_quantize(_ptr(gu), _rows(gu, "gu"), M, F, _ptr(codes), _ptr(scale),
+                                           _ptr(zero), _ptr(y), _stream()),
+           "offq_swiglu_rotate_quantize")
+    return codes, scale, zero, y
 
 
 def offq_swiglu(gu):

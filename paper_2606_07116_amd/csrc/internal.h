@@ -64,6 +64,13 @@ hipError_t launch_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* re
                               uint16_t* y_out, int64_t ldy, hipStream_t stream);
 hipError_t launch_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t* out,
                          int64_t ldo, hipStream_t stream);
+hipError_t launch_add_rmsnorm_quant(const uint16_t* x, int64_t ldx, const uint16_t* res,
+                                    int64_t ldr, int64_t M, int64_t D, float eps, int log2g,
+                                    uint16_t* h_out, int64_t ldh, uint8_t* codes, uint16_t* scale,
+                                    int16_t* zero, uint16_t* y_dbg, int64_t ldy,
+                                    hipStream_t stream);
+hipError_t launch_swiglu_rq(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint8_t* codes,
+                            uint16_t* scale, int16_t* zero, float* y_dbg, hipStream_t stream);
 hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq,
                                  int64_t Hkv, const int32_t* positions, double rope_base,
                                  bool k_had, bool v_had, uint16_t* q_out, uint8_t* kc,

@@ -124,12 +124,17 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
 
   // ---- key codes of the wave's 256 positions, issued first ---------------
   const uint8_t* kbase = kc + row0 * (DH / 2);
+  // blocks of 32 positions of this wave that hold any of the chunk's n
+  // positions (all of them in a full chunk); the others are skipped
+  const int nact = FULL ? NIT : min(NIT, max(0, (n - wave * WROWS + 31) / 32));
   uint4 kd[NIT][2];
 #pragma unroll
   for (int it = 0; it < NIT; ++it)
+    if (FULL || it < nact)
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-      kd[it][h] = *reinterpret_cast<const uint4*>(kbase + (uint32_t)(row(it, h) * (DH / 2) + qd * 16));
+      for (int h = 0; h < 2; ++h)
+        kd[it][h] =
+            *reinterpret_cast<const uint4*>(kbase + (uint32_t)(row(it, h) * (DH / 2) + qd * 16));
 
   // ---- query: FWHT across the lanes of wave 0 (lane holds dims 2l, 2l+1) --
   if (wave == 0) {
@@ -196,6 +201,10 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
   float mloc = -__builtin_inff();
 #pragma unroll
   for (int it = 0; it < NIT; ++it) {
+    if (!FULL && it >= nact) {
+      sc[it][0] = sc[it][1] = -__builtin_inff();
+      continue;
+    }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const uint32_t w4[4] = {kd[it][h].x, kd[it][h].y, kd[it][h].z, kd[it][h].w};
@@ -214,7 +223,7 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
       sc[it][h] = __builtin_fmaf(ab.x, d, ab.y);
       mloc = fmaxf(mloc, sc[it][h]);
     }
-    if (it == 1) {
+    if (FULL && it == 1) {
 #pragma unroll
       for (int jt = 0; jt < NIT; ++jt)
 #pragma unroll
@@ -222,6 +231,15 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
           vd[jt][h] =
               *reinterpret_cast<const uint4*>(vbase + (uint32_t)(row(jt, h) * (DH / 2) + qd * 16));
     }
+  }
+  if (!FULL) {
+#pragma unroll
+    for (int jt = 0; jt < NIT; ++jt)
+      if (jt < nact)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          vd[jt][h] =
+              *reinterpret_cast<const uint4*>(vbase + (uint32_t)(row(jt, h) * (DH / 2) + qd * 16));
   }
   mloc = wave_max(mloc);
   if (lane == 0) S.red[0][wave] = mloc;
@@ -254,6 +272,7 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
   for (int k = 0; k < 32; ++k) acc[k] = 0.0f;
 #pragma unroll
   for (int it = 0; it < NIT; ++it) {
+    if (!FULL && it >= nact) continue;
     const uint32_t a4[4] = {vd[it][0].x, vd[it][0].y, vd[it][0].z, vd[it][0].w};
     const uint32_t b4[4] = {vd[it][1].x, vd[it][1].y, vd[it][1].z, vd[it][1].w};
 #pragma unroll

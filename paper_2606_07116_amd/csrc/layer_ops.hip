@@ -205,7 +205,220 @@ __global__ __launch_bounds__(256) void rope_kv_append_kernel(
   }
 }
 
+// ---------------------------------------------------------------- fused variants
+// add + RMSNorm + the quantizer (no online rotation: the inputs of QKV and
+// up/gate, whose rotations are fused offline): the same arithmetic as
+// add_rmsnorm followed by rotate_quantize(apply_hadamard = 0) on the bf16 y,
+// in one pass.  One workgroup per row; thread t holds the E = D / 256
+// consecutive channels [t E, t E + E) (E a multiple of 8); a group of g
+// channels spans g / E adjacent lanes (1 ... 64).
+template <int E>
+__global__ __launch_bounds__(RN_THREADS) void add_rmsnorm_quant_kernel(
+    const uint16_t* __restrict__ x, int64_t ldx, const uint16_t* __restrict__ res, int64_t ldr,
+    int D, float eps, int log2g, uint16_t* __restrict__ h_out, int64_t ldh,
+    uint8_t* __restrict__ codes, uint16_t* __restrict__ scale, int16_t* __restrict__ zero,
+    uint16_t* __restrict__ y_dbg, int64_t ldy) {
+  __shared__ float s_red[RN_THREADS / 64];
+  const int tid = (int)__builtin_amdgcn_workitem_id_x();
+  const int64_t row = __builtin_amdgcn_workgroup_id_x();
+  float h[E];
+  const uint4* xr = reinterpret_cast<const uint4*>(x + row * ldx) + tid * (E / 8);
+#pragma unroll
+  for (int c = 0; c < E / 8; ++c) {
+    const uint4 a = xr[c];
+    const uint32_t aw[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      h[8 * c + 2 * k] = bf16_lo(aw[k]);
+      h[8 * c + 2 * k + 1] = bf16_hi(aw[k]);
+    }
+  }
+  if (res) {
+    const uint4* rr = reinterpret_cast<const uint4*>(res + row * ldr) + tid * (E / 8);
+#pragma unroll
+    for (int c = 0; c < E / 8; ++c) {
+      const uint4 b = rr[c];
+      const uint32_t bw[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        h[8 * c + 2 * k] = bf16_lo(f32_to_bf16_rne(h[8 * c + 2 * k] + bf16_lo(bw[k])));
+        h[8 * c + 2 * k + 1] = bf16_lo(f32_to_bf16_rne(h[8 * c + 2 * k + 1] + bf16_hi(bw[k])));
+      }
+    }
+  }
+  if (h_out) {
+    uint4* ho = reinterpret_cast<uint4*>(h_out + row * ldh) + tid * (E / 8);
+#pragma unroll
+    for (int c = 0; c < E / 8; ++c)
+      ho[c] = make_uint4(bf16x2_rne(h[8 * c], h[8 * c + 1]), bf16x2_rne(h[8 * c + 2], h[8 * c + 3]),
+                         bf16x2_rne(h[8 * c + 4], h[8 * c + 5]),
+                         bf16x2_rne(h[8 * c + 6], h[8 * c + 7]));
+  }
+  float ss = 0.0f;
+#pragma unroll
+  for (int k = 0; k < E; ++k) ss = __builtin_fmaf(h[k], h[k], ss);
+  ss = wsum(ss);
+  if ((tid & 63) == 0) s_red[tid >> 6] = ss;
+  __syncthreads();
+  ss = s_red[0] + s_red[1] + s_red[2] + s_red[3];
+  const float inv = 1.0f / __builtin_sqrtf(ss / (float)D + eps);
+  float y[E];
+#pragma unroll
+  for (int k = 0; k < E; ++k) y[k] = bf16_lo(f32_to_bf16_rne(h[k] * inv));
+  if (y_dbg) {
+    uint4* yo = reinterpret_cast<uint4*>(y_dbg + row * ldy) + tid * (E / 8);
+#pragma unroll
+    for (int c = 0; c < E / 8; ++c)
+      yo[c] = make_uint4(bf16x2_rne(y[8 * c], y[8 * c + 1]), bf16x2_rne(y[8 * c + 2], y[8 * c + 3]),
+                         bf16x2_rne(y[8 * c + 4], y[8 * c + 5]),
+                         bf16x2_rne(y[8 * c + 6], y[8 * c + 7]));
+  }
+  // group min / max over the g / E lanes of the group
+  float mx = y[0], mn = y[0];
+#pragma unroll
+  for (int k = 1; k < E; ++k) {
+    mx = fmaxf(mx, y[k]);
+    mn = fminf(mn, y[k]);
+  }
+  const int lanes = (1 << log2g) / E;
+  for (int o = 1; o < lanes; o <<= 1) {
+    mx = fmaxf(mx, __shfl_xor(mx, o));
+    mn = fminf(mn, __shfl_xor(mn, o));
+  }
+  const QParams p = quant_params(mx, mn);
+  const uint32_t lo = __float_as_uint(p.lo);
+  uint32_t cw[E / 8];
+#pragma unroll
+  for (int c = 0; c < E / 8; ++c) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) w |= (quant_bits(y[8 * c + k], p) - lo) << (4 * k);
+    cw[c] = w;
+  }
+  uint32_t* co = reinterpret_cast<uint32_t*>(codes + row * (D / 2)) + tid * (E / 8);
+#pragma unroll
+  for (int c = 0; c < E / 8; ++c) co[c] = cw[c];
+  if ((tid & (lanes - 1)) == 0) {
+    const int64_t gi = row * (D >> log2g) + (int64_t)tid * E / (1 << log2g);
+    scale[gi] = p.s16;
+    zero[gi] = p.z;
+  }
+}
+
+// SwiGLU + the online 128-point Hadamard H4 + the quantizer (g = 128) for
+// the down-projection input: a = bf16(fl32(silu(gate) * up)) as swiglu_kernel,
+// then y = c H a per group of 128 (fp32 butterflies, c = fl32(1/sqrt(128))
+// after them) and the codes of Eq. 1.  A group is 16 lanes x 8 channels:
+// butterfly stages over channel bits 0..2 inside the lane, bits 3..6 across
+// the lanes.  Workgroup: 16 groups of one row.
+__global__ __launch_bounds__(256) void swiglu_rq_kernel(const uint16_t* __restrict__ gu,
+                                                        int64_t ldg, int F,
+                                                        uint8_t* __restrict__ codes,
+                                                        uint16_t* __restrict__ scale,
+                                                        int16_t* __restrict__ zero,
+                                                        float* __restrict__ y_dbg,
+                                                        int64_t groups_per_row, int64_t M) {
+  const int tid = (int)__builtin_amdgcn_workitem_id_x();
+  const int64_t gidx = (int64_t)__builtin_amdgcn_workgroup_id_x() * 16 + (tid >> 4);
+  const int64_t m = gidx / groups_per_row;
+  const int grp = (int)(gidx - m * groups_per_row);
+  if (m >= M) return;  // whole groups of 16 lanes leave together
+  const int l16 = tid & 15;
+  const int c0 = grp * 128 + l16 * 8;  // first channel of this lane
+  const uint4 g4 = *reinterpret_cast<const uint4*>(gu + m * ldg + c0);
+  const uint4 u4 = *reinterpret_cast<const uint4*>(gu + m * ldg + F + c0);
+  const uint32_t gw[4] = {g4.x, g4.y, g4.z, g4.w}, uw[4] = {u4.x, u4.y, u4.z, u4.w};
+  float v[8];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float g0 = bf16_lo(gw[k]), g1 = bf16_hi(gw[k]);
+    const float a0 = g0 / (1.0f + expf(-g0)), a1 = g1 / (1.0f + expf(-g1));
+    const uint32_t ab = bf16x2_rne(a0 * bf16_lo(uw[k]), a1 * bf16_hi(uw[k]));
+    v[2 * k] = bf16_lo(ab);
+    v[2 * k + 1] = bf16_hi(ab);
+  }
+  // butterflies over channel bits 0, 1, 2 (inside the lane)
+#pragma unroll
+  for (int h = 1; h < 8; h <<= 1)
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (!(i & h)) {
+        const float a = v[i], b = v[i + h];
+        v[i] = a + b;
+        v[i + h] = a - b;
+      }
+  // bits 3 .. 6: across the 16 lanes of the group (lane bit 0 .. 3)
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const bool up = (l16 >> s) & 1;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float o = __shfl_xor(v[i], 1 << s);
+      v[i] = up ? o - v[i] : v[i] + o;
+    }
+  }
+  const float c = 0.08838834764831845f;  // fl32(1 / sqrt(128))
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] *= c;
+  if (y_dbg) {
+    float4* yo = reinterpret_cast<float4*>(y_dbg + m * F + c0);
+    yo[0] = make_float4(v[0], v[1], v[2], v[3]);
+    yo[1] = make_float4(v[4], v[5], v[6], v[7]);
+  }
+  float mx = v[0], mn = v[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) {
+    mx = fmaxf(mx, v[i]);
+    mn = fminf(mn, v[i]);
+  }
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) {
+    mx = fmaxf(mx, __shfl_xor(mx, o));
+    mn = fminf(mn, __shfl_xor(mn, o));
+  }
+  const QParams p = quant_params(mx, mn);
+  const uint32_t lo = __float_as_uint(p.lo);
+  uint32_t w = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) w |= (quant_bits(v[k], p) - lo) << (4 * k);
+  reinterpret_cast<uint32_t*>(codes + m * (F / 2))[c0 / 8] = w;
+  if (l16 == 0) {
+    scale[m * groups_per_row + grp] = p.s16;
+    zero[m * groups_per_row + grp] = p.z;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_add_rmsnorm_quant(const uint16_t* x, int64_t ldx, const uint16_t* res,
+                                    int64_t ldr, int64_t M, int64_t D, float eps, int log2g,
+                                    uint16_t* h_out, int64_t ldh, uint8_t* codes, uint16_t* scale,
+                                    int16_t* zero, uint16_t* y_dbg, int64_t ldy,
+                                    hipStream_t stream) {
+  const int E = (int)(D / RN_THREADS);
+#define OFFQ_ARQ(E_)                                                                         \
+  hipLaunchKernelGGL(add_rmsnorm_quant_kernel<E_>, dim3((unsigned)M), dim3(RN_THREADS), 0,   \
+                     stream, x, ldx, res, ldr, (int)D, eps, log2g, h_out, ldh, codes, scale, \
+                     zero, y_dbg, ldy)
+  switch (E) {
+    case 8: OFFQ_ARQ(8); break;
+    case 16: OFFQ_ARQ(16); break;
+    case 32: OFFQ_ARQ(32); break;
+    case 64: OFFQ_ARQ(64); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef OFFQ_ARQ
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_rq(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint8_t* codes,
+                            uint16_t* scale, int16_t* zero, float* y_dbg, hipStream_t stream) {
+  const int64_t gpr = F / 128;
+  const int64_t groups = M * gpr;
+  hipLaunchKernelGGL(swiglu_rq_kernel, dim3((unsigned)((groups + 15) / 16)), dim3(256), 0, stream,
+                     gu, ldg, (int)F, codes, scale, zero, y_dbg, gpr, M);
+  return hipGetLastError();
+}
 
 hipError_t launch_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr,
                               int64_t M, int64_t D, float eps, uint16_t* h_out, int64_t ldh,

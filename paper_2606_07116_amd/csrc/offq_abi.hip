@@ -443,4 +443,52 @@ int offq_permute_rows(const float* W, int64_t ldW, int64_t N, int64_t K, const i
                   "permute_rows");
 }
 
+int offq_add_rmsnorm_quantize(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr,
+                              int64_t M, int64_t D, float eps, int32_t g, uint16_t* h_out,
+                              int64_t ldh, uint8_t* codes, uint16_t* scale, int16_t* zero,
+                              uint16_t* y_debug, int64_t ldy, void* stream) {
+  if (M < 0) return fail(OFFQ_ERR_INVALID, "M < 0");
+  const int64_t E = D / 256;
+  if (D % 256 || (E != 8 && E != 16 && E != 32 && E != 64))
+    return fail(OFFQ_ERR_UNSUPPORTED, "D = %lld (D / 256 must be 8, 16, 32 or 64)", (long long)D);
+  const int lg = ilog2_pow2(g);
+  if (lg < 0 || g < E || g > D / 4 || D % g)
+    return fail(OFFQ_ERR_UNSUPPORTED, "g = %d (a power of two with D/256 <= g <= D/4)", g);
+  if (!(eps >= 0.0f) || eps > 1e30f) return fail(OFFQ_ERR_INVALID, "eps must be finite and >= 0");
+  if (!x || !codes || !scale || !zero) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (ldx < D || ldx % 8 || (res && (ldr < D || ldr % 8)) || (h_out && (ldh < D || ldh % 8)) ||
+      (y_debug && (ldy < D || ldy % 8)))
+    return fail(OFFQ_ERR_INVALID, "row strides must be >= D and multiples of 8");
+  if (!aligned(x, 16) || (res && !aligned(res, 16)) || (h_out && !aligned(h_out, 16)) ||
+      (y_debug && !aligned(y_debug, 16)) || !aligned(codes, 16) || !aligned(scale, 2) ||
+      !aligned(zero, 2))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (rows and codes: 16 B)");
+  if (M > (int64_t(1) << 31) - 1) return fail(OFFQ_ERR_UNSUPPORTED, "M too large");
+  if (M == 0) return ok();
+  if (int st = check_device()) return st;
+  return launched(offq::launch_add_rmsnorm_quant(x, ldx, res, ldr, M, D, eps, lg, h_out, ldh,
+                                                 codes, scale, zero, y_debug, ldy,
+                                                 (hipStream_t)stream),
+                  "add_rmsnorm_quantize");
+}
+
+int offq_swiglu_rotate_quantize(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F,
+                                uint8_t* codes, uint16_t* scale, int16_t* zero, float* y_debug,
+                                void* stream) {
+  if (M < 0) return fail(OFFQ_ERR_INVALID, "M < 0");
+  if (F < 128 || F % 128) return fail(OFFQ_ERR_INVALID, "F must be a positive multiple of 128");
+  if (ldg < 2 * F || ldg % 8) return fail(OFFQ_ERR_INVALID, "need ldg >= 2F, a multiple of 8");
+  if (F > (1 << 24) || M * (F / 128) > (int64_t(1) << 34))
+    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
+  if (!gu || !codes || !scale || !zero) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(gu, 16) || !aligned(codes, 4) || !aligned(scale, 2) || !aligned(zero, 2) ||
+      (y_debug && !aligned(y_debug, 16)))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (gu: 16 B)");
+  if (M == 0) return ok();
+  if (int st = check_device()) return st;
+  return launched(offq::launch_swiglu_rq(gu, ldg, M, F, codes, scale, zero, y_debug,
+                                         (hipStream_t)stream),
+                  "swiglu_rotate_quantize");
+}
+
 }  // extern "C"

@@ -81,6 +81,51 @@ def test_swiglu(M, F):
     _within_ulp(P.host(out.float()), ref, atol=1e-30)
 
 
+@pytest.mark.parametrize("M,D,g,with_res", [(16, 4096, 128, True), (5, 2048, 8, False),
+                                            (3, 16384, 256, True), (7, 8192, 2048, False),
+                                            (1, 4096, 1024, True)])
+def test_add_rmsnorm_quantize(M, D, g, with_res):
+    """Fused add + RMSNorm + quantize: h bit-exact, y within one bf16 ulp, the
+    codes, scales and zero-points bit-exact against the oracle quantizer fed
+    the kernel's y (the 4-bit decisions taken on the same values)."""
+    x = _rand_bf16((M, D), M + D + g, 3.0)
+    r = _rand_bf16((M, D), M + D + g + 1) if with_res else None
+    codes, scale, zero, h, y = offq.offq_add_rmsnorm_quantize(
+        _bf16_dev(x), g, _bf16_dev(r) if with_res else None, want_h=True, debug=True)
+    torch.cuda.synchronize()
+    h_ref, y_ref = OL.add_rmsnorm(x, r, 1e-5)
+    assert np.array_equal(P.host(h.float()), h_ref)
+    yg = P.host(y.float())
+    _within_ulp(yg, y_ref)
+    q, s, z = OQ.quantize_groups(yg, g)
+    assert np.array_equal(P.host(codes), OQ.pack_nibbles(q))
+    assert np.array_equal(P.fp16_bits(P.host(scale)), P.fp16_bits(s))
+    assert np.array_equal(P.host(zero), z)
+
+
+@pytest.mark.parametrize("M,F", [(16, 14336), (1, 128), (3, 1024)])
+def test_swiglu_rotate_quantize(M, F):
+    """Fused SwiGLU + H4 (128) + quantize: the rotated rows within the fp32
+    butterfly bound of the oracle's rotation of bf16(SwiGLU) plus one bf16 ulp
+    per input (an fp32 SwiGLU may round to the other bf16 neighbour), the
+    codes bit-exact against the oracle quantizer fed the kernel's rows."""
+    from oracle import hadamard as OH
+    gu = _rand_bf16((M, 2 * F), F + M, 4.0)
+    codes, scale, zero, y = offq.offq_swiglu_rotate_quantize(_bf16_dev(gu), debug=True)
+    torch.cuda.synchronize()
+    a = OL.bf16(OL.swiglu(gu))
+    y_ref = OH.rotate(a, 128)
+    yg = P.host(y).astype(np.float64)
+    ag = np.abs(a).reshape(M, -1, 128)
+    bound = ((7 + 2) * 2.0 ** -24 * ag.sum(-1, keepdims=True) +
+             OG.bf16_ulp(a).reshape(M, -1, 128).sum(-1, keepdims=True)) / math.sqrt(128)
+    assert np.all(np.abs(yg - y_ref).reshape(M, -1, 128) <= bound + 1e-30)
+    q, s, z = OQ.quantize_groups(P.host(y), 128)
+    assert np.array_equal(P.host(codes), OQ.pack_nibbles(q))
+    assert np.array_equal(P.fp16_bits(P.host(scale)), P.fp16_bits(s))
+    assert np.array_equal(P.host(zero), z)
+
+
 def _cache(M, Hkv, s_cap, fill):
     z = lambda *s, dt: torch.full(s, fill, dtype=dt, device=P.DEV)
     return dict(k_codes=z(M, Hkv, s_cap, 64, dt=torch.uint8), v_codes=z(M, Hkv, s_cap, 64, dt=torch.uint8),
@@ -172,14 +217,18 @@ def _llama_layer(M, ctx, seed=0, D=4096, Hq=32, Hkv=8, F=14336, g=128):
     return x, wf, cache, np.full(M, ctx, np.int32), ctx + 1, cfg
 
 
-def run_gpu_layer(x, wpk, cache, pos, seq_len, cfg, debug=False):
+def run_gpu_layer(x, wpk, cache, pos, seq_len, cfg, debug=False, fused=False):
     """One decode step through the C ABI: the sequence of library calls a
-    serving loop makes for a layer.  With debug, also the fp32 rows the
-    quantizers saw (the rotated MLP down input and the new K/V rows)."""
+    serving loop makes for a layer (fused: the norm steps and the SwiGLU step
+    each merged with the quantizer that follows them).  With debug, also the
+    rows the quantizers saw (the rotated MLP down input, the new K/V rows)."""
     Hq, Hkv, g, eps = cfg["Hq"], cfg["Hkv"], cfg["g"], cfg["eps"]
     M = x.shape[0]
-    _, y0 = offq.offq_add_rmsnorm(x, None, eps, want_h=False)
-    c, s, z, _ = offq.offq_rotate_quantize(y0, g, apply_hadamard=False)
+    if fused:
+        c, s, z, _, y0 = offq.offq_add_rmsnorm_quantize(x, g, eps=eps, debug=True)
+    else:
+        _, y0 = offq.offq_add_rmsnorm(x, None, eps, want_h=False)
+        c, s, z, _ = offq.offq_rotate_quantize(y0, g, apply_hadamard=False)
     qkv, _ = offq.offq_w4a4_gemm(c, s, z, *wpk["qkv"], g)
     q, ky, vy = offq.offq_rope_kv_append(qkv, Hq, Hkv, pos, cache, rope_base=cfg["rope_base"],
                                          debug=debug)
@@ -187,11 +236,19 @@ def run_gpu_layer(x, wpk, cache, pos, seq_len, cfg, debug=False):
                                       cache["v_codes"], cache["v_scale"], cache["v_zero"], seq_len)
     c, s, z, _ = offq.offq_rotate_quantize(o.reshape(M, Hq * 128), g, apply_hadamard=False)
     attn_out, _ = offq.offq_w4a4_gemm(c, s, z, *wpk["o"], g)
-    h1, y1 = offq.offq_add_rmsnorm(x, attn_out, eps)
-    c, s, z, _ = offq.offq_rotate_quantize(y1, g, apply_hadamard=False)
+    if fused:
+        c, s, z, h1, y1 = offq.offq_add_rmsnorm_quantize(x, g, attn_out, eps=eps, want_h=True,
+                                                         debug=True)
+    else:
+        h1, y1 = offq.offq_add_rmsnorm(x, attn_out, eps)
+        c, s, z, _ = offq.offq_rotate_quantize(y1, g, apply_hadamard=False)
     gu, _ = offq.offq_w4a4_gemm(c, s, z, *wpk["ug"], g)
-    a = offq.offq_swiglu(gu)
-    c, s, z, ya = offq.offq_rotate_quantize(a, g, apply_hadamard=True, debug=debug)
+    if fused:
+        a = None
+        c, s, z, ya = offq.offq_swiglu_rotate_quantize(gu, debug=debug)
+    else:
+        a = offq.offq_swiglu(gu)
+        c, s, z, ya = offq.offq_rotate_quantize(a, g, apply_hadamard=True, debug=debug)
     down, _ = offq.offq_w4a4_gemm(c, s, z, *wpk["down"], g)
     out, _ = offq.offq_add_rmsnorm(h1, down, eps, want_y=False)
     return out, dict(y0=y0, qkv=qkv, q=q, k_y=ky, v_y=vy, o=o, attn_out=attn_out, h1=h1, y1=y1,
@@ -209,8 +266,9 @@ def _gemm_bar(got, y_in, weights, g, y_rot=None):
                    OQ.colsum(q_w, g))
 
 
+@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("M,ctx", [(4, 300), (16, 2048)])
-def test_decode_layer_chain(M, ctx):
+def test_decode_layer_chain(M, ctx, fused):
     """Stage by stage, each GPU step meets its bar against the oracle step fed
     the previous GPU step's output (the steps end in 4-bit decisions, which
     both sides then take on the same values); end to end, the GPU step stays
@@ -221,9 +279,12 @@ def test_decode_layer_chain(M, ctx):
     wpk = {k: offq.offq_pack_weights(torch.from_numpy(w).to(P.DEV), g) for k, w in wf.items()}
     dcache = {k: torch.from_numpy(np.ascontiguousarray(v)).to(P.DEV) for k, v in cache.items()}
     out, it = run_gpu_layer(_bf16_dev(x), wpk, dcache, torch.from_numpy(pos).to(P.DEV), seq_len,
-                            cfg, debug=True)
+                            cfg, debug=True, fused=fused)
     torch.cuda.synchronize()
-    H = {k: (P.host(v.float()) if v.dtype == torch.bfloat16 else P.host(v)) for k, v in it.items()}
+    H = {k: (P.host(v.float()) if v.dtype == torch.bfloat16 else P.host(v))
+         for k, v in it.items() if v is not None}
+    if fused:
+        H["a"] = OL.bf16(OL.swiglu(H["gu"]))  # the SwiGLU values the fused kernel rounds
     Hq, Hkv = cfg["Hq"], cfg["Hkv"]
     # norm and residual steps
     _within_ulp(H["y0"], OL.add_rmsnorm(x, None, eps)[1])
@@ -236,10 +297,13 @@ def test_decode_layer_chain(M, ctx):
     _gemm_bar(H["attn_out"], H["o"].reshape(M, -1), weights["o"], g)
     _gemm_bar(H["gu"], H["y1"], weights["ug"], g)
     from oracle import hadamard as OH
+    flips = OG.bf16_ulp(H["a"]).reshape(M, -1, g).sum(-1).repeat(g, -1) if fused else 0.0
     assert np.all(np.abs(H["a_rot"] - OH.rotate(H["a"], g)) <=
-                  9 * 2.0 ** -24 * np.abs(H["a"]).reshape(M, -1, g).sum(-1).repeat(g, -1) / math.sqrt(g))
+                  (9 * 2.0 ** -24 * np.abs(H["a"]).reshape(M, -1, g).sum(-1).repeat(g, -1) + flips)
+                  / math.sqrt(g))
     _gemm_bar(H["down"], H["a"], weights["down"], g, y_rot=H["a_rot"])
-    _within_ulp(H["a"], OL.swiglu(H["gu"]), atol=1e-30)
+    if not fused:
+        _within_ulp(H["a"], OL.swiglu(H["gu"]), atol=1e-30)
     # RoPE + the new cache rows
     q_ref, ky_ref, vy_ref = OL.kv_rows(H["qkv"], Hq, Hkv, pos, cfg["rope_base"])
     _within_ulp(H["q"], OL.bf16(q_ref), atol=1e-6 * np.abs(q_ref).max())
