@@ -329,6 +329,291 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
   }
 }
 
+// ---------------------------------------------------------------------------
+// Grouped heads together: one workgroup per (key/value head, chunk) serves
+// the G query heads that share it, so each code word is loaded and unpacked
+// once for all of them.  Scores: as above, with G sets of query pairs (each
+// query scaled by its own power of two); every lane of a quad ends with the
+// G dot products of its position and lane qd stores query qd's score to LDS.
+// Weights: per pair of adjacent positions and query, fp16 pairs in LDS.
+// Values: a lane (word dg = lane & 15 of the row, position pair pg =
+// lane >> 4) takes 4 code bytes (8 dimensions) of two adjacent positions per
+// step; the interleave and the masks are shared by the G queries' dots.
+template <int G>
+struct GqaSmem {
+  float qf[G][DH];
+  uint32_t qp[G][DH / 2];
+  float qsum[G], qexp[G];
+  float2 kab[CH];           // (sm2 sk, -sm2 sk zk)
+  float2 vsz[CH];           // (sv, zv)
+  float sc[G][CH];          // scores, log2 domain
+  uint32_t wp[G][CH / 2];   // fp16 weight pairs of positions (2k, 2k + 1)
+  float red[3][G][WAVES];   // per wave: max, sum p, sum w zv
+  float o[WAVES][G][DH];    // per wave partial outputs
+};
+
+template <int G, bool FULL>
+__device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restrict__ q,
+                                          const uint8_t* __restrict__ kc,
+                                          const uint16_t* __restrict__ ks,
+                                          const int16_t* __restrict__ kz,
+                                          const uint8_t* __restrict__ vc,
+                                          const uint16_t* __restrict__ vs,
+                                          const int16_t* __restrict__ vz, int64_t row0, int kvh,
+                                          int n, float sm2, float cnorm, float* __restrict__ ws,
+                                          int nchunk, int chunk) {
+  const int tid = (int)__builtin_amdgcn_workitem_id_x();
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qd = lane & 3, rg = lane >> 2;
+  const int nact = FULL ? NIT : min(NIT, max(0, (n - wave * WROWS + 31) / 32));
+  auto row = [&](int it, int h) {
+    const int r = wave * WROWS + it * 32 + h * 16 + rg;
+    return FULL ? r : min(r, n - 1);
+  };
+
+  // ---- key codes ------------------------------------------------------------
+  const uint8_t* kbase = kc + row0 * (DH / 2);
+  uint4 kd[NIT][2];
+#pragma unroll
+  for (int it = 0; it < NIT; ++it)
+    if (FULL || it < nact)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        kd[it][h] =
+            *reinterpret_cast<const uint4*>(kbase + (uint32_t)(row(it, h) * (DH / 2) + qd * 16));
+
+  // ---- queries: wave w rotates query w --------------------------------------
+  if (wave < G) {
+    const uint16_t* qh = q + ((int64_t)kvh * G + wave) * DH;
+    const float a = bf16_lo(qh[2 * lane]), b = bf16_lo(qh[2 * lane + 1]);
+    float x0 = a + b, x1 = a - b;
+#pragma unroll
+    for (int s = 0; s < 6; ++s) {
+      const float y0 = __shfl_xor(x0, 1 << s), y1 = __shfl_xor(x1, 1 << s);
+      const bool up = (lane >> s) & 1;
+      x0 = up ? y0 - x0 : x0 + y0;
+      x1 = up ? y1 - x1 : x1 + y1;
+    }
+    const float r0 = bf16_lo(f32_to_bf16_rne(cnorm * x0));
+    const float r1 = bf16_lo(f32_to_bf16_rne(cnorm * x1));
+    const float qsum = wave_sum(r0 + r1);
+    const float qmax = wave_max(fmaxf(fabsf(r0), fabsf(r1)));
+    const int e = __builtin_amdgcn_frexp_expf(qmax);
+    S.qf[wave][2 * lane] = __builtin_amdgcn_ldexpf(r0, 15 - e);
+    S.qf[wave][2 * lane + 1] = __builtin_amdgcn_ldexpf(r1, 15 - e);
+    if (lane == 0) {
+      S.qsum[wave] = qsum;
+      S.qexp[wave] = (float)e;
+    }
+  }
+  __syncthreads();
+  if (tid < 64 * G) {
+    const int gq = tid >> 6, p = tid & 63;
+    const int i = p >> 2, j = p & 3;
+    const float f = (j & 1) ? 0.0625f : 1.0f;
+    S.qp[gq][p] = pack_f16(S.qf[gq][8 * i + j] * f, S.qf[gq][8 * i + j + 4] * f);
+  }
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int r = tid * 4 + t;
+    const int64_t rr = row0 + (FULL ? r : min(r, n - 1));
+    const float skm = sm2 * fp16_bits_to_f32(ks[rr]);
+    S.kab[r] = make_float2(skm, -skm * (float)kz[rr]);
+    S.vsz[r] = (FULL || r < n) ? make_float2(fp16_bits_to_f32(vs[rr]), (float)vz[rr])
+                               : make_float2(0.0f, 0.0f);
+  }
+  __syncthreads();
+
+  uint32_t qp[G][4][4];
+  float cq[G], qs[G];
+#pragma unroll
+  for (int gq = 0; gq < G; ++gq) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) qp[gq][u][j] = S.qp[gq][16 * qd + 4 * u + j];
+    cq[gq] = __builtin_amdgcn_ldexpf(1.0f, 9 + (int)S.qexp[gq]);  // dot = 2^-24 sum q' c
+    qs[gq] = S.qsum[gq];
+  }
+
+  // ---- scores ---------------------------------------------------------------
+  float mloc[G];
+#pragma unroll
+  for (int gq = 0; gq < G; ++gq) mloc[gq] = -__builtin_inff();
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = wave * WROWS + it * 32 + h * 16 + rg;
+      if (!FULL && it >= nact) {
+        if (qd < G) S.sc[qd][r] = -__builtin_inff();
+        continue;
+      }
+      const uint32_t w4[4] = {kd[it][h].x, kd[it][h].y, kd[it][h].z, kd[it][h].w};
+      float d[G];
+#pragma unroll
+      for (int gq = 0; gq < G; ++gq) d[gq] = 0.0f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t w = w4[u], w8 = w >> 8;
+        const uint32_t t0 = w & 0x000F000Fu, t1 = w & 0x00F000F0u;
+        const uint32_t t2 = w8 & 0x000F000Fu, t3 = w8 & 0x00F000F0u;
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq) {
+          d[gq] = dot2_f16(qp[gq][u][0], t0, d[gq]);
+          d[gq] = dot2_f16(qp[gq][u][1], t1, d[gq]);
+          d[gq] = dot2_f16(qp[gq][u][2], t2, d[gq]);
+          d[gq] = dot2_f16(qp[gq][u][3], t3, d[gq]);
+        }
+      }
+      const float2 ab = S.kab[r];
+      float mine = -__builtin_inff();
+#pragma unroll
+      for (int gq = 0; gq < G; ++gq) {
+        d[gq] += dpp<0xB1>(d[gq]);
+        d[gq] += dpp<0x4E>(d[gq]);
+        float sg = __builtin_fmaf(ab.x * cq[gq], d[gq], ab.y * qs[gq]);
+        if (!FULL && r >= n) sg = -__builtin_inff();
+        mloc[gq] = fmaxf(mloc[gq], sg);
+        if (qd == gq) mine = sg;
+      }
+      if (qd < G) S.sc[qd][r] = mine;
+    }
+  }
+#pragma unroll
+  for (int gq = 0; gq < G; ++gq) {
+    const float m = wave_max(mloc[gq]);
+    if (lane == 0) S.red[0][gq][wave] = m;
+  }
+
+  // ---- value codes: lane (word dg, position pair pg) -------------------------
+  const int dg = lane & 15, pg = lane >> 4;
+  const uint32_t* vrow = reinterpret_cast<const uint32_t*>(vc + row0 * (DH / 2)) + dg;
+  constexpr int VIT = WROWS / 8;  // steps of 8 positions (4 pairs) per wave
+  constexpr int BT = 8;           // steps per batch of loads
+  __syncthreads();
+
+  // ---- weights: fp16 pairs per (position pair, query) ------------------------
+  float m[G];
+#pragma unroll
+  for (int gq = 0; gq < G; ++gq)
+    m[gq] = fmaxf(fmaxf(S.red[0][gq][0], S.red[0][gq][1]), fmaxf(S.red[0][gq][2], S.red[0][gq][3]));
+  float lsum[G], zsum[G];
+#pragma unroll
+  for (int gq = 0; gq < G; ++gq) lsum[gq] = zsum[gq] = 0.0f;
+#pragma unroll
+  for (int t = 0; t < CH / 2 / THREADS; ++t) {
+    const int k = tid + t * THREADS;
+    const float2 sz0 = S.vsz[2 * k], sz1 = S.vsz[2 * k + 1];
+#pragma unroll
+    for (int gq = 0; gq < G; ++gq) {
+      const float p0 = __builtin_amdgcn_exp2f(S.sc[gq][2 * k] - m[gq]);
+      const float p1 = __builtin_amdgcn_exp2f(S.sc[gq][2 * k + 1] - m[gq]);
+      const uint32_t w = pack_f16(p0 * sz0.x, p1 * sz1.x);
+      S.wp[gq][k] = w;
+      const f16x2_t wh = __builtin_bit_cast(f16x2_t, w);
+      lsum[gq] += p0 + p1;
+      zsum[gq] = __builtin_fmaf((float)wh.x, sz0.y, zsum[gq]);
+      zsum[gq] = __builtin_fmaf((float)wh.y, sz1.y, zsum[gq]);
+    }
+  }
+#pragma unroll
+  for (int gq = 0; gq < G; ++gq) {
+    const float l = wave_sum(lsum[gq]), z = wave_sum(zsum[gq]);
+    if (lane == 0) {
+      S.red[1][gq][wave] = l;
+      S.red[2][gq][wave] = z;
+    }
+  }
+  __syncthreads();
+
+  // ---- values ---------------------------------------------------------------
+  float acc[G][8];
+#pragma unroll
+  for (int gq = 0; gq < G; ++gq)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[gq][k] = 0.0f;
+  const int vact = FULL ? VIT : min(VIT, max(0, (n - wave * WROWS + 7) / 8));
+#pragma unroll 1
+  for (int t0 = 0; t0 < VIT; t0 += BT) {
+    if (!FULL && t0 >= vact) break;
+    uint32_t va[BT], vb[BT];
+#pragma unroll
+    for (int t = 0; t < BT; ++t) {
+      const int ra = wave * WROWS + (t0 + t) * 8 + 2 * pg;
+      const int rA = FULL ? ra : min(ra, n - 1), rB = FULL ? ra + 1 : min(ra + 1, n - 1);
+      va[t] = vrow[(int64_t)rA * (DH / 8)];
+      vb[t] = vrow[(int64_t)rB * (DH / 8)];
+    }
+#pragma unroll
+    for (int t = 0; t < BT; ++t) {
+      const int pair = (wave * WROWS + (t0 + t) * 8) / 2 + pg;
+      const uint32_t x0 = __builtin_amdgcn_perm(vb[t], va[t], 0x05040100u);
+      const uint32_t x1 = __builtin_amdgcn_perm(vb[t], va[t], 0x07060302u);
+      const uint32_t x08 = x0 >> 8, x18 = x1 >> 8;
+      const uint32_t c[8] = {x0 & 0x000F000Fu,  x0 & 0x00F000F0u, x08 & 0x000F000Fu,
+                             x08 & 0x00F000F0u, x1 & 0x000F000Fu, x1 & 0x00F000F0u,
+                             x18 & 0x000F000Fu, x18 & 0x00F000F0u};
+#pragma unroll
+      for (int gq = 0; gq < G; ++gq) {
+        const uint32_t w = S.wp[gq][pair];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[gq][k] = dot2_f16(w, c[k], acc[gq][k]);
+      }
+    }
+  }
+  // sum over the 4 position-pair lanes of each word, then over the waves
+#pragma unroll
+  for (int gq = 0; gq < G; ++gq)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      acc[gq][k] += __shfl_xor(acc[gq][k], 16);
+      acc[gq][k] += __shfl_xor(acc[gq][k], 32);
+    }
+  if (pg == 0) {
+#pragma unroll
+    for (int gq = 0; gq < G; ++gq) {
+      float* dst = &S.o[wave][gq][8 * dg];
+      *reinterpret_cast<float4*>(dst) = make_float4(acc[gq][0], acc[gq][1], acc[gq][2], acc[gq][3]);
+      *reinterpret_cast<float4*>(dst + 4) =
+          make_float4(acc[gq][4], acc[gq][5], acc[gq][6], acc[gq][7]);
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < G * DH; e += THREADS) {
+    const int gq = e / DH, dd = e - gq * DH;
+    float o = S.o[0][gq][dd] + S.o[1][gq][dd] + S.o[2][gq][dd] + S.o[3][gq][dd];
+    o *= (dd & 1) ? 0x1p20f : 0x1p24f;  // codes entered as c 2^-24 / 16 c 2^-24
+    const float zw = S.red[2][gq][0] + S.red[2][gq][1] + S.red[2][gq][2] + S.red[2][gq][3];
+    float* rec = ws + (((int64_t)kvh * G + gq) * nchunk + chunk) * WS_FLOATS;
+    rec[2 + dd] = o - zw;
+    if (dd == 0) {
+      rec[0] = fmaxf(fmaxf(S.red[0][gq][0], S.red[0][gq][1]), fmaxf(S.red[0][gq][2], S.red[0][gq][3]));
+      rec[1] = S.red[1][gq][0] + S.red[1][gq][1] + S.red[1][gq][2] + S.red[1][gq][3];
+    }
+  }
+}
+
+template <int G>
+__global__ __launch_bounds__(THREADS) void kv_attention_gqa_kernel(
+    const uint16_t* __restrict__ q, const uint8_t* __restrict__ kc, const uint16_t* __restrict__ ks,
+    const int16_t* __restrict__ kz, const uint8_t* __restrict__ vc, const uint16_t* __restrict__ vs,
+    const int16_t* __restrict__ vz, int64_t S_cap, int seq_len, int nchunk, int units, float sm2,
+    float cnorm, float* __restrict__ ws) {
+  __shared__ GqaSmem<G> S;
+  const int unit = (int)__builtin_amdgcn_workgroup_id_x();
+  if (unit >= units) return;
+  const int kvh = unit / nchunk, chunk = unit - kvh * nchunk;
+  const int j0 = chunk * CH;
+  const int n = min(CH, seq_len - j0);
+  const int64_t row0 = (int64_t)kvh * S_cap + j0;
+  if (n == CH)
+    gqa_chunk<G, true>(S, q, kc, ks, kz, vc, vs, vz, row0, kvh, n, sm2, cnorm, ws, nchunk, chunk);
+  else
+    gqa_chunk<G, false>(S, q, kc, ks, kz, vc, vs, vz, row0, kvh, n, sm2, cnorm, ws, nchunk, chunk);
+}
+
 __global__ __launch_bounds__(THREADS) void kv_attention_chunk_kernel(
     const uint16_t* __restrict__ q, const uint8_t* __restrict__ kc, const uint16_t* __restrict__ ks,
     const int16_t* __restrict__ kz, const uint8_t* __restrict__ vc, const uint16_t* __restrict__ vs,
@@ -436,10 +721,21 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
   const int nchunk = (int)((seq_len + CH - 1) / CH);
   const float cnorm = (float)(1.0 / __builtin_sqrt((double)DH));
   const int64_t units = BH / group * nchunk;  // (key/value head, chunk) pairs
-  const int64_t grid = (units + 7) / 8 * 8 * group;
-  hipLaunchKernelGGL(kv_attention_chunk_kernel, dim3((unsigned)grid), dim3(THREADS), 0, stream, q,
-                     k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, S_cap, (int)seq_len,
-                     nchunk, (int)units, (int)group, sm_scale * LOG2E, cnorm, workspace);
+  if (group == 2 || group == 4) {
+    // the query heads of a key/value head in one workgroup
+#define OFFQ_GQA(G_)                                                                        \
+  hipLaunchKernelGGL(kv_attention_gqa_kernel<G_>, dim3((unsigned)units), dim3(THREADS), 0,  \
+                     stream, q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, S_cap, \
+                     (int)seq_len, nchunk, (int)units, sm_scale * LOG2E, cnorm, workspace)
+    if (group == 2) OFFQ_GQA(2);
+    else OFFQ_GQA(4);
+#undef OFFQ_GQA
+  } else {
+    const int64_t grid = (units + 7) / 8 * 8 * group;
+    hipLaunchKernelGGL(kv_attention_chunk_kernel, dim3((unsigned)grid), dim3(THREADS), 0, stream,
+                       q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, S_cap, (int)seq_len,
+                       nchunk, (int)units, (int)group, sm_scale * LOG2E, cnorm, workspace);
+  }
   hipLaunchKernelGGL(kv_attention_combine_kernel, dim3((unsigned)BH), dim3(DH), 0, stream,
                      workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out);
   return hipGetLastError();
