@@ -199,8 +199,9 @@ int offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const ui
                              float sm_scale, int32_t v_hadamard, uint16_t* out, void* workspace,
                              int64_t workspace_bytes, void* stream);
 
-/* Bytes of workspace offq_kv_attention_decode needs (0 for invalid sizes);
- * H is the number of query heads. */
+/* Bytes of workspace offq_kv_attention_decode needs (0 for invalid sizes):
+ * 130 floats per query head and chunk of up to 512 positions; H is the number
+ * of query heads. */
 int64_t offq_kv_attention_workspace_bytes(int64_t B, int64_t H, int64_t seq_len);
 
 /*

@@ -339,15 +339,19 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
 // Values: a lane (word dg = lane & 15 of the row, position pair pg =
 // lane >> 4) takes 4 code bytes (8 dimensions) of two adjacent positions per
 // step; the interleave and the masks are shared by the G queries' dots.
+constexpr int CHG = 512;        // positions per grouped-head workgroup
+constexpr int GROWS = CHG / WAVES;
+constexpr int GNIT = GROWS / 32;
+
 template <int G>
 struct GqaSmem {
   float qf[G][DH];
   uint32_t qp[G][DH / 2];
   float qsum[G], qexp[G];
-  float2 kab[CH];           // (sm2 sk, -sm2 sk zk)
-  float2 vsz[CH];           // (sv, zv)
-  float sc[G][CH];          // scores, log2 domain
-  uint32_t wp[G][CH / 2];   // fp16 weight pairs of positions (2k, 2k + 1)
+  float2 kab[CHG];          // (sm2 sk, -sm2 sk zk)
+  float2 vsz[CHG];          // (sv, zv)
+  float sc[G][CHG];         // scores, log2 domain
+  uint32_t wp[G][CHG / 2];  // fp16 weight pairs of positions (2k, 2k + 1)
   float red[3][G][WAVES];   // per wave: max, sum p, sum w zv
   float o[WAVES][G][DH];    // per wave partial outputs
 };
@@ -366,17 +370,17 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qd = lane & 3, rg = lane >> 2;
-  const int nact = FULL ? NIT : min(NIT, max(0, (n - wave * WROWS + 31) / 32));
+  const int nact = FULL ? GNIT : min(GNIT, max(0, (n - wave * GROWS + 31) / 32));
   auto row = [&](int it, int h) {
-    const int r = wave * WROWS + it * 32 + h * 16 + rg;
+    const int r = wave * GROWS + it * 32 + h * 16 + rg;
     return FULL ? r : min(r, n - 1);
   };
 
   // ---- key codes ------------------------------------------------------------
   const uint8_t* kbase = kc + row0 * (DH / 2);
-  uint4 kd[NIT][2];
+  uint4 kd[GNIT][2];
 #pragma unroll
-  for (int it = 0; it < NIT; ++it)
+  for (int it = 0; it < GNIT; ++it)
     if (FULL || it < nact)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
@@ -415,8 +419,8 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
     S.qp[gq][p] = pack_f16(S.qf[gq][8 * i + j] * f, S.qf[gq][8 * i + j + 4] * f);
   }
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int r = tid * 4 + t;
+  for (int t = 0; t < CHG / THREADS; ++t) {
+    const int r = tid * (CHG / THREADS) + t;
     const int64_t rr = row0 + (FULL ? r : min(r, n - 1));
     const float skm = sm2 * fp16_bits_to_f32(ks[rr]);
     S.kab[r] = make_float2(skm, -skm * (float)kz[rr]);
@@ -442,10 +446,10 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
 #pragma unroll
   for (int gq = 0; gq < G; ++gq) mloc[gq] = -__builtin_inff();
 #pragma unroll
-  for (int it = 0; it < NIT; ++it) {
+  for (int it = 0; it < GNIT; ++it) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int r = wave * WROWS + it * 32 + h * 16 + rg;
+      const int r = wave * GROWS + it * 32 + h * 16 + rg;
       if (!FULL && it >= nact) {
         if (qd < G) S.sc[qd][r] = -__builtin_inff();
         continue;
@@ -490,7 +494,7 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
   // ---- value codes: lane (word dg, position pair pg) -------------------------
   const int dg = lane & 15, pg = lane >> 4;
   const uint32_t* vrow = reinterpret_cast<const uint32_t*>(vc + row0 * (DH / 2)) + dg;
-  constexpr int VIT = WROWS / 8;  // steps of 8 positions (4 pairs) per wave
+  constexpr int VIT = GROWS / 8;  // steps of 8 positions (4 pairs) per wave
   constexpr int BT = 8;           // steps per batch of loads
   __syncthreads();
 
@@ -503,7 +507,7 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
 #pragma unroll
   for (int gq = 0; gq < G; ++gq) lsum[gq] = zsum[gq] = 0.0f;
 #pragma unroll
-  for (int t = 0; t < CH / 2 / THREADS; ++t) {
+  for (int t = 0; t < CHG / 2 / THREADS; ++t) {
     const int k = tid + t * THREADS;
     const float2 sz0 = S.vsz[2 * k], sz1 = S.vsz[2 * k + 1];
 #pragma unroll
@@ -534,21 +538,21 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
   for (int gq = 0; gq < G; ++gq)
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[gq][k] = 0.0f;
-  const int vact = FULL ? VIT : min(VIT, max(0, (n - wave * WROWS + 7) / 8));
+  const int vact = FULL ? VIT : min(VIT, max(0, (n - wave * GROWS + 7) / 8));
 #pragma unroll 1
   for (int t0 = 0; t0 < VIT; t0 += BT) {
     if (!FULL && t0 >= vact) break;
     uint32_t va[BT], vb[BT];
 #pragma unroll
     for (int t = 0; t < BT; ++t) {
-      const int ra = wave * WROWS + (t0 + t) * 8 + 2 * pg;
+      const int ra = wave * GROWS + (t0 + t) * 8 + 2 * pg;
       const int rA = FULL ? ra : min(ra, n - 1), rB = FULL ? ra + 1 : min(ra + 1, n - 1);
       va[t] = vrow[(int64_t)rA * (DH / 8)];
       vb[t] = vrow[(int64_t)rB * (DH / 8)];
     }
 #pragma unroll
     for (int t = 0; t < BT; ++t) {
-      const int pair = (wave * WROWS + (t0 + t) * 8) / 2 + pg;
+      const int pair = (wave * GROWS + (t0 + t) * 8) / 2 + pg;
       const uint32_t x0 = __builtin_amdgcn_perm(vb[t], va[t], 0x05040100u);
       const uint32_t x1 = __builtin_amdgcn_perm(vb[t], va[t], 0x07060302u);
       const uint32_t x08 = x0 >> 8, x18 = x1 >> 8;
@@ -605,10 +609,10 @@ __global__ __launch_bounds__(THREADS) void kv_attention_gqa_kernel(
   const int unit = (int)__builtin_amdgcn_workgroup_id_x();
   if (unit >= units) return;
   const int kvh = unit / nchunk, chunk = unit - kvh * nchunk;
-  const int j0 = chunk * CH;
-  const int n = min(CH, seq_len - j0);
+  const int j0 = chunk * CHG;
+  const int n = min(CHG, seq_len - j0);
   const int64_t row0 = (int64_t)kvh * S_cap + j0;
-  if (n == CH)
+  if (n == CHG)
     gqa_chunk<G, true>(S, q, kc, ks, kz, vc, vs, vz, row0, kvh, n, sm2, cnorm, ws, nchunk, chunk);
   else
     gqa_chunk<G, false>(S, q, kc, ks, kz, vc, vs, vz, row0, kvh, n, sm2, cnorm, ws, nchunk, chunk);
@@ -708,7 +712,9 @@ __global__ __launch_bounds__(DH) void kv_attention_combine_kernel(const float* _
 }  // namespace
 
 int64_t kv_attention_workspace_floats(int64_t BH, int64_t seq_len) {
-  return BH * ((seq_len + CH - 1) / CH) * WS_FLOATS;
+  // one record per (query head, chunk); the grouped-head path uses the
+  // smaller chunks, so their count bounds both paths
+  return BH * ((seq_len + CHG - 1) / CHG) * WS_FLOATS;
 }
 
 hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
@@ -718,10 +724,10 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
                                       int64_t S_cap, int64_t seq_len, float sm_scale,
                                       bool v_hadamard, uint16_t* out, float* workspace,
                                       hipStream_t stream) {
-  const int nchunk = (int)((seq_len + CH - 1) / CH);
   const float cnorm = (float)(1.0 / __builtin_sqrt((double)DH));
-  const int64_t units = BH / group * nchunk;  // (key/value head, chunk) pairs
   if (group == 2 || group == 4) {
+    const int nchunk = (int)((seq_len + CHG - 1) / CHG);
+    const int64_t units = BH / group * nchunk;  // (key/value head, chunk) pairs
     // the query heads of a key/value head in one workgroup
 #define OFFQ_GQA(G_)                                                                        \
   hipLaunchKernelGGL(kv_attention_gqa_kernel<G_>, dim3((unsigned)units), dim3(THREADS), 0,  \
@@ -730,14 +736,18 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
     if (group == 2) OFFQ_GQA(2);
     else OFFQ_GQA(4);
 #undef OFFQ_GQA
+    hipLaunchKernelGGL(kv_attention_combine_kernel, dim3((unsigned)BH), dim3(DH), 0, stream,
+                       workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out);
   } else {
+    const int nchunk = (int)((seq_len + CH - 1) / CH);
+    const int64_t units = BH / group * nchunk;  // (key/value head, chunk) pairs
     const int64_t grid = (units + 7) / 8 * 8 * group;
     hipLaunchKernelGGL(kv_attention_chunk_kernel, dim3((unsigned)grid), dim3(THREADS), 0, stream,
                        q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, S_cap, (int)seq_len,
                        nchunk, (int)units, (int)group, sm_scale * LOG2E, cnorm, workspace);
+    hipLaunchKernelGGL(kv_attention_combine_kernel, dim3((unsigned)BH), dim3(DH), 0, stream,
+                       workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out);
   }
-  hipLaunchKernelGGL(kv_attention_combine_kernel, dim3((unsigned)BH), dim3(DH), 0, stream,
-                     workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out);
   return hipGetLastError();
 }
 

@@ -201,8 +201,8 @@ int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
   if (seq_len < 1 || seq_len > s_cap)
     return fail(OFFQ_ERR_INVALID, "need 1 <= seq_len <= s_cap");
   if (B * Hq > (1 << 24) || seq_len > (int64_t(1) << 30) ||
-      s_cap > (int64_t(1) << 40) / (B * Hkv) || B * Hq * ((seq_len + 1023) / 1024) > (1 << 24))
-    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large (B Hq ceil(seq_len / 1024) <= 2^24)");
+      s_cap > (int64_t(1) << 40) / (B * Hkv) || B * Hq * ((seq_len + 511) / 512) > (1 << 24))
+    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large (B Hq ceil(seq_len / 512) <= 2^24)");
   if (v_hadamard != 0 && v_hadamard != 1) return fail(OFFQ_ERR_INVALID, "v_hadamard must be 0 or 1");
   if (!(sm_scale == sm_scale)) return fail(OFFQ_ERR_INVALID, "sm_scale is NaN");
   if (!q || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale || !v_zero || !out ||

@@ -117,7 +117,7 @@ def test_valid_call_without_gpu_reports_hip_error():
     ((0, 4, 100, 100, 128, 0.1, 0, 1 << 20), _lib.OFFQ_ERR_INVALID),      # B = 0
     ((2, 4, 100, 100, 128, 0.1, 2, 1 << 20), _lib.OFFQ_ERR_INVALID),      # bad flag
     ((2, 4, 100, 100, 128, float("nan"), 0, 1 << 20), _lib.OFFQ_ERR_INVALID),
-    ((2, 4, 2048, 2048, 128, 0.1, 0, 8 * 2 * 130 * 4 - 4), _lib.OFFQ_ERR_INVALID),  # small ws
+    ((2, 4, 2048, 2048, 128, 0.1, 0, 8 * 4 * 130 * 4 - 4), _lib.OFFQ_ERR_INVALID),  # small ws
     ((1 << 12, 1 << 12, 1 << 20, 1 << 20, 128, 0.1, 0, 1 << 60), _lib.OFFQ_ERR_UNSUPPORTED),
 ])
 def test_kv_attention_validation(args, expect):
@@ -137,11 +137,11 @@ def test_kv_attention_misaligned_and_null():
 
 
 def test_kv_attention_workspace_bytes():
-    # one record of 2 + 128 floats per (b, h, chunk of 1024 positions)
+    # one record of 2 + 128 floats per (b, h, chunk of up to 512 positions)
     assert _lib.offq_kv_attention_workspace_bytes(2, 4, 1) == 8 * 130 * 4
-    assert _lib.offq_kv_attention_workspace_bytes(2, 4, 1024) == 8 * 130 * 4
-    assert _lib.offq_kv_attention_workspace_bytes(2, 4, 1025) == 8 * 2 * 130 * 4
-    assert _lib.offq_kv_attention_workspace_bytes(8, 32, 32768) == 256 * 32 * 130 * 4
+    assert _lib.offq_kv_attention_workspace_bytes(2, 4, 512) == 8 * 130 * 4
+    assert _lib.offq_kv_attention_workspace_bytes(2, 4, 1025) == 8 * 3 * 130 * 4
+    assert _lib.offq_kv_attention_workspace_bytes(8, 32, 32768) == 256 * 64 * 130 * 4
     assert _lib.offq_kv_attention_workspace_bytes(0, 4, 10) == 0
     assert _lib.offq_kv_attention_workspace_bytes(1, 1, 0) == 0
 

@@ -110,7 +110,7 @@ def test_attention_workspace_too_small_raises():
     c = torch.zeros((B, H, S, 64), dtype=torch.uint8, device=P.DEV)
     s = torch.ones((B, H, S), dtype=torch.float16, device=P.DEV)
     z = torch.zeros((B, H, S), dtype=torch.int16, device=P.DEV)
-    ws = torch.empty(130, dtype=torch.float32, device=P.DEV)  # one chunk; two are needed
+    ws = torch.empty(130, dtype=torch.float32, device=P.DEV)  # one record; four are needed
     with pytest.raises(offq.OffqError):
         offq.offq_kv_attention_decode(q, c, s, z, c, s, z, S, workspace=ws)
 
