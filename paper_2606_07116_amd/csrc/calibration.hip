@@ -170,7 +170,7 @@ __global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ X, 
 // others move one place around the ring 1 -> 2 -> 4 -> ... -> 2P-2 ->
 // 2P-1 -> 2P-3 -> ... -> 3 -> 1.
 __device__ __forceinline__ int next_slot(int x, int P) {
-  if (x == 0) return 0;
+  if (x == 0 || P == 1) return x;  // D = 2: one pair, nothing moves
   if (x & 1) return x == 1 ? 2 : x - 2;
   return x == 2 * P - 2 ? 2 * P - 1 : x + 2;
 }
@@ -250,6 +250,57 @@ __global__ __launch_bounds__(256) void identity_kernel(double* __restrict__ V, i
   const int c = blockIdx.x * 256 + threadIdx.x;
   const int64_t r = blockIdx.y;
   if (c < D) V[r * ldV + c] = (c == r) ? 1.0 : 0.0;
+}
+
+// The slots other than 0 form one ring under next_slot: R = 1, 2, 4, ...,
+// 2P-2, 2P-1, 2P-3, ..., 3.  ring_index(x) is x's place in it; ring_slot is
+// the inverse.
+__device__ __forceinline__ int ring_index(int x, int P) {
+  if (x == 1) return 0;
+  if (!(x & 1)) return x >> 1;
+  return x == 2 * P - 1 ? P : 2 * P - 1 - (x >> 1);
+}
+__device__ __forceinline__ int ring_slot(int i, int P) {
+  if (i == 0) return 1;
+  return i < P ? 2 * i : 4 * P - 1 - 2 * i;
+}
+// Where the entry that sits in slot x after tau steps of a batch was at the
+// batch's start (every step moves slot R[i] to R[i + 1]).
+__device__ __forceinline__ int batch_loc(int x, int tau, int P) {
+  if (x == 0) return 0;
+  const int L = 2 * P - 1;
+  int i = ring_index(x, P) - tau;
+  i %= L;
+  if (i < 0) i += L;
+  return ring_slot(i, P);
+}
+
+// V <- V J_1 ... J_S for S steps at once: one workgroup per row of V, kept in
+// LDS at its batch-start slots; step tau rotates the pairs (2k, 2k+1) of that
+// step's slots, found through batch_loc, so nothing moves until the row is
+// written back in the slot order after the S steps.  V is then read and
+// written once per S steps instead of once per step.
+__global__ __launch_bounds__(256) void jacobi_v_batch_kernel(const double* __restrict__ V,
+                                                             int64_t ldV, int D, int P,
+                                                             const double2* __restrict__ cs,
+                                                             int S, double* __restrict__ Vo) {
+  extern __shared__ double row[];
+  const int64_t r = blockIdx.x;
+  const int tid = threadIdx.x;
+  for (int c = tid; c < D; c += 256) row[c] = V[r * ldV + c];
+  __syncthreads();
+  for (int tau = 0; tau < S; ++tau) {
+    const double2* rot = cs + (int64_t)tau * P;
+    for (int k = tid; k < P; k += 256) {
+      const int lp = batch_loc(2 * k, tau, P), lq = batch_loc(2 * k + 1, tau, P);
+      const double2 rk = rot[k];
+      const double vp = row[lp], vq = row[lq];
+      row[lp] = vp * rk.x - vq * rk.y;
+      row[lq] = vp * rk.y + vq * rk.x;
+    }
+    __syncthreads();
+  }
+  for (int c = tid; c < D; c += 256) Vo[r * ldV + c] = row[batch_loc(c, S, P)];
 }
 
 // Partial sums of the off-diagonal and total squares of A (one per row).
@@ -508,7 +559,13 @@ hipError_t launch_gram(const float* X, int64_t N, int64_t D, int64_t ldX, double
   return hipGetLastError();
 }
 
-int64_t eigh_workspace_doubles(int64_t D) { return 4 * D * D + 3 * D + 2 + D / 2 * 2 + D; }
+constexpr int JB = 64;  // Jacobi steps per batch of V updates
+
+int64_t eigh_workspace_doubles(int64_t D) {
+  // A, A', V, V'; partial norms (2 D) and totals (2); the rotations of a
+  // batch (JB steps of D / 2 pairs, 2 doubles each); ranks (D int32)
+  return 4 * D * D + 2 * D + 2 + (int64_t)JB * D + D / 2 + 2;
+}
 
 hipError_t launch_eigh(const double* C, int64_t ldC, int64_t D, double* evals, double* U,
                        int64_t ldU, double* ws, int max_sweeps, double tol, int* sweeps_done,
@@ -520,15 +577,15 @@ hipError_t launch_eigh(const double* C, int64_t ldC, int64_t D, double* evals, d
   double* V1 = V0 + D * D;
   double* part = V1 + D * D;          // 2 D
   double* tot = part + 2 * D;         // 2
-  double2* cs = reinterpret_cast<double2*>(tot + 2);  // P pairs (16-byte aligned: even offset)
-  int32_t* rank = reinterpret_cast<int32_t*>(cs + P);  // D ints
+  double2* cs = reinterpret_cast<double2*>(tot + 2);  // JB x P pairs (16-byte aligned)
+  int32_t* rank = reinterpret_cast<int32_t*>(cs + (int64_t)JB * P);  // D ints
   hipError_t e;
   e = hipMemcpy2DAsync(A0, D * sizeof(double), C, ldC * sizeof(double), D * sizeof(double), D,
                        hipMemcpyDeviceToDevice, stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(identity_kernel, dim3((unsigned)((D + 255) / 256), (unsigned)D), dim3(256), 0,
                      stream, V0, D, (int)D);
-  const dim3 ga((unsigned)((P + 15) / 16), (unsigned)((P + 15) / 16)), gv((unsigned)((P + 255) / 256), (unsigned)D);
+  const dim3 ga((unsigned)((P + 15) / 16), (unsigned)((P + 15) / 16));
   double h_tot[2] = {0.0, 0.0};
   int sweeps = 0;
   double rel = 0.0;
@@ -541,12 +598,17 @@ hipError_t launch_eigh(const double* C, int64_t ldC, int64_t D, double* evals, d
     if (e != hipSuccess) return e;
     rel = h_tot[1] > 0.0 ? __builtin_sqrt(h_tot[0] / h_tot[1]) : 0.0;
     if (rel <= tol || sweeps >= max_sweeps) break;
-    for (int step = 0; step < D - 1; ++step) {
-      hipLaunchKernelGGL(jacobi_rot_kernel, dim3((unsigned)((P + 255) / 256)), dim3(256), 0,
-                         stream, A0, D, P, cs);
-      hipLaunchKernelGGL(jacobi_a_kernel, ga, dim3(256), 0, stream, A0, D, P, cs, A1);
-      hipLaunchKernelGGL(jacobi_v_kernel, gv, dim3(256), 0, stream, V0, D, (int)D, P, cs, V1);
-      std::swap(A0, A1);
+    for (int step = 0; step < D - 1; step += JB) {
+      const int nb = (int)std::min<int64_t>(JB, D - 1 - step);
+      for (int tau = 0; tau < nb; ++tau) {
+        double2* cst = cs + (int64_t)tau * P;
+        hipLaunchKernelGGL(jacobi_rot_kernel, dim3((unsigned)((P + 255) / 256)), dim3(256), 0,
+                           stream, A0, D, P, cst);
+        hipLaunchKernelGGL(jacobi_a_kernel, ga, dim3(256), 0, stream, A0, D, P, cst, A1);
+        std::swap(A0, A1);
+      }
+      hipLaunchKernelGGL(jacobi_v_batch_kernel, dim3((unsigned)D), dim3(256),
+                         (size_t)D * sizeof(double), stream, V0, D, (int)D, P, cs, nb, V1);
       std::swap(V0, V1);
     }
     e = hipGetLastError();

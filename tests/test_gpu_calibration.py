@@ -85,7 +85,7 @@ def _check_eig(C, ev, U, gap_tol=1e-6):
     return sep.sum()
 
 
-@pytest.mark.parametrize("D,N", [(64, 200), (256, 64), (1024, 256)])
+@pytest.mark.parametrize("D,N", [(64, 200), (256, 64), (1024, 256), (130, 300), (2, 5)])
 def test_eigh(D, N):
     x = _calib_acts(N, 1, D, seed=D, n_dirs=3).reshape(N, D)
     C = OC.gram(x)
