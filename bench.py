@@ -513,9 +513,10 @@ def main():
         comp["gram"]["fp64_TFLOPs"] = round(2 * gf / (comp["gram"]["us"] * 1e-6) / 1e12, 3)
         nf = sum(2.0 * n_ * D * D for n_ in cc["layers"].values())
         comp["fuse_weights"]["fp32_TFLOPs"] = round(nf / (comp["fuse_weights"]["us"] * 1e-6) / 1e12, 2)
-        # every Jacobi step reads and writes A (16 D^2 bytes); V is read and
-        # written once per batch of 64 steps
-        eb = 16.0 * D * D * ((D - 1) + -(-(D - 1) // 64)) * cal["sweeps"]
+        # every Jacobi step reads and writes the upper triangle of the
+        # symmetric A (8 D (D + 1) bytes); V is read and written once per
+        # batch of 64 steps (16 D^2 bytes)
+        eb = (8.0 * D * (D + 1) * (D - 1) + 16.0 * D * D * -(-(D - 1) // 64)) * cal["sweeps"]
         comp["eigh"].update({"sweeps": cal["sweeps"], "rel_offdiag": cal["rel"], "alg_bytes": eb,
                              "GBs": round(eb / (comp["eigh"]["us"] * 1e-6) / 1e9, 1)})
         comp["eigh"]["frac_hbm"] = round(comp["eigh"]["GBs"] / PEAK_HBM_GBS, 4)

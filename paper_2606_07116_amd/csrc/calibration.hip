@@ -178,11 +178,8 @@ __device__ __forceinline__ int next_slot(int x, int P) {
 // (c, s) of the rotation that zeroes a[p][q] of pair k (Golub & Van Loan's
 // symmetric Schur decomposition of a 2 x 2 block); identity when the entry is
 // negligible against the diagonal.
-__global__ __launch_bounds__(256) void jacobi_rot_kernel(const double* __restrict__ A,
-                                                         int64_t ldA, int P,
-                                                         double2* __restrict__ cs) {
-  const int k = blockIdx.x * 256 + threadIdx.x;
-  if (k >= P) return;
+__device__ __forceinline__ double2 jacobi_rotation(const double* __restrict__ A, int64_t ldA,
+                                                   int k) {
   const double app = A[(int64_t)(2 * k) * ldA + 2 * k];
   const double aqq = A[(int64_t)(2 * k + 1) * ldA + 2 * k + 1];
   const double apq = A[(int64_t)(2 * k) * ldA + 2 * k + 1];
@@ -193,57 +190,83 @@ __global__ __launch_bounds__(256) void jacobi_rot_kernel(const double* __restric
     c = 1.0 / __builtin_sqrt(1.0 + t * t);
     s = t * c;
   }
-  cs[k] = make_double2(c, s);
+  return make_double2(c, s);
 }
 
-// A_out = perm(J^T A_in J): thread (pair i, pair j), i <= j, rotates the 2x2
-// block B of rows (2i, 2i+1), columns (2j, 2j+1): B' = R_i^T B R_j with
-// R = [[c, s], [-s, c]], and writes B' and its transpose to the moved slots.
-__global__ __launch_bounds__(256) void jacobi_a_kernel(const double* __restrict__ A, int64_t ldA,
-                                                       int P, const double2* __restrict__ cs,
-                                                       double* __restrict__ Ao) {
-  const int j = blockIdx.x * 16 + (threadIdx.x & 15);
-  const int i = blockIdx.y * 16 + (threadIdx.x >> 4);
-  if (i >= P || j >= P || i > j) return;
-  const double2 ri = cs[i], rj = cs[j];
-  const double* a0 = A + (int64_t)(2 * i) * ldA + 2 * j;
-  const double b00 = a0[0], b01 = a0[1], b10 = a0[ldA], b11 = a0[ldA + 1];
-  // T = B R_j
-  const double t00 = b00 * rj.x - b01 * rj.y, t01 = b00 * rj.y + b01 * rj.x;
-  const double t10 = b10 * rj.x - b11 * rj.y, t11 = b10 * rj.y + b11 * rj.x;
-  // B' = R_i^T T,  R_i^T = [[c, -s], [s, c]]
-  double n00 = ri.x * t00 - ri.y * t10, n01 = ri.x * t01 - ri.y * t11;
-  double n10 = ri.y * t00 + ri.x * t10, n11 = ri.y * t01 + ri.x * t11;
-  if (i == j) {
-    n01 = 0.0;  // the rotation's purpose; keep the block exactly symmetric
-    n10 = 0.0;
+// One Jacobi step, A_out = perm(J^T A_in J), on the upper triangle: the
+// matrices hold (and the steps read and write) only the entries (r, c) with
+// r <= c; the lower ones are left stale.  A workgroup takes a 16 x 16 tile of
+// 2 x 2 blocks (pair rows bi, pair columns bj >= bi); block (i, j), i <= j,
+// becomes B' = R_i^T B R_j with R = [[c, s], [-s, c]].  The rotations come
+// from A_in's diagonal blocks, which every workgroup reads (the step writes
+// A_out only), and the diagonal tiles store them for the eigenvector update.
+// An entry moved to (r', c') with r' > c' is stored at (c', r'); the rotated
+// tile is staged in LDS and written by rows.
+__global__ __launch_bounds__(256) void jacobi_a_tile_kernel(const double* __restrict__ A,
+                                                            int64_t ld, int P,
+                                                            double2* __restrict__ cs_out,
+                                                            double* __restrict__ Ao) {
+  // workgroup b -> tile (bi, bj) of the upper triangle, b = bj (bj + 1) / 2 + bi
+  const int b = blockIdx.x;
+  int bj = (int)((__builtin_sqrtf(8.0f * (float)b + 1.0f) - 1.0f) * 0.5f);
+  while ((bj + 1) * (bj + 2) / 2 <= b) ++bj;
+  while (bj * (bj + 1) / 2 > b) --bj;
+  const int bi = b - bj * (bj + 1) / 2;
+  __shared__ double2 s_r[2][16];
+  __shared__ double s_t[32][33];
+  const int tid = threadIdx.x;
+  const int pi = tid >> 4, pj = tid & 15;
+  const int i = bi * 16 + pi, j = bj * 16 + pj;
+  const bool ok = i < P && j < P;
+  double b00 = 0.0, b01 = 0.0, b10 = 0.0, b11 = 0.0;
+  if (ok && i <= j) {
+    const double* a0 = A + (int64_t)(2 * i) * ld + 2 * j;
+    b00 = a0[0];
+    b01 = a0[1];
+    b10 = i == j ? b01 : a0[ld];  // (2i + 1, 2i) is below the diagonal
+    b11 = a0[ld + 1];
   }
-  const int r0 = next_slot(2 * i, P), r1 = next_slot(2 * i + 1, P);
-  const int c0 = next_slot(2 * j, P), c1 = next_slot(2 * j + 1, P);
-  Ao[(int64_t)r0 * ldA + c0] = n00;
-  Ao[(int64_t)r0 * ldA + c1] = n01;
-  Ao[(int64_t)r1 * ldA + c0] = n10;
-  Ao[(int64_t)r1 * ldA + c1] = n11;
-  if (i != j) {
-    Ao[(int64_t)c0 * ldA + r0] = n00;
-    Ao[(int64_t)c1 * ldA + r0] = n01;
-    Ao[(int64_t)c0 * ldA + r1] = n10;
-    Ao[(int64_t)c1 * ldA + r1] = n11;
+  if (tid < 32) {
+    const int k = (tid < 16 ? bi : bj) * 16 + (tid & 15);
+    if (k < P) {
+      const double2 r = jacobi_rotation(A, ld, k);
+      s_r[tid >> 4][tid & 15] = r;
+      if (bi == bj && tid < 16) cs_out[k] = r;
+    }
   }
-}
-
-// V_out = perm_cols(V_in J): row r, pair j.
-__global__ __launch_bounds__(256) void jacobi_v_kernel(const double* __restrict__ V, int64_t ldV,
-                                                       int D, int P,
-                                                       const double2* __restrict__ cs,
-                                                       double* __restrict__ Vo) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  const int64_t r = blockIdx.y;
-  if (j >= P) return;
-  const double2 rj = cs[j];
-  const double vp = V[r * ldV + 2 * j], vq = V[r * ldV + 2 * j + 1];
-  Vo[r * ldV + next_slot(2 * j, P)] = vp * rj.x - vq * rj.y;
-  Vo[r * ldV + next_slot(2 * j + 1, P)] = vp * rj.y + vq * rj.x;
+  __syncthreads();
+  double n00 = 0.0, n01 = 0.0, n10 = 0.0, n11 = 0.0;
+  if (ok) {
+    const double2 ri = s_r[0][pi], rj = s_r[1][pj];
+    const double t00 = b00 * rj.x - b01 * rj.y, t01 = b00 * rj.y + b01 * rj.x;
+    const double t10 = b10 * rj.x - b11 * rj.y, t11 = b10 * rj.y + b11 * rj.x;
+    n00 = ri.x * t00 - ri.y * t10;
+    n01 = ri.x * t01 - ri.y * t11;
+    n10 = ri.y * t00 + ri.x * t10;
+    n11 = ri.y * t01 + ri.x * t11;
+    if (i == j) {
+      n01 = 0.0;  // what the rotation is for
+      n10 = 0.0;
+    }
+  }
+  s_t[2 * pi][2 * pj] = n00;
+  s_t[2 * pi][2 * pj + 1] = n01;
+  s_t[2 * pi + 1][2 * pj] = n10;
+  s_t[2 * pi + 1][2 * pj + 1] = n11;
+  __syncthreads();
+  // writes: 32 lanes per tile row, 8 rows per pass; in a diagonal tile only
+  // the entries on and above the diagonal
+  const int ec = tid & 31;
+  const int D = 2 * P;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int er = (tid >> 5) + 8 * u;
+    const int gr = bi * 32 + er, gc = bj * 32 + ec;
+    if (gr < D && gc < D && (bi != bj || er <= ec)) {
+      const int r1 = next_slot(gr, P), c1 = next_slot(gc, P);
+      Ao[(int64_t)min(r1, c1) * ld + max(r1, c1)] = s_t[er][ec];
+    }
+  }
 }
 
 __global__ __launch_bounds__(256) void identity_kernel(double* __restrict__ V, int64_t ldV, int D) {
@@ -264,57 +287,97 @@ __device__ __forceinline__ int ring_slot(int i, int P) {
   if (i == 0) return 1;
   return i < P ? 2 * i : 4 * P - 1 - 2 * i;
 }
-// Where the entry that sits in slot x after tau steps of a batch was at the
-// batch's start (every step moves slot R[i] to R[i + 1]).
-__device__ __forceinline__ int batch_loc(int x, int tau, int P) {
+// Where the entry that sits in slot x after t steps of a batch was at the
+// batch's start (every step moves slot R[i] to R[i + 1]); t = steps mod
+// (2P - 1), the length of the ring.
+__device__ __forceinline__ int batch_loc(int x, int t, int P) {
   if (x == 0) return 0;
-  const int L = 2 * P - 1;
-  int i = ring_index(x, P) - tau;
-  i %= L;
-  if (i < 0) i += L;
+  int i = ring_index(x, P) - t;
+  if (i < 0) i += 2 * P - 1;
   return ring_slot(i, P);
 }
 
-// V <- V J_1 ... J_S for S steps at once: one workgroup per row of V, kept in
-// LDS at its batch-start slots; step tau rotates the pairs (2k, 2k+1) of that
-// step's slots, found through batch_loc, so nothing moves until the row is
-// written back in the slot order after the S steps.  V is then read and
-// written once per S steps instead of once per step.
-__global__ __launch_bounds__(256) void jacobi_v_batch_kernel(const double* __restrict__ V,
+// LDS position of slot x of a row: even slots first, then odd ones, so that
+// the pair members of consecutive pairs are consecutive (unit-stride LDS
+// accesses).
+__device__ __forceinline__ int lds_pos(int x, int P) { return (x & 1) * P + (x >> 1); }
+
+// V <- V J_1 ... J_S for S steps at once: a workgroup holds NR rows of V in
+// LDS at their batch-start slots; step tau rotates the pairs (2k, 2k+1) of
+// that step's slots, found through batch_loc, so nothing moves until the
+// rows are written back in the slot order after the S steps.  V is read and
+// written once per S steps instead of once per step, and each rotation and
+// slot lookup serves the NR rows.
+template <int NR>
+__global__ __launch_bounds__(512) void jacobi_v_batch_kernel(const double* __restrict__ V,
                                                              int64_t ldV, int D, int P,
                                                              const double2* __restrict__ cs,
                                                              int S, double* __restrict__ Vo) {
-  extern __shared__ double row[];
-  const int64_t r = blockIdx.x;
+  extern __shared__ double rows[];
+  const int64_t r0 = (int64_t)blockIdx.x * NR;
+  const int nr = (int)min((int64_t)NR, (int64_t)D - r0);
   const int tid = threadIdx.x;
-  for (int c = tid; c < D; c += 256) row[c] = V[r * ldV + c];
+  const int L = 2 * P - 1;
+  for (int q = 0; q < nr; ++q)
+    for (int c = tid; c < D; c += 512) rows[q * D + lds_pos(c, P)] = V[(r0 + q) * ldV + c];
   __syncthreads();
   for (int tau = 0; tau < S; ++tau) {
     const double2* rot = cs + (int64_t)tau * P;
-    for (int k = tid; k < P; k += 256) {
-      const int lp = batch_loc(2 * k, tau, P), lq = batch_loc(2 * k + 1, tau, P);
-      const double2 rk = rot[k];
-      const double vp = row[lp], vq = row[lq];
-      row[lp] = vp * rk.x - vq * rk.y;
-      row[lq] = vp * rk.y + vq * rk.x;
+    const int t = tau % L;
+    // the pairs of a step are disjoint: up to 4 per thread are all loaded
+    // before any is stored, so the LDS latencies overlap
+    for (int k0 = tid; k0 < P; k0 += 4 * 512) {
+      int lp[4], lq[4];
+      double2 rk[4];
+      double vp[4][NR], vq[4][NR];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int k = k0 + u * 512;
+        if (k < P) {
+          lp[u] = lds_pos(batch_loc(2 * k, t, P), P);
+          lq[u] = lds_pos(batch_loc(2 * k + 1, t, P), P);
+          rk[u] = rot[k];
+#pragma unroll
+          for (int q = 0; q < NR; ++q) {
+            vp[u][q] = rows[q * D + lp[u]];
+            vq[u][q] = rows[q * D + lq[u]];
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (k0 + u * 512 < P) {
+#pragma unroll
+          for (int q = 0; q < NR; ++q) {
+            rows[q * D + lp[u]] = vp[u][q] * rk[u].x - vq[u][q] * rk[u].y;
+            rows[q * D + lq[u]] = vp[u][q] * rk[u].y + vq[u][q] * rk[u].x;
+          }
+        }
+      }
     }
     __syncthreads();
   }
-  for (int c = tid; c < D; c += 256) Vo[r * ldV + c] = row[batch_loc(c, S, P)];
+  const int t = S % L;
+  for (int q = 0; q < nr; ++q)
+    for (int c = tid; c < D; c += 512)
+      Vo[(r0 + q) * ldV + c] = rows[q * D + lds_pos(batch_loc(c, t, P), P)];
 }
 
-// Partial sums of the off-diagonal and total squares of A (one per row).
+// Partial sums of the off-diagonal and total squares of a symmetric A held in
+// its upper triangle (one per row).
 __global__ __launch_bounds__(256) void offnorm_kernel(const double* __restrict__ A, int64_t ldA,
                                                       int D, double* __restrict__ part) {
   __shared__ double s_off[4], s_all[4];
   const int64_t r = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   double off = 0.0, all = 0.0;
-  for (int c = tid; c < D; c += 256) {
+  for (int c = (int)r + tid; c < D; c += 256) {
     const double v = A[r * ldA + c];
-    all = __builtin_fma(v, v, all);
     if (c != r) off = __builtin_fma(v, v, off);
+    else all = v * v;
   }
+  off *= 2.0;  // (r, c) and (c, r)
+  all += off;
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
     off += __shfl_xor(off, o);
@@ -585,7 +648,10 @@ hipError_t launch_eigh(const double* C, int64_t ldC, int64_t D, double* evals, d
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(identity_kernel, dim3((unsigned)((D + 255) / 256), (unsigned)D), dim3(256), 0,
                      stream, V0, D, (int)D);
-  const dim3 ga((unsigned)((P + 15) / 16), (unsigned)((P + 15) / 16));
+  const unsigned nt = (unsigned)((P + 15) / 16);
+  const dim3 ga(nt * (nt + 1) / 2);  // tiles of the upper triangle
+  // V rows per workgroup of the batched update: as many as 128 KB of LDS hold, at most 4
+  const int nr = D <= 4096 ? 4 : 2;  // D <= 8192
   double h_tot[2] = {0.0, 0.0};
   int sweeps = 0;
   double rel = 0.0;
@@ -602,13 +668,20 @@ hipError_t launch_eigh(const double* C, int64_t ldC, int64_t D, double* evals, d
       const int nb = (int)std::min<int64_t>(JB, D - 1 - step);
       for (int tau = 0; tau < nb; ++tau) {
         double2* cst = cs + (int64_t)tau * P;
-        hipLaunchKernelGGL(jacobi_rot_kernel, dim3((unsigned)((P + 255) / 256)), dim3(256), 0,
-                           stream, A0, D, P, cst);
-        hipLaunchKernelGGL(jacobi_a_kernel, ga, dim3(256), 0, stream, A0, D, P, cst, A1);
+        hipLaunchKernelGGL(jacobi_a_tile_kernel, ga, dim3(256), 0, stream, A0, D, P, cst, A1);
         std::swap(A0, A1);
       }
-      hipLaunchKernelGGL(jacobi_v_batch_kernel, dim3((unsigned)D), dim3(256),
-                         (size_t)D * sizeof(double), stream, V0, D, (int)D, P, cs, nb, V1);
+      const dim3 gv((unsigned)((D + nr - 1) / nr)), bv(512);
+      const size_t lv = (size_t)(nr * D) * sizeof(double);
+      if (nr == 4)
+        hipLaunchKernelGGL(jacobi_v_batch_kernel<4>, gv, bv, lv, stream, V0, D, (int)D, P, cs, nb,
+                           V1);
+      else if (nr == 2)
+        hipLaunchKernelGGL(jacobi_v_batch_kernel<2>, gv, bv, lv, stream, V0, D, (int)D, P, cs, nb,
+                           V1);
+      else
+        hipLaunchKernelGGL(jacobi_v_batch_kernel<1>, gv, bv, lv, stream, V0, D, (int)D, P, cs, nb,
+                           V1);
       std::swap(V0, V1);
     }
     e = hipGetLastError();
