@@ -481,6 +481,9 @@ def main():
         comp[name]["TOPS"] = round(ops / (comp[name]["us"] * 1e-6) / 1e12, 1)
         comp[name]["frac_int8_peak"] = round(comp[name]["TOPS"] / PEAK_INT8_TOPS, 4)
 
+    # counter-measured HBM bytes are keyed by workload (and group size when
+    # --group-size overrides the workload's own)
+    tkey = wl if not args.group_size else f"{wl}:g{args.group_size}"
     if wl in ("attn_proj_prefill", "kv_chain"):
         ann_rq("rotate_quantize", M, K, g)
         ann_mm("w4a4_gemm", M, N, K)
@@ -491,7 +494,7 @@ def main():
         dom = "w4a4_gemm"
         roof = {"bound": "mfma", "achieved": comp[dom]["TOPS"], "peak": PEAK_INT8_TOPS,
                 "unit": "TOP/s", "frac": comp[dom]["frac_int8_peak"],
-                "traffic": traffic_for(f"w4a4_gemm:{wl}"), "kernel": dom,
+                "traffic": traffic_for(f"w4a4_gemm:{tkey}"), "kernel": dom,
                 "alg_ops_per_launch": comp[dom]["alg_ops"], "avg_launch_us": comp[dom]["us"]}
     elif wl == "mlp_prefill":
         ann_rq("rotate_quantize_up", up["M"], up["K"], up["g"])
@@ -503,7 +506,7 @@ def main():
         dom = "w4a4_gemm_upgate"
         roof = {"bound": "mfma", "achieved": comp[dom]["TOPS"], "peak": PEAK_INT8_TOPS,
                 "unit": "TOP/s", "frac": comp[dom]["frac_int8_peak"],
-                "traffic": traffic_for(f"w4a4_gemm:{wl}"), "kernel": dom,
+                "traffic": traffic_for(f"w4a4_gemm:{tkey}"), "kernel": dom,
                 "alg_ops_per_launch": comp[dom]["alg_ops"], "avg_launch_us": comp[dom]["us"]}
     elif wl == "calibration":
         tb = n_seq * L * D * 2
@@ -546,7 +549,7 @@ def main():
         unit = "GB/s"
         roof = {"bound": "hbm", "achieved": comp[name]["GBs"], "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": comp[name]["frac_hbm"],
-                "traffic": traffic_for("kv_attention:kv_decode_attention"), "kernel": name,
+                "traffic": traffic_for(f"kv_attention:{tkey}"), "kernel": name,
                 "alg_bytes_per_launch": b_, "avg_launch_us": comp[name]["us"]}
     else:
         ann_rq("rotate_quantize_up", Md, up["K"], up["g"])
@@ -560,10 +563,21 @@ def main():
         unit = "GB/s"
         dom = "w4a4_gemv_up"
         roof = {"bound": "hbm", "achieved": comp[dom]["GBs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": comp[dom]["frac_hbm"], "traffic": traffic_for(f"w4a4_gemv:{wl}"),
+                "frac": comp[dom]["frac_hbm"], "traffic": traffic_for(f"w4a4_gemv:{tkey}"),
                 "kernel": dom, "alg_bytes_per_launch": comp[dom]["alg_bytes"],
                 "avg_launch_us": comp[dom]["us"]}
 
+    # measured HBM bytes per launch of the other kernels, where counters exist
+    tnames = {"rotate_quantize": "rotate_quantize", "w4a4_gemm": "w4a4_gemm",
+              "kv_quantize": "kv_quantize", "rotate_quantize_up": "rotate_quantize_up",
+              "rotate_quantize_down": "rotate_quantize_down", "w4a4_gemm_upgate": "w4a4_gemm",
+              "w4a4_gemm_down": "w4a4_gemm_down", "w4a4_gemv_up": "w4a4_gemv",
+              "w4a4_gemv_down": "w4a4_gemv_down", "kv_attention_decode": "kv_attention"}
+    for name, c in comp.items():
+        if name in tnames:
+            tb = traffic_for(f"{tnames[name]}:{tkey}")
+            if tb is not None:
+                c["traffic_bytes"] = tb
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": unit, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
