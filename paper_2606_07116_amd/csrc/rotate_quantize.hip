@@ -212,13 +212,15 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
   constexpr bool FOLD = HAD && (LOGG % 2 == 0);
   constexpr bool STATS_B = LOGG >= 7;
   __shared__ __attribute__((aligned(16))) float lds[Gm::WORDS];
-  __shared__ uint32_t s_lo[STATS_B ? GPT : 1];
+  __shared__ uint32_t s_corr[STATS_B ? GPT : 1];  // bits(lo) * 0x11111111 per group
 
   // (the id builtins directly: this file's NaN/IEEE flags keep the device
   // library's id functions from being inlined)
   const int lane = (int)__builtin_amdgcn_workitem_id_x();
   const int64_t gbase = (int64_t)__builtin_amdgcn_workgroup_id_x() * GPT;
-  const bool full = gbase + GPT <= n_groups;
+  // (a 64-bit comparison is vector work on gfx950; readfirstlane keeps the
+  // flag, and the addressing chosen by it, in scalar registers)
+  const bool full = __builtin_amdgcn_readfirstlane((int)(gbase + GPT <= n_groups)) != 0;
   float* const la = lds + Gm::a_base(lane);
   float* const lb = lds + Gm::b_base(lane);
 
@@ -226,24 +228,44 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
   // elements this lane holds in layout A.  For g >= 512 the chunk's group is
   // the same for every lane (scalar arithmetic).  Groups past the end are
   // clamped to the last one: read, never stored.
-  // With one group per row and g < 512 the tile is GPT whole rows: offsets
-  // are taken from the tile's first row (a wave-uniform base) in 32 bits
-  // (the launcher checks that GPT rows fit).
+  // With one group per row and g < 512 the tile is GPT whole rows: a chunk's
+  // elements are addressed from a wave-uniform base (the chunk's first row in
+  // a full tile, the tile's first row otherwise) plus a 32-bit lane offset,
+  // which in a full tile is the same for every chunk (the launcher checks
+  // that GPT rows fit in 32-bit offsets).
   constexpr bool ROWS = LOGG < 9 && G1;
   const uint16_t* const xt = ROWS ? x + gbase * ldx : x;
   uint8_t* const ct = ROWS ? codes + gbase * ldc : codes;
   int64_t xoff[NCH], coff[NCH];
+  const uint16_t* xb[NCH];
+  uint8_t* cb[NCH];
+  uint32_t xo[NCH], co[NCH];
   if constexpr (ROWS) {
     // row gbase + (ch << (9 - log2 g)) + (lane >> (log2 g - 3)), clamped
     const int lr = lane >> (LOGG - 3);
     const int c = 8 * (lane & ((1 << (LOGG - 3)) - 1));
-    const int last = (int)min<int64_t>(n_groups - 1 - gbase, GPT - 1);
+    if (full) {
+      // (24-bit multiplies: lr < 64 and the launcher keeps strides below 2^24)
+      const uint32_t xl = (uint32_t)lr * ((uint32_t)ldx & 0xffffffu) + c;
+      const uint32_t cl = (uint32_t)lr * ((uint32_t)ldc & 0xffffffu) + (c >> 1);
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      int r = (ch << (9 - LOGG)) + lr;
-      if (!full) r = min(r, last);
-      xoff[ch] = (uint32_t)(r * (int)ldx + c);
-      coff[ch] = (uint32_t)(r * (int)ldc + (c >> 1));
+      for (int ch = 0; ch < NCH; ++ch) {
+        const int r0 = ch << (9 - LOGG);
+        xb[ch] = xt + (int64_t)r0 * ldx;
+        cb[ch] = ct + (int64_t)r0 * ldc;
+        xo[ch] = xl;
+        co[ch] = cl;
+      }
+    } else {
+      const int last = (int)(n_groups - 1 - gbase);  // < GPT - 1 here
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        const int r = min((ch << (9 - LOGG)) + lr, last);
+        xb[ch] = xt;
+        cb[ch] = ct;
+        xo[ch] = (uint32_t)(r * (int)ldx + c);
+        co[ch] = (uint32_t)(r * (int)ldc + (c >> 1));
+      }
     }
   } else {
 #pragma unroll
@@ -264,9 +286,16 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
       coff[ch] = (int64_t)row * ldc + ((col0 + c) >> 1);
     }
   }
-  auto stored = [&](int ch) -> bool {
-    const int64_t q = gbase + (((ch << 9) | (lane << 3)) >> LOGG);
-    return full || q < n_groups;
+  // groups of the tile that exist (uniform)
+  const int nleft = full ? GPT : (int)(n_groups - gbase);
+  auto stored = [&](int ch) -> bool { return full || (((ch << 9) | (lane << 3)) >> LOGG) < nleft; };
+  auto xptr = [&](int ch) -> const uint16_t* {
+    if constexpr (ROWS) return xb[ch] + xo[ch];
+    else return xt + xoff[ch];
+  };
+  auto cptr = [&](int ch) -> uint8_t* {
+    if constexpr (ROWS) return cb[ch] + co[ch];
+    else return ct + coff[ch];
   };
 
   float v[E];
@@ -277,7 +306,7 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
   // for the sum and the difference.
 #pragma unroll
   for (int ch = 0; ch < NCH; ++ch) {
-    uint4 d = *reinterpret_cast<const uint4*>(xt + xoff[ch]);
+    uint4 d = *reinterpret_cast<const uint4*>(xptr(ch));
     const uint32_t w[4] = {d.x, d.y, d.z, d.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -316,9 +345,9 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
       if (stored(ch)) {
-        const int64_t xo = (xt - x) + xoff[ch];
-        const int64_t row = xo / ldx;
-        float* yp = ydbg + row * ldy + (xo - row * ldx);
+        const int64_t xe = xptr(ch) - x;
+        const int64_t row = xe / ldx;
+        float* yp = ydbg + row * ldy + (xe - row * ldx);
         *reinterpret_cast<float4*>(yp) = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
         *reinterpret_cast<float4*>(yp + 4) =
             *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
@@ -344,8 +373,8 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
     if constexpr (FOLD) P.r *= cnorm;  // exact: cnorm is a power of two
     const int gi = lane >> NB;
     if ((lane & ((1 << NB) - 1)) == 0) {
-      s_lo[gi] = __float_as_uint(P.lo);
-      if (full || gbase + gi < n_groups) {
+      s_corr[gi] = __float_as_uint(P.lo) * 0x11111111u;
+      if (gi < nleft) {
         scale[gbase + gi] = P.s16;
         zero[gbase + gi] = P.z;
       }
@@ -367,7 +396,7 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
       v[ch * 8 + 5] = b.y;
       v[ch * 8 + 6] = b.z;
       v[ch * 8 + 7] = b.w;
-      corr[ch] = s_lo[((ch << 9) | (lane << 3)) >> LOGG] * 0x11111111u;
+      corr[ch] = s_corr[((ch << 9) | (lane << 3)) >> LOGG];
     }
   } else {
     // ---- back to layout A; statistics, parameters and codes there ----------
@@ -400,8 +429,9 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
       lane_reduce<LOGG - 3>(mx, mn);
       QParams P = FOLD ? quant_params(mx * cnorm, mn * cnorm) : quant_params(mx, mn);
       if constexpr (FOLD) P.r *= cnorm;
-      const int64_t q = gbase + (((ch << 9) | (lane << 3)) >> LOGG);
-      if ((lane & ((1 << (LOGG - 3)) - 1)) == 0 && (full || q < n_groups)) {
+      const int qt = ((ch << 9) | (lane << 3)) >> LOGG;  // group within the tile
+      const int64_t q = gbase + qt;
+      if ((lane & ((1 << (LOGG - 3)) - 1)) == 0 && qt < nleft) {
         scale[q] = P.s16;
         zero[q] = P.z;
       }
@@ -418,7 +448,7 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
 #pragma unroll
     for (int j = 0; j < 8; ++j) w += __float_as_uint(v[ch * 8 + j]) << (4 * j);
     w -= corr[ch];
-    if (stored(ch)) *reinterpret_cast<uint32_t*>(ct + coff[ch]) = w;
+    if (stored(ch)) *reinterpret_cast<uint32_t*>(cptr(ch)) = w;
   }
 }
 
@@ -439,9 +469,11 @@ hipError_t launch_t(const uint16_t* x, int64_t n_groups, int G, int64_t ldx, boo
   hipLaunchKernelGGL((rotate_quantize_kernel<LOGG, HD, DB, G1>), grid, block, 0, stream, x, \
                      n_groups, G, dm, dsh, ldx, codes, ldc, scale, zero, ydbg, ldy,         \
                      HD ? cnorm : 1.0f)
-  // one group per row: the fast addressing when GPT rows fit in 32-bit offsets
+  // one group per row: the fast addressing when GPT rows fit in 32-bit
+  // offsets and the strides in 24 bits
   const bool g1 = G == 1 && (LOGG >= 9 || (GPT * ldx < (int64_t(1) << 31) &&
-                                           GPT * ldc < (int64_t(1) << 31)));
+                                           GPT * ldc < (int64_t(1) << 31) &&
+                                           ldx < (int64_t(1) << 24) && ldc < (int64_t(1) << 24)));
 #define OFFQ_RQ_G(HD, DB) \
   if (g1) OFFQ_RQ(HD, DB, true); else OFFQ_RQ(HD, DB, false);
   if (had) {
