@@ -309,8 +309,8 @@ def main():
                       pos=torch.full((M,), ctx, dtype=torch.int32, device="cuda"))
             e = lambda *sh, dt=bf: torch.empty(sh, dtype=dt, device="cuda")
             st.update(y0=e(M, D), qkv=e(M, NQKV), q=e(M, Hq, 128), o=e(M, Hq, 128),
-                      ao=e(M, D), h1=e(M, D), y1=e(M, D), gu=e(M, 2 * F), a=e(M, F),
-                      dn=e(M, D), out=e(M, D))
+                      ao=e(M, D), h0=e(M, D), h1=e(M, D), y1=e(M, D), gu=e(M, 2 * F), a=e(M, F),
+                      dn=torch.zeros((M, D), dtype=bf, device="cuda"))
             for name, K_ in (("c_in", D), ("c_o", Hq * 128), ("c_d", F)):
                 st[name] = (e(M, K_ // 2, dt=u8), e(M, K_ // g, dt=f16), e(M, K_ // g, dt=i16))
             st["wsb"] = offq.offq_kv_attention_workspace_bytes(M, Hq, seq_len)
@@ -319,14 +319,16 @@ def main():
 
         lbytes = sum(weight_bytes(n_, k_, g) for n_, k_ in lshapes.values())
         kvbytes = M * Hkv * seq_len * 136
-        step_bytes = lbytes + kvbytes + M * (D * 2 * 4 + NQKV * 2 + F * 6)
+        step_bytes = lbytes + kvbytes + M * (D * 2 * 8 + NQKV * 2 + F * 6)
         lsets = Sets(make_layer, lbytes + kvbytes)
         layers = []
         work_ops = None
         config = {"workload": wl, "M": M, "D": D, "heads": [Hq, Hkv], "mlp": F, "g": g,
-                  "context": ctx, "step": "add+RMSNorm+quantize, QKV GEMV, RoPE + H3 + KV4 append, "
-                  "GQA decode attention, quantize, O GEMV, add+RMSNorm+quantize, up/gate GEMV, "
-                  "SwiGLU+H4+quantize, down GEMV, add", "input_sets": lsets.n}
+                  "context": ctx, "step": "add (the previous layer's residual) + RMSNorm + "
+                  "quantize, QKV GEMV, RoPE + H3 + KV4 append, GQA decode attention with the "
+                  "output quantized in its combine pass, O GEMV, add + RMSNorm + quantize, "
+                  "up/gate GEMV, SwiGLU + H4 + quantize, down GEMV (its residual add is the next "
+                  "layer's first add)", "input_sets": lsets.n}
     else:  # decode
         up = regroup(inputs.WORKLOADS["decode_up"])
         dn = regroup(inputs.WORKLOADS["decode_down"])
@@ -397,34 +399,37 @@ def main():
                                                 None, sp), "rotate_quantize")
             return gemm(st, cname, K_, N_, wname, dst)
 
-        def norm_quant(st, res, h_out):
+        def norm_quant(st, xname, res, h_out):
             c_, s_, z_ = st["c_in"]
             check(_lib.offq_add_rmsnorm_quantize_raw(
-                P_(st["x"]), D, P_(res) if res is not None else None, D, M, D, eps, g,
+                P_(st[xname]), D, P_(res) if res is not None else None, D, M, D, eps, g,
                 P_(h_out) if h_out is not None else None, D, P_(c_), P_(s_), P_(z_), None, 0, sp),
                 "add_rmsnorm_quantize")
 
         def step_layer(i):
             st = lsets[i]
-            norm_quant(st, None, None)
+            # steady state: the previous layer's residual add (its h1 + down)
+            # is this layer's first add (x stands for that h1, dn holds the
+            # down output of the set's previous step), as the next layer would
+            # take this one's h1 and dn
+            norm_quant(st, "x", st["dn"], st["h0"])
             check(gemm(st, "c_in", D, NQKV, "w_qkv", st["qkv"]), "gemv qkv")
             check(_lib.offq_rope_kv_append_raw(
                 P_(st["qkv"]), NQKV, M, Hq, Hkv, 128, P_(st["pos"]), base, 1, 0, P_(st["q"]),
                 P_(st["kc"]), P_(st["ks"]), P_(st["kz"]), P_(st["vc"]), P_(st["vs"]), P_(st["vz"]),
                 s_cap, None, None, sp), "rope_kv_append")
-            check(_lib.offq_kv_attention_decode_gqa_raw(
+            co_, so_, zo_ = st["c_o"]  # attention output quantized in its combine pass
+            check(_lib.offq_kv_attention_decode_quantize_raw(
                 P_(st["q"]), P_(st["kc"]), P_(st["ks"]), P_(st["kz"]), P_(st["vc"]), P_(st["vs"]),
-                P_(st["vz"]), M, Hq, Hkv, s_cap, seq_len, 128, sm, 0, P_(st["o"]), P_(st["ws"]),
-                st["wsb"], sp), "attention")
-            check(lin(st, "c_o", st["o"], Hq * 128, D, "w_o", st["ao"], 0), "gemv o")
-            norm_quant(st, st["ao"], st["h1"])
+                P_(st["vz"]), M, Hq, Hkv, s_cap, seq_len, 128, sm, 0, None, P_(co_), P_(so_),
+                P_(zo_), P_(st["ws"]), st["wsb"], sp), "attention")
+            check(gemm(st, "c_o", Hq * 128, D, "w_o", st["ao"]), "gemv o")
+            norm_quant(st, "h0", st["ao"], st["h1"])
             check(gemm(st, "c_in", D, 2 * F, "w_ug", st["gu"]), "gemv up/gate")
             c_, s_, z_ = st["c_d"]
             check(_lib.offq_swiglu_rotate_quantize_raw(P_(st["gu"]), 2 * F, M, F, P_(c_), P_(s_),
                                                        P_(z_), None, sp), "swiglu_rotate_quantize")
-            check(gemm(st, "c_d", F, D, "w_down", st["dn"]), "gemv down")
-            return _lib.offq_add_rmsnorm_raw(P_(st["h1"]), D, P_(st["dn"]), D, M, D, eps,
-                                             P_(st["out"]), D, None, 0, sp)
+            return gemm(st, "c_d", F, D, "w_down", st["dn"])
         # the whole layer is one phase: its kernels depend on each other
         phases.append(("decode_layer", step_layer))
     if wl == "kv_decode_attention":
@@ -440,7 +445,7 @@ def main():
         phases.append((mm_name, lambda i, s_=sets_: run_gemm(_lib, s_[i], sp)))
 
     # library launches per step (the spin below covers the host's enqueue time)
-    launches_per_step = 12 if wl == "decode_layer" else len(phases)
+    launches_per_step = 10 if wl == "decode_layer" else len(phases)
     for i in range(args.warmup):
         for name, fn in phases:
             check(fn(i), name)

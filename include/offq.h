@@ -222,6 +222,28 @@ int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
                                  int32_t v_hadamard, uint16_t* out, void* workspace,
                                  int64_t workspace_bytes, void* stream);
 
+/*
+ * offq_kv_attention_decode_quantize -- offq_kv_attention_decode_gqa whose
+ * output rows also come out quantized for the next linear layer (the
+ * O-projection, whose input is quantized without an online rotation, its
+ * rotation being fused into the weights offline: sec. 3.3 step 2(1)).  Each
+ * head's 128 outputs, rounded to bf16, form one group of the quantizer of
+ * Eq. 1: out_codes [B, Hq * 64] bytes (two codes per byte, element 2k in the
+ * low nibble), out_scale [B, Hq] fp16 bits, out_zero [B, Hq] int16 -- exactly
+ * what offq_rotate_quantize(out, g = 128, hadamard = 0) writes for the bf16
+ * output [B, Hq * 128].  out (bf16 [B, Hq, 128]) may be NULL; out_codes,
+ * out_scale and out_zero may not.  Other arguments, the workspace and the
+ * errors as for offq_kv_attention_decode_gqa.
+ */
+int offq_kv_attention_decode_quantize(const uint16_t* q, const uint8_t* k_codes,
+                                      const uint16_t* k_scale, const int16_t* k_zero,
+                                      const uint8_t* v_codes, const uint16_t* v_scale,
+                                      const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv,
+                                      int64_t s_cap, int64_t seq_len, int32_t head_dim,
+                                      float sm_scale, int32_t v_hadamard, uint16_t* out,
+                                      uint8_t* out_codes, uint16_t* out_scale, int16_t* out_zero,
+                                      void* workspace, int64_t workspace_bytes, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Decoder-layer steps around the quantized linear layers (one decode step,
  * one new token per sequence), following the pipeline of sec. 3.3 / Fig. 2.

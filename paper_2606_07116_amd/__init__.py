@@ -37,6 +37,7 @@ from ._lib import (  # noqa: F401
     offq_rope_kv_append,
     offq_swiglu,
     offq_kv_attention_decode,
+    offq_kv_attention_decode_quantize,
     offq_kv_attention_workspace_bytes,
     offq_kv_quantize,
     offq_pack_weights,

@@ -31,6 +31,7 @@ EXPORTED = (
     "offq_kv_attention_decode",
     "offq_kv_attention_workspace_bytes",
     "offq_kv_attention_decode_gqa",
+    "offq_kv_attention_decode_quantize",
     "offq_add_rmsnorm",
     "offq_swiglu",
     "offq_rope_kv_append",
@@ -89,6 +90,10 @@ def _load():
     lib.offq_kv_attention_decode_gqa.restype = ctypes.c_int
     lib.offq_kv_attention_decode_gqa.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64,
                                                  i32, ctypes.c_float, i32, vp, vp, i64, vp]
+    lib.offq_kv_attention_decode_quantize.restype = ctypes.c_int
+    lib.offq_kv_attention_decode_quantize.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64,
+                                                      i64, i32, ctypes.c_float, i32, vp, vp, vp, vp,
+                                                      vp, i64, vp]
     lib.offq_add_rmsnorm.restype = ctypes.c_int
     lib.offq_add_rmsnorm.argtypes = [vp, i64, vp, i64, i64, i64, ctypes.c_float, vp, i64, vp, i64,
                                      vp]
@@ -177,6 +182,16 @@ def offq_kv_attention_decode_gqa_raw(q, k_codes, k_scale, k_zero, v_codes, v_sca
     return lib.offq_kv_attention_decode_gqa(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B,
                                             Hq, Hkv, s_cap, seq_len, head_dim, sm_scale, v_hadamard,
                                             out, workspace, workspace_bytes, stream)
+
+
+def offq_kv_attention_decode_quantize_raw(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B,
+                                          Hq, Hkv, s_cap, seq_len, head_dim, sm_scale, v_hadamard,
+                                          out, out_codes, out_scale, out_zero, workspace,
+                                          workspace_bytes, stream):
+    return lib.offq_kv_attention_decode_quantize(q, k_codes, k_scale, k_zero, v_codes, v_scale,
+                                                 v_zero, B, Hq, Hkv, s_cap, seq_len, head_dim,
+                                                 sm_scale, v_hadamard, out, out_codes, out_scale,
+                                                 out_zero, workspace, workspace_bytes, stream)
 
 
 def offq_add_rmsnorm_raw(x, ldx, res, ldr, M, D, eps, h_out, ldh, y_out, ldy, stream):
@@ -319,14 +334,7 @@ def offq_pack_weights(w, g):
     return wc, ws, cs
 
 
-def offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, seq_len,
-                             sm_scale=None, v_hadamard=False, out=None, workspace=None):
-    """One decode step of attention over the 4-bit cache.
-
-    q: bf16 [B, H, 128]; k_codes / v_codes: u8 [B, H, s_cap, 64];
-    k_scale / v_scale: fp16 [B, H, s_cap]; k_zero / v_zero: int16 [B, H, s_cap]
-    (all contiguous).  Positions 0 .. seq_len-1 are attended.  sm_scale
-    defaults to 1/sqrt(128).  Returns out bf16 [B, H, 128]."""
+def _attention_operands(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, sm_scale):
     torch = _torch()
     _need(q, torch.bfloat16, "q", 3)
     for t, dt, n in ((k_codes, torch.uint8, "k_codes"), (v_codes, torch.uint8, "v_codes")):
@@ -346,6 +354,21 @@ def offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_ze
         raise ValueError("operand shapes do not match")
     if sm_scale is None:
         sm_scale = 1.0 / float(Dh) ** 0.5
+    return B, H, Dh, Hkv, s_cap, sm_scale
+
+
+def offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, seq_len,
+                             sm_scale=None, v_hadamard=False, out=None, workspace=None):
+    """One decode step of attention over the 4-bit cache.
+
+    q: bf16 [B, H, 128]; k_codes / v_codes: u8 [B, Hkv, s_cap, 64];
+    k_scale / v_scale: fp16 [B, Hkv, s_cap]; k_zero / v_zero: int16
+    [B, Hkv, s_cap] (all contiguous; H a multiple of Hkv: grouped-query
+    attention).  Positions 0 .. seq_len-1 are attended.  sm_scale defaults to
+    1/sqrt(128).  Returns out bf16 [B, H, 128]."""
+    torch = _torch()
+    B, H, Dh, Hkv, s_cap, sm_scale = _attention_operands(q, k_codes, k_scale, k_zero, v_codes,
+                                                         v_scale, v_zero, sm_scale)
     dev = q.device
     if out is None:
         out = torch.empty((B, H, Dh), dtype=torch.bfloat16, device=dev)
@@ -363,6 +386,36 @@ def offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_ze
                                             workspace.numel() * 4, _stream()),
            "offq_kv_attention_decode")
     return out
+
+
+def offq_kv_attention_decode_quantize(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero,
+                                      seq_len, sm_scale=None, v_hadamard=False, out=None,
+                                      workspace=None):
+    """offq_kv_attention_decode with each head's output row also quantized
+    (one group of 128, no rotation): returns (codes u8 [B, H * 64], scale fp16
+    [B, H], zero int16 [B, H], out), out being the bf16 [B, H, 128] output
+    when given (it is then also written), else None."""
+    torch = _torch()
+    B, H, Dh, Hkv, s_cap, sm_scale = _attention_operands(q, k_codes, k_scale, k_zero, v_codes,
+                                                         v_scale, v_zero, sm_scale)
+    dev = q.device
+    if out is not None:
+        _need(out, torch.bfloat16, "out", 3)
+        if not out.is_contiguous() or out.shape != (B, H, Dh):
+            raise ValueError("out must be a contiguous [B, H, head_dim] tensor")
+    codes = torch.empty((B, H * Dh // 2), dtype=torch.uint8, device=dev)
+    scale = torch.empty((B, H), dtype=torch.float16, device=dev)
+    zero = torch.empty((B, H), dtype=torch.int16, device=dev)
+    need = lib.offq_kv_attention_workspace_bytes(B, H, int(seq_len))
+    if workspace is None:
+        workspace = torch.empty((max(need, 4) + 3) // 4, dtype=torch.float32, device=dev)
+    _need(workspace, torch.float32, "workspace", 1)
+    _check(lib.offq_kv_attention_decode_quantize(
+        _ptr(q), _ptr(k_codes), _ptr(k_scale), _ptr(k_zero), _ptr(v_codes), _ptr(v_scale),
+        _ptr(v_zero), B, H, Hkv, s_cap, int(seq_len), Dh, float(sm_scale), int(bool(v_hadamard)),
+        _ptr(out) if out is not None else None, _ptr(codes), _ptr(scale), _ptr(zero),
+        _ptr(workspace), workspace.numel() * 4, _stream()), "offq_kv_attention_decode_quantize")
+    return codes, scale, zero, out
 
 
 def _rows(t, name):

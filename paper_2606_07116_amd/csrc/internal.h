@@ -55,7 +55,8 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
                                       const uint8_t* v_codes, const uint16_t* v_scale,
                                       const int16_t* v_zero, int64_t BH, int64_t group,
                                       int64_t S_cap, int64_t seq_len, float sm_scale,
-                                      bool v_hadamard, uint16_t* out, float* workspace,
+                                      bool v_hadamard, uint16_t* out, uint8_t* qcodes,
+                                      uint16_t* qscale, int16_t* qzero, float* workspace,
                                       hipStream_t stream);
 
 // decoder-layer kernels (layer_ops.hip)

@@ -85,6 +85,11 @@ __device__ __forceinline__ float wave_max(float v) {
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
   return v;
 }
+__device__ __forceinline__ float wave_min(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fminf(v, __shfl_xor(v, o));
+  return v;
+}
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
@@ -652,10 +657,15 @@ __global__ __launch_bounds__(THREADS) void kv_attention_chunk_kernel(
 // thread then sums its dimension over the chunks with independent loads.
 constexpr int CT = 1024;  // chunk factors held in LDS per round
 
-__global__ __launch_bounds__(DH) void kv_attention_combine_kernel(const float* __restrict__ ws,
-                                                                  int nchunk, int v_had,
-                                                                  float cnorm,
-                                                                  uint16_t* __restrict__ out) {
+// QUANT: the head's output row, rounded to bf16, is also quantized as one
+// group of the quantizer (Eq. 1, no rotation): codes two per byte (element
+// 2k in the low nibble), fp16 scale and int16 zero-point per (b, h), the
+// layout offq_rotate_quantize writes for a [B, Hq * 128] input with g = 128;
+// out may then be NULL.
+template <bool QUANT>
+__global__ __launch_bounds__(DH) void kv_attention_combine_kernel(
+    const float* __restrict__ ws, int nchunk, int v_had, float cnorm, uint16_t* __restrict__ out,
+    uint8_t* __restrict__ qcodes, uint16_t* __restrict__ qscale, int16_t* __restrict__ qzero) {
   __shared__ float s_e[CT];
   __shared__ float s_red[2][DH / 64];
   __shared__ float s_o[DH];
@@ -706,7 +716,26 @@ __global__ __launch_bounds__(DH) void kv_attention_combine_kernel(const float* _
       a = __builtin_fmaf(s_o[i], (__builtin_popcount(i & d) & 1) ? -1.0f : 1.0f, a);
     o = a * cnorm;
   }
-  out[(int64_t)bh * DH + d] = f32_to_bf16_rne(o);
+  const uint16_t ob = f32_to_bf16_rne(o);
+  if (out) out[(int64_t)bh * DH + d] = ob;
+  if constexpr (QUANT) {
+    const float y = bf16_lo(ob);
+    const float mx = wave_max(y), mn = wave_min(y);
+    __syncthreads();  // s_red's sums are consumed
+    if (lane == 0) {
+      s_red[0][wave] = mx;
+      s_red[1][wave] = mn;
+    }
+    __syncthreads();
+    const QParams P = quant_params(fmaxf(s_red[0][0], s_red[0][1]), fminf(s_red[1][0], s_red[1][1]));
+    const uint32_t c = quant_bits(y, P) - __float_as_uint(P.lo);  // the code, 0..15
+    const uint32_t c1 = __shfl_down(c, 1);                         // element d + 1's
+    if (!(d & 1)) qcodes[(int64_t)bh * (DH / 2) + (d >> 1)] = (uint8_t)(c | (c1 << 4));
+    if (d == 0) {
+      qscale[bh] = P.s16;
+      qzero[bh] = P.z;
+    }
+  }
 }
 
 }  // namespace
@@ -722,9 +751,19 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
                                       const uint8_t* v_codes, const uint16_t* v_scale,
                                       const int16_t* v_zero, int64_t BH, int64_t group,
                                       int64_t S_cap, int64_t seq_len, float sm_scale,
-                                      bool v_hadamard, uint16_t* out, float* workspace,
+                                      bool v_hadamard, uint16_t* out, uint8_t* qcodes,
+                                      uint16_t* qscale, int16_t* qzero, float* workspace,
                                       hipStream_t stream) {
   const float cnorm = (float)(1.0 / __builtin_sqrt((double)DH));
+  auto combine = [&](int nchunk) {
+    if (qcodes)
+      hipLaunchKernelGGL(kv_attention_combine_kernel<true>, dim3((unsigned)BH), dim3(DH), 0, stream,
+                         workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out, qcodes, qscale, qzero);
+    else
+      hipLaunchKernelGGL(kv_attention_combine_kernel<false>, dim3((unsigned)BH), dim3(DH), 0,
+                         stream, workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out, nullptr,
+                         nullptr, nullptr);
+  };
   if (group == 2 || group == 4) {
     const int nchunk = (int)((seq_len + CHG - 1) / CHG);
     const int64_t units = BH / group * nchunk;  // (key/value head, chunk) pairs
@@ -736,8 +775,7 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
     if (group == 2) OFFQ_GQA(2);
     else OFFQ_GQA(4);
 #undef OFFQ_GQA
-    hipLaunchKernelGGL(kv_attention_combine_kernel, dim3((unsigned)BH), dim3(DH), 0, stream,
-                       workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out);
+    combine(nchunk);
   } else {
     const int nchunk = (int)((seq_len + CH - 1) / CH);
     const int64_t units = BH / group * nchunk;  // (key/value head, chunk) pairs
@@ -745,8 +783,7 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
     hipLaunchKernelGGL(kv_attention_chunk_kernel, dim3((unsigned)grid), dim3(THREADS), 0, stream,
                        q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, S_cap, (int)seq_len,
                        nchunk, (int)units, (int)group, sm_scale * LOG2E, cnorm, workspace);
-    hipLaunchKernelGGL(kv_attention_combine_kernel, dim3((unsigned)BH), dim3(DH), 0, stream,
-                       workspace, nchunk, v_hadamard ? 1 : 0, cnorm, out);
+    combine(nchunk);
   }
   return hipGetLastError();
 }

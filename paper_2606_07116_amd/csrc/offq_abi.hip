@@ -187,13 +187,13 @@ int64_t offq_kv_attention_workspace_bytes(int64_t B, int64_t H, int64_t seq_len)
   return offq::kv_attention_workspace_floats(B * H, seq_len) * (int64_t)sizeof(float);
 }
 
-int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
-                                 const uint16_t* k_scale, const int16_t* k_zero,
-                                 const uint8_t* v_codes, const uint16_t* v_scale,
-                                 const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv,
-                                 int64_t s_cap, int64_t seq_len, int32_t head_dim, float sm_scale,
-                                 int32_t v_hadamard, uint16_t* out, void* workspace,
-                                 int64_t workspace_bytes, void* stream) {
+namespace {
+int kv_attention_checked(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,
+                         const int16_t* k_zero, const uint8_t* v_codes, const uint16_t* v_scale,
+                         const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv, int64_t s_cap,
+                         int64_t seq_len, int32_t head_dim, float sm_scale, int32_t v_hadamard,
+                         uint16_t* out, uint8_t* qcodes, uint16_t* qscale, int16_t* qzero,
+                         void* workspace, int64_t workspace_bytes, void* stream) {
   if (B <= 0 || Hq <= 0 || Hkv <= 0) return fail(OFFQ_ERR_INVALID, "need B, Hq, Hkv > 0");
   if (Hq % Hkv) return fail(OFFQ_ERR_INVALID, "Hq = %lld is not a multiple of Hkv = %lld",
                             (long long)Hq, (long long)Hkv);
@@ -205,12 +205,12 @@ int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
     return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large (B Hq ceil(seq_len / 512) <= 2^24)");
   if (v_hadamard != 0 && v_hadamard != 1) return fail(OFFQ_ERR_INVALID, "v_hadamard must be 0 or 1");
   if (!(sm_scale == sm_scale)) return fail(OFFQ_ERR_INVALID, "sm_scale is NaN");
-  if (!q || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale || !v_zero || !out ||
-      !workspace)
+  if (!q || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale || !v_zero || !workspace ||
+      (!out && !qcodes) || (qcodes && (!qscale || !qzero)))
     return fail(OFFQ_ERR_INVALID, "null pointer argument");
   if (!aligned(q, 2) || !aligned(k_codes, 16) || !aligned(v_codes, 16) || !aligned(k_scale, 2) ||
       !aligned(k_zero, 2) || !aligned(v_scale, 2) || !aligned(v_zero, 2) || !aligned(out, 2) ||
-      !aligned(workspace, 4))
+      !aligned(qscale, 2) || !aligned(qzero, 2) || !aligned(workspace, 4))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (codes: 16 B; workspace: 4 B)");
   const int64_t need = offq_kv_attention_workspace_bytes(B, Hq, seq_len);
   if (workspace_bytes < need)
@@ -219,10 +219,38 @@ int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
   if (int st = check_device()) return st;
   return launched(offq::launch_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale,
                                                    v_zero, B * Hq, Hq / Hkv, s_cap, seq_len,
-                                                   sm_scale, v_hadamard != 0, out,
-                                                   static_cast<float*>(workspace),
+                                                   sm_scale, v_hadamard != 0, out, qcodes,
+                                                   qscale, qzero, static_cast<float*>(workspace),
                                                    (hipStream_t)stream),
                   "kv_attention_decode");
+}
+}  // namespace
+
+int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
+                                 const uint16_t* k_scale, const int16_t* k_zero,
+                                 const uint8_t* v_codes, const uint16_t* v_scale,
+                                 const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv,
+                                 int64_t s_cap, int64_t seq_len, int32_t head_dim, float sm_scale,
+                                 int32_t v_hadamard, uint16_t* out, void* workspace,
+                                 int64_t workspace_bytes, void* stream) {
+  if (!out) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  return kv_attention_checked(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B, Hq, Hkv,
+                              s_cap, seq_len, head_dim, sm_scale, v_hadamard, out, nullptr, nullptr,
+                              nullptr, workspace, workspace_bytes, stream);
+}
+
+int offq_kv_attention_decode_quantize(const uint16_t* q, const uint8_t* k_codes,
+                                      const uint16_t* k_scale, const int16_t* k_zero,
+                                      const uint8_t* v_codes, const uint16_t* v_scale,
+                                      const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv,
+                                      int64_t s_cap, int64_t seq_len, int32_t head_dim,
+                                      float sm_scale, int32_t v_hadamard, uint16_t* out,
+                                      uint8_t* out_codes, uint16_t* out_scale, int16_t* out_zero,
+                                      void* workspace, int64_t workspace_bytes, void* stream) {
+  if (!out_codes) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  return kv_attention_checked(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B, Hq, Hkv,
+                              s_cap, seq_len, head_dim, sm_scale, v_hadamard, out, out_codes,
+                              out_scale, out_zero, workspace, workspace_bytes, stream);
 }
 
 int offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,

@@ -136,6 +136,27 @@ def test_kv_attention_misaligned_and_null():
         assert _lib.offq_kv_attention_decode_raw(*a) == _lib.OFFQ_ERR_INVALID, i
 
 
+def test_kv_attention_quantize_validation():
+    # q, 6 cache arrays, B, Hq, Hkv, s_cap, seq_len, head_dim, sm_scale, v_had,
+    # out, out_codes, out_scale, out_zero, workspace, workspace_bytes, stream
+    names = ["q", "kc", "ks", "kz", "vc", "vs", "vz", "B", "Hq", "Hkv", "s_cap", "seq_len",
+             "head_dim", "sm", "v_had", "out", "codes", "scale", "zero", "ws", "wsb", "stream"]
+    base = dict(zip(names, [P] * 7 + [2, 8, 2, 100, 100, 128, 0.1, 0, None, P, P, P, P, 1 << 20,
+                                      None]))
+    f = _lib.offq_kv_attention_decode_quantize_raw
+    for k, bad in (("codes", None), ("scale", None), ("zero", None), ("scale", P + 1),
+                   ("zero", P + 1), ("q", None), ("seq_len", 101), ("Hkv", 3), ("v_had", 2)):
+        a = dict(base)
+        a[k] = bad
+        assert f(*[a[n] for n in names]) == _lib.OFFQ_ERR_INVALID, k
+    a = dict(base)
+    a["head_dim"] = 64
+    assert f(*[a[n] for n in names]) == _lib.OFFQ_ERR_UNSUPPORTED
+    # the plain entry point still requires its output
+    assert _lib.offq_kv_attention_decode_gqa_raw(P, P, P, P, P, P, P, 2, 8, 2, 100, 100, 128, 0.1, 0,
+                                                 None, P, 1 << 20, None) == _lib.OFFQ_ERR_INVALID
+
+
 def test_kv_attention_workspace_bytes():
     # one record of 2 + 128 floats per (b, h, chunk of up to 512 positions)
     assert _lib.offq_kv_attention_workspace_bytes(2, 4, 1) == 8 * 130 * 4

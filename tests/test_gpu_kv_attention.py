@@ -136,6 +136,38 @@ def test_attention_quantized_cache_chain():
     check(P.host(out.float()), ref, _magnitude(q, kc, ks, kz, vc, vs, vz, seq_len, SM))
 
 
+@pytest.mark.parametrize("B,Hq,Hkv,S,seq_len,v_had,with_out",
+                         [(2, 4, 4, 700, 700, 0, True), (3, 8, 2, 1100, 1025, 1, False),
+                          (2, 16, 4, 2100, 1, 0, True), (1, 6, 2, 600, 513, 0, False),
+                          (2, 4, 2, 900, 777, 1, True)])
+def test_attention_quantized_output(B, Hq, Hkv, S, seq_len, v_had, with_out):
+    """offq_kv_attention_decode_quantize: the bf16 output equals the plain
+    call's, and its codes, scales and zero-points equal both the quantizer
+    entry point's on that output (g = 128, no rotation) and the oracle
+    quantizer's fed the same bf16 values (sec. 3.3 step 2(1): the O-projection
+    input is quantized without an online rotation)."""
+    from oracle import quantizer as OQ
+    kc, ks, kz = inputs.kv4_cache_device(B, Hkv, S, 128, seed=S, device=P.DEV)
+    vc, vs, vz = inputs.kv4_cache_device(B, Hkv, S, 128, seed=S + 1, device=P.DEV)
+    q = P.to_dev_bf16(inputs.queries(B, Hq, 128, seed=S))
+    args = (q, kc, ks, kz, vc, vs, vz, seq_len)
+    ref = offq.offq_kv_attention_decode(*args, v_hadamard=v_had)
+    out = torch.full_like(ref, float("nan")) if with_out else None
+    codes, scale, zero, o2 = offq.offq_kv_attention_decode_quantize(*args, v_hadamard=v_had, out=out)
+    c2, s2, z2, _ = offq.offq_rotate_quantize(ref.view(B, Hq * 128), 128, apply_hadamard=False)
+    torch.cuda.synchronize()
+    if with_out:
+        assert torch.equal(o2.view(torch.int16), ref.view(torch.int16))
+    else:
+        assert o2 is None
+    assert torch.equal(codes, c2) and torch.equal(scale.view(torch.int16), s2.view(torch.int16))
+    assert torch.equal(zero, z2)
+    yq, ys, yz = OQ.quantize_groups(P.host(ref.float()).reshape(B, Hq * 128), 128)
+    assert np.array_equal(P.host(codes), OQ.pack_nibbles(yq))
+    assert np.array_equal(P.host(scale).view(np.uint16), ys.view(np.uint16))
+    assert np.array_equal(P.host(zero), yz)
+
+
 @pytest.mark.parametrize("seq_len", [32768, 30001])
 def test_attention_full_size_sampled(seq_len):
     """[8, 32, 32768, 128] cache (the decode-attention workload, one launch as
