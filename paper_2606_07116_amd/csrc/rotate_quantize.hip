@@ -452,6 +452,157 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
   }
 }
 
+// g = 2048 NW (4096 or 8192) with one group per row, NW waves per row: wave
+// w holds the row's elements [2048 w, 2048 w + 2048) in the E = 32 layouts
+// of Geom<8>.  The butterflies on index bits 0-2, 9, 10 run in layout A's
+// registers and on bits 3-7 in layout B's; bit 8 is lane bit 3 in layout B
+// (a DPP exchange with the lane 8 away, rotating each 16-lane row by 8); bits
+// 11 and up are the wave (one exchange through LDS each).  The row's max and
+// min meet in LDS; every wave then quantizes its part with the row's
+// parameters.  The normalisation is folded into the reciprocal scale when it
+// is a power of two (g = 4096) and applied in the last exchange otherwise.
+// Rows then run on NW waves each: more waves in flight for a few thousand
+// rows, and a shorter chain per wave for a decode step's few rows.
+template <int NW, bool HAD, bool DBG>
+__global__ __launch_bounds__(64 * NW) void rotate_quantize_rows_kernel(
+    const uint16_t* __restrict__ x, int64_t ldx, uint8_t* __restrict__ codes, int64_t ldc,
+    uint16_t* __restrict__ scale, int16_t* __restrict__ zero, float* __restrict__ ydbg,
+    int64_t ldy, float cnorm) {
+  using Gm = Geom<8>;
+  constexpr int E = Gm::E, NCH = Gm::NCH;
+  static_assert(E == 32 && NCH == 4 && Gm::T == 2048, "2048-element tiles");
+  constexpr int LOGW = NW == 2 ? 1 : 2;
+  static_assert(NW == (1 << LOGW), "two or four waves");
+  constexpr bool FOLD = (11 + LOGW) % 2 == 0;  // 1 / sqrt(g) a power of two
+  __shared__ __attribute__((aligned(16))) float lds[NW * Gm::WORDS];
+  __shared__ float s_st[NW][2];
+  const int tid = (int)__builtin_amdgcn_workitem_id_x();
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t row = (int64_t)__builtin_amdgcn_workgroup_id_x();
+  const uint16_t* const xr = x + row * ldx + 2048 * w;
+  float* const la = lds + w * Gm::WORDS + Gm::a_base(lane);
+  float* const lb = lds + w * Gm::WORDS + Gm::b_base(lane);
+
+  float v[E];
+#pragma unroll
+  for (int ch = 0; ch < NCH; ++ch) {
+    const uint4 d = *reinterpret_cast<const uint4*>(xr + 512 * ch + 8 * lane);
+    const uint32_t wd[4] = {d.x, d.y, d.z, d.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if constexpr (HAD) {
+        v[ch * 8 + 2 * j] = dot2_bf16(wd[j], 0x3f803f80u);      // (1, 1)
+        v[ch * 8 + 2 * j + 1] = dot2_bf16(wd[j], 0xbf803f80u);  // (1, -1)
+      } else {
+        v[ch * 8 + 2 * j] = bf16_lo(wd[j]);
+        v[ch * 8 + 2 * j + 1] = bf16_hi(wd[j]);
+      }
+    }
+  }
+  if constexpr (HAD) stages_A<5, 11>(v);  // index bits 1, 2, 9, 10
+
+  // ---- A -> B ---------------------------------------------------------------
+#pragma unroll
+  for (int ch = 0; ch < NCH; ++ch) {
+    *reinterpret_cast<float4*>(la + Gm::a_off(ch)) =
+        make_float4(v[ch * 8 + 0], v[ch * 8 + 1], v[ch * 8 + 2], v[ch * 8 + 3]);
+    *reinterpret_cast<float4*>(la + Gm::a_off(ch) + 4) =
+        make_float4(v[ch * 8 + 4], v[ch * 8 + 5], v[ch * 8 + 6], v[ch * 8 + 7]);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < E; ++r) v[r] = lb[Gm::b_off(r)];
+  if constexpr (HAD) {
+    stages_B<5, 8, false>(v, 1.0f);  // index bits 3..7
+    // bit 8: lanes l and l ^ 8; the lower one keeps a + b, the upper one a - b
+    const float sg = (lane & 8) ? -1.0f : 1.0f;
+#pragma unroll
+    for (int r = 0; r < E; ++r) v[r] = __builtin_fmaf(v[r], sg, dpp<0x128>(v[r]));  // row_ror:8
+    // bits 11..: the waves w and w ^ 2^b, through LDS
+#pragma unroll
+    for (int b = 0; b < LOGW; ++b) {
+      __syncthreads();  // every wave is done reading the regions it read last
+#pragma unroll
+      for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = v[r];
+      __syncthreads();
+      const float* const lp = lds + (w ^ (1 << b)) * Gm::WORDS + Gm::b_base(lane);
+      const bool upper = (w >> b) & 1;
+      if (FOLD || b < LOGW - 1) {
+        const float sw = upper ? -1.0f : 1.0f;
+#pragma unroll
+        for (int r = 0; r < E; ++r) v[r] = __builtin_fmaf(v[r], sw, lp[Gm::b_off(r)]);
+      } else {  // the last stage carries 1 / sqrt(g): a c + b c, a c - b c
+        const float sc = upper ? -cnorm : cnorm;
+#pragma unroll
+        for (int r = 0; r < E; ++r) v[r] = __builtin_fmaf(v[r], sc, lp[Gm::b_off(r)] * cnorm);
+      }
+    }
+  }
+  // v now holds y (y / 2^-6 when folded), or x without the rotation, in layout B
+
+  // ---- the row's max and min --------------------------------------------------
+  float mx = v[0], mn = v[0];
+#pragma unroll
+  for (int r = 1; r < E; ++r) {
+    mx = fmaxf(mx, v[r]);
+    mn = fminf(mn, v[r]);
+  }
+  lane_reduce<6>(mx, mn);
+  if (lane == 0) {
+    s_st[w][0] = mx;
+    s_st[w][1] = mn;
+  }
+  __syncthreads();  // (also: every wave is done reading the others' parts)
+  mx = s_st[0][0];
+  mn = s_st[0][1];
+#pragma unroll
+  for (int u = 1; u < NW; ++u) {
+    mx = fmaxf(mx, s_st[u][0]);
+    mn = fminf(mn, s_st[u][1]);
+  }
+  constexpr bool FOLDED = HAD && FOLD;
+  QParams P = FOLDED ? quant_params(mx * cnorm, mn * cnorm) : quant_params(mx, mn);
+  if constexpr (FOLDED) P.r *= cnorm;  // exact: cnorm is a power of two
+  if (w == 0 && lane == 0) {
+    scale[row] = P.s16;
+    zero[row] = P.z;
+  }
+
+  if constexpr (DBG) {
+    // y to global through LDS, in layout A (16-byte stores)
+#pragma unroll
+    for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = FOLDED ? v[r] * cnorm : v[r];
+    __syncthreads();
+    float* const yr = ydbg + row * ldy + 2048 * w;
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      *reinterpret_cast<float4*>(yr + 512 * ch + 8 * lane) =
+          *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
+      *reinterpret_cast<float4*>(yr + 512 * ch + 8 * lane + 4) =
+          *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
+    }
+    __syncthreads();
+  }
+
+  // ---- codes as float bits, back to layout A, 8 per dword --------------------
+#pragma unroll
+  for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = __uint_as_float(quant_bits(v[r], P));
+  __syncthreads();
+  const uint32_t corr = __float_as_uint(P.lo) * 0x11111111u;
+  uint8_t* const cr = codes + row * ldc + 1024 * w;
+#pragma unroll
+  for (int ch = 0; ch < NCH; ++ch) {
+    const float4 a = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
+    const float4 b = *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
+    const float u[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    uint32_t wd = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) wd += __float_as_uint(u[j]) << (4 * j);
+    *reinterpret_cast<uint32_t*>(cr + 256 * ch + 4 * lane) = wd - corr;
+  }
+}
+
 template <int LOGG>
 hipError_t launch_t(const uint16_t* x, int64_t n_groups, int G, int64_t ldx, bool had,
                     uint8_t* codes, int64_t ldc, uint16_t* scale, int16_t* zero, float* ydbg,
@@ -474,6 +625,22 @@ hipError_t launch_t(const uint16_t* x, int64_t n_groups, int G, int64_t ldx, boo
   const bool g1 = G == 1 && (LOGG >= 9 || (GPT * ldx < (int64_t(1) << 31) &&
                                            GPT * ldc < (int64_t(1) << 31) &&
                                            ldx < (int64_t(1) << 24) && ldc < (int64_t(1) << 24)));
+  if constexpr (LOGG == 12 || LOGG == 13) {
+    // one group per row: a row on 2 (g = 4096) or 4 (g = 8192) waves
+    if (G == 1) {
+      constexpr int NW = 1 << (LOGG - 11);
+#define OFFQ_RQW(HD, DB)                                                                \
+  hipLaunchKernelGGL((rotate_quantize_rows_kernel<NW, HD, DB>), dim3((unsigned)n_groups), \
+                     dim3(64 * NW), 0, stream, x, ldx, codes, ldc, scale, zero, ydbg, ldy, cnorm)
+      if (had) {
+        if (ydbg) OFFQ_RQW(true, true); else OFFQ_RQW(true, false);
+      } else {
+        if (ydbg) OFFQ_RQW(false, true); else OFFQ_RQW(false, false);
+      }
+#undef OFFQ_RQW
+      return hipGetLastError();
+    }
+  }
 #define OFFQ_RQ_G(HD, DB) \
   if (g1) OFFQ_RQ(HD, DB, true); else OFFQ_RQ(HD, DB, false);
   if (had) {
