@@ -38,6 +38,23 @@ def test_strided_rows():
     P.check_quant(P.host(y), P.host(codes), P.host(scale), P.host(zero), g)
 
 
+@pytest.mark.parametrize("M,K,g,pad,had", [(3, 4096, 4096, 128, True), (5, 8192, 8192, 64, True),
+                                            (1, 8192, 8192, 8, False), (2, 4096, 4096, 8, False)])
+def test_strided_rows_whole_row_groups(M, K, g, pad, had):
+    """One group per row of 4096 or 8192 channels (rows split over 2 or 4
+    waves) with a row stride above K."""
+    big = inputs.activations(M, K + pad, seed=K + pad, n_outliers=2, lo=40, hi=120)
+    xd = P.to_dev_bf16(big)[:, :K]
+    assert xd.stride(0) == K + pad
+    codes, scale, zero, y = offq.offq_rotate_quantize(xd, g, apply_hadamard=had, debug=True)
+    codes2, scale2, zero2, _ = offq.offq_rotate_quantize(xd, g, apply_hadamard=had)
+    torch.cuda.synchronize()
+    x = big[:, :K]
+    P.check_rotation(x, P.host(y), g, had)
+    P.check_quant(P.host(y), P.host(codes), P.host(scale), P.host(zero), g)
+    assert torch.equal(codes, codes2) and torch.equal(scale, scale2) and torch.equal(zero, zero2)
+
+
 def test_offset_channel_absorbed():
     """A pure first-channel outlier per group becomes a constant group (Eq. 5):
     the quantizer takes the degenerate branch, codes 0, and s (0 - z) ~ a/sqrt(g)."""
