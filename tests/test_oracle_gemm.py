@@ -1,4 +1,7 @@
 """Pins of the oracle integer GEMM and epilogue (algebra of Eq. 1)."""
+import os
+from fractions import Fraction
+
 import numpy as np
 import pytest
 
@@ -82,3 +85,91 @@ def test_bf16_helpers():
     assert Gm.bf16_round(np.array([1.0 + 2 ** -9]))[0] == 1.0        # tie -> even
     assert Gm.bf16_round(np.array([1.0 + 3 * 2 ** -9]))[0] == 1.0 + 2 ** -7
     assert Gm.bf16_ulp(np.array([1.0]))[0] == 2 ** -7
+
+
+def _golden_epilogue(golden_dir):
+    rows = [ln.split() for ln in open(os.path.join(golden_dir, "epilogue_cancellation.txt"))
+            if ln.strip() and not ln.startswith("#")]
+    q_a = np.array([rows[0]], dtype=np.int64)
+    q_w = np.array([rows[1]], dtype=np.int64)
+    s = np.array([rows[2]], dtype=np.float16)
+    z = np.array([rows[3]], dtype=np.int64)
+    sw = np.array(rows[4], dtype=np.float16)
+    acc0, acc1, cs0, cs1 = (int(v) for v in rows[5])
+    y, e = (float(v) for v in rows[6])
+    return q_a, q_w, s, z, sw, (acc0, acc1), (cs0, cs1), y, e
+
+
+def test_epilogue_hand_worked_cancellation(golden_dir):
+    """Eq. 1's epilogue on a hand-worked case whose two group terms nearly
+    cancel: the output and its magnitude E (the sum of the absolute terms,
+    which sets the cancellation floor of the output tolerance) both equal the
+    values worked out by hand, so an E that is too large or too small fails."""
+    q_a, q_w, s, z, sw, acc_h, cs_h, y_h, e_h = _golden_epilogue(golden_dir)
+    acc = Gm.int_gemm_bruteforce(q_a, q_w, 2)
+    assert acc[:, 0, 0].tolist() == list(acc_h)
+    cs = Q.colsum(q_w.astype(np.int8), 2)
+    assert cs[:, 0].tolist() == list(cs_h)
+    assert Gm.epilogue(acc, s, z, sw, cs)[0, 0] == y_h
+    assert Gm.epilogue_magnitude(acc, s, z, sw, cs)[0, 0] == e_h
+    assert Gm.dequant_matmul(q_a, s, z, q_w, sw, 2)[0, 0] == y_h
+
+
+@pytest.mark.parametrize("G,seed", [(1, 0), (3, 1), (8, 2), (28, 3)])
+def test_epilogue_and_magnitude_match_exact_rationals(G, seed):
+    """Y and E against their definitions evaluated in exact rational
+    arithmetic (fp16 scales are dyadic rationals; codes, zero-points and
+    column sums are integers).  The fp64 oracle may differ only by its own
+    rounding: at most (G + 2) * 2^-53 * E for both."""
+    g = 4
+    M, N = 3, 4
+    rng = np.random.default_rng(seed)
+    q_a = rng.integers(0, 16, size=(M, G * g))
+    q_w = rng.integers(-8, 8, size=(N, G * g))
+    s = rng.uniform(0.01, 3.0, size=(M, G)).astype(np.float16)
+    z = rng.integers(-32768, 32768, size=(M, G))
+    sw = rng.uniform(-0.02, 0.02, size=N).astype(np.float16)
+    acc = Gm.int_gemm_bruteforce(q_a, q_w, g)
+    cs = Q.colsum(q_w.astype(np.int8), g)
+    y = Gm.epilogue(acc, s, z, sw, cs)
+    e = Gm.epilogue_magnitude(acc, s, z, sw, cs)
+    for m in range(M):
+        for n in range(N):
+            terms = []
+            for b in range(G):
+                a_b = sum(int(q_a[m, k]) * int(q_w[n, k]) for k in range(b * g, (b + 1) * g))
+                c_b = sum(int(q_w[n, k]) for k in range(b * g, (b + 1) * g))
+                terms.append(Fraction(float(s[m, b])) * (a_b - int(z[m, b]) * c_b))
+            swf = Fraction(float(sw[n]))
+            y_ex = swf * sum(terms)
+            e_ex = abs(swf) * sum(abs(t) for t in terms)
+            tol = (G + 2) * 2.0 ** -53 * float(e_ex)
+            assert abs(Fraction(float(y[m, n])) - y_ex) <= tol
+            assert abs(Fraction(float(e[m, n])) - e_ex) <= tol
+            assert e[m, n] >= abs(y[m, n]) * (1 - 1e-15)
+
+
+def test_bf16_ulp_binades():
+    """ulp of bfloat16 (8 significant bits, fp32's exponent range) at chosen
+    values: powers of two take the spacing above them, subnormals 2^-133."""
+    cases = {1.0: 2 ** -7, 1.9921875: 2 ** -7, 2.0: 2 ** -6, 3.0: 2 ** -6, 0.75: 2 ** -8,
+             -3.0: 2 ** -6, 65504.0: 2.0 ** 8, 1e30: 2.0 ** 92, 2.0 ** -126: 2.0 ** -133,
+             2.0 ** -127: 2.0 ** -133, 2.0 ** -133: 2.0 ** -133, 0.0: 2.0 ** -133,
+             3.0e38: 2.0 ** 120}
+    got = Gm.bf16_ulp(np.array(list(cases)))
+    assert got.tolist() == list(cases.values())
+
+
+def test_bf16_ulp_equals_bit_increment():
+    """ulp of bf16 at x = the gap between the bf16 value below |x| (|x|'s fp32
+    bit pattern truncated to 16 bits) and the next bf16 pattern, over random
+    normal and subnormal inputs."""
+    rng = np.random.default_rng(7)
+    hi = rng.integers(0, 0x7F7F, size=20000).astype(np.uint32)      # finite, next also finite
+    lo = rng.integers(0, 1 << 16, size=hi.size).astype(np.uint32)
+    x = ((hi << 16) | lo).view(np.float32)
+    x = np.where(rng.random(hi.size) < 0.5, -x, x)
+    b = (np.abs(x).view(np.uint32) >> 16).astype(np.uint32)
+    below = (b << 16).view(np.float32).astype(np.float64)
+    above = ((b + 1) << 16).view(np.float32).astype(np.float64)
+    assert np.array_equal(Gm.bf16_ulp(x.astype(np.float64)), above - below)
