@@ -64,7 +64,7 @@ typedef enum {
 int offq_abi_version(void);
 
 /* Static, human-readable name of a status code. */
-const char* offq_status_string(int status);
+const char* offq_status_string(offq_status_t status);
 
 /* Message describing the last failing call made by the calling thread
  * (empty string if none).  Valid until the next call on that thread. */
@@ -94,7 +94,7 @@ const char* offq_last_error(void);
  *   y_debug  nullable fp32 [M, K] contiguous, 16-byte aligned: if non-NULL,
  *            receives exactly the fp32 values that were quantized.
  */
-int offq_rotate_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
+offq_status_t offq_rotate_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
                          int32_t g, int32_t apply_hadamard,
                          uint8_t* codes, uint16_t* scale, int16_t* zero,
                          float* y_debug, void* stream);
@@ -122,7 +122,7 @@ int offq_rotate_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
  *   acc_debug nullable int32 [K/g, M, N] contiguous: if non-NULL, receives
  *            every per-group integer accumulator acc_b.
  */
-int offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale,
+offq_status_t offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale,
                    const int16_t* a_zero, const uint8_t* w_codes,
                    const uint16_t* w_scale, const int32_t* w_colsum,
                    int64_t M, int64_t N, int64_t K, int32_t g,
@@ -141,7 +141,7 @@ int offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale,
  *   codes     uint8 [rows, head_dim/2]; scale fp16 [rows]; zero int16 [rows].
  *   y_debug   nullable fp32 [rows, head_dim].
  */
-int offq_kv_quantize(const uint16_t* kv, int64_t rows, int32_t head_dim,
+offq_status_t offq_kv_quantize(const uint16_t* kv, int64_t rows, int32_t head_dim,
                      int64_t row_stride, int32_t apply_hadamard,
                      uint8_t* codes, uint16_t* scale, int16_t* zero,
                      float* y_debug, void* stream);
@@ -159,7 +159,7 @@ int offq_kv_quantize(const uint16_t* kv, int64_t rows, int32_t head_dim,
  *   g        group size the activations will use (power of two, 64..8192, K % g == 0).
  *   w_codes  uint8 [N, K/2]; w_scale fp16 [N]; w_colsum int32 [K/g, N].
  */
-int offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g,
+offq_status_t offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g,
                       uint8_t* w_codes, uint16_t* w_scale, int32_t* w_colsum,
                       void* stream);
 
@@ -192,7 +192,7 @@ int offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g,
  *                a workspace must be ordered on one stream.
  * head_dim is 128; other sizes return OFFQ_ERR_UNSUPPORTED.
  */
-int offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,
+offq_status_t offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,
                              const int16_t* k_zero, const uint8_t* v_codes,
                              const uint16_t* v_scale, const int16_t* v_zero, int64_t B,
                              int64_t H, int64_t s_cap, int64_t seq_len, int32_t head_dim,
@@ -214,7 +214,7 @@ int64_t offq_kv_attention_workspace_bytes(int64_t B, int64_t H, int64_t seq_len)
  * of Hkv (OFFQ_ERR_INVALID otherwise).  offq_kv_attention_decode is this call
  * with Hkv = Hq.
  */
-int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
+offq_status_t offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
                                  const uint16_t* k_scale, const int16_t* k_zero,
                                  const uint8_t* v_codes, const uint16_t* v_scale,
                                  const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv,
@@ -235,7 +235,7 @@ int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
  * out_scale and out_zero may not.  Other arguments, the workspace and the
  * errors as for offq_kv_attention_decode_gqa.
  */
-int offq_kv_attention_decode_quantize(const uint16_t* q, const uint8_t* k_codes,
+offq_status_t offq_kv_attention_decode_quantize(const uint16_t* q, const uint8_t* k_codes,
                                       const uint16_t* k_scale, const int16_t* k_zero,
                                       const uint8_t* v_codes, const uint16_t* v_scale,
                                       const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv,
@@ -260,7 +260,7 @@ int offq_kv_attention_decode_quantize(const uint16_t* q, const uint8_t* k_codes,
  *   y_out [M, D] (ldy) or NULL (at least one output).  D a multiple of 8,
  *   strides multiples of 8, pointers 16-byte aligned.  M = 0 is a no-op.
  */
-int offq_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr, int64_t M,
+offq_status_t offq_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr, int64_t M,
                      int64_t D, float eps, uint16_t* h_out, int64_t ldh, uint16_t* y_out,
                      int64_t ldy, void* stream);
 
@@ -272,7 +272,7 @@ int offq_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_
  *   gu [M, 2F] (ldg >= 2F), out [M, F] (ldo >= F); F, ldg, ldo multiples of
  *   8; pointers 16-byte aligned.
  */
-int offq_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t* out, int64_t ldo,
+offq_status_t offq_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t* out, int64_t ldo,
                 void* stream);
 
 /*
@@ -285,7 +285,7 @@ int offq_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t*
  * D / 256 in {8, 16, 32, 64} (D = 2048 ... 16384); g a power of two with
  * D/256 <= g <= D/4 dividing D.
  */
-int offq_add_rmsnorm_quantize(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr,
+offq_status_t offq_add_rmsnorm_quantize(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr,
                               int64_t M, int64_t D, float eps, int32_t g, uint16_t* h_out,
                               int64_t ldh, uint8_t* codes, uint16_t* scale, int16_t* zero,
                               uint16_t* y_debug, int64_t ldy, void* stream);
@@ -298,7 +298,7 @@ int offq_add_rmsnorm_quantize(const uint16_t* x, int64_t ldx, const uint16_t* re
  * and zero int16 [M, F/128]; y_debug fp32 [M, F] or NULL: the rotated rows
  * that were quantized.  F a multiple of 128; ldg >= 2F, a multiple of 8.
  */
-int offq_swiglu_rotate_quantize(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F,
+offq_status_t offq_swiglu_rotate_quantize(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F,
                                 uint8_t* codes, uint16_t* scale, int16_t* zero, float* y_debug,
                                 void* stream);
 
@@ -323,7 +323,7 @@ int offq_swiglu_rotate_quantize(const uint16_t* gu, int64_t ldg, int64_t M, int6
  *     quantized.
  * head_dim must be 128.
  */
-int offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq, int64_t Hkv,
+offq_status_t offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq, int64_t Hkv,
                         int32_t head_dim, const int32_t* positions, double rope_base,
                         int32_t k_hadamard, int32_t v_hadamard, uint16_t* q_out,
                         uint8_t* k_codes, uint16_t* k_scale, int16_t* k_zero, uint8_t* v_codes,
@@ -349,20 +349,20 @@ int64_t offq_top1_workspace_bytes(int64_t n_seq, int64_t seq_len);
  *   idx int32 [n_seq] (the selected token), X fp32 [n_seq, D] (row stride ldX).
  * Inputs must be finite.
  */
-int offq_top1_select(const uint16_t* x, int64_t n_seq, int64_t seq_len, int64_t D, int64_t ld_tok,
+offq_status_t offq_top1_select(const uint16_t* x, int64_t n_seq, int64_t seq_len, int64_t D, int64_t ld_tok,
                      int64_t ld_seq, int32_t* idx, float* X, int64_t ldX, void* workspace,
                      int64_t workspace_bytes, void* stream);
 
 /* offq_channel_absmax -- out fp64 [D] = max over rows of |x[r, c]| (bf16 x
  * [rows, D], row stride ldx): the statistic that picks the outlier channels of
  * the down-projection input (sec. 3.3 step 2(4)). */
-int offq_channel_absmax(const uint16_t* x, int64_t rows, int64_t D, int64_t ldx, double* out,
+offq_status_t offq_channel_absmax(const uint16_t* x, int64_t rows, int64_t D, int64_t ldx, double* out,
                         void* stream);
 
 /* offq_gram -- C fp64 [D, D] (row stride ldC) = X^T X / N for X fp32 [N, D]
  * (row stride ldX), accumulated in fp64 (Eq. 2; zero-mean assumed, as there).
  * C is exactly symmetric. */
-int offq_gram(const float* X, int64_t N, int64_t D, int64_t ldX, double* C, int64_t ldC,
+offq_status_t offq_gram(const float* X, int64_t N, int64_t D, int64_t ldX, double* C, int64_t ldC,
               void* stream);
 
 /* Bytes of workspace offq_eigh needs (about 32 D^2). */
@@ -377,7 +377,7 @@ int64_t offq_eigh_workspace_bytes(int64_t D);
  * *sweeps and *rel_off (nullable) report what was reached.  workspace: at least
  * offq_eigh_workspace_bytes(D), 16-byte aligned.
  */
-int offq_eigh(const double* C, int64_t D, int64_t ldC, double* evals, double* U, int64_t ldU,
+offq_status_t offq_eigh(const double* C, int64_t D, int64_t ldC, double* evals, double* U, int64_t ldU,
               void* workspace, int64_t workspace_bytes, int32_t max_sweeps, double tol,
               int32_t* sweeps, double* rel_off, void* stream);
 
@@ -389,7 +389,7 @@ int offq_eigh(const double* C, int64_t D, int64_t ldC, double* evals, double* U,
  * (ties by channel index).  perm int32 [D]: new slot -> original channel.
  * workspace: D int32.
  */
-int offq_group_permutation(const double* key, int64_t D, int32_t g, int32_t* perm,
+offq_status_t offq_group_permutation(const double* key, int64_t D, int32_t g, int32_t* perm,
                            void* workspace, int64_t workspace_bytes, void* stream);
 
 /*
@@ -399,18 +399,18 @@ int offq_group_permutation(const double* key, int64_t D, int32_t g, int32_t* per
  * consecutive groups of g columns when apply_hadamard (else identity); the
  * product is formed in fp64.  D <= 8192, D a multiple of g (power of two).
  */
-int offq_build_rotation(const double* U, int64_t ldU, int64_t D, const int32_t* perm, int32_t g,
+offq_status_t offq_build_rotation(const double* U, int64_t ldU, int64_t D, const int32_t* perm, int32_t g,
                         int32_t apply_hadamard, float* R, int64_t ldR, void* stream);
 
 /* offq_fuse_weights -- W_out fp32 [N, K] = W R for W fp32 [N, K] and R fp32
  * [K, K] (the rotation a linear layer's input receives, fused into its
  * weights: y = x W^T = (x R)(W R)^T). */
-int offq_fuse_weights(const float* W, int64_t ldW, int64_t N, int64_t K, const float* R,
+offq_status_t offq_fuse_weights(const float* W, int64_t ldW, int64_t N, int64_t K, const float* R,
                       int64_t ldR, float* W_out, int64_t ldo, void* stream);
 
 /* offq_permute_rows -- W_out[s, :] = W[perm[s], :] (fp32 [N, K]): an output-
  * channel permutation fused into the producing weights (P4 into up/gate). */
-int offq_permute_rows(const float* W, int64_t ldW, int64_t N, int64_t K, const int32_t* perm,
+offq_status_t offq_permute_rows(const float* W, int64_t ldW, int64_t N, int64_t K, const int32_t* perm,
                       float* W_out, int64_t ldo, void* stream);
 
 #ifdef __cplusplus

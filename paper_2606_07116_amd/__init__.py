@@ -15,33 +15,46 @@ arguments.  Entry points (same names as ``include/offq.h``):
 Offline calibration: offq_top1_select, offq_channel_absmax, offq_gram, offq_eigh,
 offq_group_permutation, offq_build_rotation, offq_fuse_weights, offq_permute_rows.
 
-Importing the package loads the library and raises if it has not been built.
+The library is loaded on first use of an entry point (not by importing the
+package or its seeded input generators), and that first use raises if the
+library has not been built: there is no other path.
 """
 
-from ._lib import (  # noqa: F401
-    ABI_VERSION,
-    EXPORTED,
-    OffqError,
-    last_error,
-    offq_build_rotation,
-    offq_channel_absmax,
-    offq_eigh,
-    offq_fuse_weights,
-    offq_gram,
-    offq_group_permutation,
-    offq_permute_rows,
-    offq_top1_select,
-    offq_add_rmsnorm,
-    offq_add_rmsnorm_quantize,
-    offq_swiglu_rotate_quantize,
-    offq_rope_kv_append,
-    offq_swiglu,
-    offq_kv_attention_decode,
-    offq_kv_attention_decode_quantize,
-    offq_kv_attention_workspace_bytes,
-    offq_kv_quantize,
-    offq_pack_weights,
-    offq_rotate_quantize,
-    offq_w4a4_gemm,
-    status_name,
-)
+_EXPORTS = frozenset((
+    "ABI_VERSION",
+    "EXPORTED",
+    "OffqError",
+    "last_error",
+    "offq_build_rotation",
+    "offq_channel_absmax",
+    "offq_eigh",
+    "offq_fuse_weights",
+    "offq_gram",
+    "offq_group_permutation",
+    "offq_permute_rows",
+    "offq_top1_select",
+    "offq_add_rmsnorm",
+    "offq_add_rmsnorm_quantize",
+    "offq_swiglu_rotate_quantize",
+    "offq_rope_kv_append",
+    "offq_swiglu",
+    "offq_kv_attention_decode",
+    "offq_kv_attention_decode_quantize",
+    "offq_kv_attention_workspace_bytes",
+    "offq_kv_quantize",
+    "offq_pack_weights",
+    "offq_rotate_quantize",
+    "offq_w4a4_gemm",
+    "status_name",
+))
+
+
+def __getattr__(name):
+    if name in _EXPORTS:
+        from . import _lib
+        return getattr(_lib, name)
+    raise AttributeError(f"module {__name__!r} has no attribute {name!r}")
+
+
+def __dir__():
+    return sorted(set(globals()) | _EXPORTS)

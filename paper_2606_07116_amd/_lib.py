@@ -288,6 +288,9 @@ def offq_w4a4_gemm(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, g, debu
     dev = a_codes.device
     y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=dev)
     _need(y, torch.bfloat16, "out", 2)
+    # the kernels write rows 0..M-1, columns 0..N-1 at row stride y.stride(0)
+    if tuple(y.shape) != (M, N) or y.stride(1) != 1 or y.stride(0) < N:
+        raise ValueError(f"out must be a [{M}, {N}] tensor with a contiguous last dimension")
     acc = torch.empty((K // g, M, N), dtype=torch.int32, device=dev) if debug else None
     _check(lib.offq_w4a4_gemm(_ptr(a_codes), _ptr(a_scale), _ptr(a_zero), _ptr(w_codes), _ptr(w_scale),
                               _ptr(w_colsum), M, N, K, int(g), _ptr(y), y.stride(0), _ptr(acc),

@@ -12,7 +12,7 @@ namespace {
 
 thread_local char g_last_error[512] = "";
 
-int fail(int status, const char* fmt, ...) {
+offq_status_t fail(offq_status_t status, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
   vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
@@ -20,7 +20,7 @@ int fail(int status, const char* fmt, ...) {
   return status;
 }
 
-int ok() {
+offq_status_t ok() {
   g_last_error[0] = '\0';
   return OFFQ_OK;
 }
@@ -35,7 +35,7 @@ int ilog2_pow2(int64_t v) {
 }
 
 // The kernels are built for gfx950 only; refuse other devices up front.
-int check_device() {
+offq_status_t check_device() {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(OFFQ_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
@@ -56,7 +56,7 @@ int check_device() {
   return OFFQ_OK;
 }
 
-int launched(hipError_t e, const char* what) {
+offq_status_t launched(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(OFFQ_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
   return ok();
 }
@@ -69,7 +69,7 @@ extern "C" {
 
 int offq_abi_version(void) { return OFFQ_ABI_VERSION; }
 
-const char* offq_status_string(int status) {
+const char* offq_status_string(offq_status_t status) {
   switch (status) {
     case OFFQ_OK: return "OFFQ_OK";
     case OFFQ_ERR_INVALID: return "OFFQ_ERR_INVALID";
@@ -81,7 +81,7 @@ const char* offq_status_string(int status) {
 
 const char* offq_last_error(void) { return g_last_error; }
 
-int offq_rotate_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, int32_t g,
+offq_status_t offq_rotate_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, int32_t g,
                          int32_t apply_hadamard, uint8_t* codes, uint16_t* scale,
                          int16_t* zero, float* y_debug, void* stream) {
   if (M < 0 || K <= 0) return fail(OFFQ_ERR_INVALID, "M must be >= 0 and K > 0");
@@ -98,14 +98,14 @@ int offq_rotate_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, i
       (y_debug && !aligned(y_debug, 16)))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (x, y_debug: 16 B; codes: 4 B)");
   if (M * (K / g) >= kMaxGroups) return fail(OFFQ_ERR_UNSUPPORTED, "too many groups");
-  if (int s = check_device()) return s;
+  if (offq_status_t s = check_device()) return s;
   return launched(offq::launch_rotate_quantize(x, M * (K / g), (int)(K / g), ldx, lg,
                                                apply_hadamard != 0, codes, K / 2, scale, zero,
                                                y_debug, K, (hipStream_t)stream),
                   "rotate_quantize");
 }
 
-int offq_kv_quantize(const uint16_t* kv, int64_t rows, int32_t head_dim, int64_t row_stride,
+offq_status_t offq_kv_quantize(const uint16_t* kv, int64_t rows, int32_t head_dim, int64_t row_stride,
                      int32_t apply_hadamard, uint8_t* codes, uint16_t* scale, int16_t* zero,
                      float* y_debug, void* stream) {
   if (rows < 0) return fail(OFFQ_ERR_INVALID, "rows must be >= 0");
@@ -122,14 +122,14 @@ int offq_kv_quantize(const uint16_t* kv, int64_t rows, int32_t head_dim, int64_t
       (y_debug && !aligned(y_debug, 16)))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (kv, y_debug: 16 B; codes: 4 B)");
   if (rows >= kMaxGroups) return fail(OFFQ_ERR_UNSUPPORTED, "too many rows");
-  if (int s = check_device()) return s;
+  if (offq_status_t s = check_device()) return s;
   return launched(offq::launch_rotate_quantize(kv, rows, 1, row_stride, lg, apply_hadamard != 0,
                                                codes, head_dim / 2, scale, zero, y_debug,
                                                head_dim, (hipStream_t)stream),
                   "kv_quantize");
 }
 
-int offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale, const int16_t* a_zero,
+offq_status_t offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale, const int16_t* a_zero,
                    const uint8_t* w_codes, const uint16_t* w_scale, const int32_t* w_colsum,
                    int64_t M, int64_t N, int64_t K, int32_t g, uint16_t* y, int64_t ldy,
                    int32_t* acc_debug, void* stream) {
@@ -148,7 +148,7 @@ int offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale, const int16_
       !aligned(a_zero, 2) || !aligned(w_scale, 2) || !aligned(w_colsum, 4) || !aligned(y, 2) ||
       (acc_debug && !aligned(acc_debug, 4)))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (codes: 16 B)");
-  if (int s = check_device()) return s;
+  if (offq_status_t s = check_device()) return s;
   hipError_t e;
   if (M <= 16 && offq::gemv_mfma_supported(M, N, K, lg))
     e = offq::launch_w4a4_gemv_mfma(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N,
@@ -162,7 +162,7 @@ int offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale, const int16_
   return launched(e, M <= 16 ? "w4a4_gemv" : "w4a4_gemm");
 }
 
-int offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g, uint8_t* w_codes,
+offq_status_t offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g, uint8_t* w_codes,
                       uint16_t* w_scale, int32_t* w_colsum, void* stream) {
   if (N <= 0 || K <= 0) return fail(OFFQ_ERR_INVALID, "need N > 0, K > 0");
   const int lg = ilog2_pow2(g);
@@ -174,7 +174,7 @@ int offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g, uint8_t* 
   if (!w || !w_codes || !w_scale || !w_colsum) return fail(OFFQ_ERR_INVALID, "null pointer argument");
   if (!aligned(w, 16) || !aligned(w_codes, 4) || !aligned(w_scale, 2) || !aligned(w_colsum, 4))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (w: 16 B; w_codes: 4 B)");
-  if (int s = check_device()) return s;
+  if (offq_status_t s = check_device()) return s;
   return launched(offq::launch_pack_weights(w, N, K, lg, w_codes, w_scale, w_colsum,
                                             (hipStream_t)stream),
                   "pack_weights");
@@ -188,7 +188,7 @@ int64_t offq_kv_attention_workspace_bytes(int64_t B, int64_t H, int64_t seq_len)
 }
 
 namespace {
-int kv_attention_checked(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,
+offq_status_t kv_attention_checked(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,
                          const int16_t* k_zero, const uint8_t* v_codes, const uint16_t* v_scale,
                          const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv, int64_t s_cap,
                          int64_t seq_len, int32_t head_dim, float sm_scale, int32_t v_hadamard,
@@ -216,7 +216,7 @@ int kv_attention_checked(const uint16_t* q, const uint8_t* k_codes, const uint16
   if (workspace_bytes < need)
     return fail(OFFQ_ERR_INVALID, "workspace of %lld bytes, need %lld", (long long)workspace_bytes,
                 (long long)need);
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale,
                                                    v_zero, B * Hq, Hq / Hkv, s_cap, seq_len,
                                                    sm_scale, v_hadamard != 0, out, qcodes,
@@ -226,7 +226,7 @@ int kv_attention_checked(const uint16_t* q, const uint8_t* k_codes, const uint16
 }
 }  // namespace
 
-int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
+offq_status_t offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
                                  const uint16_t* k_scale, const int16_t* k_zero,
                                  const uint8_t* v_codes, const uint16_t* v_scale,
                                  const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv,
@@ -239,7 +239,7 @@ int offq_kv_attention_decode_gqa(const uint16_t* q, const uint8_t* k_codes,
                               nullptr, workspace, workspace_bytes, stream);
 }
 
-int offq_kv_attention_decode_quantize(const uint16_t* q, const uint8_t* k_codes,
+offq_status_t offq_kv_attention_decode_quantize(const uint16_t* q, const uint8_t* k_codes,
                                       const uint16_t* k_scale, const int16_t* k_zero,
                                       const uint8_t* v_codes, const uint16_t* v_scale,
                                       const int16_t* v_zero, int64_t B, int64_t Hq, int64_t Hkv,
@@ -253,7 +253,7 @@ int offq_kv_attention_decode_quantize(const uint16_t* q, const uint8_t* k_codes,
                               out_scale, out_zero, workspace, workspace_bytes, stream);
 }
 
-int offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,
+offq_status_t offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const uint16_t* k_scale,
                              const int16_t* k_zero, const uint8_t* v_codes,
                              const uint16_t* v_scale, const int16_t* v_zero, int64_t B,
                              int64_t H, int64_t s_cap, int64_t seq_len, int32_t head_dim,
@@ -264,7 +264,7 @@ int offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes, const ui
                                       workspace, workspace_bytes, stream);
 }
 
-int offq_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr, int64_t M,
+offq_status_t offq_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr, int64_t M,
                      int64_t D, float eps, uint16_t* h_out, int64_t ldh, uint16_t* y_out,
                      int64_t ldy, void* stream) {
   if (M < 0) return fail(OFFQ_ERR_INVALID, "M < 0");
@@ -281,13 +281,13 @@ int offq_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_
       (y_out && !aligned(y_out, 16)))
     return fail(OFFQ_ERR_INVALID, "pointers must be 16-byte aligned");
   if (M == 0) return ok();
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_add_rmsnorm(x, ldx, res, ldr, M, D, eps, h_out, ldh, y_out, ldy,
                                            (hipStream_t)stream),
                   "add_rmsnorm");
 }
 
-int offq_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t* out, int64_t ldo,
+offq_status_t offq_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t* out, int64_t ldo,
                 void* stream) {
   if (M < 0) return fail(OFFQ_ERR_INVALID, "M < 0");
   if (F < 8 || F % 8) return fail(OFFQ_ERR_INVALID, "F must be a positive multiple of 8");
@@ -299,11 +299,11 @@ int offq_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint16_t*
   if (!aligned(gu, 16) || !aligned(out, 16))
     return fail(OFFQ_ERR_INVALID, "pointers must be 16-byte aligned");
   if (M == 0) return ok();
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_swiglu(gu, ldg, M, F, out, ldo, (hipStream_t)stream), "swiglu");
 }
 
-int offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq, int64_t Hkv,
+offq_status_t offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq, int64_t Hkv,
                         int32_t head_dim, const int32_t* positions, double rope_base,
                         int32_t k_hadamard, int32_t v_hadamard, uint16_t* q_out,
                         uint8_t* k_codes, uint16_t* k_scale, int16_t* k_zero, uint8_t* v_codes,
@@ -328,7 +328,7 @@ int offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq,
       (k_y_debug && !aligned(k_y_debug, 8)) || (v_y_debug && !aligned(v_y_debug, 8)))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (qkv, q_out, positions: 4 B; debug: 8 B)");
   if (M == 0) return ok();
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_rope_kv_append(qkv, ldq, M, Hq, Hkv, positions, rope_base,
                                               k_hadamard != 0, v_hadamard != 0, q_out, k_codes,
                                               k_scale, k_zero, v_codes, v_scale, v_zero, s_cap,
@@ -341,7 +341,7 @@ int64_t offq_top1_workspace_bytes(int64_t n_seq, int64_t seq_len) {
   return n_seq * seq_len * (int64_t)sizeof(float);
 }
 
-int offq_top1_select(const uint16_t* x, int64_t n_seq, int64_t seq_len, int64_t D, int64_t ld_tok,
+offq_status_t offq_top1_select(const uint16_t* x, int64_t n_seq, int64_t seq_len, int64_t D, int64_t ld_tok,
                      int64_t ld_seq, int32_t* idx, float* X, int64_t ldX, void* workspace,
                      int64_t workspace_bytes, void* stream) {
   if (n_seq <= 0 || seq_len <= 0) return fail(OFFQ_ERR_INVALID, "need n_seq, seq_len > 0");
@@ -356,31 +356,31 @@ int offq_top1_select(const uint16_t* x, int64_t n_seq, int64_t seq_len, int64_t 
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (x: 16 B)");
   if (workspace_bytes < offq_top1_workspace_bytes(n_seq, seq_len))
     return fail(OFFQ_ERR_INVALID, "workspace too small");
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_top1_select(x, n_seq, seq_len, D, ld_tok, ld_seq, idx, X, ldX,
                                            static_cast<float*>(workspace), (hipStream_t)stream),
                   "top1_select");
 }
 
-int offq_channel_absmax(const uint16_t* x, int64_t rows, int64_t D, int64_t ldx, double* out,
+offq_status_t offq_channel_absmax(const uint16_t* x, int64_t rows, int64_t D, int64_t ldx, double* out,
                         void* stream) {
   if (rows <= 0 || D <= 0 || ldx < D) return fail(OFFQ_ERR_INVALID, "need rows, D > 0, ldx >= D");
   if (D > (1 << 24)) return fail(OFFQ_ERR_UNSUPPORTED, "D too large");
   if (!x || !out) return fail(OFFQ_ERR_INVALID, "null pointer argument");
   if (!aligned(x, 2) || !aligned(out, 8)) return fail(OFFQ_ERR_INVALID, "misaligned pointer");
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_channel_absmax(x, rows, D, ldx, out, (hipStream_t)stream),
                   "channel_absmax");
 }
 
-int offq_gram(const float* X, int64_t N, int64_t D, int64_t ldX, double* C, int64_t ldC,
+offq_status_t offq_gram(const float* X, int64_t N, int64_t D, int64_t ldX, double* C, int64_t ldC,
               void* stream) {
   if (N <= 0 || D <= 0 || ldX < D || ldC < D)
     return fail(OFFQ_ERR_INVALID, "need N, D > 0, ldX >= D, ldC >= D");
   if (D > 65536 || N > (int64_t(1) << 30)) return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
   if (!X || !C) return fail(OFFQ_ERR_INVALID, "null pointer argument");
   if (!aligned(X, 4) || !aligned(C, 8)) return fail(OFFQ_ERR_INVALID, "misaligned pointer");
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_gram(X, N, D, ldX, C, ldC, (hipStream_t)stream), "gram");
 }
 
@@ -389,7 +389,7 @@ int64_t offq_eigh_workspace_bytes(int64_t D) {
   return offq::eigh_workspace_doubles(D) * (int64_t)sizeof(double);
 }
 
-int offq_eigh(const double* C, int64_t D, int64_t ldC, double* evals, double* U, int64_t ldU,
+offq_status_t offq_eigh(const double* C, int64_t D, int64_t ldC, double* evals, double* U, int64_t ldU,
               void* workspace, int64_t workspace_bytes, int32_t max_sweeps, double tol,
               int32_t* sweeps, double* rel_off, void* stream) {
   if (D < 2 || D % 2) return fail(OFFQ_ERR_INVALID, "D must be even and >= 2");
@@ -402,7 +402,7 @@ int offq_eigh(const double* C, int64_t D, int64_t ldC, double* evals, double* U,
   if (workspace_bytes < offq_eigh_workspace_bytes(D))
     return fail(OFFQ_ERR_INVALID, "workspace of %lld bytes, need %lld", (long long)workspace_bytes,
                 (long long)offq_eigh_workspace_bytes(D));
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   int sw = 0;
   double ro = 0.0;
   const hipError_t e = offq::launch_eigh(C, ldC, D, evals, U, ldU, static_cast<double*>(workspace),
@@ -412,7 +412,7 @@ int offq_eigh(const double* C, int64_t D, int64_t ldC, double* evals, double* U,
   return launched(e, "eigh");
 }
 
-int offq_group_permutation(const double* key, int64_t D, int32_t g, int32_t* perm,
+offq_status_t offq_group_permutation(const double* key, int64_t D, int32_t g, int32_t* perm,
                            void* workspace, int64_t workspace_bytes, void* stream) {
   if (D <= 0 || g <= 0 || D % g) return fail(OFFQ_ERR_INVALID, "need D > 0 a multiple of g > 0");
   if (D > (1 << 20)) return fail(OFFQ_ERR_UNSUPPORTED, "D too large");
@@ -420,13 +420,13 @@ int offq_group_permutation(const double* key, int64_t D, int32_t g, int32_t* per
   if (!aligned(key, 8) || !aligned(perm, 4) || !aligned(workspace, 4))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer");
   if (workspace_bytes < D * 4) return fail(OFFQ_ERR_INVALID, "workspace too small (D int32)");
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_group_permutation(key, D, g, perm, static_cast<int32_t*>(workspace),
                                                  (hipStream_t)stream),
                   "group_permutation");
 }
 
-int offq_build_rotation(const double* U, int64_t ldU, int64_t D, const int32_t* perm, int32_t g,
+offq_status_t offq_build_rotation(const double* U, int64_t ldU, int64_t D, const int32_t* perm, int32_t g,
                         int32_t apply_hadamard, float* R, int64_t ldR, void* stream) {
   if (D <= 0 || D > 8192) return fail(OFFQ_ERR_UNSUPPORTED, "need 0 < D <= 8192");
   if (apply_hadamard != 0 && apply_hadamard != 1)
@@ -440,12 +440,12 @@ int offq_build_rotation(const double* U, int64_t ldU, int64_t D, const int32_t* 
   if (!R) return fail(OFFQ_ERR_INVALID, "null output");
   if ((U && !aligned(U, 8)) || (perm && !aligned(perm, 4)) || !aligned(R, 4))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer");
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_build_rotation(U, ldU, D, perm, lg, R, ldR, (hipStream_t)stream),
                   "build_rotation");
 }
 
-int offq_fuse_weights(const float* W, int64_t ldW, int64_t N, int64_t K, const float* R,
+offq_status_t offq_fuse_weights(const float* W, int64_t ldW, int64_t N, int64_t K, const float* R,
                       int64_t ldR, float* W_out, int64_t ldo, void* stream) {
   if (N <= 0 || K <= 0 || ldW < K || ldR < K || ldo < K)
     return fail(OFFQ_ERR_INVALID, "need N, K > 0 and row strides >= K");
@@ -453,12 +453,12 @@ int offq_fuse_weights(const float* W, int64_t ldW, int64_t N, int64_t K, const f
   if (!W || !R || !W_out) return fail(OFFQ_ERR_INVALID, "null pointer argument");
   if (!aligned(W, 4) || !aligned(R, 4) || !aligned(W_out, 4))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer");
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_fuse_weights(W, ldW, N, K, R, ldR, W_out, ldo, (hipStream_t)stream),
                   "fuse_weights");
 }
 
-int offq_permute_rows(const float* W, int64_t ldW, int64_t N, int64_t K, const int32_t* perm,
+offq_status_t offq_permute_rows(const float* W, int64_t ldW, int64_t N, int64_t K, const int32_t* perm,
                       float* W_out, int64_t ldo, void* stream) {
   if (N <= 0 || K <= 0 || ldW < K || ldo < K)
     return fail(OFFQ_ERR_INVALID, "need N, K > 0 and row strides >= K");
@@ -466,12 +466,12 @@ int offq_permute_rows(const float* W, int64_t ldW, int64_t N, int64_t K, const i
   if (!W || !perm || !W_out) return fail(OFFQ_ERR_INVALID, "null pointer argument");
   if (!aligned(W, 4) || !aligned(perm, 4) || !aligned(W_out, 4))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer");
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_permute_rows(W, ldW, N, K, perm, W_out, ldo, (hipStream_t)stream),
                   "permute_rows");
 }
 
-int offq_add_rmsnorm_quantize(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr,
+offq_status_t offq_add_rmsnorm_quantize(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr,
                               int64_t M, int64_t D, float eps, int32_t g, uint16_t* h_out,
                               int64_t ldh, uint8_t* codes, uint16_t* scale, int16_t* zero,
                               uint16_t* y_debug, int64_t ldy, void* stream) {
@@ -493,14 +493,14 @@ int offq_add_rmsnorm_quantize(const uint16_t* x, int64_t ldx, const uint16_t* re
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (rows and codes: 16 B)");
   if (M > (int64_t(1) << 31) - 1) return fail(OFFQ_ERR_UNSUPPORTED, "M too large");
   if (M == 0) return ok();
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_add_rmsnorm_quant(x, ldx, res, ldr, M, D, eps, lg, h_out, ldh,
                                                  codes, scale, zero, y_debug, ldy,
                                                  (hipStream_t)stream),
                   "add_rmsnorm_quantize");
 }
 
-int offq_swiglu_rotate_quantize(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F,
+offq_status_t offq_swiglu_rotate_quantize(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F,
                                 uint8_t* codes, uint16_t* scale, int16_t* zero, float* y_debug,
                                 void* stream) {
   if (M < 0) return fail(OFFQ_ERR_INVALID, "M < 0");
@@ -513,7 +513,7 @@ int offq_swiglu_rotate_quantize(const uint16_t* gu, int64_t ldg, int64_t M, int6
       (y_debug && !aligned(y_debug, 16)))
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (gu: 16 B)");
   if (M == 0) return ok();
-  if (int st = check_device()) return st;
+  if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_swiglu_rq(gu, ldg, M, F, codes, scale, zero, y_debug,
                                          (hipStream_t)stream),
                   "swiglu_rotate_quantize");

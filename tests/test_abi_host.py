@@ -198,3 +198,14 @@ def test_layer_and_calibration_validation():
     assert L.lib.offq_build_rotation(None, 0, 96, None, 24, 1, P, 96, None) == L.OFFQ_ERR_INVALID
     # top-1: D not a multiple of 8
     assert L.lib.offq_top1_select(P, 2, 3, 12, 16, 48, P, P, 12, P, 1 << 10, None) == L.OFFQ_ERR_INVALID
+
+
+def test_package_import_does_not_load_the_library():
+    """The oracle's CPU pins use the seeded generators of the package; importing
+    them must not need the HIP build (the library loads on first use)."""
+    import subprocess
+    import sys
+    code = ("import sys; import paper_2606_07116_amd.inputs, oracle.gemm; "
+            "assert 'paper_2606_07116_amd._lib' not in sys.modules")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
