@@ -196,10 +196,15 @@ __global__ __launch_bounds__(256) void w4a4_gemm_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Decode GEMV (M <= 16): one wavefront per output channel n streams the
-// weight row with 16-byte coalesced loads; v_dot8_i32_i4 on
-// (q_a - 8, q_w) (activation codes re-biased by xor 0x8 per nibble), folded
-// per group in fp32:  acc_b = dot_b + 8 colsum_b.
+// Decode GEMV (M <= 16) for the shapes the MFMA GEMV does not take (g = 64,
+// very many groups): one wavefront per output channel n streams the weight
+// row with 16-byte coalesced loads, lane l taking chunk 64 p + l (32 k) in
+// pass p.  v_dot8_i32_i4 on (q_a - 8, q_w) (activation codes re-biased by
+// xor 0x8 per nibble) accumulates each group in int32: a group covers
+// g / 32 consecutive lanes of one pass (g <= 2048) or whole passes
+// (g > 2048); when it ends, its lanes add their int32 sums (exact), and the
+// group's first lane folds acc_b = sum (q_a - 8) q_w + 8 colsum_b into the
+// fp32 output, F += s (acc_b - z colsum_b).  DBG also stores acc_b.
 template <int MT, bool DBG>
 __global__ __launch_bounds__(256) void w4a4_gemv_kernel(
     const uint8_t* __restrict__ A, const uint16_t* __restrict__ a_scale,
@@ -209,42 +214,61 @@ __global__ __launch_bounds__(256) void w4a4_gemv_kernel(
     int32_t* __restrict__ acc_dbg) {
   const int lane = threadIdx.x & 63;
   const int n = (int)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (n >= N) return;
+  if (n >= N) return;  // wave-uniform
   const int64_t ldk = K >> 1;
   const int G = K >> log2g;
   const uint8_t* wrow = W + (int64_t)n * ldk;
+  const int nchunks = (int)(ldk >> 4);            // 16-byte chunks (32 k) per row
+  const int seg = 1 << min(log2g - 5, 6);        // lanes of one group in one pass
+  const int passes = (nchunks + 63) >> 6;
   float part[MT];
+  int acc[MT];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) part[m] = 0.0f;
-  const int nchunks = (int)(ldk >> 4);  // 16-byte chunks per row
-  // chunk c covers k in [32c, 32c+32): group 32c >> log2g
-  for (int c = lane; c < nchunks; c += 64) {
-    const uint4 w = *reinterpret_cast<const uint4*>(wrow + (int64_t)c * 16);
-    const int b = (c << 5) >> log2g;
+  for (int m = 0; m < MT; ++m) {
+    part[m] = 0.0f;
+    acc[m] = 0;
+  }
+  const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
+  for (int p = 0; p < passes; ++p) {
+    const int c = (p << 6) + lane;
+    const bool live = c < nchunks;  // a dead lane's zero weights add nothing
+    const uint4 w = live ? *reinterpret_cast<const uint4*>(wrow + (int64_t)c * 16) : z4;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       if (m < M) {
-        const uint4 a = *reinterpret_cast<const uint4*>(A + (int64_t)m * ldk + (int64_t)c * 16);
-        int d = 0;
+        const uint4 a = live ? *reinterpret_cast<const uint4*>(A + (int64_t)m * ldk + (int64_t)c * 16) : z4;
+        int d = acc[m];
         d = __builtin_amdgcn_sdot8((int)(a.x ^ 0x88888888u), (int)w.x, d, false);
         d = __builtin_amdgcn_sdot8((int)(a.y ^ 0x88888888u), (int)w.y, d, false);
         d = __builtin_amdgcn_sdot8((int)(a.z ^ 0x88888888u), (int)w.z, d, false);
         d = __builtin_amdgcn_sdot8((int)(a.w ^ 0x88888888u), (int)w.w, d, false);
-        const float s = fp16_bits_to_f32(a_scale[(int64_t)m * G + b]);
-        part[m] += s * (float)d;
+        acc[m] = d;
       }
     }
-  }
-  // zero-point / re-bias correction: sum_b s_b (8 - z_b) colsum_b, spread over lanes
-  for (int b = lane; b < G; b += 64) {
-    const int cs = w_colsum[(int64_t)b * N + n];
+    // groups end in every pass (g <= 2048), or after g / 2048 passes
+    if (log2g <= 11 || ((((int64_t)p + 1) << 11) & ((int64_t(1) << log2g) - 1)) == 0) {
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      if (m < M) {
-        const float s = fp16_bits_to_f32(a_scale[(int64_t)m * G + b]);
-        const int z = a_zero[(int64_t)m * G + b];
-        part[m] += s * (float)((long long)(8 - z) * (long long)cs);
+      for (int m = 0; m < MT; ++m) {
+        int t = acc[m];
+        for (int off = 1; off < seg; off <<= 1) t += __shfl_xor(t, off);
+        acc[m] = t;
       }
+      if (live && (lane & (seg - 1)) == 0) {
+        const int b = (int)(((int64_t)c << 5) >> log2g);
+        const int cs = w_colsum[(int64_t)b * N + n];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          if (m < M) {
+            const int a_b = acc[m] + 8 * cs;  // sum_{k in b} q_a q_w
+            const float s = fp16_bits_to_f32(a_scale[(int64_t)m * G + b]);
+            const int z = a_zero[(int64_t)m * G + b];
+            part[m] += s * (float)((long long)a_b - (long long)z * (long long)cs);
+            if constexpr (DBG) acc_dbg[((int64_t)b * M + m) * N + n] = a_b;
+          }
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[m] = 0;
     }
   }
 #pragma unroll
@@ -257,24 +281,6 @@ __global__ __launch_bounds__(256) void w4a4_gemv_kernel(
 #pragma unroll
     for (int m = 0; m < MT; ++m)
       if (m < M) Y[(int64_t)m * ldy + n] = f32_to_bf16_rne(sw * part[m]);
-  }
-  if constexpr (DBG) {
-    // exact per-group accumulators: one lane per group, scalar dot loop
-    for (int b = lane; b < G; b += 64) {
-      const int64_t k0 = (int64_t)b << log2g;
-      for (int m = 0; m < M; ++m) {
-        int acc = 0;
-        for (int64_t c = k0 >> 5; c < (k0 + (1 << log2g)) >> 5; ++c) {
-          const uint4 w = *reinterpret_cast<const uint4*>(wrow + c * 16);
-          const uint4 a = *reinterpret_cast<const uint4*>(A + (int64_t)m * ldk + c * 16);
-          acc = __builtin_amdgcn_sdot8((int)(a.x ^ 0x88888888u), (int)w.x, acc, false);
-          acc = __builtin_amdgcn_sdot8((int)(a.y ^ 0x88888888u), (int)w.y, acc, false);
-          acc = __builtin_amdgcn_sdot8((int)(a.z ^ 0x88888888u), (int)w.z, acc, false);
-          acc = __builtin_amdgcn_sdot8((int)(a.w ^ 0x88888888u), (int)w.w, acc, false);
-        }
-        acc_dbg[((int64_t)b * M + m) * N + n] = acc + 8 * w_colsum[(int64_t)b * N + n];
-      }
-    }
   }
 }
 

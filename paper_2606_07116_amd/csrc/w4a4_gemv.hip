@@ -37,21 +37,20 @@ constexpr int KSTEP = 128;  // k per step (64 packed bytes per row)
 constexpr int GMAX = 256;   // groups whose parameters fit in LDS
 
 // T: 16-channel row tiles per wave (one activation load serves T weight
-// loads); P: waves per workgroup, each taking 1/P of K.
-template <int T, int P>
+// loads); P: waves per workgroup, each taking 1/P of K; BATCH: steps of 128 k
+// per batch of loads (registers).
+template <int T, int P, int BATCH>
 struct GvCfg {
-  static constexpr int BATCH = T >= 4 ? 2 : 4;  // steps per batch (registers)
   static constexpr int THREADS = 64 * P;
 };
 
-template <int T, int P, bool DBG>
+template <int T, int P, int BATCH, bool DBG>
 __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
     const uint8_t* __restrict__ A, const uint16_t* __restrict__ a_scale,
     const int16_t* __restrict__ a_zero, const uint8_t* __restrict__ W,
     const uint16_t* __restrict__ w_scale, const int32_t* __restrict__ w_colsum, int M, int N,
     int K, int log2g, uint16_t* __restrict__ Y, int64_t ldy, int32_t* __restrict__ acc_dbg) {
-  constexpr int BATCH = GvCfg<T, P>::BATCH;
-  constexpr int NT = GvCfg<T, P>::THREADS;
+  constexpr int NT = GvCfg<T, P, BATCH>::THREADS;
   __shared__ float red[P][64][T * 4];
   // per group: s / 16 and -s z of the 16 token rows, colsum of the tile's channels
   extern __shared__ float gpar[];
@@ -219,13 +218,16 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
 
 }  // namespace
 
-// Launch shape (T row tiles per wave, K in P parts), as measured at M = 16
-// (g = 128 ... 8192): wide layers (>= 16384 channels) take four row tiles per
-// wave (one activation load serves four weight loads) and K in quarters;
-// narrower ones need more waves in flight: K in eighths with two tiles per
-// wave from 6144 channels, one below, where K splits into eighths of whole
-// batches; else one tile per wave and K in quarters (e.g. K = 14336).
-static void gemv_shape(int64_t N, int64_t K, int& T, int& P) {
+// Launch shape (T row tiles per wave, K in P parts, BATCH steps per load
+// batch), as measured at M = 16 (g = 128 ... 8192): wide layers (>= 16384
+// channels) take four row tiles per wave (one activation load serves four
+// weight loads) and K in quarters; narrower ones need more waves in flight:
+// K in eighths with two tiles per wave from 6144 channels, one below, where K
+// splits into eighths of whole batches; else one tile per wave and K in
+// quarters (e.g. K = 14336).  A K that is not a whole number of such batches
+// (short rows, e.g. K = 256) takes one tile per wave, batches of one step and
+// K in as many parts (4, 2, 1) as it divides into.
+static void gemv_shape(int64_t N, int64_t K, int& T, int& P, int& B) {
   if (N >= 16384) {
     T = 4, P = 4;
   } else if (K % 4096 == 0) {
@@ -235,6 +237,11 @@ static void gemv_shape(int64_t N, int64_t K, int& T, int& P) {
   } else {
     T = 4, P = 4;
   }
+  B = T >= 4 ? 2 : 4;
+  if (K % ((int64_t)P * KSTEP * B) != 0) {
+    T = 1, B = 1;
+    P = K % (4 * KSTEP) == 0 ? 4 : K % (2 * KSTEP) == 0 ? 2 : 1;
+  }
 }
 
 bool gemv_mfma_supported(int64_t M, int64_t N, int64_t K, int log2g) {
@@ -242,9 +249,9 @@ bool gemv_mfma_supported(int64_t M, int64_t N, int64_t K, int log2g) {
   // a group: the group's zero-point term is added once, by the wave holding
   // its first k); no step straddles a group; the group parameters fit in LDS;
   // 32-bit buffer offsets
-  int T, P;
-  gemv_shape(N, K, T, P);
-  const int64_t batch = (int64_t)P * KSTEP * (T >= 4 ? 2 : 4);
+  int T, P, B;
+  gemv_shape(N, K, T, P, B);
+  const int64_t batch = (int64_t)P * KSTEP * B;
   // group parameters (dynamic) + the partial sums of the P waves (static)
   const int64_t lds = (K >> log2g) * (32 + 16 * T) * 4 + (int64_t)P * 64 * 4 * T * 4;
   return M <= 16 && log2g >= 7 && K % batch == 0 && (K >> log2g) <= GMAX &&
@@ -252,7 +259,7 @@ bool gemv_mfma_supported(int64_t M, int64_t N, int64_t K, int log2g) {
          32 * (K / 2) < (int64_t(1) << 31) && M * (K / 2) < (int64_t(1) << 31);
 }
 
-template <int T, int P>
+template <int T, int P, int BATCH>
 hipError_t launch_gv(const uint8_t* a_codes, const uint16_t* a_scale, const int16_t* a_zero,
                      const uint8_t* w_codes, const uint16_t* w_scale, const int32_t* w_colsum,
                      int64_t M, int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
@@ -266,11 +273,11 @@ hipError_t launch_gv(const uint8_t* a_codes, const uint16_t* a_scale, const int1
     hipError_t e = hipMemsetAsync(acc_debug, 0, (size_t)(K >> log2g) * M * N * sizeof(int32_t),
                                   stream);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((w4a4_gemv_kernel<T, P, true>), grid, block, lds, stream, a_codes,
+    hipLaunchKernelGGL((w4a4_gemv_kernel<T, P, BATCH, true>), grid, block, lds, stream, a_codes,
                        a_scale, a_zero, w_codes, w_scale, w_colsum, (int)M, (int)N, (int)K, log2g,
                        y, ldy, acc_debug);
   }
-  hipLaunchKernelGGL((w4a4_gemv_kernel<T, P, false>), grid, block, lds, stream, a_codes, a_scale,
+  hipLaunchKernelGGL((w4a4_gemv_kernel<T, P, BATCH, false>), grid, block, lds, stream, a_codes, a_scale,
                      a_zero, w_codes, w_scale, w_colsum, (int)M, (int)N, (int)K, log2g, y, ldy,
                      acc_debug);
   return hipGetLastError();
@@ -281,15 +288,20 @@ hipError_t launch_w4a4_gemv_mfma(const uint8_t* a_codes, const uint16_t* a_scale
                                  const uint16_t* w_scale, const int32_t* w_colsum, int64_t M,
                                  int64_t N, int64_t K, int log2g, uint16_t* y, int64_t ldy,
                                  int32_t* acc_debug, hipStream_t stream) {
-  int T, P;
-  gemv_shape(N, K, T, P);
-#define OFFQ_GV(T, P)                                                                         \
-  return launch_gv<T, P>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, \
-                         y, ldy, acc_debug, stream)
-  if (T == 4) OFFQ_GV(4, 4);
-  if (T == 2) OFFQ_GV(2, 8);
-  if (P == 8) OFFQ_GV(1, 8);
-  OFFQ_GV(1, 4);
+  int T, P, B;
+  gemv_shape(N, K, T, P, B);
+#define OFFQ_GV(T, P, B)                                                                         \
+  return launch_gv<T, P, B>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, \
+                            y, ldy, acc_debug, stream)
+  if (B == 1) {
+    if (P == 4) OFFQ_GV(1, 4, 1);
+    if (P == 2) OFFQ_GV(1, 2, 1);
+    OFFQ_GV(1, 1, 1);
+  }
+  if (T == 4) OFFQ_GV(4, 4, 2);
+  if (T == 2) OFFQ_GV(2, 8, 4);
+  if (P == 8) OFFQ_GV(1, 8, 4);
+  OFFQ_GV(1, 4, 4);
 #undef OFFQ_GV
 }
 
