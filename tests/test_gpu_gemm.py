@@ -46,6 +46,32 @@ def test_gemm_shapes(M, N, K, g):
     _layer(M, N, K, g, seed=M * 7 + N)
 
 
+@pytest.mark.parametrize("M,N,K", [(4096, 6144, 4096), (4000, 6100, 1024)])
+def test_wide_tile_gemm_accumulators(M, N, K):
+    """One group per row on at least 384 tiles of 256 x 256: the wide-tile
+    kernel that the MLP up/gate projection and the 8192-row projection run.
+    Every accumulator bit-exact, once on whole tiles and once ragged in M and
+    N (384 tiles again)."""
+    _layer(M, N, K, K, seed=M + N)
+
+
+def test_out_must_cover_the_output():
+    """The GEMM writes M x N values at the output's row stride: a short or a
+    transposed output is refused before any launch."""
+    M, N, K, g = 32, 64, 256, 256
+    codes = torch.zeros((M, K // 2), dtype=torch.uint8, device=P.DEV)
+    sc = torch.ones((M, 1), dtype=torch.float16, device=P.DEV)
+    zp = torch.zeros((M, 1), dtype=torch.int16, device=P.DEV)
+    wc = torch.zeros((N, K // 2), dtype=torch.uint8, device=P.DEV)
+    ws = torch.ones(N, dtype=torch.float16, device=P.DEV)
+    cs = torch.zeros((1, N), dtype=torch.int32, device=P.DEV)
+    short = torch.empty((M - 1, N), dtype=torch.bfloat16, device=P.DEV)
+    trans = torch.empty((N, M), dtype=torch.bfloat16, device=P.DEV).t()
+    for bad in (short, trans):
+        with pytest.raises(ValueError):
+            offq.offq_w4a4_gemm(codes, sc, zp, wc, ws, cs, g, out=bad)
+
+
 @pytest.mark.parametrize("M", [1, 2, 4, 5, 16])
 @pytest.mark.parametrize("K,g", [(256, 256), (2048, 512), (8192, 8192), (1024, 64),
                                  (4096, 128), (1536, 512), (2048, 1024)])

@@ -187,3 +187,67 @@ def test_attention_full_size_sampled(seq_len):
         qq = q[b:b + 1, h:h + 1]
         ref = OA.decode_attention(qq, *sel, seq_len, SM)
         check(got[b:b + 1, h:h + 1], ref, _magnitude(qq, *sel, seq_len, SM))
+
+
+def _offset_key_cache(B, H, S, seed, lo, hi):
+    """Cache rows quantized by the oracle's KV quantizer after H3, from rows
+    whose first channel carries a large per-position offset (a massive key
+    activation on the channel the offline rotation concentrates): H3 spreads
+    it over the row as a constant and the zero-point absorbs it (Eq. 5), so
+    |z| reaches the hundreds."""
+    from oracle import kv as OKV
+    from oracle import quantizer as OQ
+    rng = np.random.default_rng(seed)
+    rows = inputs.kv_rows(B * H * S, 128, seed=seed, heads=H)
+    sign = np.where(rng.random(H) < 0.5, -1.0, 1.0)
+    mag = rng.uniform(lo, hi, size=B * H * S) * np.tile(np.repeat(sign, S), B)
+    rows[:, 0] = inputs.round_to_bf16(rows[:, 0] + mag.astype(np.float32))
+    cq, cs, cz = OKV.kv_quantize(OKV.kv_rotate(rows, True).astype(np.float32))
+    shp = (B, H, S)
+    return OQ.pack_nibbles(cq).reshape(shp + (64,)), cs.reshape(shp), cz.reshape(shp)
+
+
+@pytest.mark.parametrize("case", ["offset_keys", "common_offset", "int16_range"])
+@pytest.mark.parametrize("Hq,Hkv", [(4, 4), (8, 2)])
+def test_attention_large_zero_points(case, Hq, Hkv):
+    """Attended cache rows whose zero-points are large, the regime the method
+    creates by pushing the offset into the zero-point (Eq. 1, Eq. 5; the
+    footnote to Eq. 5: 0 need not lie in the quantized range).  The kernel
+    forms each score as a * dot + b with b proportional to z * sum(q_r), in
+    fp32.  Cases: rows quantized by the oracle from keys and values whose
+    first channel carries an offset of 300..3000 (|z| in the hundreds); a
+    shared offset near the bottom of the int16 range (z = -30000 +- 8 with
+    scale 2^-7: every key and value row sits near -234, the softmax stays
+    flat, so the fp32 terms b nearly cancel between positions); zero-points
+    drawn over the whole int16 range.  Held to the bar of the other cases."""
+    B, S, seq_len = 2, 1100, 1037
+    rng = np.random.default_rng(Hq * 10 + Hkv)
+    if case == "offset_keys":
+        kc, ks, kz = _offset_key_cache(B, Hkv, S, 11, 300.0, 3000.0)
+        vc, vs, vz = _offset_key_cache(B, Hkv, S, 12, 300.0, 3000.0)
+        assert np.abs(kz).max() >= 100
+        sm = 0.002  # scores spread over a few units: a mixed softmax
+    else:
+        kc, _, _ = inputs.kv4_cache(B, Hkv, S, 128, seed=13)
+        vc, _, _ = inputs.kv4_cache(B, Hkv, S, 128, seed=14)
+        if case == "common_offset":
+            ks = np.full((B, Hkv, S), 2.0 ** -7, np.float16)
+            vs = ks.copy()
+            kz = (-30000 + rng.integers(-8, 9, size=(B, Hkv, S))).astype(np.int16)
+            vz = (-30000 + rng.integers(-8, 9, size=(B, Hkv, S))).astype(np.int16)
+        else:
+            ks = rng.uniform(0.005, 0.02, size=(B, Hkv, S)).astype(np.float16)
+            vs = rng.uniform(0.005, 0.02, size=(B, Hkv, S)).astype(np.float16)
+            kz = rng.integers(-32768, 32768, size=(B, Hkv, S)).astype(np.int16)
+            vz = rng.integers(-32768, 32768, size=(B, Hkv, S)).astype(np.int16)
+        sm = SM
+    q = inputs.queries(B, Hq, 128, seed=15)
+    out = offq.offq_kv_attention_decode(P.to_dev_bf16(q), _dev(kc), _dev(ks), _dev(kz), _dev(vc),
+                                        _dev(vs), _dev(vz), seq_len, sm_scale=sm)
+    torch.cuda.synchronize()
+    got = P.host(out.float())
+    g = Hq // Hkv
+    rep = lambda a: np.repeat(a, g, axis=1)  # noqa: E731  query head h reads kv head h // g
+    kr, ksr, kzr, vr, vsr, vzr = (rep(a) for a in (kc, ks, kz, vc, vs, vz))
+    ref = OA.decode_attention(q, kr, ksr, kzr, vr, vsr, vzr, seq_len, sm)
+    check(got, ref, _magnitude(q, kr, ksr, kzr, vr, vsr, vzr, seq_len, sm))
