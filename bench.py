@@ -2,25 +2,37 @@
 """Benchmark of the OffQ W4A4 online path on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+                    [--no-components]
 
-One step = the whole online path of one quantized linear layer on one batch:
-fused rotate + quantize of the bf16 activations (offq_rotate_quantize), then
-the int4 x int4 GEMM with the dequantising epilogue (offq_w4a4_gemm).  The
-default workload is the attention-projection prefill layer
-X bf16 [2048, 4096] -> Y bf16 [2048, 4096] with W int4 [4096, 4096] and a
-4096-point Hadamard.  Inputs are synthetic (seeded), resident in HBM before
-the timed region; several input/weight sets whose total exceeds the 256 MB
-last-level cache are cycled so that every step reads from HBM.
+One step = the whole online path of the MLP of a Llama-3-8B-shaped layer at
+prefill (the largest single-GPU workload): fused rotate + quantize of the
+bf16 up/gate input X [4096, 4096] (offq_rotate_quantize, 4096-point
+Hadamard), the int4 x int4 GEMM with the dequantising epilogue against the
+stacked up and gate weights [28672, 4096] (offq_w4a4_gemm), then rotate +
+quantize of the down input [4096, 14336] (block-diagonal Hadamard, 28 blocks
+of 512) and the down GEMM [4096, 14336] x [4096, 14336]^T.  Inputs are
+synthetic (seeded), resident in HBM before the timed region; several
+input/weight sets whose total exceeds the 256 MB last-level cache are cycled
+so that every step reads from HBM.
 
 Prints ONE JSON line: the step throughput (integer TOP/s of the GEMM work per
-step time), per-kernel times from HIP events recorded on the launch stream,
-the roofline of the dominant kernel, and the CPU oracle timed on the host.
+step time), per-kernel times, the roofline of the dominant kernel, and the
+CPU oracle timed on the host.  With the default workload the line also
+carries, as "configs", every other workload's kernels measured the same way:
+the attention-projection prefill layer, the decode GEMVs at M = 1, 4, 16 and
+the KV4 cache quantize of K and V [8, 32, 32768, 128] with the 8192-row
+projection after it.
 
-Timed region: the K steps run kernel by kernel -- the first kernel of the
-step for steps 1..K, then the second for steps 1..K, and so on (step i's
-kernels still run in their order on step i's buffers) -- with one HIP event
-between these phases, so that each kernel's average duration is its phase
-time / K with no event between two launches of it.
+Timing.  The timed region runs the K steps kernel by kernel -- the first
+kernel of the step for steps 1..K, then the second for steps 1..K, and so on
+(step i's kernels still run in their order on step i's buffers) -- with one
+HIP event between these phases on the launch stream, so that each kernel's
+mean duration ("us") is its phase time / K with no event between two
+launches of it.  Then every kernel is launched again max(100, K) times with
+an event after each launch ("median_us", "p10_us", "p90_us": cold, cycling
+the buffer sets; "warm_median_us": one set, so inputs may sit in the
+last-level cache); "event_gap_us" is the median gap between two events with
+nothing between them, which each of those per-launch times includes.
 """
 
 import argparse
@@ -44,11 +56,13 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--workload", default="attn_proj_prefill",
+    p.add_argument("--workload", default="mlp_prefill",
                    choices=["attn_proj_prefill", "mlp_prefill", "decode", "kv_chain",
                             "kv_decode_attention", "decode_layer", "calibration"])
     p.add_argument("--decode-m", type=int, default=16)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-components", action="store_true",
+                   help="default workload: skip the other workloads' kernels")
     p.add_argument("--group-size", type=int, default=0,
                    help="quantization group (= Hadamard block) size for every layer of the "
                         "workload, e.g. 128 (the paper's default); 0 keeps the workload's own")
@@ -140,37 +154,140 @@ def run_gemm(lib, s, stream):
                                   stream)
 
 
-def cpu_baseline(M, K, N, g, spec, seed):
-    """The CPU oracle on the same workload (full step, repeated to >= 10 s)."""
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_layer_prep(np, inputs, OQ, K, N, g, spec, seed, n_cols=None):
+    """Offline weight preparation of one layer (not timed): the oracle's
+    symmetric weight quantizer and column sums, on the first n_cols output
+    channels when given."""
+    w = inputs.weights(N, K, seed=seed)
+    if n_cols is not None:
+        w = np.ascontiguousarray(w[:n_cols])
+    q_w, sw = OQ.quantize_weights(w)
+    del w
+    return q_w, sw, OQ.colsum(q_w, g)
+
+
+def _oracle_stages(np, OH, OQ, OG, x, g, q_w, sw, cs, t):
+    """One pass of the oracle over a layer: rotate (fp64), quantize (fp32),
+    integer GEMM (fp64 BLAS), epilogue (fp64); seconds added to t."""
+    t0 = time.perf_counter()
+    y = OH.rotate(x, g).astype(np.float32)
+    t1 = time.perf_counter()
+    q, s_, z = OQ.quantize_groups(y, g)
+    t2 = time.perf_counter()
+    acc = OG.int_gemm_groups(q, q_w, g)
+    t3 = time.perf_counter()
+    OG.epilogue(acc, s_, z, sw, cs)
+    t4 = time.perf_counter()
+    for k, v in (("rotate", t1 - t0), ("quantize", t2 - t1), ("int_gemm", t3 - t2),
+                 ("epilogue", t4 - t3)):
+        t[k] = t.get(k, 0.0) + v
+
+
+def cpu_baseline(layers, sample_rows, min_s=10.0, per_config=None):
+    """The CPU oracle, as it stands, on a bounded sample of the workload: the
+    first ``sample_rows`` token rows of each layer (full K and N), the whole
+    step repeated until ``min_s`` seconds; per-stage seconds; the rate in the
+    metric's unit (integer TOP/s of the sampled GEMM work).  ``per_config``:
+    other workloads, one pass each on their own samples, per-stage."""
     import numpy as np
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import gemm as OG
     from oracle import hadamard as OH
     from oracle import quantizer as OQ
     from paper_2606_07116_amd import inputs
 
-    x = inputs.activations(M, K, seed=seed, **spec)
-    w = inputs.weights(N, K, seed=seed)
-    q_w, sw = OQ.quantize_weights(w)          # offline weight prep: not timed
-    cs = OQ.colsum(q_w, g)
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        y = OH.rotate(x, g).astype(np.float32)
-        q, s, z = OQ.quantize_groups(y, g)
-        acc = OG.int_gemm_groups(q, q_w, g)
-        out = OG.epilogue(acc, s, z, sw, cs)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= 10.0 or reps >= 50:
-            break
-    del out
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    return {"value": round(2.0 * M * N * K * reps / el / 1e12, 4), "unit": "TOPS",
-            "cores": int(threads), "kind": "oracle",
-            "sample": f"full step (rotate fp64, quantize, int GEMM via fp64 BLAS, epilogue) "
-                      f"on M={M},K={K},N={N}, {reps} repetition(s) in {el:.1f} s; BLAS "
-                      f"threads={threads}, elementwise stages single-threaded"}
+    ncpu = len(os.sched_getaffinity(0))
+    with threadpool_limits(limits=ncpu):
+        prepped = []
+        for (name, M, K, N, g, spec, seed, n_cols) in layers:
+            x = inputs.activations(sample_rows, K, seed=seed, **spec)
+            prepped.append((name, x, g) + _oracle_layer_prep(np, inputs, OQ, K, N, g, spec, seed,
+                                                             n_cols))
+        stages = {}
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            for (name, x, g, q_w, sw, cs) in prepped:
+                _oracle_stages(np, OH, OQ, OG, x, g, q_w, sw, cs, stages)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= min_s or reps >= 50:
+                break
+        del prepped
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        ops = sum(2.0 * sample_rows * (nc or N) * K for (_, M, K, N, g, _, _, nc) in layers) * reps
+        desc = ", ".join(f"{n}: K={K}, N={N}" + (f" (first {nc} output channels)" if nc else "")
+                         + f", g={g}" for (n, _, K, N, g, _, _, nc) in layers)
+        out = {"value": round(ops / el / 1e12, 4), "unit": "TOPS", "cores": int(threads),
+               "kind": "oracle",
+               "sample": f"first {sample_rows} of the {layers[0][1]} token rows of each layer "
+                         f"({desc}), whole step {reps} time(s) in {el:.1f} s; rate = sampled GEMM "
+                         "ops / s",
+               "stage_seconds": {k: round(v, 3) for k, v in stages.items()},
+               "cpu_model": _cpu_model(), "host_cpus": ncpu,
+               "threads_note": "BLAS (the integer GEMM via fp64 matmul) uses the threads above; "
+                               "the rotate, quantize and epilogue stages are single-threaded numpy"}
+        if per_config:
+            out["per_config"] = {}
+            for cname, fn in per_config.items():
+                out["per_config"][cname] = fn(np, inputs, OH, OQ, OG)
+    return out
+
+
+def _cpu_layer_config(layers, rows, n_cols=None, unit="TOPS"):
+    """One oracle pass over each layer of a workload on its first ``rows``
+    rows (and first ``n_cols`` output channels when given), per-stage
+    seconds and the rate in the workload's unit."""
+    def run(np, inputs, OH, OQ, OG):
+        t, ops, nbytes = {}, 0.0, 0.0
+        for (name, M, K, N, g, spec, seed) in layers:
+            x = inputs.activations(rows, K, seed=seed, **spec)
+            q_w, sw, cs = _oracle_layer_prep(np, inputs, OQ, K, N, g, spec, seed, n_cols)
+            nc = N if n_cols is None else n_cols
+            _oracle_stages(np, OH, OQ, OG, x, g, q_w, sw, cs, t)
+            ops += 2.0 * rows * nc * K
+            nbytes += gemv_bytes(rows, nc, K, g) + rq_bytes(rows, K, g)
+        el = sum(t.values())
+        r = {"stage_seconds": {k: round(v, 4) for k, v in t.items()},
+             "sample": f"first {rows} rows" + (f", first {n_cols} output channels" if n_cols else "")
+             + " of " + ", ".join(f"{n}: M={M}, K={K}, N={N}, g={g}" for (n, M, K, N, g, _, _) in layers)}
+        if unit == "TOPS":
+            r["TOPS"] = round(ops / el / 1e12, 5)
+        else:
+            r["GBs"] = round(nbytes / el / 1e9, 3)
+        return r
+    return run
+
+
+def _cpu_kv_config(rows, Dh=128):
+    """The oracle's KV quantizer (128-point H3 in fp64, then the quantizer)
+    on ``rows`` cache rows drawn as the KV workload's; per-stage seconds and
+    algorithmic GB/s."""
+    def run(np, inputs, OH, OQ, OG):
+        from oracle import kv as OKV
+        kc = inputs.WORKLOADS["kv_cache"]
+        x = inputs.kv_rows(rows, Dh, seed=kc["seed"], n_outliers=kc["n_outliers"], lo=kc["lo"],
+                           hi=kc["hi"], heads=kc["H"])
+        t0 = time.perf_counter()
+        y = OKV.kv_rotate(x, True).astype(np.float32)
+        t1 = time.perf_counter()
+        OKV.kv_quantize(y)
+        t2 = time.perf_counter()
+        return {"stage_seconds": {"rotate": round(t1 - t0, 4), "quantize": round(t2 - t1, 4)},
+                "GBs": round(rq_bytes(rows, Dh, Dh) / (t2 - t0) / 1e9, 3),
+                "sample": f"{rows} rows [.., 128] of the KV cache recipe"}
+    return run
 
 
 def main():
@@ -446,73 +563,32 @@ def main():
 
     # library launches per step (the spin below covers the host's enqueue time)
     launches_per_step = 10 if wl == "decode_layer" else len(phases)
-    for i in range(args.warmup):
-        for name, fn in phases:
-            check(fn(i), name)
-    torch.cuda.synchronize()
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)]
-    # The GPU first spins (about 50 us per launch to come) while the host
-    # enqueues the whole timed region, so that no kernel waits for its launch
-    # call (a launch from Python takes longer than the shortest kernels here).
-    if hasattr(torch.cuda, "_sleep"):
-        torch.cuda._sleep(100_000 * launches_per_step * args.steps)
-    evs[0].record(stream)
-    for p, (name, fn) in enumerate(phases):
-        for i in range(args.steps):
-            check(fn(args.warmup + i), name)
-        evs[p + 1].record(stream)
-    torch.cuda.synchronize()
-    ms = evs[0].elapsed_time(evs[-1]) / args.steps
-
-    comp = {}
-    for p, (name, fn) in enumerate(phases):
-        us = 1000.0 * evs[p].elapsed_time(evs[p + 1]) / args.steps
-        if name in comp:  # a kernel launched twice per step (K and V): per launch
-            comp[name]["us"] = round((comp[name]["us"] * comp[name]["launches"] + us) /
-                                     (comp[name]["launches"] + 1), 3)
-            comp[name]["launches"] += 1
-        else:
-            comp[name] = {"us": round(us, 3), "launches": 1}
-
-    def ann_rq(name, M, K, g, n=1):
-        b = rq_bytes(M, K, g) * n
-        comp[name]["alg_bytes"] = b
-        comp[name]["GBs"] = round(b / (comp[name]["us"] * 1e-6) / 1e9, 1)
-        comp[name]["frac_hbm"] = round(comp[name]["GBs"] / PEAK_HBM_GBS, 4)
-
-    def ann_mm(name, M, N, K):
-        ops = 2.0 * M * N * K
-        comp[name]["alg_ops"] = ops
-        comp[name]["TOPS"] = round(ops / (comp[name]["us"] * 1e-6) / 1e12, 1)
-        comp[name]["frac_int8_peak"] = round(comp[name]["TOPS"] / PEAK_INT8_TOPS, 4)
+    ms, comp = run_phases(torch, stream, phases, args.steps, args.warmup, check,
+                          launches_per_step)
+    n_dist = max(100, args.steps)
+    if wl != "calibration":
+        add_dist(torch, stream, phases, comp, n_dist, check)
+    gap = event_gap(torch, stream)
 
     # counter-measured HBM bytes are keyed by workload (and group size when
     # --group-size overrides the workload's own)
     tkey = wl if not args.group_size else f"{wl}:g{args.group_size}"
     if wl in ("attn_proj_prefill", "kv_chain"):
-        ann_rq("rotate_quantize", M, K, g)
-        ann_mm("w4a4_gemm", M, N, K)
+        ann_rq(comp["rotate_quantize"], M, K, g)
+        ann_mm(comp["w4a4_gemm"], M, N, K)
         if wl == "kv_chain":
-            ann_rq("kv_quantize", R, Dh, Dh)
+            ann_rq(comp["kv_quantize"], R, Dh, Dh)
         value = work_ops / (ms * 1e-3) / 1e12
         unit = "TOPS"
-        dom = "w4a4_gemm"
-        roof = {"bound": "mfma", "achieved": comp[dom]["TOPS"], "peak": PEAK_INT8_TOPS,
-                "unit": "TOP/s", "frac": comp[dom]["frac_int8_peak"],
-                "traffic": traffic_for(f"w4a4_gemm:{tkey}"), "kernel": dom,
-                "alg_ops_per_launch": comp[dom]["alg_ops"], "avg_launch_us": comp[dom]["us"]}
+        roof = mfma_roof(comp, "w4a4_gemm", traffic_for(f"w4a4_gemm:{tkey}"))
     elif wl == "mlp_prefill":
-        ann_rq("rotate_quantize_up", up["M"], up["K"], up["g"])
-        ann_rq("rotate_quantize_down", dn["M"], dn["K"], dn["g"])
-        ann_mm("w4a4_gemm_upgate", up["M"], 2 * up["N"], up["K"])
-        ann_mm("w4a4_gemm_down", dn["M"], dn["N"], dn["K"])
+        ann_rq(comp["rotate_quantize_up"], up["M"], up["K"], up["g"])
+        ann_rq(comp["rotate_quantize_down"], dn["M"], dn["K"], dn["g"])
+        ann_mm(comp["w4a4_gemm_upgate"], up["M"], 2 * up["N"], up["K"])
+        ann_mm(comp["w4a4_gemm_down"], dn["M"], dn["N"], dn["K"])
         value = work_ops / (ms * 1e-3) / 1e12
         unit = "TOPS"
-        dom = "w4a4_gemm_upgate"
-        roof = {"bound": "mfma", "achieved": comp[dom]["TOPS"], "peak": PEAK_INT8_TOPS,
-                "unit": "TOP/s", "frac": comp[dom]["frac_int8_peak"],
-                "traffic": traffic_for(f"w4a4_gemm:{tkey}"), "kernel": dom,
-                "alg_ops_per_launch": comp[dom]["alg_ops"], "avg_launch_us": comp[dom]["us"]}
+        roof = mfma_roof(comp, "w4a4_gemm_upgate", traffic_for(f"w4a4_gemm:{tkey}"))
     elif wl == "calibration":
         tb = n_seq * L * D * 2
         comp["top1_select"]["alg_bytes"] = tb
@@ -535,42 +611,25 @@ def main():
                 "alg_bytes_per_launch": eb, "avg_launch_us": comp["eigh"]["us"]}
     elif wl == "decode_layer":
         name = "decode_layer"
-        comp[name]["alg_bytes"] = step_bytes
-        comp[name]["GBs"] = round(step_bytes / (comp[name]["us"] * 1e-6) / 1e9, 1)
-        comp[name]["frac_hbm"] = round(comp[name]["GBs"] / PEAK_HBM_GBS, 4)
+        ann_bytes(comp[name], step_bytes)
         comp[name]["tokens_per_s"] = round(M / (comp[name]["us"] * 1e-6), 1)
         value = comp[name]["GBs"]
         unit = "GB/s"
-        roof = {"bound": "hbm", "achieved": comp[name]["GBs"], "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": comp[name]["frac_hbm"], "traffic": None, "kernel": name,
-                "alg_bytes_per_launch": step_bytes, "avg_launch_us": comp[name]["us"]}
+        roof = hbm_roof(comp, name, None)
     elif wl == "kv_decode_attention":
         name = "kv_attention_decode"
-        b_ = attn_bytes(B * H, S, Dh)
-        comp[name]["alg_bytes"] = b_
-        comp[name]["GBs"] = round(b_ / (comp[name]["us"] * 1e-6) / 1e9, 1)
-        comp[name]["frac_hbm"] = round(comp[name]["GBs"] / PEAK_HBM_GBS, 4)
+        ann_bytes(comp[name], attn_bytes(B * H, S, Dh))
         value = comp[name]["GBs"]
         unit = "GB/s"
-        roof = {"bound": "hbm", "achieved": comp[name]["GBs"], "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": comp[name]["frac_hbm"],
-                "traffic": traffic_for(f"kv_attention:{tkey}"), "kernel": name,
-                "alg_bytes_per_launch": b_, "avg_launch_us": comp[name]["us"]}
+        roof = hbm_roof(comp, name, traffic_for(f"kv_attention:{tkey}"))
     else:
-        ann_rq("rotate_quantize_up", Md, up["K"], up["g"])
-        ann_rq("rotate_quantize_down", Md, dn["K"], dn["g"])
+        ann_rq(comp["rotate_quantize_up"], Md, up["K"], up["g"])
+        ann_rq(comp["rotate_quantize_down"], Md, dn["K"], dn["g"])
         for name, c in (("w4a4_gemv_up", up), ("w4a4_gemv_down", dn)):
-            b = gemv_bytes(Md, c["N"], c["K"], c["g"])
-            comp[name]["alg_bytes"] = b
-            comp[name]["GBs"] = round(b / (comp[name]["us"] * 1e-6) / 1e9, 1)
-            comp[name]["frac_hbm"] = round(comp[name]["GBs"] / PEAK_HBM_GBS, 4)
+            ann_bytes(comp[name], gemv_bytes(Md, c["N"], c["K"], c["g"]))
         value = gbytes / (ms * 1e-3) / 1e9
         unit = "GB/s"
-        dom = "w4a4_gemv_up"
-        roof = {"bound": "hbm", "achieved": comp[dom]["GBs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": comp[dom]["frac_hbm"], "traffic": traffic_for(f"w4a4_gemv:{tkey}"),
-                "kernel": dom, "alg_bytes_per_launch": comp[dom]["alg_bytes"],
-                "avg_launch_us": comp[dom]["us"]}
+        roof = hbm_roof(comp, "w4a4_gemv_up", traffic_for(f"w4a4_gemv:{tkey}"))
 
     # measured HBM bytes per launch of the other kernels, where counters exist
     tnames = {"rotate_quantize": "rotate_quantize", "w4a4_gemm": "w4a4_gemm",
@@ -589,11 +648,242 @@ def main():
         "higher_is_better": wl != "calibration", "scaling": "weak", "vs_baseline": None,
         "dtype": "int8",
         "data": "synthetic (seeded Llama-shaped activations with structured outliers; random weights)",
-        "config": config, "roofline": roof, "components": comp,
+        "config": config, "roofline": roof, "components": comp, "event_gap_us": round(gap, 3),
+        "timing": f"us = phase mean over {args.steps} launches with no event between them; "
+                  f"median/p10/p90 over {n_dist} launches with an event after each "
+                  "(cold: buffer sets cycled; warm: one set)",
     }
-    if not args.no_cpu_baseline and wl in ("attn_proj_prefill",):
-        out["cpu_baseline"] = cpu_baseline(M, K, N, g, spec, cfg["seed"])
+    if wl == "mlp_prefill" and not args.no_components and not args.group_size:
+        for sets_ in (su, sd):
+            sets_.sets.clear()
+        torch.cuda.empty_cache()
+        out["configs"] = other_configs(torch, offq, _lib, inputs, stream, sp, check, args, n_dist)
+    if not args.no_cpu_baseline and wl == "mlp_prefill":
+        lay = [("up_gate", up["M"], up["K"], 2 * up["N"], up["g"], spec_u, up["seed"], 8192),
+               ("down", dn["M"], dn["K"], dn["N"], dn["g"], spec_d, dn["seed"], None)]
+        per_config = None
+        if not args.group_size:
+            ap = inputs.WORKLOADS["attn_proj_prefill"]
+            du = inputs.WORKLOADS["decode_up"]
+            dd = inputs.WORKLOADS["decode_down"]
+            sp2 = dict(n_outliers=ap["n_outliers"], lo=ap["lo"], hi=ap["hi"])
+            sp4 = dict(n_outliers=du["n_outliers"], lo=du["lo"], hi=du["hi"])
+            per_config = {
+                "attn_proj_prefill": _cpu_layer_config(
+                    [("proj", ap["M"], ap["K"], ap["N"], ap["g"], sp2, ap["seed"])], 128),
+                "decode_M16": _cpu_layer_config(
+                    [("up", 16, du["K"], du["N"], du["g"], sp4, du["seed"]),
+                     ("down", 16, dd["K"], dd["N"], dd["g"], sp4, dd["seed"])], 16, n_cols=2048,
+                    unit="GBs"),
+                "kv_quantize": _cpu_kv_config(1 << 16),
+            }
+        out["cpu_baseline"] = cpu_baseline(lay, 256, 10.0, per_config)
+    elif not args.no_cpu_baseline and wl == "attn_proj_prefill":
+        out["cpu_baseline"] = cpu_baseline([("proj", M, K, N, g, spec, cfg["seed"], None)], 512, 10.0)
     print(json.dumps(out), flush=True)
+
+
+# ------------------------------------------------------------------ timing
+def run_phases(torch, stream, phases, steps, warmup, check, launches_per_step):
+    """Warm-up, then the K steps phase by phase (one event between phases)."""
+    for i in range(warmup):
+        for name, fn in phases:
+            check(fn(i), name)
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)]
+    # The GPU first spins (about 50 us per launch to come) while the host
+    # enqueues the whole timed region, so that no kernel waits for its launch
+    # call (a launch from Python takes longer than the shortest kernels here).
+    if hasattr(torch.cuda, "_sleep"):
+        torch.cuda._sleep(100_000 * launches_per_step * steps)
+    evs[0].record(stream)
+    for p, (name, fn) in enumerate(phases):
+        for i in range(steps):
+            check(fn(warmup + i), name)
+        evs[p + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = evs[0].elapsed_time(evs[-1]) / steps
+    comp = {}
+    for p, (name, fn) in enumerate(phases):
+        us = 1000.0 * evs[p].elapsed_time(evs[p + 1]) / steps
+        if name in comp:  # a kernel launched twice per step (K and V): per launch
+            c = comp[name]
+            c["us"] = round((c["us"] * c["launches"] + us) / (c["launches"] + 1), 3)
+            c["launches"] += 1
+        else:
+            comp[name] = {"us": round(us, 3), "launches": 1}
+    return ms, comp
+
+
+def launch_times(torch, stream, fn, n, check, name, warm):
+    """n launches with an event after each; per-launch microseconds, sorted."""
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    if hasattr(torch.cuda, "_sleep"):
+        torch.cuda._sleep(100_000 * n)
+    evs[0].record(stream)
+    for i in range(n):
+        check(fn(0 if warm else i), name)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    return sorted(1000.0 * evs[i].elapsed_time(evs[i + 1]) for i in range(n))
+
+
+def _pct(t, q):
+    return round(t[min(len(t) - 1, int(round(q * (len(t) - 1))))], 3)
+
+
+def add_dist(torch, stream, phases, comp, n, check):
+    """Per-launch median, p10 and p90 over n cold launches and the median of
+    n warm launches of every phase (a phase launched twice per step, K and V,
+    is measured on its first launch function)."""
+    seen = set()
+    for name, fn in phases:
+        if name in seen:
+            continue
+        seen.add(name)
+        t = launch_times(torch, stream, fn, n, check, name, warm=False)
+        tw = launch_times(torch, stream, fn, n, check, name, warm=True)
+        comp[name].update({"median_us": _pct(t, 0.5), "p10_us": _pct(t, 0.1),
+                           "p90_us": _pct(t, 0.9), "n_dist": n, "warm_median_us": _pct(tw, 0.5)})
+
+
+def event_gap(torch, stream, n=64):
+    """Median time between two events recorded back to back on the stream."""
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    for e in evs:
+        e.record(stream)
+    torch.cuda.synchronize()
+    t = sorted(1000.0 * evs[i].elapsed_time(evs[i + 1]) for i in range(n))
+    return t[n // 2]
+
+
+def ann_bytes(c, b):
+    """Algorithmic bytes per launch and the rates of the mean and median."""
+    c["alg_bytes"] = b
+    c["GBs"] = round(b / (c["us"] * 1e-6) / 1e9, 1)
+    c["frac_hbm"] = round(c["GBs"] / PEAK_HBM_GBS, 4)
+    if "median_us" in c:
+        c["GBs_median"] = round(b / (c["median_us"] * 1e-6) / 1e9, 1)
+
+
+def ann_rq(c, M, K, g, n=1):
+    ann_bytes(c, rq_bytes(M, K, g) * n)
+
+
+def ann_mm(c, M, N, K):
+    ops = 2.0 * M * N * K
+    c["alg_ops"] = ops
+    c["TOPS"] = round(ops / (c["us"] * 1e-6) / 1e12, 1)
+    c["frac_int8_peak"] = round(c["TOPS"] / PEAK_INT8_TOPS, 4)
+    if "median_us" in c:
+        c["TOPS_median"] = round(ops / (c["median_us"] * 1e-6) / 1e12, 1)
+
+
+def mfma_roof(comp, dom, traffic):
+    c = comp[dom]
+    return {"bound": "mfma", "achieved": c["TOPS"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+            "frac": c["frac_int8_peak"], "traffic": traffic, "kernel": dom,
+            "alg_ops_per_launch": c["alg_ops"], "avg_launch_us": c["us"]}
+
+
+def hbm_roof(comp, dom, traffic):
+    c = comp[dom]
+    return {"bound": "hbm", "achieved": c["GBs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": c["frac_hbm"], "traffic": traffic, "kernel": dom,
+            "alg_bytes_per_launch": c["alg_bytes"], "avg_launch_us": c["us"]}
+
+
+# ------------------------------------------------- the other workloads' kernels
+def other_configs(torch, offq, _lib, inputs, stream, sp, check, args, n_dist):
+    """Every other workload's kernels, timed like the main step (phase mean
+    over max(20, K) launches, then the per-launch distributions): the
+    attention-projection prefill layer, the decode GEMVs at M = 1, 4, 16 and
+    the KV4 cache quantize with the 8192-row projection."""
+    steps = max(20, args.steps)
+    W = inputs.WORKLOADS
+    res = {}
+
+    def layer(name_rq, name_mm, cfg, M, N, seed_off=0):
+        spec = dict(n_outliers=cfg["n_outliers"], lo=cfg["lo"], hi=cfg["hi"])
+        K, g = cfg["K"], cfg["g"]
+        per = M * K * 2 + N * K // 2 + M * K // 2 + M * N * 2
+        sets = Sets(lambda i: make_layer_set(offq, inputs, torch, M, K, N, g,
+                                             cfg["seed"] + seed_off + 100 * i, spec), per)
+        return sets, [(name_rq, lambda i, s_=sets: run_rq(_lib, s_[i], sp)),
+                      (name_mm, lambda i, s_=sets: run_gemm(_lib, s_[i], sp))]
+
+    def measure(phases):
+        _, comp = run_phases(torch, stream, phases, steps, 3, check, len(phases))
+        add_dist(torch, stream, phases, comp, n_dist, check)
+        return comp
+
+    ap = W["attn_proj_prefill"]
+    sets, ph = layer("rotate_quantize", "w4a4_gemm", ap, ap["M"], ap["N"])
+    comp = measure(ph)
+    ann_rq(comp["rotate_quantize"], ap["M"], ap["K"], ap["g"])
+    ann_mm(comp["w4a4_gemm"], ap["M"], ap["N"], ap["K"])
+    for k, t in (("rotate_quantize", "rotate_quantize"), ("w4a4_gemm", "w4a4_gemm")):
+        tb = traffic_for(f"{t}:attn_proj_prefill")
+        if tb is not None:
+            comp[k]["traffic_bytes"] = tb
+    res["attn_proj_prefill"] = {"shape": [ap["M"], ap["K"], ap["N"], ap["g"]], "kernels": comp}
+    del sets, ph
+    torch.cuda.empty_cache()
+
+    du, dd = W["decode_up"], W["decode_down"]
+    for Md in (16, 4, 1):
+        su, pu = layer("rotate_quantize_up", "w4a4_gemv_up", du, Md, du["N"], Md)
+        sd, pd = layer("rotate_quantize_down", "w4a4_gemv_down", dd, Md, dd["N"], Md)
+        comp = measure(pu + pd)
+        ann_rq(comp["rotate_quantize_up"], Md, du["K"], du["g"])
+        ann_rq(comp["rotate_quantize_down"], Md, dd["K"], dd["g"])
+        ann_bytes(comp["w4a4_gemv_up"], gemv_bytes(Md, du["N"], du["K"], du["g"]))
+        ann_bytes(comp["w4a4_gemv_down"], gemv_bytes(Md, dd["N"], dd["K"], dd["g"]))
+        if Md == 16:
+            for k, t in (("w4a4_gemv_up", "w4a4_gemv"), ("w4a4_gemv_down", "w4a4_gemv_down")):
+                tb = traffic_for(f"{t}:decode")
+                if tb is not None:
+                    comp[k]["traffic_bytes"] = tb
+        res[f"decode_M{Md}"] = {"up": [Md, du["K"], du["N"], du["g"]],
+                                "down": [Md, dd["K"], dd["N"], dd["g"]], "kernels": comp}
+        del su, sd, pu, pd
+        torch.cuda.empty_cache()
+
+    kc = W["kv_cache"]
+    B, H, S, Dh = kc["B"], kc["H"], kc["S"], kc["Dh"]
+    R = B * H * S
+    kv = [inputs.kv_cache_device(B, H, S, Dh, seed=kc["seed"] + j, device="cuda",
+                                 n_outliers=kc["n_outliers"], lo=kc["lo"], hi=kc["hi"])
+          for j in range(2)]
+    kvo = [dict(codes=torch.empty((R, Dh // 2), dtype=torch.uint8, device="cuda"),
+                scale=torch.empty((R,), dtype=torch.float16, device="cuda"),
+                zero=torch.empty((R,), dtype=torch.int16, device="cuda")) for _ in range(2)]
+
+    def kvq(i):  # K and V tensors alternate (2 GiB each, far beyond the cache)
+        j = i % 2
+        return _lib.offq_kv_quantize_raw(kv[j].data_ptr(), R, Dh, Dh, 1, kvo[j]["codes"].data_ptr(),
+                                         kvo[j]["scale"].data_ptr(), kvo[j]["zero"].data_ptr(),
+                                         None, sp)
+    pc = W["kv_chain_proj"]
+    sets, ph = layer("rotate_quantize", "w4a4_gemm", pc, pc["M"], pc["N"])
+    comp = measure([("kv_quantize", kvq)] + ph)
+    ann_rq(comp["kv_quantize"], R, Dh, Dh)
+    ann_rq(comp["rotate_quantize"], pc["M"], pc["K"], pc["g"])
+    ann_mm(comp["w4a4_gemm"], pc["M"], pc["N"], pc["K"])
+    for k, t in (("kv_quantize", "kv_quantize"), ("rotate_quantize", "rotate_quantize"),
+                 ("w4a4_gemm", "w4a4_gemm")):
+        tb = traffic_for(f"{t}:kv_chain")
+        if tb is not None:
+            comp[k]["traffic_bytes"] = tb
+    res["kv_chain"] = {"kv_shape": [B, H, S, Dh], "proj": [pc["M"], pc["K"], pc["N"], pc["g"]],
+                       "kernels": comp,
+                       "note": "kv_quantize: one [8, 32, 32768, 128] tensor per launch (K and V "
+                               "alternate); the step quantizes both"}
+    del sets, ph, kv, kvo
+    torch.cuda.empty_cache()
+    return res
 
 
 if __name__ == "__main__":
