@@ -244,6 +244,32 @@ offq_status_t offq_kv_attention_decode_quantize(const uint16_t* q, const uint8_t
                                       uint8_t* out_codes, uint16_t* out_scale, int16_t* out_zero,
                                       void* workspace, int64_t workspace_bytes, void* stream);
 
+/*
+ * offq_kv_attention_decode_noalloc -- offq_kv_attention_decode_gqa for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops that must not call hipMalloc): the same kernels and results,
+ * with the per-chunk records kept in a static device array of the library
+ * instead of a caller-owned workspace.  The call itself allocates nothing;
+ * the caller passes every input and the output.
+ *
+ *   Arguments as for offq_kv_attention_decode_gqa, without workspace.
+ *   Limit: the records need offq_kv_attention_workspace_bytes(B, Hq, seq_len)
+ *   bytes, at most 16 MiB (B * Hq * ceil(seq_len / 512) <= 32263, e.g.
+ *   B = 8, Hq = 32, seq_len = 32768 uses half); larger sizes return
+ *   OFFQ_ERR_UNSUPPORTED before anything is enqueued.
+ *   Each device holds its own 16 MiB array from the first call until the
+ *   process ends.  All calls on one device share that array: calls that can
+ *   overlap on one device (different streams, or host threads without
+ *   ordering) race and must be serialised by the caller.
+ */
+offq_status_t offq_kv_attention_decode_noalloc(const uint16_t* q, const uint8_t* k_codes,
+                                               const uint16_t* k_scale, const int16_t* k_zero,
+                                               const uint8_t* v_codes, const uint16_t* v_scale,
+                                               const int16_t* v_zero, int64_t B, int64_t Hq,
+                                               int64_t Hkv, int64_t s_cap, int64_t seq_len,
+                                               int32_t head_dim, float sm_scale,
+                                               int32_t v_hadamard, uint16_t* out, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Decoder-layer steps around the quantized linear layers (one decode step,
  * one new token per sequence), following the pipeline of sec. 3.3 / Fig. 2.

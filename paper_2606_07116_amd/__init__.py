@@ -40,6 +40,7 @@ _EXPORTS = frozenset((
     "offq_swiglu",
     "offq_kv_attention_decode",
     "offq_kv_attention_decode_quantize",
+    "offq_kv_attention_decode_noalloc",
     "offq_kv_attention_workspace_bytes",
     "offq_kv_quantize",
     "offq_pack_weights",

@@ -32,6 +32,7 @@ EXPORTED = (
     "offq_kv_attention_workspace_bytes",
     "offq_kv_attention_decode_gqa",
     "offq_kv_attention_decode_quantize",
+    "offq_kv_attention_decode_noalloc",
     "offq_add_rmsnorm",
     "offq_swiglu",
     "offq_rope_kv_append",
@@ -107,6 +108,9 @@ def _load():
         "offq_add_rmsnorm_quantize": (ctypes.c_int, [vp, i64, vp, i64, i64, i64, ctypes.c_float,
                                                      i32, vp, i64, vp, vp, vp, vp, i64, vp]),
         "offq_swiglu_rotate_quantize": (ctypes.c_int, [vp, i64, i64, i64, vp, vp, vp, vp, vp]),
+        "offq_kv_attention_decode_noalloc": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64,
+                                                            i64, i64, i32, ctypes.c_float, i32, vp,
+                                                            vp]),
         "offq_top1_workspace_bytes": (i64, [i64, i64]),
         "offq_top1_select": (ctypes.c_int, [vp, i64, i64, i64, i64, i64, vp, vp, i64, vp, i64, vp]),
         "offq_channel_absmax": (ctypes.c_int, [vp, i64, i64, i64, vp, vp]),
@@ -192,6 +196,14 @@ def offq_kv_attention_decode_quantize_raw(q, k_codes, k_scale, k_zero, v_codes, 
                                                  v_zero, B, Hq, Hkv, s_cap, seq_len, head_dim,
                                                  sm_scale, v_hadamard, out, out_codes, out_scale,
                                                  out_zero, workspace, workspace_bytes, stream)
+
+
+def offq_kv_attention_decode_noalloc_raw(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B,
+                                         Hq, Hkv, s_cap, seq_len, head_dim, sm_scale, v_hadamard,
+                                         out, stream):
+    return lib.offq_kv_attention_decode_noalloc(q, k_codes, k_scale, k_zero, v_codes, v_scale,
+                                                v_zero, B, Hq, Hkv, s_cap, seq_len, head_dim,
+                                                sm_scale, v_hadamard, out, stream)
 
 
 def offq_add_rmsnorm_raw(x, ldx, res, ldr, M, D, eps, h_out, ldh, y_out, ldy, stream):
@@ -388,6 +400,24 @@ def offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_ze
                                             int(bool(v_hadamard)), _ptr(out), _ptr(workspace),
                                             workspace.numel() * 4, _stream()),
            "offq_kv_attention_decode")
+    return out
+
+
+def offq_kv_attention_decode_noalloc(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero,
+                                     seq_len, out, sm_scale=None, v_hadamard=False):
+    """offq_kv_attention_decode without a workspace (the library's static
+    scratch holds the chunk records; nothing is allocated, so the caller
+    passes out, bf16 [B, H, 128] contiguous).  Returns out."""
+    torch = _torch()
+    B, H, Dh, Hkv, s_cap, sm_scale = _attention_operands(q, k_codes, k_scale, k_zero, v_codes,
+                                                         v_scale, v_zero, sm_scale)
+    _need(out, torch.bfloat16, "out", 3)
+    if not out.is_contiguous() or out.shape != (B, H, Dh):
+        raise ValueError("out must be a contiguous [B, H, head_dim] tensor")
+    _check(lib.offq_kv_attention_decode_noalloc(
+        _ptr(q), _ptr(k_codes), _ptr(k_scale), _ptr(k_zero), _ptr(v_codes), _ptr(v_scale),
+        _ptr(v_zero), B, H, Hkv, s_cap, int(seq_len), Dh, float(sm_scale), int(bool(v_hadamard)),
+        _ptr(out), _stream()), "offq_kv_attention_decode_noalloc")
     return out
 
 

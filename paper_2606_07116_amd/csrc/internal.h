@@ -59,6 +59,12 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
                                       uint16_t* qscale, int16_t* qzero, float* workspace,
                                       hipStream_t stream);
 
+// The same step's chunk records in a static device array (16 MiB per device,
+// kept until the process ends) for callers that cannot allocate:
+// kv_attention_scratch gives the current device's address of that array.
+constexpr int64_t kKvScratchBytes = int64_t(16) << 20;
+hipError_t kv_attention_scratch(float** ptr);
+
 // decoder-layer kernels (layer_ops.hip)
 hipError_t launch_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr,
                               int64_t M, int64_t D, float eps, uint16_t* h_out, int64_t ldh,

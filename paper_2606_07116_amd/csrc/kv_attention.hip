@@ -44,6 +44,8 @@
 //   go to the workspace.
 // * Pass 2: one workgroup per (b, h) merges the chunks (rescaled by
 //   2^(m_i - m)), divides by the sum, optionally rotates back, stores bf16.
+#include <mutex>
+
 #include "common.h"
 #include "internal.h"
 
@@ -786,6 +788,40 @@ hipError_t launch_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes,
     combine(nchunk);
   }
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// The same step for callers that cannot allocate: the chunk records live in a
+// file-scope device array instead of a caller-owned workspace.  Host code
+// never passes the array's name to a kernel (on the host it only names the
+// symbol); it passes the device address hipGetSymbolAddress returns, looked
+// up once per device with that device current.  Every call on a device shares
+// that device's array: calls that overlap on one device race.  Nothing in it
+// needs to start at zero: pass 1 writes every record that pass 2 reads.
+namespace {
+
+static __device__ __align__(256) float scratch[kKvScratchBytes / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+}  // namespace
+
+hipError_t kv_attention_scratch(float** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace offq

@@ -264,6 +264,35 @@ offq_status_t offq_kv_attention_decode(const uint16_t* q, const uint8_t* k_codes
                                       workspace, workspace_bytes, stream);
 }
 
+offq_status_t offq_kv_attention_decode_noalloc(const uint16_t* q, const uint8_t* k_codes,
+                                               const uint16_t* k_scale, const int16_t* k_zero,
+                                               const uint8_t* v_codes, const uint16_t* v_scale,
+                                               const int16_t* v_zero, int64_t B, int64_t Hq,
+                                               int64_t Hkv, int64_t s_cap, int64_t seq_len,
+                                               int32_t head_dim, float sm_scale,
+                                               int32_t v_hadamard, uint16_t* out, void* stream) {
+  if (!out) return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (B > 0 && Hq > 0 && seq_len > 0) {
+    const int64_t need = offq_kv_attention_workspace_bytes(B, Hq, seq_len);
+    if (need > offq::kKvScratchBytes)
+      return fail(OFFQ_ERR_UNSUPPORTED,
+                  "B Hq ceil(seq_len / 512) = %lld chunk records need %lld bytes; the static "
+                  "scratch holds %lld",
+                  (long long)(need / (130 * 4)), (long long)need,
+                  (long long)offq::kKvScratchBytes);
+  }
+  // the other checks (sizes, pointers, device) are the plain call's, with the
+  // scratch standing in for the workspace
+  if (offq_status_t st = check_device()) return st;
+  float* ws = nullptr;
+  const hipError_t e = offq::kv_attention_scratch(&ws);
+  if (e != hipSuccess)
+    return fail(OFFQ_ERR_HIP, "static scratch address: %s", hipGetErrorString(e));
+  return kv_attention_checked(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B, Hq, Hkv,
+                              s_cap, seq_len, head_dim, sm_scale, v_hadamard, out, nullptr,
+                              nullptr, nullptr, ws, offq::kKvScratchBytes, stream);
+}
+
 offq_status_t offq_add_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr, int64_t M,
                      int64_t D, float eps, uint16_t* h_out, int64_t ldh, uint16_t* y_out,
                      int64_t ldy, void* stream) {
