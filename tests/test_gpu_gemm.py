@@ -55,6 +55,20 @@ def test_wide_tile_gemm_accumulators(M, N, K):
     _layer(M, N, K, K, seed=M + N)
 
 
+@pytest.mark.parametrize("M,N,K,g", [
+    (4096, 8192, 1024, 1024), (4000, 8104, 512, 512),      # one group: 512 tiles of 256 x 256
+    (4000, 8100, 512, 512),                                # ragged in M and N, N not a multiple of 8
+    (4096, 4096, 2048, 256), (4001, 4000, 1024, 512),      # groups: 512 tiles of 256 x 128
+    (4096, 4100, 3584, 512), (3900, 4096, 8192, 2048),     # odd group count; 16 stages per group
+])
+def test_large_gemm_shapes(M, N, K, g):
+    """Prefill-sized grids (at least 512 tiles, several tiles per CU): every
+    accumulator bit-exact and the output within the bar, on whole and ragged
+    tile grids, with one group per row, 2 to 8 groups, an odd number of groups
+    and long groups."""
+    _layer(M, N, K, g, seed=M + N + g)
+
+
 def test_out_must_cover_the_output():
     """The GEMM writes M x N values at the output's row stride: a short or a
     transposed output is refused before any launch."""
