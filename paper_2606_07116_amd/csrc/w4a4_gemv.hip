@@ -33,6 +33,8 @@ namespace {
 
 using namespace gemm;
 
+typedef unsigned int p_u32x2 __attribute__((ext_vector_type(2)));
+
 constexpr int KSTEP = 128;  // k per step (64 packed bytes per row)
 constexpr int GMAX = 256;   // groups whose parameters fit in LDS
 
@@ -68,6 +70,7 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
   float* const sS = gpar;                // [G][16]
   float* const sSZ = gpar + G * 16;      // [G][16]
   float* const sCS = gpar + G * 32;      // [G][16 T]
+  float* const sSW = gpar + G * (32 + 16 * T);  // [16 T] weight scales of the tile
 
 
   // rows past N (weights) and past M (tokens) read as zero
@@ -183,6 +186,9 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
   }
   for (int i = tid + PRE * NT; i < G * 16; i += NT) par_s(i, sS[i], sSZ[i]);
   for (int i = tid + PRE * NT; i < G * 16 * T; i += NT) sCS[i] = par_c(i);
+  // the tile's weight scales, for the end (a load there would add one memory
+  // latency after the last step)
+  for (int i = tid; i < 16 * T; i += NT) sSW[i] = n0 + i < N ? fp16_bits_to_f32(w_scale[n0 + i]) : 0.0f;
   __syncthreads();
   int bt = 0;
   for (; bt + 2 <= nb; bt += 2) {
@@ -195,24 +201,36 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
   if constexpr (DBG) return;
 
   // ---- sum the P parts of K and store ---------------------------------------
+  // Wave w finishes row tiles w, w + P, ...: four consecutive channels per
+  // lane and tile, one 8-byte store where the row allows it.
 #pragma unroll
   for (int t = 0; t < T; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) red[wave][lane][t * 4 + i] = F[t][i];
   __syncthreads();
-  if (wave == 0 && r16 < M) {
+  const bool vec = (ldy & 3) == 0 && (reinterpret_cast<uintptr_t>(Y) & 7) == 0;
 #pragma unroll
-    for (int t = 0; t < T; ++t)
+  for (int t = 0; t < T; ++t) {
+    if (t % P != wave || r16 >= M) continue;
+    const int c = 16 * t + 4 * kb;
+    const int n = n0 + c;
+    float f[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int n = n0 + 16 * t + 4 * kb + i;
-        if (n < N) {
-          float f = 0.0f;
+    for (int i = 0; i < 4; ++i) {
+      f[i] = 0.0f;
 #pragma unroll
-          for (int w = 0; w < P; ++w) f += red[w][lane][t * 4 + i];
-          Y[(int64_t)r16 * ldy + n] = f32_to_bf16_rne(fp16_bits_to_f32(w_scale[n]) * f);
-        }
-      }
+      for (int w = 0; w < P; ++w) f[i] += red[w][lane][t * 4 + i];
+      f[i] *= sSW[c + i];
+    }
+    uint16_t* const yp = Y + (int64_t)r16 * ldy + n;
+    if (vec && n + 3 < N) {
+      const p_u32x2 v = {bf16x2_rne(f[0], f[1]), bf16x2_rne(f[2], f[3])};
+      *reinterpret_cast<p_u32x2*>(yp) = v;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (n + i < N) yp[i] = f32_to_bf16_rne(f[i]);
+    }
   }
 }
 
@@ -254,7 +272,7 @@ bool gemv_mfma_supported(int64_t M, int64_t N, int64_t K, int log2g) {
   gemv_shape(N, K, T, P, B);
   const int64_t batch = (int64_t)P * KSTEP * B;
   // group parameters (dynamic) + the partial sums of the P waves (static)
-  const int64_t lds = (K >> log2g) * (32 + 16 * T) * 4 + (int64_t)P * 64 * 4 * T * 4;
+  const int64_t lds = ((K >> log2g) * (32 + 16 * T) + 16 * T) * 4 + (int64_t)P * 64 * 4 * T * 4;
   return M <= 16 && log2g >= 7 && K % batch == 0 && (K >> log2g) <= GMAX &&
          lds <= 160 * 1024 &&
          32 * (K / 2) < (int64_t(1) << 31) && M * (K / 2) < (int64_t(1) << 31);
@@ -267,7 +285,7 @@ hipError_t launch_gv(const uint8_t* a_codes, const uint16_t* a_scale, const int1
                      int32_t* acc_debug, hipStream_t stream) {
   const int rows = 16 * T;
   const dim3 grid((unsigned)((N + rows - 1) / rows)), block(64 * P);
-  const size_t lds = (size_t)(K >> log2g) * (32 + rows) * sizeof(float);
+  const size_t lds = ((size_t)(K >> log2g) * (32 + rows) + rows) * sizeof(float);
   // A debug request runs an accumulator-only pass (partial sums added
   // atomically into the zeroed buffer), then the regular kernel.
   if (acc_debug) {
