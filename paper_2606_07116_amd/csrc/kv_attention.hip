@@ -350,6 +350,14 @@ constexpr int CHG = 512;        // positions per grouped-head workgroup
 constexpr int GROWS = CHG / WAVES;
 constexpr int GNIT = GROWS / 32;
 
+// Workgroup barrier for LDS traffic only: global loads still in flight stay
+// in flight (a full barrier would first wait for them).
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 template <int G>
 struct GqaSmem {
   float qf[G][DH];
@@ -499,11 +507,22 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
   }
 
   // ---- value codes: lane (word dg, position pair pg) -------------------------
+  // All of the wave's value words are requested here, into the registers the
+  // key codes held: their latency runs under the softmax below instead of
+  // after it.  Rows past the chunk's end read the last row (their weights
+  // are zero).
   const int dg = lane & 15, pg = lane >> 4;
   const uint32_t* vrow = reinterpret_cast<const uint32_t*>(vc + row0 * (DH / 2)) + dg;
   constexpr int VIT = GROWS / 8;  // steps of 8 positions (4 pairs) per wave
-  constexpr int BT = 8;           // steps per batch of loads
-  __syncthreads();
+  uint32_t va[VIT], vb[VIT];
+#pragma unroll
+  for (int t = 0; t < VIT; ++t) {
+    const int ra = wave * GROWS + t * 8 + 2 * pg;
+    const int rA = FULL ? ra : min(ra, n - 1), rB = FULL ? ra + 1 : min(ra + 1, n - 1);
+    va[t] = vrow[(int64_t)rA * (DH / 8)];
+    vb[t] = vrow[(int64_t)rB * (DH / 8)];
+  }
+  lds_sync();
 
   // ---- weights: fp16 pairs per (position pair, query) ------------------------
   float m[G];
@@ -537,7 +556,7 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
       S.red[2][gq][wave] = z;
     }
   }
-  __syncthreads();
+  lds_sync();
 
   // ---- values ---------------------------------------------------------------
   float acc[G][8];
@@ -545,21 +564,10 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
   for (int gq = 0; gq < G; ++gq)
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[gq][k] = 0.0f;
-  const int vact = FULL ? VIT : min(VIT, max(0, (n - wave * GROWS + 7) / 8));
-#pragma unroll 1
-  for (int t0 = 0; t0 < VIT; t0 += BT) {
-    if (!FULL && t0 >= vact) break;
-    uint32_t va[BT], vb[BT];
+  {
 #pragma unroll
-    for (int t = 0; t < BT; ++t) {
-      const int ra = wave * GROWS + (t0 + t) * 8 + 2 * pg;
-      const int rA = FULL ? ra : min(ra, n - 1), rB = FULL ? ra + 1 : min(ra + 1, n - 1);
-      va[t] = vrow[(int64_t)rA * (DH / 8)];
-      vb[t] = vrow[(int64_t)rB * (DH / 8)];
-    }
-#pragma unroll
-    for (int t = 0; t < BT; ++t) {
-      const int pair = (wave * GROWS + (t0 + t) * 8) / 2 + pg;
+    for (int t = 0; t < VIT; ++t) {
+      const int pair = (wave * GROWS + t * 8) / 2 + pg;
       const uint32_t x0 = __builtin_amdgcn_perm(vb[t], va[t], 0x05040100u);
       const uint32_t x1 = __builtin_amdgcn_perm(vb[t], va[t], 0x07060302u);
       const uint32_t x08 = x0 >> 8, x18 = x1 >> 8;
