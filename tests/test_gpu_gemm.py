@@ -114,19 +114,27 @@ def test_raw_layout_and_spikes():
     _layer(150, 192, 1024, 1024, seed=5, layout="raw", n_out=6)
 
 
-def test_output_row_stride():
-    M, N, K, g = 140, 72, 512, 256
+@pytest.mark.parametrize("M,N,ld,off", [
+    (140, 72, 100, 10),   # GEMM
+    (16, 72, 100, 10),    # decode GEMV, output start not 8-byte aligned
+    (16, 70, 101, 3),     # GEMV: odd row stride, N not a multiple of 4
+    (5, 66, 99, 1),
+])
+def test_output_row_stride(M, N, ld, off):
+    """The output is a view inside a larger matrix: the M x N values land at
+    its row stride and offset, nothing around them is written."""
+    K, g = 512, 256
     x = inputs.activations(M, K, seed=3, n_outliers=2, lo=50, hi=60, layout="concentrated", g=g)
     w = inputs.weights(N, K, seed=3)
     (q, s, z), (codes, scale, zero) = P.rotate_quantize_and_check(x, g, True)
     q_w, sw, cs, packed = P.oracle_weights(w, g)
     wc, ws, wcs = P.upload_weights(packed, sw, cs)
-    big = torch.full((M, 100), 7.0, dtype=torch.bfloat16, device=P.DEV)
-    offq.offq_w4a4_gemm(codes, scale, zero, wc, ws, wcs, g, out=big[:, 10:10 + N])
+    big = torch.full((M, ld), 7.0, dtype=torch.bfloat16, device=P.DEV)
+    offq.offq_w4a4_gemm(codes, scale, zero, wc, ws, wcs, g, out=big[:, off:off + N])
     torch.cuda.synchronize()
     yb = P.host(big.float())
-    assert np.all(yb[:, :10] == 7.0) and np.all(yb[:, 10 + N:] == 7.0)
-    P.check_output(yb[:, 10:10 + N], OG.int_gemm_groups(q, q_w, g), s, z, sw, cs)
+    assert np.all(yb[:, :off] == 7.0) and np.all(yb[:, off + N:] == 7.0)
+    P.check_output(yb[:, off:off + N], OG.int_gemm_groups(q, q_w, g), s, z, sw, cs)
 
 
 def test_extreme_codes_and_zero_points():
