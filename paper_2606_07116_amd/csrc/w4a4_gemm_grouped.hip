@@ -22,7 +22,10 @@
 //   is unpacked in registers by each of the two waves that read it.
 // * Stages of 128 k go global memory -> registers (two or four stages ahead)
 //   -> an LDS ring of three or four slots; one LDS-only barrier per stage.
-//   16-byte chunks are XOR-swizzled by row to spread the LDS banks.
+//   16-byte chunks are XOR-swizzled by row to spread the LDS banks.  For
+//   FM = 2 the packed parts of all slots form one LDS region and the
+//   unpacked parts another, each addressed from one register per lane
+//   pattern with immediate offsets.
 // * Activation codes (0..15) feed the signed i8 MFMA unchanged; weight nibbles
 //   are widened to 16 q (high nibble masked, low nibble shifted), so every
 //   accumulator holds 16 acc exactly.  Both operands split each 16-byte chunk
@@ -128,6 +131,24 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   const int G = K >> log2g;
   const int spg = 1 << (log2g - 7);  // stages per group
 
+  // LDS addressing.  FM = 2: the packed parts of all ring slots form one
+  // region and the unpacked parts another (each at most 64 KB), and every
+  // lane pattern (row, swizzled chunk) has one element index, region start
+  // included, computed once and hidden from the optimiser: slot and fragment
+  // offsets then stay within the 16-bit immediate of ds_read / ds_write,
+  // and the loop holds one address register per pattern.  (Folded into
+  // per-slot addresses, slots beyond 64 KB each took a register of their
+  // own.)  FM = 4: slot s holds its packed then its unpacked part.
+  constexpr bool SPLIT = FM == 2;
+  constexpr int PBASE = 0, XBASE = SPLIT ? C::NBUF * C::P_SLOTS : C::P_SLOTS;
+  constexpr int PSTEP = SPLIT ? C::P_SLOTS : C::STAGE_SLOTS;  // slot stride, packed part
+  constexpr int XSTEP = SPLIT ? C::X_SLOTS : C::STAGE_SLOTS;  // slot stride, unpacked part
+  static_assert(!SPLIT || (C::NBUF * C::P_SLOTS * 16 <= 65536 && C::NBUF * C::X_SLOTS * 16 <= 65536),
+                "each region within one 16-bit LDS offset");
+  auto opaque = [](int v) __attribute__((always_inline)) {
+    asm volatile("" : "+v"(v));
+    return v;
+  };
   // ---- global -> registers -> LDS staging -----------------------------------
   // Chunk s = tid + 512 i of an operand's stage is row s / 4, packed chunk
   // s % 4 (16 bytes = 32 k); rows past M (N) read as zero.
@@ -159,18 +180,24 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     for (int i = 0; i < C::X_LD; ++i)
       rg[C::P_LD + i] = __builtin_amdgcn_raw_buffer_load_b128(xr, voff + i * vstep, soff, 0);
   };
+  // element index of this thread's chunk in slot 0 (row crow + 128 i adds
+  // 512 i packed / 1024 i unpacked slots: the swizzles repeat every 128 rows)
+  const int ps_idx = SPLIT ? opaque(PBASE + pslot(crow, cch)) : 0;
+  const int xs_idx0 = SPLIT ? opaque(XBASE + xslot(crow, 2 * cch)) : 0;
+  const int xs_idx1 = SPLIT ? opaque(XBASE + xslot(crow, 2 * cch + 1)) : 0;
   auto lstore_p = [&](int slot, const v4i (&rg)[NLD]) __attribute__((always_inline)) {
-    uint4* P = ring + slot * C::STAGE_SLOTS;
 #pragma unroll
-    for (int i = 0; i < C::P_LD; ++i)
-      P[pslot(crow + 128 * i, cch)] = __builtin_bit_cast(uint4, rg[i]);
+    for (int i = 0; i < C::P_LD; ++i) {
+      if constexpr (SPLIT)
+        ring[ps_idx + slot * PSTEP + 512 * i] = __builtin_bit_cast(uint4, rg[i]);
+      else
+        ring[slot * PSTEP + pslot(crow + 128 * i, cch)] = __builtin_bit_cast(uint4, rg[i]);
+    }
   };
   auto lstore_x = [&](int slot, const v4i (&rg)[NLD]) __attribute__((always_inline)) {
-    uint4* X = ring + slot * C::STAGE_SLOTS + C::P_SLOTS;
 #pragma unroll
     for (int i = 0; i < C::X_LD; ++i) {
       const uint4 d = __builtin_bit_cast(uint4, rg[C::P_LD + i]);
-      const int r = crow + 128 * i;
       v4i lo, hi;
       if constexpr (XW) {
         lo = wgt_lo16(d);
@@ -179,8 +206,14 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
         lo = act_lo(d);
         hi = act_hi(d);
       }
-      X[xslot(r, 2 * cch)] = __builtin_bit_cast(uint4, lo);
-      X[xslot(r, 2 * cch + 1)] = __builtin_bit_cast(uint4, hi);
+      if constexpr (SPLIT) {
+        ring[xs_idx0 + slot * XSTEP + 1024 * i] = __builtin_bit_cast(uint4, lo);
+        ring[xs_idx1 + slot * XSTEP + 1024 * i] = __builtin_bit_cast(uint4, hi);
+      } else {
+        uint4* X = ring + slot * XSTEP + XBASE;
+        X[xslot(crow + 128 * i, 2 * cch)] = __builtin_bit_cast(uint4, lo);
+        X[xslot(crow + 128 * i, 2 * cch + 1)] = __builtin_bit_cast(uint4, hi);
+      }
     }
   };
   auto lstore = [&](int slot, const v4i (&rg)[NLD]) __attribute__((always_inline)) {
@@ -201,8 +234,13 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
       0x00020000);
   const __amdgpu_buffer_rsrc_t crsrc = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(w_colsum + tn), 0, STREAM ? (int)(((int64_t)G * N - tn) * 4) : 0, 0x00020000);
+  // Waves 0-3 carry the row parameters, waves 4-5 the column sums (tests on
+  // the wave index: scalar branches).  A column past N reads its neighbour's
+  // sum in the same buffer (or 0 past its end); it only reaches outputs past
+  // N, which are never stored.
+  static_assert(C::BM % 64 == 0 && C::BN % 64 == 0, "whole waves per parameter kind");
   const int gt_c = tid - C::BM;  // column of a colsum thread
-  const bool g_row = tid < C::BM, g_col = gt_c >= 0 && gt_c < C::BN && tn + gt_c < N;
+  const bool g_row = wave < C::BM / 64, g_col = !g_row && wave < (C::BM + C::BN) / 64;
   auto gload_g = [&](int st, uint32_t (&gq)[2]) __attribute__((always_inline)) {
     if constexpr (STREAM) {
       const int b = min(st, nst - 1) >> lgs;
@@ -236,15 +274,27 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   constexpr int NXF = XW ? 2 : FM;  // unpacked fragments per wave
   const int prow0 = (XW ? wm * C::WROWS : wn * 64) + fr;
   const int xrow0 = (XW ? wn * 64 : wm * C::WROWS) + fr;
-  auto pread = [&](int slot, int jj, uint4 (&pp)[NPF]) __attribute__((always_inline)) {
-    const uint4* P = ring + slot * C::STAGE_SLOTS;
+  // element indices of the lane's fragments in slot 0, per chunk column
+  int pr_idx[2] = {}, xr_idx[4] = {};
+  if constexpr (SPLIT) {
 #pragma unroll
-    for (int f = 0; f < NPF; ++f) pp[f] = P[pslot(prow0, 2 * h + jj) + f * 32 * 4];
+    for (int jj = 0; jj < 2; ++jj) pr_idx[jj] = opaque(PBASE + pslot(prow0, 2 * h + jj));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) xr_idx[q] = opaque(XBASE + xslot(xrow0, 4 * h + q));
+  }
+  auto pread = [&](int slot, int jj, uint4 (&pp)[NPF]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int f = 0; f < NPF; ++f) {
+      if constexpr (SPLIT) pp[f] = ring[pr_idx[jj] + slot * PSTEP + f * 32 * 4];
+      else pp[f] = ring[slot * PSTEP + pslot(prow0, 2 * h + jj) + f * 32 * 4];
+    }
   };
   auto xread = [&](int slot, int jj, int pl, uint4 (&px)[NXF]) __attribute__((always_inline)) {
-    const uint4* X = ring + slot * C::STAGE_SLOTS + C::P_SLOTS;
 #pragma unroll
-    for (int f = 0; f < NXF; ++f) px[f] = X[xslot(xrow0, 4 * h + 2 * jj + pl) + f * 32 * 8];
+    for (int f = 0; f < NXF; ++f) {
+      if constexpr (SPLIT) px[f] = ring[xr_idx[2 * jj + pl] + slot * XSTEP + f * 32 * 8];
+      else px[f] = ring[slot * XSTEP + XBASE + xslot(xrow0, 4 * h + 2 * jj + pl) + f * 32 * 8];
+    }
   };
 
   // With one group per row (the only case of FM = 4) F is first written by
@@ -294,6 +344,16 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
       for (int i = 0; i < 16; ++i)
         F[fm][fn][i] = SINGLE ? rs[fm] * (float)acc[fm][fn][i]
                               : __builtin_fmaf(rs[fm], (float)acc[fm][fn][i], F[fm][fn][i]);
+  };
+  // several groups: the fold of group b (and, STREAM, the zero-point terms
+  // of the pair of groups that b completes)
+  auto fold_group = [&](int b) __attribute__((always_inline)) {
+    read_rs(b);
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) fold_row(fm);
+    if constexpr (STREAM) {
+      if ((b & 1) || b == G - 1) zp_pair(b & ~1);
+    }
   };
 
   // one k-step of 32: plane pl of the packed fragments pp against the
@@ -412,10 +472,10 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   lstore(1, rb);
   lstore_g(1, gqa1);
   lds_barrier();
-  // With one group, FM = 2 reads each k-step's unpacked fragments two
-  // k-steps ahead (xa, xb, x2, x3 hold k-steps 0..3 of a stage); otherwise,
-  // short of registers, one ahead.
-  constexpr bool PF2 = FM == 2 && ONEG;
+  // FM = 2 reads each k-step's unpacked fragments two k-steps ahead (xa, xb,
+  // x2, x3 hold k-steps 0..3 of a stage), except with streamed group
+  // parameters, whose registers leave room for one ahead only.
+  constexpr bool PF2 = FM == 2 && !STREAM;
   uint4 pa[NPF], pb[NPF], xa[NXF], xb[NXF], x2[NXF], x3[NXF];
   pread(0, 0, pa);
   xread(0, 0, 0, xa);
@@ -470,8 +530,9 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
       __builtin_amdgcn_sched_barrier(0);
       mma1(pb, x3, HI{}, LO{});
     } else if constexpr (!ONEG) {
-      // several groups (the fold's registers are live): the stage's stores and
-      // loads first, which needs fewer registers
+      // streamed group parameters (the fold's registers and the parameter
+      // stages are live): the stage's stores and loads first, which needs
+      // fewer registers
       lstore(slot_of(2), rg);
       lstore_g(st + 2, gq);
       gload(st + 2 + C::NRB, rg);
@@ -510,12 +571,7 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
       if constexpr (DBG) {
         dump(b);
       } else if constexpr (!SINGLE) {
-        read_rs(b);
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm) fold_row(fm);
-        if constexpr (STREAM) {
-          if ((b & 1) || b == G - 1) zp_pair(b & ~1);
-        }
+        fold_group(b);
       }
     }
     lds_barrier();
