@@ -9,28 +9,42 @@
 //
 // Work decomposition: one wavefront owns a tile of T = 64 * E consecutive
 // elements of the group sequence, i.e. T / g whole groups, with E registers
-// per lane: E = max(16, min(64, g / 8)), and 128 for g = 8192.  Tile element i
-// sits in
+// per lane: 16 for g <= 128, 32 for g = 256 and 512, 64 for g = 1024 .. 4096,
+// 128 for g = 8192.  A workgroup takes one tile, except with 4096-element
+// tiles, whose LDS buffer leaves two waves per SIMD: there the grid holds the
+// resident workgroups and each walks its tiles with the next one's loads in
+// flight.  Tile element i sits in
 //   layout A: lane i[8:3], register i[2:0] | i[high:9] << 3
 //             (16-byte chunks: coalesced bf16 loads, packed code stores)
 //   layout B: lane i[2:0] | i[S+2:S] << 3, register i[S-1:3] (| i[12] << 6
 //             when E = 128), with S = 3 + min(log2 E, 6)
 // The Walsh-Hadamard butterflies for the index bits held in registers run in
 // registers: bits {0, 1, 2, 9, ...} in layout A, then bits {3, ..., S-1} in
-// layout B, which completes every group.  Group statistics, parameters and
+// layout B, which completes every group (for g = 512, bit 8 is lane bit 3 of
+// layout B: one DPP exchange between lanes l and l ^ 8).  Group statistics, parameters and
 // codes are computed in layout B for g >= 128 (a lane then holds 16 or more
 // elements of a single group), in layout A for smaller groups.  The codes
 // return to layout A through LDS and are packed 8 per dword.  The layouts are
 // exchanged through a padded LDS buffer; one wave per workgroup.
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
 namespace offq {
 namespace {
 
+// Tiles of 2^LOGE registers per lane that one workgroup walks in a loop (the
+// next tile's loads in flight) rather than one per workgroup: those whose LDS
+// buffer leaves few waves resident.
+#ifndef RQ_LOOP_MIN_LOGE
+#define RQ_LOOP_MIN_LOGE 6
+#endif
+#define RQ_LOOPS(LOGE) ((LOGE) >= RQ_LOOP_MIN_LOGE)
+
 template <int LOGG>
 struct Geom {
-  static constexpr int LOGE = LOGG <= 7 ? 4 : LOGG == 8 ? 5 : LOGG <= 12 ? 6 : 7;
+  static constexpr int LOGE = LOGG <= 7 ? 4 : LOGG <= 9 ? 5 : LOGG <= 12 ? 6 : 7;
   static constexpr int E = 1 << LOGE;
   static constexpr int T = 64 * E;
   static constexpr int NCH = E / 8;      // 16-byte chunks per lane in layout A
@@ -211,18 +225,21 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
   // quantizer's reciprocal scale, which gives bit-identical codes.
   constexpr bool FOLD = HAD && (LOGG % 2 == 0);
   constexpr bool STATS_B = LOGG >= 7;
+  // g = 512 on 2048-element tiles: index bit 8 is lane bit 3 of layout B
+  constexpr bool LANE8 = LOGG == 9 && LOGE == 5;
+  static_assert(!LANE8 || !FOLD, "g = 512 carries the normalisation in its last stage");
   __shared__ __attribute__((aligned(16))) float lds[Gm::WORDS];
   __shared__ uint32_t s_corr[STATS_B ? GPT : 1];  // bits(lo) * 0x11111111 per group
 
   // (the id builtins directly: this file's NaN/IEEE flags keep the device
   // library's id functions from being inlined)
   const int lane = (int)__builtin_amdgcn_workitem_id_x();
-  const int64_t gbase = (int64_t)__builtin_amdgcn_workgroup_id_x() * GPT;
-  // (a 64-bit comparison is vector work on gfx950; readfirstlane keeps the
-  // flag, and the addressing chosen by it, in scalar registers)
-  const bool full = __builtin_amdgcn_readfirstlane((int)(gbase + GPT <= n_groups)) != 0;
   float* const la = lds + Gm::a_base(lane);
   float* const lb = lds + Gm::b_base(lane);
+  // GPT is a power of two: tiles by shift (no 64-bit division)
+  constexpr int LOG_GPT = LOGE + 6 - LOGG;
+  static_assert((1 << LOG_GPT) == GPT, "groups per tile");
+  const int64_t n_tiles = (n_groups + GPT - 1) >> LOG_GPT;
 
   // Per chunk: element offset into x and byte offset into the codes of the 8
   // elements this lane holds in layout A.  For g >= 512 the chunk's group is
@@ -234,221 +251,287 @@ __global__ __launch_bounds__(64) void rotate_quantize_kernel(
   // which in a full tile is the same for every chunk (the launcher checks
   // that GPT rows fit in 32-bit offsets).
   constexpr bool ROWS = LOGG < 9 && G1;
-  const uint16_t* const xt = ROWS ? x + gbase * ldx : x;
-  uint8_t* const ct = ROWS ? codes + gbase * ldc : codes;
-  int64_t xoff[NCH], coff[NCH];
-  const uint16_t* xb[NCH];
-  uint8_t* cb[NCH];
-  uint32_t xo[NCH], co[NCH];
-  if constexpr (ROWS) {
-    // row gbase + (ch << (9 - log2 g)) + (lane >> (log2 g - 3)), clamped
-    const int lr = lane >> (LOGG - 3);
-    const int c = 8 * (lane & ((1 << (LOGG - 3)) - 1));
-    if (full) {
-      // (24-bit multiplies: lr < 64 and the launcher keeps strides below 2^24)
-      const uint32_t xl = (uint32_t)lr * ((uint32_t)ldx & 0xffffffu) + c;
-      const uint32_t cl = (uint32_t)lr * ((uint32_t)ldc & 0xffffffu) + (c >> 1);
+  struct Addr {
+    int64_t xoff[NCH], coff[NCH];
+    const uint16_t* xb[NCH];
+    uint8_t* cb[NCH];
+    uint32_t xo[NCH], co[NCH];
+  };
+  // (a 64-bit comparison is vector work on gfx950; readfirstlane keeps the
+  // flag, and the addressing chosen by it, in scalar registers)
+  auto is_full = [&](int64_t gbase) -> bool {
+    return __builtin_amdgcn_readfirstlane((int)(gbase + GPT <= n_groups)) != 0;
+  };
+  auto locate = [&](int64_t gbase, bool full, Addr& A) __attribute__((always_inline)) {
+    if constexpr (ROWS) {
+      const uint16_t* const xt = x + gbase * ldx;
+      uint8_t* const ct = codes + gbase * ldc;
+      // row gbase + (ch << (9 - log2 g)) + (lane >> (log2 g - 3)), clamped
+      const int lr = lane >> (LOGG - 3);
+      const int c = 8 * (lane & ((1 << (LOGG - 3)) - 1));
+      if (full) {
+        // (24-bit multiplies: lr < 64 and the launcher keeps strides below 2^24)
+        const uint32_t xl = (uint32_t)lr * ((uint32_t)ldx & 0xffffffu) + c;
+        const uint32_t cl = (uint32_t)lr * ((uint32_t)ldc & 0xffffffu) + (c >> 1);
 #pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        const int r0 = ch << (9 - LOGG);
-        xb[ch] = xt + (int64_t)r0 * ldx;
-        cb[ch] = ct + (int64_t)r0 * ldc;
-        xo[ch] = xl;
-        co[ch] = cl;
+        for (int ch = 0; ch < NCH; ++ch) {
+          const int r0 = ch << (9 - LOGG);
+          A.xb[ch] = xt + (int64_t)r0 * ldx;
+          A.cb[ch] = ct + (int64_t)r0 * ldc;
+          A.xo[ch] = xl;
+          A.co[ch] = cl;
+        }
+      } else {
+        const int last = (int)(n_groups - 1 - gbase);  // < GPT - 1 here
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch) {
+          const int r = min((ch << (9 - LOGG)) + lr, last);
+          A.xb[ch] = xt;
+          A.cb[ch] = ct;
+          A.xo[ch] = (uint32_t)(r * (int)ldx + c);
+          A.co[ch] = (uint32_t)(r * (int)ldc + (c >> 1));
+        }
       }
     } else {
-      const int last = (int)(n_groups - 1 - gbase);  // < GPT - 1 here
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) {
-        const int r = min((ch << (9 - LOGG)) + lr, last);
-        xb[ch] = xt;
-        cb[ch] = ct;
-        xo[ch] = (uint32_t)(r * (int)ldx + c);
-        co[ch] = (uint32_t)(r * (int)ldc + (c >> 1));
+        int64_t q;
+        int c;  // channel of the chunk's first element inside its group
+        if constexpr (LOGG >= 9) {
+          q = gbase + (ch >> (LOGG - 9));
+          c = ((ch & ((1 << (LOGG - 9)) - 1)) << 9) + 8 * lane;
+        } else {
+          q = gbase + (ch << (9 - LOGG)) + (lane >> (LOGG - 3));
+          c = 8 * (lane & ((1 << (LOGG - 3)) - 1));
+        }
+        if (q >= n_groups) q = n_groups - 1;
+        uint32_t row, col0;
+        group_loc<G1>((uint32_t)q, G, dm, dsh, LOGG, row, col0);
+        A.xoff[ch] = (int64_t)row * ldx + col0 + c;
+        A.coff[ch] = (int64_t)row * ldc + ((col0 + c) >> 1);
       }
     }
-  } else {
+  };
+  auto xptr = [&](const Addr& A, int ch) -> const uint16_t* {
+    if constexpr (ROWS) return A.xb[ch] + A.xo[ch];
+    else return x + A.xoff[ch];
+  };
+  auto cptr = [&](const Addr& A, int ch) -> uint8_t* {
+    if constexpr (ROWS) return A.cb[ch] + A.co[ch];
+    else return codes + A.coff[ch];
+  };
+
+  // Each workgroup walks the tiles blockIdx.x, + gridDim.x, ...; a tile's
+  // 16-byte chunks (layout A: chunk ch of a lane = 8 consecutive bf16) are
+  // requested while the previous tile is rotated and quantized, so that a
+  // resident wave always has a load in flight (a 4096-element tile's LDS
+  // leaves two waves per SIMD).
+  uint4 raw[NCH];
+  auto request = [&](int64_t gbase) __attribute__((always_inline)) {
+    Addr A;
+    locate(gbase, is_full(gbase), A);
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      int64_t q;
-      int c;  // channel of the chunk's first element inside its group
-      if constexpr (LOGG >= 9) {
-        q = gbase + (ch >> (LOGG - 9));
-        c = ((ch & ((1 << (LOGG - 9)) - 1)) << 9) + 8 * lane;
-      } else {
-        q = gbase + (ch << (9 - LOGG)) + (lane >> (LOGG - 3));
-        c = 8 * (lane & ((1 << (LOGG - 3)) - 1));
-      }
-      if (q >= n_groups) q = n_groups - 1;
-      uint32_t row, col0;
-      group_loc<G1>((uint32_t)q, G, dm, dsh, LOGG, row, col0);
-      xoff[ch] = (int64_t)row * ldx + col0 + c;
-      coff[ch] = (int64_t)row * ldc + ((col0 + c) >> 1);
-    }
-  }
-  // groups of the tile that exist (uniform)
-  const int nleft = full ? GPT : (int)(n_groups - gbase);
-  auto stored = [&](int ch) -> bool { return full || (((ch << 9) | (lane << 3)) >> LOGG) < nleft; };
-  auto xptr = [&](int ch) -> const uint16_t* {
-    if constexpr (ROWS) return xb[ch] + xo[ch];
-    else return xt + xoff[ch];
+    for (int ch = 0; ch < NCH; ++ch) raw[ch] = *reinterpret_cast<const uint4*>(xptr(A, ch));
   };
-  auto cptr = [&](int ch) -> uint8_t* {
-    if constexpr (ROWS) return cb[ch] + co[ch];
-    else return ct + coff[ch];
-  };
-
   float v[E];
-
-  // ---- load (layout A): chunk ch of lane = 8 consecutive bf16 -------------
+  // ---- widen (layout A) ------------------------------------------------------
   // With the rotation, butterfly stage 0 (pairs 2j, 2j+1 = the two halves of
   // one 32-bit word) is fused with the bf16 -> fp32 conversion: one dot2 each
   // for the sum and the difference.
-#pragma unroll
-  for (int ch = 0; ch < NCH; ++ch) {
-    uint4 d = *reinterpret_cast<const uint4*>(xptr(ch));
-    const uint32_t w[4] = {d.x, d.y, d.z, d.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if constexpr (HAD) {
-        v[ch * 8 + 2 * j] = dot2_bf16(w[j], 0x3f803f80u);      // (1, 1)
-        v[ch * 8 + 2 * j + 1] = dot2_bf16(w[j], 0xbf803f80u);  // (1, -1)
-      } else {
-        v[ch * 8 + 2 * j] = bf16_lo(w[j]);
-        v[ch * 8 + 2 * j + 1] = bf16_hi(w[j]);
-      }
-    }
-  }
-  if constexpr (HAD) stages_A<LOGE, LOGG>(v);
-
-  // ---- A -> B ---------------------------------------------------------------
-#pragma unroll
-  for (int ch = 0; ch < NCH; ++ch) {
-    *reinterpret_cast<float4*>(la + Gm::a_off(ch)) =
-        make_float4(v[ch * 8 + 0], v[ch * 8 + 1], v[ch * 8 + 2], v[ch * 8 + 3]);
-    *reinterpret_cast<float4*>(la + Gm::a_off(ch) + 4) =
-        make_float4(v[ch * 8 + 4], v[ch * 8 + 5], v[ch * 8 + 6], v[ch * 8 + 7]);
-  }
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < E; ++r) v[r] = lb[Gm::b_off(r)];
-  if constexpr (HAD) stages_B<LOGE, LOGG, !FOLD>(v, cnorm);
-  // v now holds y in layout B (y / cnorm when folded)
-
-  if constexpr (DBG) {
-    // y to global through LDS, in layout A (16-byte stores)
-    const float c = FOLD ? cnorm : 1.0f;
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = v[r] * c;
-    __syncthreads();
+  auto widen = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
-      if (stored(ch)) {
-        const int64_t xe = xptr(ch) - x;
-        const int64_t row = xe / ldx;
-        float* yp = ydbg + row * ldy + (xe - row * ldx);
-        *reinterpret_cast<float4*>(yp) = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
-        *reinterpret_cast<float4*>(yp + 4) =
-            *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
+      const uint4 d = raw[ch];
+      const uint32_t w[4] = {d.x, d.y, d.z, d.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if constexpr (HAD) {
+          v[ch * 8 + 2 * j] = dot2_bf16(w[j], 0x3f803f80u);      // (1, 1)
+          v[ch * 8 + 2 * j + 1] = dot2_bf16(w[j], 0xbf803f80u);  // (1, -1)
+        } else {
+          v[ch * 8 + 2 * j] = bf16_lo(w[j]);
+          v[ch * 8 + 2 * j + 1] = bf16_hi(w[j]);
+        }
       }
     }
-  }
+  };
+  // The rest of a tile (its chunks widened in v), in one copy for full tiles,
+  // whose stores are all unconditional (so that the wait for the next tile's
+  // chunks, issued before them, counts them exactly instead of draining
+  // them), and one for the partial last tile.
+  auto rest = [&](int64_t gbase, auto FULLC) __attribute__((always_inline)) {
+    constexpr bool full = decltype(FULLC)::value;
+    Addr A;
+    locate(gbase, full, A);
+    // groups of the tile that exist (uniform)
+    const int nleft = full ? GPT : (int)(n_groups - gbase);
+    auto stored = [&](int ch) -> bool { return full || (((ch << 9) | (lane << 3)) >> LOGG) < nleft; };
 
-  uint32_t corr[NCH];  // per chunk: bits(lo) * 0x11111111 of its group
-  if constexpr (STATS_B) {
-    // ---- statistics, parameters and codes in layout B ----------------------
-    // All E registers of a lane belong to one group, which spans lane bits
-    // 0 .. NB-1: group lane >> 3 of the tile when g <= 512, lane >> (log2 g - 6)
-    // when g >= 1024.
-    constexpr int NB = LOGG <= 9 ? 3 : LOGG - 6;
-    float mx = v[0], mn = v[0];
-#pragma unroll
-    for (int r = 1; r < E; ++r) {
-      mx = fmaxf(mx, v[r]);
-      mn = fminf(mn, v[r]);
+    if constexpr (HAD) stages_A<LOGE, LOGG>(v);
+
+    // ---- A -> B ---------------------------------------------------------------
+  #pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      *reinterpret_cast<float4*>(la + Gm::a_off(ch)) =
+          make_float4(v[ch * 8 + 0], v[ch * 8 + 1], v[ch * 8 + 2], v[ch * 8 + 3]);
+      *reinterpret_cast<float4*>(la + Gm::a_off(ch) + 4) =
+          make_float4(v[ch * 8 + 4], v[ch * 8 + 5], v[ch * 8 + 6], v[ch * 8 + 7]);
     }
-    lane_reduce<NB < 6 ? NB : 6>(mx, mn);
-    QParams P = FOLD ? quant_params(mx * cnorm, mn * cnorm) : quant_params(mx, mn);
-    if constexpr (FOLD) P.r *= cnorm;  // exact: cnorm is a power of two
-    const int gi = lane >> NB;
-    if ((lane & ((1 << NB) - 1)) == 0) {
-      s_corr[gi] = __float_as_uint(P.lo) * 0x11111111u;
-      if (gi < nleft) {
+    __syncthreads();
+  #pragma unroll
+    for (int r = 0; r < E; ++r) v[r] = lb[Gm::b_off(r)];
+    if constexpr (HAD) {
+      if constexpr (LANE8) {
+        stages_B<LOGE, 8, false>(v, 1.0f);  // index bits 3..7
+        // bit 8 (g = 512 on 2048-element tiles): lanes l and l ^ 8, the lower
+        // one keeps a + b, the upper one a - b; the last stage carries
+        // 1 / sqrt(g): a c + b c, a c - b c
+        const float sc = (lane & 8) ? -cnorm : cnorm;
+#pragma unroll
+        for (int r = 0; r < E; ++r) v[r] = __builtin_fmaf(v[r], sc, dpp<0x128>(v[r]) * cnorm);  // row_ror:8
+      } else {
+        stages_B<LOGE, LOGG, !FOLD>(v, cnorm);
+      }
+    }
+    // v now holds y in layout B (y / cnorm when folded)
+
+    if constexpr (DBG) {
+      // y to global through LDS, in layout A (16-byte stores)
+      const float c = FOLD ? cnorm : 1.0f;
+      __syncthreads();
+  #pragma unroll
+      for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = v[r] * c;
+      __syncthreads();
+  #pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        if (stored(ch)) {
+          const int64_t xe = xptr(A, ch) - x;
+          const int64_t row = xe / ldx;
+          float* yp = ydbg + row * ldy + (xe - row * ldx);
+          *reinterpret_cast<float4*>(yp) = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
+          *reinterpret_cast<float4*>(yp + 4) =
+              *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
+        }
+      }
+    }
+
+    uint32_t corr[NCH];  // per chunk: bits(lo) * 0x11111111 of its group
+    if constexpr (STATS_B) {
+      // ---- statistics, parameters and codes in layout B ----------------------
+      // All E registers of a lane belong to one group, which spans lane bits
+      // 0 .. NB-1: group lane >> 3 of the tile when g <= 256, lane >> 4 for
+      // g = 512 (2048-element tiles), lane >> (log2 g - 6) when g >= 1024.
+      constexpr int NB = LANE8 ? 4 : LOGG <= 9 ? 3 : LOGG - 6;
+      float mx = v[0], mn = v[0];
+  #pragma unroll
+      for (int r = 1; r < E; ++r) {
+        mx = fmaxf(mx, v[r]);
+        mn = fminf(mn, v[r]);
+      }
+      lane_reduce<NB < 6 ? NB : 6>(mx, mn);
+      QParams P = FOLD ? quant_params(mx * cnorm, mn * cnorm) : quant_params(mx, mn);
+      if constexpr (FOLD) P.r *= cnorm;  // exact: cnorm is a power of two
+      const int gi = lane >> NB;
+      if ((lane & ((1 << NB) - 1)) == 0) s_corr[gi] = __float_as_uint(P.lo) * 0x11111111u;
+      // (full tile: every lane of the group stores the same values)
+      if (full || ((lane & ((1 << NB) - 1)) == 0 && gi < nleft)) {
         scale[gbase + gi] = P.s16;
         zero[gbase + gi] = P.z;
       }
-    }
-    // codes as float bits, back to layout A
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = __uint_as_float(quant_bits(v[r], P));
-    __syncthreads();
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      const float4 a = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
-      const float4 b = *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
-      v[ch * 8 + 0] = a.x;
-      v[ch * 8 + 1] = a.y;
-      v[ch * 8 + 2] = a.z;
-      v[ch * 8 + 3] = a.w;
-      v[ch * 8 + 4] = b.x;
-      v[ch * 8 + 5] = b.y;
-      v[ch * 8 + 6] = b.z;
-      v[ch * 8 + 7] = b.w;
-      corr[ch] = s_corr[((ch << 9) | (lane << 3)) >> LOGG];
-    }
-  } else {
-    // ---- back to layout A; statistics, parameters and codes there ----------
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = v[r];
-    __syncthreads();
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      const float4 a = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
-      const float4 b = *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
-      v[ch * 8 + 0] = a.x;
-      v[ch * 8 + 1] = a.y;
-      v[ch * 8 + 2] = a.z;
-      v[ch * 8 + 3] = a.w;
-      v[ch * 8 + 4] = b.x;
-      v[ch * 8 + 5] = b.y;
-      v[ch * 8 + 6] = b.z;
-      v[ch * 8 + 7] = b.w;
-    }
-    // a group is 2^(log2 g - 3) consecutive lanes of one chunk
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      float mx = v[ch * 8], mn = v[ch * 8];
-#pragma unroll
-      for (int j = 1; j < 8; ++j) {
-        mx = fmaxf(mx, v[ch * 8 + j]);
-        mn = fminf(mn, v[ch * 8 + j]);
+      // codes as float bits, back to layout A
+      __syncthreads();
+  #pragma unroll
+      for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = __uint_as_float(quant_bits(v[r], P));
+      __syncthreads();
+  #pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        const float4 a = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
+        const float4 b = *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
+        v[ch * 8 + 0] = a.x;
+        v[ch * 8 + 1] = a.y;
+        v[ch * 8 + 2] = a.z;
+        v[ch * 8 + 3] = a.w;
+        v[ch * 8 + 4] = b.x;
+        v[ch * 8 + 5] = b.y;
+        v[ch * 8 + 6] = b.z;
+        v[ch * 8 + 7] = b.w;
+        corr[ch] = s_corr[((ch << 9) | (lane << 3)) >> LOGG];
       }
-      lane_reduce<LOGG - 3>(mx, mn);
-      QParams P = FOLD ? quant_params(mx * cnorm, mn * cnorm) : quant_params(mx, mn);
-      if constexpr (FOLD) P.r *= cnorm;
-      const int qt = ((ch << 9) | (lane << 3)) >> LOGG;  // group within the tile
-      const int64_t q = gbase + qt;
-      if ((lane & ((1 << (LOGG - 3)) - 1)) == 0 && qt < nleft) {
-        scale[q] = P.s16;
-        zero[q] = P.z;
+    } else {
+      // ---- back to layout A; statistics, parameters and codes there ----------
+      __syncthreads();
+  #pragma unroll
+      for (int r = 0; r < E; ++r) lb[Gm::b_off(r)] = v[r];
+      __syncthreads();
+  #pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        const float4 a = *reinterpret_cast<const float4*>(la + Gm::a_off(ch));
+        const float4 b = *reinterpret_cast<const float4*>(la + Gm::a_off(ch) + 4);
+        v[ch * 8 + 0] = a.x;
+        v[ch * 8 + 1] = a.y;
+        v[ch * 8 + 2] = a.z;
+        v[ch * 8 + 3] = a.w;
+        v[ch * 8 + 4] = b.x;
+        v[ch * 8 + 5] = b.y;
+        v[ch * 8 + 6] = b.z;
+        v[ch * 8 + 7] = b.w;
       }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) v[ch * 8 + j] = __uint_as_float(quant_bits(v[ch * 8 + j], P));
-      corr[ch] = __float_as_uint(P.lo) * 0x11111111u;
+      // a group is 2^(log2 g - 3) consecutive lanes of one chunk
+  #pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        float mx = v[ch * 8], mn = v[ch * 8];
+  #pragma unroll
+        for (int j = 1; j < 8; ++j) {
+          mx = fmaxf(mx, v[ch * 8 + j]);
+          mn = fminf(mn, v[ch * 8 + j]);
+        }
+        lane_reduce<LOGG - 3>(mx, mn);
+        QParams P = FOLD ? quant_params(mx * cnorm, mn * cnorm) : quant_params(mx, mn);
+        if constexpr (FOLD) P.r *= cnorm;
+        const int qt = ((ch << 9) | (lane << 3)) >> LOGG;  // group within the tile
+        const int64_t q = gbase + qt;
+        if (full || ((lane & ((1 << (LOGG - 3)) - 1)) == 0 && qt < nleft)) {
+          scale[q] = P.s16;
+          zero[q] = P.z;
+        }
+  #pragma unroll
+        for (int j = 0; j < 8; ++j) v[ch * 8 + j] = __uint_as_float(quant_bits(v[ch * 8 + j], P));
+        corr[ch] = __float_as_uint(P.lo) * 0x11111111u;
+      }
     }
-  }
 
-  // ---- pack 8 codes per dword and store (layout A) -------------------------
-#pragma unroll
-  for (int ch = 0; ch < NCH; ++ch) {
-    uint32_t w = 0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) w += __float_as_uint(v[ch * 8 + j]) << (4 * j);
-    w -= corr[ch];
-    if (stored(ch)) *reinterpret_cast<uint32_t*>(cptr(ch)) = w;
+    // ---- pack 8 codes per dword and store (layout A) -------------------------
+  #pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      uint32_t w = 0;
+  #pragma unroll
+      for (int j = 0; j < 8; ++j) w += __float_as_uint(v[ch * 8 + j]) << (4 * j);
+      w -= corr[ch];
+      if (stored(ch)) *reinterpret_cast<uint32_t*>(cptr(A, ch)) = w;
+    }
+  };
+  const int64_t nfull = n_groups >> LOG_GPT;
+  int64_t tile = __builtin_amdgcn_workgroup_id_x();
+  request(tile << LOG_GPT);
+  widen();
+  if constexpr (RQ_LOOPS(LOGE)) {
+    // Full tiles in a loop with one exit and no branch around the loads: the
+    // next tile's chunks are always requested (past the last tile, the
+    // current tile's again, which the cache serves), so that the loop's wait
+    // for them counts exactly the loads and stores issued since.
+    const int64_t step = __builtin_amdgcn_readfirstlane((int)gridDim.x);
+    while (tile < nfull) {
+      const int64_t next = tile + step;
+      request((next < n_tiles ? next : tile) << LOG_GPT);
+      rest(tile << LOG_GPT, std::true_type{});
+      tile = next;
+      __syncthreads();  // the next tile's exchanges reuse the LDS buffer
+      widen();
+    }
+    if (tile < n_tiles) rest(tile << LOG_GPT, std::false_type{});
+  } else {  // one tile per workgroup
+    if (tile < nfull) rest(tile << LOG_GPT, std::true_type{});
+    else rest(tile << LOG_GPT, std::false_type{});
   }
 }
 
@@ -603,23 +686,44 @@ __global__ __launch_bounds__(64 * NW) void rotate_quantize_rows_kernel(
   }
 }
 
+// Workgroups of a kernel that are resident on the current device at once (0
+// if the runtime cannot tell): compute units times workgroups per unit.
+int64_t resident_workgroups(const void* kern, int threads) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, threads, 0) != hipSuccess)
+    return 0;
+  return (int64_t)cus * per_cu;
+}
+
 template <int LOGG>
 hipError_t launch_t(const uint16_t* x, int64_t n_groups, int G, int64_t ldx, bool had,
                     uint8_t* codes, int64_t ldc, uint16_t* scale, int16_t* zero, float* ydbg,
                     int64_t ldy, hipStream_t stream) {
   constexpr int GPT = Geom<LOGG>::GPT;
   const int64_t nblk = (n_groups + GPT - 1) / GPT;
-  const dim3 grid((unsigned)nblk), block(64);
+  const dim3 block(64);
   const float cnorm = (float)(1.0 / __builtin_sqrt((double)(1 << LOGG)));
   // magic multiplier for q / G (q < 2^31)
   int lg = 0;
   while ((1 << lg) < G) ++lg;
   const int dsh = 31 + lg;
   const uint32_t dm = (uint32_t)(((uint64_t(1) << dsh) + (uint64_t)G - 1) / (uint64_t)G);
-#define OFFQ_RQ(HD, DB, G1)                                                                  \
-  hipLaunchKernelGGL((rotate_quantize_kernel<LOGG, HD, DB, G1>), grid, block, 0, stream, x, \
-                     n_groups, G, dm, dsh, ldx, codes, ldc, scale, zero, ydbg, ldy,         \
-                     HD ? cnorm : 1.0f)
+  // 4096-element tiles (g >= 512): as many workgroups as stay resident, each
+  // walking its tiles with the next one's loads in flight; smaller tiles
+  // leave enough waves resident, one tile per workgroup
+#define OFFQ_RQ(HD, DB, G1)                                                                     \
+  {                                                                                            \
+    auto kern = rotate_quantize_kernel<LOGG, HD, DB, G1>;                                       \
+    int64_t nwg = nblk;                                                                         \
+    if (RQ_LOOPS(Geom<LOGG>::LOGE)) {                                                           \
+      const int64_t res = resident_workgroups((const void*)kern, 64);                           \
+      if (res > 0 && res < nwg) nwg = res;                                                      \
+    }                                                                                           \
+    hipLaunchKernelGGL(kern, dim3((unsigned)nwg), block, 0, stream, x, n_groups, G, dm, dsh,    \
+                       ldx, codes, ldc, scale, zero, ydbg, ldy, HD ? cnorm : 1.0f);              \
+  }
   // one group per row: the fast addressing when GPT rows fit in 32-bit
   // offsets and the strides in 24 bits
   const bool g1 = G == 1 && (LOGG >= 9 || (GPT * ldx < (int64_t(1) << 31) &&
@@ -642,7 +746,7 @@ hipError_t launch_t(const uint16_t* x, int64_t n_groups, int G, int64_t ldx, boo
     }
   }
 #define OFFQ_RQ_G(HD, DB) \
-  if (g1) OFFQ_RQ(HD, DB, true); else OFFQ_RQ(HD, DB, false);
+  if (g1) OFFQ_RQ(HD, DB, true) else OFFQ_RQ(HD, DB, false)
   if (had) {
     if (ydbg) { OFFQ_RQ_G(true, true) } else { OFFQ_RQ_G(true, false) }
   } else {
