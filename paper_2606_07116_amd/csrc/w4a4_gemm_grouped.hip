@@ -77,8 +77,10 @@ struct GCfg {
   static constexpr int NBUF = (FM == 2 && (ONEG || STREAM)) ? 4 : 3;
   static constexpr int GR = STREAM ? 4 : 1;
   // stages held in registers between their global load and their LDS store:
-  // the loads are issued NRB stages before the store
-  static constexpr int NRB = (FM == 2 && ONEG) ? 4 : 2;
+  // the loads are issued NRB stages before the store (one with streamed
+  // group parameters, which leaves the registers for reading fragments two
+  // k-steps ahead)
+  static constexpr int NRB = (FM == 2 && ONEG) ? 4 : STREAM ? 1 : 2;
 };
 
 // packed rows: 4 chunks, swizzle c ^ (row/4 mod 4); int8 rows: 8 chunks,
@@ -473,9 +475,8 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   lstore_g(1, gqa1);
   lds_barrier();
   // FM = 2 reads each k-step's unpacked fragments two k-steps ahead (xa, xb,
-  // x2, x3 hold k-steps 0..3 of a stage), except with streamed group
-  // parameters, whose registers leave room for one ahead only.
-  constexpr bool PF2 = FM == 2 && !STREAM;
+  // x2, x3 hold k-steps 0..3 of a stage).
+  constexpr bool PF2 = FM == 2;
   uint4 pa[NPF], pb[NPF], xa[NXF], xb[NXF], x2[NXF], x3[NXF];
   pread(0, 0, pa);
   xread(0, 0, 0, xa);
@@ -511,6 +512,10 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     // scheduling barriers keep this order.
     using LO = std::false_type;
     using HI = std::true_type;
+    if constexpr (STREAM) {  // the group parameters of stage st + 2 in, stage st + 2 + NRB out
+      lstore_g(st + 2, gq);
+      gload_g(st + 2 + C::NRB, gq);
+    }
     if constexpr (PF2) {  // on entry pa, xa (k-step 0) and xb (k-step 1) are loaded
       pread(slot, 1, pb);
       xread(slot, 1, 0, x2);
@@ -529,25 +534,7 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
       gload(st + 2 + C::NRB, rg);
       __builtin_amdgcn_sched_barrier(0);
       mma1(pb, x3, HI{}, LO{});
-    } else if constexpr (!ONEG) {
-      // streamed group parameters (the fold's registers and the parameter
-      // stages are live): the stage's stores and loads first, which needs
-      // fewer registers
-      lstore(slot_of(2), rg);
-      lstore_g(st + 2, gq);
-      gload(st + 2 + C::NRB, rg);
-      gload_g(st + 2 + C::NRB, gq);
-      xread(slot, 0, 1, xb);
-      mma1(pa, xa, LO{}, FC);
-      pread(slot, 1, pb);
-      xread(slot, 1, 0, xa);
-      mma1(pa, xb, HI{}, LO{});
-      xread(slot, 1, 1, xb);
-      mma1(pb, xa, LO{}, LO{});
-      pread(slot_of(1), 0, pa);  // past the last stage: stale, unused
-      xread(slot_of(1), 0, 0, xa);
-      mma1(pb, xb, HI{}, LO{});
-    } else {  // on entry pa, xa (k-step 0) are loaded
+    } else {  // FM = 4 (one group); on entry pa, xa (k-step 0) are loaded
       xread(slot, 0, 1, xb);
       __builtin_amdgcn_sched_barrier(0);
       mma1(pa, xa, LO{}, FC);
