@@ -495,13 +495,16 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   // that the compiler can interleave the LDS traffic, the unpacking and the
   // global loads with the MFMAs: past the last stage the stores fill a slot
   // that is never read again and the loads read zeros.
-  auto body = [&](auto JC, auto FC, auto LC, int st) __attribute__((always_inline)) {
+  // PH: st mod 3 when the caller knows it (three-slot ring), else -1.
+  auto body = [&](auto JC, auto FC, auto LC, int st, auto PHC) __attribute__((always_inline)) {
     constexpr int J = decltype(JC)::value;
+    constexpr int PH = decltype(PHC)::value;
     v4i(&rg)[NLD] = rgb[(J + 2) % C::NRB];
     uint32_t(&gq)[2] = gqb[(J + 2) % C::NRB];
-    // ring slot of stage st + d (J = st mod 4)
+    // ring slot of stage st + d (J = st mod 4): a compile-time constant with
+    // four slots, or with three when the phase is known
     auto slot_of = [&](int d) __attribute__((always_inline)) {
-      return C::NBUF == 4 ? ((J + d) & 3) : (st + d) % 3;
+      return C::NBUF == 4 ? ((J + d) & 3) : PH >= 0 ? (PH + d) % 3 : (st + d) % 3;
     };
     const int slot = slot_of(0);
     // Four k-steps.  Stage st + 2 goes into the slot read during stage
@@ -564,12 +567,17 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
     lds_barrier();
   };
   // four stages from st (a multiple of 4); FIRST / LASTG: they start / end a group
-  auto four = [&](int st, auto FIRST, auto LASTG) __attribute__((always_inline)) {
+  // (PHC: st mod 3, or -1 when not known at compile time)
+  using PN = std::integral_constant<int, -1>;
+  auto four = [&](int st, auto FIRST, auto LASTG, auto PHC) __attribute__((always_inline)) {
     using Fl = std::false_type;
-    body(I0{}, FIRST, Fl{}, st);
-    body(I1{}, Fl{}, Fl{}, st + 1);
-    body(I2{}, Fl{}, Fl{}, st + 2);
-    body(I3{}, Fl{}, LASTG, st + 3);
+    constexpr int P = decltype(PHC)::value;
+    using P1 = std::integral_constant<int, P < 0 ? -1 : (P + 1) % 3>;
+    using P2 = std::integral_constant<int, P < 0 ? -1 : (P + 2) % 3>;
+    body(I0{}, FIRST, Fl{}, st, PHC);
+    body(I1{}, Fl{}, Fl{}, st + 1, P1{});
+    body(I2{}, Fl{}, Fl{}, st + 2, P2{});
+    body(I3{}, Fl{}, LASTG, st + 3, PHC);
   };
 
   using T = std::true_type;
@@ -577,32 +585,46 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   int st = 0;
   if constexpr (MODE == 1) {  // every stage is a group
     for (; st + 4 <= nst; st += 4) {
-      body(I0{}, T{}, T{}, st);
-      body(I1{}, T{}, T{}, st + 1);
-      body(I2{}, T{}, T{}, st + 2);
-      body(I3{}, T{}, T{}, st + 3);
+      body(I0{}, T{}, T{}, st, PN{});
+      body(I1{}, T{}, T{}, st + 1, PN{});
+      body(I2{}, T{}, T{}, st + 2, PN{});
+      body(I3{}, T{}, T{}, st + 3, PN{});
     }
-    if (st < nst) body(I0{}, T{}, T{}, st);
-    if (st + 1 < nst) body(I1{}, T{}, T{}, st + 1);
-    if (st + 2 < nst) body(I2{}, T{}, T{}, st + 2);
+    if (st < nst) body(I0{}, T{}, T{}, st, PN{});
+    if (st + 1 < nst) body(I1{}, T{}, T{}, st + 1, PN{});
+    if (st + 2 < nst) body(I2{}, T{}, T{}, st + 2, PN{});
   } else if constexpr (MODE == 2) {  // groups of two stages
     for (; st + 4 <= nst; st += 4) {
-      body(I0{}, T{}, Fl{}, st);
-      body(I1{}, Fl{}, T{}, st + 1);
-      body(I2{}, T{}, Fl{}, st + 2);
-      body(I3{}, Fl{}, T{}, st + 3);
+      body(I0{}, T{}, Fl{}, st, PN{});
+      body(I1{}, Fl{}, T{}, st + 1, PN{});
+      body(I2{}, T{}, Fl{}, st + 2, PN{});
+      body(I3{}, Fl{}, T{}, st + 3, PN{});
     }
     if (st < nst) {
-      body(I0{}, T{}, Fl{}, st);
-      body(I1{}, Fl{}, T{}, st + 1);
+      body(I0{}, T{}, Fl{}, st, PN{});
+      body(I1{}, Fl{}, T{}, st + 1, PN{});
     }
   } else if constexpr (MODE == 4) {  // groups of four stages
-    for (; st < nst; st += 4) four(st, T{}, T{});
+    if constexpr (C::NBUF == 3) {
+      // twelve stages per iteration, so that every stage's ring slot is known
+      using Q0 = std::integral_constant<int, 0>;
+      using Q1 = std::integral_constant<int, 1>;
+      using Q2 = std::integral_constant<int, 2>;
+      for (; st + 12 <= nst; st += 12) {
+        four(st, T{}, T{}, Q0{});
+        four(st + 4, T{}, T{}, Q1{});
+        four(st + 8, T{}, T{}, Q2{});
+      }
+      if (st < nst) four(st, T{}, T{}, Q0{});
+      if (st + 4 < nst) four(st + 4, T{}, T{}, Q1{});
+    } else {
+      for (; st < nst; st += 4) four(st, T{}, T{}, PN{});
+    }
   } else {  // groups of 8k stages: first four, middle fours, last four
     for (; st < nst; st += 4) {
-      four(st, T{}, Fl{});
-      for (st += 4; (st & (spg - 1)) != spg - 4; st += 4) four(st, Fl{}, Fl{});
-      four(st, Fl{}, T{});
+      four(st, T{}, Fl{}, PN{});
+      for (st += 4; (st & (spg - 1)) != spg - 4; st += 4) four(st, Fl{}, Fl{}, PN{});
+      four(st, Fl{}, T{}, PN{});
     }
   }
   if constexpr (SINGLE && !DBG) read_rs(0);
