@@ -187,7 +187,12 @@ def test_rope_kv_append_position_outside_cache_writes_nothing():
 @pytest.mark.parametrize("B,Hq,Hkv,S,seq_len", [(2, 32, 8, 2100, 2100), (1, 8, 2, 1500, 1025),
                                                 (3, 4, 1, 64, 50), (2, 16, 8, 700, 650),
                                                 (1, 4, 2, 2048, 2048), (1, 16, 2, 1300, 1300),
-                                                (2, 8, 2, 3000, 1)])
+                                                (2, 8, 2, 3000, 1),
+                                                # a final chunk of 64 positions joins the
+                                                # chunk before it, one of 65 does not; with
+                                                # 576 one workgroup per head takes both
+                                                (1, 8, 2, 1100, 1088), (1, 8, 4, 1100, 1089),
+                                                (2, 4, 2, 600, 576)])
 def test_gqa_attention(B, Hq, Hkv, S, seq_len):
     q = inputs.queries(B, Hq, 128, seed=S)
     kc, ks, kz = inputs.kv4_cache(B, Hkv, S, 128, seed=S)
