@@ -1,4 +1,5 @@
-"""Decode attention over the 4-bit KV cache (oracle; test-only).
+"""Attention over the 4-bit KV cache: one decode step, and the causal prefill
+of a chunk of tokens (oracle; test-only).
 
 Sec. 3.3, step 2(3): the RoPE-encoded query and key of every head receive the
 same per-head online Hadamard H3, so their dot product is unchanged (H3 is
@@ -76,6 +77,39 @@ def decode_attention(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, seq_
     scores = np.float64(sm_scale) * np.einsum("bhd,bhsd->bhs", qr, k)
     p = softmax(scores)
     o = np.einsum("bhs,bhsd->bhd", p, v)
+    if v_hadamard:
+        o = hadamard.rotate(o, o.shape[-1])
+    return o
+
+
+def prefill_attention(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, past, sm_scale,
+                      v_hadamard=False, rows=None):
+    """Causal attention of T new tokens per sequence over the cache.
+
+    q: [B, T, Hq, Dh] bf16 values (the queries after RoPE); the cache arrays as
+    for decode_attention, holding the ``past`` earlier positions followed by
+    the T new ones.  Query t of a sequence sits at position past + t and
+    attends to positions 0 .. past + t (sec. 3.3 step 2(3) for the rotations;
+    the mask is ordinary causal self-attention), so row t is the decode step
+    of that token with seq_len = past + t + 1.  ``rows`` (optional) lists the
+    t to compute.  Returns fp64 [B, len(rows) or T, Hq, Dh].
+    """
+    q = np.asarray(q)
+    T = q.shape[1]
+    ts = np.arange(T) if rows is None else np.asarray(rows)
+    n = past + int(ts.max()) + 1
+    qr = rotate_query(q[:, ts])                                  # [B, R, Hq, Dh]
+    k = dequantize_rows(k_codes[:, :, :n], k_scale[:, :, :n], k_zero[:, :, :n])
+    v = dequantize_rows(v_codes[:, :, :n], v_scale[:, :, :n], v_zero[:, :, :n])
+    group = qr.shape[2] // k.shape[1]
+    if group > 1:
+        k = np.repeat(k, group, axis=1)
+        v = np.repeat(v, group, axis=1)
+    scores = np.float64(sm_scale) * np.einsum("brhd,bhsd->bhrs", qr, k)
+    allowed = np.arange(n)[None, :] <= (past + ts)[:, None]      # [R, n]
+    scores = np.where(allowed[None, None], scores, -np.inf)
+    p = softmax(scores)
+    o = np.einsum("bhrs,bhsd->brhd", p, v)
     if v_hadamard:
         o = hadamard.rotate(o, o.shape[-1])
     return o

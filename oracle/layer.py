@@ -1,6 +1,8 @@
-"""One decode step of a quantized decoder layer (oracle; test-only).
+"""A quantized decoder layer: one decode step, or the prefill of a chunk of
+tokens (oracle; test-only).
 
-The pipeline of sec. 3.3 / Fig. 2 for one new token per sequence:
+The pipeline of sec. 3.3 / Fig. 2 (decode: one new token per sequence;
+prefill: T new tokens per sequence, the attention causal over them):
 
     h  = x (+ residual);  y = RMSNorm(h)            (norm scale fused offline)
     quantize y (no online rotation: U1 P1 H1 are fused offline, step 2(1))
@@ -124,4 +126,41 @@ def decode_layer(x, weights, cache, pos, seq_len, cfg):
     out, _ = add_rmsnorm(h1, down, eps)
     inter = dict(y0=y0, qkv=qkv, q=bf16(q), o=o, attn_out=attn_out, h1=h1, y1=y1, gu=gu, a=a,
                  down=down)
+    return out, inter, cache
+
+
+def prefill_layer(x, weights, cache, past, cfg):
+    """The prefill of T tokens per sequence.  x: bf16 [B * T, D], row
+    b * T + t the token at position past + t of sequence b; cache: the 4-bit
+    K/V cache [B, Hkv, s_cap, ...] holding ``past`` positions per sequence
+    (copied, the T new positions written); weights and cfg as for
+    decode_layer.  Returns (out bf16 [B * T, D], dict of intermediates, new
+    cache)."""
+    Hq, Hkv, g, eps, base = cfg["Hq"], cfg["Hkv"], cfg["g"], cfg["eps"], cfg["rope_base"]
+    B = cache["k_codes"].shape[0]
+    M = x.shape[0]
+    T = M // B
+    pos = past + np.tile(np.arange(T), B)
+    cache = {k: v.copy() for k, v in cache.items()}
+    _, y0 = add_rmsnorm(x, None, eps)
+    qkv = quantized_linear(y0, *weights["qkv"], g)
+    q, k_y, v_y = kv_rows(qkv, Hq, Hkv, pos, base)
+    for name, rows in (("k", k_y), ("v", v_y)):
+        codes, s, z = kv.kv_quantize(rows.reshape(-1, 128).astype(np.float32))
+        packed = quantizer.pack_nibbles(codes).reshape(B, T, Hkv, 64)
+        cache[name + "_codes"][:, :, past:past + T] = packed.transpose(0, 2, 1, 3)
+        cache[name + "_scale"][:, :, past:past + T] = s.reshape(B, T, Hkv).transpose(0, 2, 1)
+        cache[name + "_zero"][:, :, past:past + T] = z.reshape(B, T, Hkv).transpose(0, 2, 1)
+    qb = bf16(q).reshape(B, T, Hq, 128)
+    o = bf16(attention.prefill_attention(qb, cache["k_codes"], cache["k_scale"], cache["k_zero"],
+                                         cache["v_codes"], cache["v_scale"], cache["v_zero"],
+                                         past, 1.0 / np.sqrt(128.0)))
+    attn_out = quantized_linear(o.reshape(M, Hq * 128), *weights["o"], g)
+    h1, y1 = add_rmsnorm(x, attn_out, eps)
+    gu = quantized_linear(y1, *weights["ug"], g)
+    a = bf16(swiglu(gu))
+    down = quantized_linear(a, *weights["down"], g, hadamard_online=True)
+    out, _ = add_rmsnorm(h1, down, eps)
+    inter = dict(y0=y0, qkv=qkv, q=qb.reshape(M, Hq, 128), o=o.reshape(M, Hq, 128),
+                 attn_out=attn_out, h1=h1, y1=y1, gu=gu, a=a, down=down)
     return out, inter, cache

@@ -146,3 +146,66 @@ def test_value_rotation_is_undone_with_the_explicit_matrix():
     err = np.linalg.norm(o - want, axis=-1)
     bound = np.sqrt(128) * 0.5 * s.reshape(2, 3, 20).astype(np.float64).max(axis=-1) * 1.001
     assert np.all(err <= bound)
+
+
+# ---------------------------------------------------------------- prefill form
+def _prefill_case(B=2, T=9, Hq=4, Hkv=2, past=5, S=None, seed=3):
+    S = S or past + T + 3
+    q = inputs.queries(B * T, Hq, 128, seed=seed).reshape(B, T, Hq, 128)
+    kc, ks, kz = inputs.kv4_cache(B, Hkv, S, 128, seed=seed)
+    vc, vs, vz = inputs.kv4_cache(B, Hkv, S, 128, seed=seed + 1)
+    return q, kc, ks, kz, vc, vs, vz
+
+
+@pytest.mark.parametrize("B,T,Hq,Hkv,past", [(2, 9, 4, 2, 5), (1, 12, 2, 2, 0), (2, 5, 8, 2, 30)])
+def test_prefill_matches_torch_sdpa_with_an_explicit_causal_mask(B, T, Hq, Hkv, past):
+    """torch's fp64 SDPA on the dequantized cache, the grouped heads expanded
+    by repeat_interleave and the mask built as a boolean matrix."""
+    q, kc, ks, kz, vc, vs, vz = _prefill_case(B, T, Hq, Hkv, past)
+    sm = 1 / math.sqrt(128)
+    o = OA.prefill_attention(q, kc, ks, kz, vc, vs, vz, past, sm)
+    n = past + T
+    qr = torch.from_numpy(OA.rotate_query(q)).permute(0, 2, 1, 3)          # [B, Hq, T, D]
+    k = torch.from_numpy(OA.dequantize_rows(kc, ks, kz)[:, :, :n]).repeat_interleave(Hq // Hkv, 1)
+    v = torch.from_numpy(OA.dequantize_rows(vc, vs, vz)[:, :, :n]).repeat_interleave(Hq // Hkv, 1)
+    mask = torch.zeros(T, n, dtype=torch.bool)
+    for t in range(T):
+        mask[t, :past + t + 1] = True
+    ref = torch.nn.functional.scaled_dot_product_attention(qr, k, v, attn_mask=mask, scale=sm)
+    assert np.allclose(o, ref.permute(0, 2, 1, 3).numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_prefill_first_token_of_an_empty_context_returns_its_value_row():
+    q, kc, ks, kz, vc, vs, vz = _prefill_case(past=0)
+    o = OA.prefill_attention(q, kc, ks, kz, vc, vs, vz, 0, 0.7)
+    v0 = OA.dequantize_rows(vc[:, :, :1], vs[:, :, :1], vz[:, :, :1])[:, :, 0]   # [B, Hkv, D]
+    want = np.repeat(v0, 2, axis=1)
+    assert np.allclose(o[:, 0], want, rtol=0, atol=1e-12)
+
+
+def test_prefill_rows_are_decode_steps_over_their_prefixes():
+    """Row t of the prefill is the decode step of that token with
+    seq_len = past + t + 1 (the other path of the oracle), and a subset of
+    rows computes the same values."""
+    q, kc, ks, kz, vc, vs, vz = _prefill_case(past=4, T=7)
+    o = OA.prefill_attention(q, kc, ks, kz, vc, vs, vz, 4, 0.2)
+    for t in range(7):
+        d = OA.decode_attention(q[:, t], kc, ks, kz, vc, vs, vz, 4 + t + 1, 0.2)
+        assert np.allclose(o[:, t], d, rtol=1e-13, atol=1e-13)
+    sub = OA.prefill_attention(q, kc, ks, kz, vc, vs, vz, 4, 0.2, rows=[6, 2])
+    assert np.array_equal(sub, o[:, [6, 2]])
+
+
+def test_prefill_later_positions_do_not_reach_earlier_queries():
+    """Changing the cache row at position j changes exactly the queries that
+    attend to it (t >= j - past)."""
+    past, T = 3, 8
+    q, kc, ks, kz, vc, vs, vz = _prefill_case(past=past, T=T)
+    o = OA.prefill_attention(q, kc, ks, kz, vc, vs, vz, past, 0.5)
+    j = past + 4
+    kc2, vc2 = kc.copy(), vc.copy()
+    kc2[:, :, j] = 255 - kc2[:, :, j]
+    vc2[:, :, j] = 255 - vc2[:, :, j]
+    o2 = OA.prefill_attention(q, kc2, ks, kz, vc2, vs, vz, past, 0.5)
+    assert np.array_equal(o[:, :4], o2[:, :4])
+    assert np.all(np.abs(o[:, 4:] - o2[:, 4:]).max(axis=(2, 3)) > 1e-6)

@@ -147,3 +147,23 @@ def test_decode_layer_writes_the_cache_and_approximates_the_float_layer():
     assert err < 0.25, err
     # and the intermediates are consistent with the final output
     assert np.array_equal(out, OL.add_rmsnorm(inter["h1"], inter["down"], cfg["eps"])[0])
+
+
+@pytest.mark.parametrize("past", [0, 6])
+def test_prefill_layer_equals_decode_steps_one_token_at_a_time(past):
+    """The prefill of T tokens gives, row for row, the outputs of T decode
+    steps taken in order (each token quantized, projected and normalised on
+    its own row; its attention over the cache the earlier steps wrote), and
+    leaves the same cache."""
+    B, T = 2, 5
+    x, weights, wf, cache, _, _, cfg = _layer_case(M=B * T, Hq=4, Hkv=2, seed=4)
+    cache = {k: v[:B] for k, v in cache.items()}
+    out, inter, new = OL.prefill_layer(x, weights, cache, past, cfg)
+    cur = cache
+    for t in range(T):
+        rows = np.arange(B) * T + t
+        o_t, it, cur = OL.decode_layer(x[rows], weights, cur, np.full(B, past + t), past + t + 1, cfg)
+        assert np.array_equal(out[rows], o_t), t
+        assert np.array_equal(inter["o"].reshape(B * T, -1)[rows], it["o"].reshape(B, -1)), t
+    for k in new:
+        assert np.array_equal(new[k], cur[k]), k
