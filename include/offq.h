@@ -356,6 +356,48 @@ offq_status_t offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, i
                         uint16_t* v_scale, int16_t* v_zero, int64_t s_cap, float* k_y_debug,
                         float* v_y_debug, void* stream);
 
+/*
+ * offq_rope_kv_prefill -- offq_rope_kv_append for the prefill of T tokens per
+ * sequence (sec. 3.3 step 2(3), Fig. 2): row b T + t of qkv is token t of
+ * sequence b, written at position positions[b T + t] of that sequence's
+ * cache, which is [B, Hkv, s_cap, 64] (codes) and [B, Hkv, s_cap] (scales,
+ * zero-points).  q_out [B T, Hq, 128]; debug rows [B T, Hkv, 128] or NULL.
+ * T >= 1; the other arguments, the arithmetic and the errors are those of
+ * offq_rope_kv_append, which is this call with T = 1.
+ */
+offq_status_t offq_rope_kv_prefill(const uint16_t* qkv, int64_t ldq, int64_t B, int64_t T,
+                        int64_t Hq, int64_t Hkv, int32_t head_dim, const int32_t* positions,
+                        double rope_base, int32_t k_hadamard, int32_t v_hadamard,
+                        uint16_t* q_out, uint8_t* k_codes, uint16_t* k_scale, int16_t* k_zero,
+                        uint8_t* v_codes, uint16_t* v_scale, int16_t* v_zero, int64_t s_cap,
+                        float* k_y_debug, float* v_y_debug, void* stream);
+
+/*
+ * offq_kv_attention_prefill -- causal attention of T new tokens per sequence
+ * over the 4-bit KV cache (sec. 3.3 step 2(3); the per-row arithmetic of
+ * offq_kv_attention_decode_gqa): query t of sequence b sits at position
+ * past + t and attends to cache positions 0 .. past + t.
+ *   q        bf16 [B, T, Hq, 128] (device): the queries after RoPE (the
+ *            q_out of offq_rope_kv_prefill), rotated by c H inside;
+ *   k_codes, v_codes uint8 [B, Hkv, s_cap, 64]; k_scale, v_scale fp16 and
+ *            k_zero, v_zero int16 [B, Hkv, s_cap]: the cache, holding the
+ *            past + T positions read (later positions are never read);
+ *   Hq a multiple of Hkv with Hq / Hkv in {1, 2, 4, 8}; past >= 0,
+ *            past + T <= s_cap;
+ *   sm_scale score scale; v_hadamard 0 or 1 as for the decode call;
+ *   out      bf16 [B, T, Hq, 128] (row b T + t, the input of the output
+ *            projection); it may not overlap q.
+ * B = 0 or T = 0 does nothing (the pointers may then be NULL).
+ * No workspace.  Errors: OFFQ_ERR_INVALID for bad sizes, pointers or
+ * alignment (16 bytes for q and out), OFFQ_ERR_UNSUPPORTED for head_dim !=
+ * 128 or another group size.
+ */
+offq_status_t offq_kv_attention_prefill(const uint16_t* q, int64_t B, int64_t T, int64_t Hq,
+                        int64_t Hkv, int32_t head_dim, int64_t past, const uint8_t* k_codes,
+                        const uint16_t* k_scale, const int16_t* k_zero, const uint8_t* v_codes,
+                        const uint16_t* v_scale, const int16_t* v_zero, int64_t s_cap,
+                        float sm_scale, int32_t v_hadamard, uint16_t* out, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Offline calibration (sec. 3.1 top-1 PCA, sec. 3.2 group-wise offsetting,
  * sec. 3.3 steps 1-2): from calibration activations to the fused, permuted

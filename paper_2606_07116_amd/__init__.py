@@ -11,6 +11,8 @@ arguments.  Entry points (same names as ``include/offq.h``):
     offq_add_rmsnorm(x, res=None, eps=1e-5)
     offq_swiglu(gu)
     offq_rope_kv_append(qkv, Hq, Hkv, positions, cache, rope_base=500000.0, ...)
+    offq_rope_kv_prefill(qkv, B, Hq, Hkv, positions, cache, rope_base=500000.0, ...)
+    offq_kv_attention_prefill(q, cache, past, sm_scale=None, v_hadamard=False, out=None)
 
 Offline calibration: offq_top1_select, offq_channel_absmax, offq_gram, offq_eigh,
 offq_group_permutation, offq_build_rotation, offq_fuse_weights, offq_permute_rows.
@@ -37,6 +39,8 @@ _EXPORTS = frozenset((
     "offq_add_rmsnorm_quantize",
     "offq_swiglu_rotate_quantize",
     "offq_rope_kv_append",
+    "offq_rope_kv_prefill",
+    "offq_kv_attention_prefill",
     "offq_swiglu",
     "offq_kv_attention_decode",
     "offq_kv_attention_decode_quantize",

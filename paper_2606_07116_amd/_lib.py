@@ -36,6 +36,8 @@ EXPORTED = (
     "offq_add_rmsnorm",
     "offq_swiglu",
     "offq_rope_kv_append",
+    "offq_rope_kv_prefill",
+    "offq_kv_attention_prefill",
     "offq_add_rmsnorm_quantize",
     "offq_swiglu_rotate_quantize",
     "offq_top1_workspace_bytes",
@@ -103,6 +105,12 @@ def _load():
     lib.offq_rope_kv_append.restype = ctypes.c_int
     lib.offq_rope_kv_append.argtypes = [vp, i64, i64, i64, i64, i32, vp, ctypes.c_double, i32, i32,
                                         vp, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp]
+    lib.offq_rope_kv_prefill.restype = ctypes.c_int
+    lib.offq_rope_kv_prefill.argtypes = [vp, i64, i64, i64, i64, i64, i32, vp, ctypes.c_double,
+                                         i32, i32, vp, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp]
+    lib.offq_kv_attention_prefill.restype = ctypes.c_int
+    lib.offq_kv_attention_prefill.argtypes = [vp, i64, i64, i64, i64, i32, i64, vp, vp, vp, vp,
+                                              vp, vp, i64, ctypes.c_float, i32, vp, vp]
     f64 = ctypes.c_double
     sigs = {
         "offq_add_rmsnorm_quantize": (ctypes.c_int, [vp, i64, vp, i64, i64, i64, ctypes.c_float,
@@ -529,39 +537,96 @@ def offq_swiglu(gu):
     return out
 
 
+def _cache_operands(cache, B, Hkv):
+    torch = _torch()
+    s_cap = cache["k_codes"].shape[2]
+    for n in ("k_codes", "v_codes"):
+        _need(cache[n], torch.uint8, n, 4)
+        if cache[n].shape != (B, Hkv, s_cap, 64) or not cache[n].is_contiguous():
+            raise ValueError(f"{n} must be a contiguous [B, Hkv, s_cap, 64] tensor")
+    for n, dt in (("k_scale", torch.float16), ("v_scale", torch.float16), ("k_zero", torch.int16),
+                  ("v_zero", torch.int16)):
+        _need(cache[n], dt, n, 3)
+        if cache[n].shape != (B, Hkv, s_cap) or not cache[n].is_contiguous():
+            raise ValueError(f"{n} must be a contiguous [B, Hkv, s_cap] tensor")
+    return s_cap
+
+
+def _rope_kv(qkv, B, T, Hq, Hkv, positions, cache, rope_base, k_hadamard, v_hadamard, debug,
+             fn, name):
+    torch = _torch()
+    _need(qkv, torch.bfloat16, "qkv", 2)
+    _need(positions, torch.int32, "positions", 1)
+    M = qkv.shape[0]
+    if M != B * (T or 1):
+        raise ValueError("qkv must have B * T rows")
+    s_cap = _cache_operands(cache, B, Hkv)
+    if positions.shape != (M,):
+        raise ValueError("positions must have one entry per qkv row")
+    dev = qkv.device
+    q = torch.empty((M, Hq, 128), dtype=torch.bfloat16, device=dev)
+    ky = torch.empty((M, Hkv, 128), dtype=torch.float32, device=dev) if debug else None
+    vy = torch.empty((M, Hkv, 128), dtype=torch.float32, device=dev) if debug else None
+    dims = (M,) if T is None else (B, T)
+    _check(fn(_ptr(qkv), _rows(qkv, "qkv"), *dims, Hq, Hkv, 128, _ptr(positions),
+              float(rope_base), int(bool(k_hadamard)), int(bool(v_hadamard)), _ptr(q),
+              _ptr(cache["k_codes"]), _ptr(cache["k_scale"]), _ptr(cache["k_zero"]),
+              _ptr(cache["v_codes"]), _ptr(cache["v_scale"]), _ptr(cache["v_zero"]), s_cap,
+              _ptr(ky), _ptr(vy), _stream()), name)
+    return q, ky, vy
+
+
 def offq_rope_kv_append(qkv, Hq, Hkv, positions, cache, rope_base=500000.0, k_hadamard=True,
                         v_hadamard=False, debug=False):
     """qkv: bf16 [M, (Hq + 2 Hkv) * 128]; positions: int32 [M] (device);
     cache: dict with k_codes/v_codes u8 [M, Hkv, s_cap, 64] and k_scale/v_scale
     fp16, k_zero/v_zero int16 [M, Hkv, s_cap] (written in place).  Returns
     (q bf16 [M, Hq, 128], k_y fp32 [M, Hkv, 128] or None, v_y or None)."""
-    torch = _torch()
-    _need(qkv, torch.bfloat16, "qkv", 2)
-    _need(positions, torch.int32, "positions", 1)
     M = qkv.shape[0]
-    s_cap = cache["k_codes"].shape[2]
-    for n in ("k_codes", "v_codes"):
-        _need(cache[n], torch.uint8, n, 4)
-        if cache[n].shape != (M, Hkv, s_cap, 64) or not cache[n].is_contiguous():
-            raise ValueError(f"{n} must be a contiguous [M, Hkv, s_cap, 64] tensor")
-    for n, dt in (("k_scale", torch.float16), ("v_scale", torch.float16), ("k_zero", torch.int16),
-                  ("v_zero", torch.int16)):
-        _need(cache[n], dt, n, 3)
-        if cache[n].shape != (M, Hkv, s_cap) or not cache[n].is_contiguous():
-            raise ValueError(f"{n} must be a contiguous [M, Hkv, s_cap] tensor")
-    if positions.shape != (M,):
-        raise ValueError("positions must be [M]")
-    dev = qkv.device
-    q = torch.empty((M, Hq, 128), dtype=torch.bfloat16, device=dev)
-    ky = torch.empty((M, Hkv, 128), dtype=torch.float32, device=dev) if debug else None
-    vy = torch.empty((M, Hkv, 128), dtype=torch.float32, device=dev) if debug else None
-    _check(lib.offq_rope_kv_append(_ptr(qkv), _rows(qkv, "qkv"), M, Hq, Hkv, 128, _ptr(positions),
-                                   float(rope_base), int(bool(k_hadamard)), int(bool(v_hadamard)),
-                                   _ptr(q), _ptr(cache["k_codes"]), _ptr(cache["k_scale"]),
-                                   _ptr(cache["k_zero"]), _ptr(cache["v_codes"]),
-                                   _ptr(cache["v_scale"]), _ptr(cache["v_zero"]), s_cap, _ptr(ky),
-                                   _ptr(vy), _stream()), "offq_rope_kv_append")
-    return q, ky, vy
+    return _rope_kv(qkv, M, None, Hq, Hkv, positions, cache, rope_base, k_hadamard, v_hadamard,
+                    debug, lib.offq_rope_kv_append, "offq_rope_kv_append")
+
+
+def offq_rope_kv_prefill(qkv, B, Hq, Hkv, positions, cache, rope_base=500000.0, k_hadamard=True,
+                         v_hadamard=False, debug=False):
+    """The prefill form: qkv bf16 [B * T, (Hq + 2 Hkv) * 128], row b * T + t
+    token t of sequence b, written at positions[b * T + t] (int32, device)
+    of the cache [B, Hkv, s_cap, ...] (in place).  Returns (q bf16
+    [B * T, Hq, 128], k_y, v_y fp32 [B * T, Hkv, 128] or None)."""
+    M = qkv.shape[0]
+    if B <= 0 or M % B:
+        raise ValueError("qkv rows must be a multiple of B")
+    return _rope_kv(qkv, B, M // B, Hq, Hkv, positions, cache, rope_base, k_hadamard, v_hadamard,
+                    debug, lib.offq_rope_kv_prefill, "offq_rope_kv_prefill")
+
+
+def offq_kv_attention_prefill(q, cache, past, sm_scale=None, v_hadamard=False, out=None):
+    """Causal attention of T new tokens per sequence over the 4-bit cache.
+
+    q: bf16 [B, T, Hq, 128] contiguous (query t at position past + t);
+    cache: dict of the arrays [B, Hkv, s_cap, ...] holding past + T
+    positions.  Returns out bf16 [B, T, Hq, 128] (or writes ``out``)."""
+    torch = _torch()
+    _need(q, torch.bfloat16, "q", 4)
+    if not q.is_contiguous():
+        raise ValueError("q must be contiguous")
+    B, T, Hq, Dh = q.shape
+    Hkv = cache["k_codes"].shape[1]
+    s_cap = _cache_operands(cache, B, Hkv)
+    if sm_scale is None:
+        sm_scale = 1.0 / float(Dh) ** 0.5
+    if out is None:
+        out = torch.empty((B, T, Hq, Dh), dtype=torch.bfloat16, device=q.device)
+    _need(out, torch.bfloat16, "out", 4)
+    if not out.is_contiguous() or out.shape != q.shape:
+        raise ValueError("out must be a contiguous tensor shaped like q")
+    _check(lib.offq_kv_attention_prefill(_ptr(q), B, T, Hq, Hkv, Dh, int(past),
+                                         _ptr(cache["k_codes"]), _ptr(cache["k_scale"]),
+                                         _ptr(cache["k_zero"]), _ptr(cache["v_codes"]),
+                                         _ptr(cache["v_scale"]), _ptr(cache["v_zero"]), s_cap,
+                                         float(sm_scale), int(bool(v_hadamard)), _ptr(out),
+                                         _stream()), "offq_kv_attention_prefill")
+    return out
 
 
 # ------------------------------------------------------- offline calibration

@@ -78,8 +78,14 @@ hipError_t launch_add_rmsnorm_quant(const uint16_t* x, int64_t ldx, const uint16
                                     hipStream_t stream);
 hipError_t launch_swiglu_rq(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, uint8_t* codes,
                             uint16_t* scale, int16_t* zero, float* y_dbg, hipStream_t stream);
-hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq,
-                                 int64_t Hkv, const int32_t* positions, double rope_base,
+hipError_t launch_kv_attention_prefill(const uint16_t* q, int64_t B, int64_t T, int64_t Hq,
+                                       int64_t Hkv, int64_t past, const uint8_t* kc,
+                                       const uint16_t* ks, const int16_t* kz, const uint8_t* vc,
+                                       const uint16_t* vs, const int16_t* vz, int64_t s_cap,
+                                       float sm_scale, bool v_had, uint16_t* out,
+                                       hipStream_t stream);
+hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t T,
+                                 int64_t Hq, int64_t Hkv, const int32_t* positions, double rope_base,
                                  bool k_had, bool v_had, uint16_t* q_out, uint8_t* kc,
                                  uint16_t* ks, int16_t* kz, uint8_t* vc, uint16_t* vs,
                                  int16_t* vz, int64_t s_cap, float* k_dbg, float* v_dbg,

@@ -135,10 +135,12 @@ struct RopeTable {
 //   x'[i] = x[i] cos(a_i) - x[i + 64] sin(a_i),  x'[i + 64] = x[i + 64] cos(a_i) + x[i] sin(a_i)
 // with a_i = fl32(pos * inv_freq[i]).  Queries are stored as bf16; keys are
 // rounded to bf16, rotated by c H (optional) and quantized; values are
-// quantized (optionally after c H).  The cache row of token m, kv head h is
-// (m * Hkv + h) * s_cap + pos[m]; positions outside [0, s_cap) write nothing.
+// quantized (optionally after c H).  Token m belongs to sequence m / T (T = 1
+// for a decode step, T new tokens per sequence for a prefill); its cache row
+// for kv head h is ((m / T) * Hkv + h) * s_cap + pos[m]; positions outside
+// [0, s_cap) write nothing.
 __global__ __launch_bounds__(256) void rope_kv_append_kernel(
-    const uint16_t* __restrict__ qkv, int64_t ldq, int M, int Hq, int Hkv,
+    const uint16_t* __restrict__ qkv, int64_t ldq, int M, int T, int Hq, int Hkv,
     const int32_t* __restrict__ positions, RopeTable tab, int k_had, int v_had,
     uint16_t* __restrict__ q_out, uint8_t* __restrict__ kc, uint16_t* __restrict__ ks,
     int16_t* __restrict__ kz, uint8_t* __restrict__ vc, uint16_t* __restrict__ vs,
@@ -197,7 +199,7 @@ __global__ __launch_bounds__(256) void rope_kv_append_kernel(
   const uint32_t lo = __float_as_uint(p.lo);
   const uint32_t code = (quant_bits(x0, p) - lo) | ((quant_bits(x1, p) - lo) << 4);
   if (pos < 0 || (int64_t)pos >= s_cap) return;
-  const int64_t row = ((int64_t)m * Hkv + h) * s_cap + pos;
+  const int64_t row = ((int64_t)(m / T) * Hkv + h) * s_cap + pos;
   (is_v ? vc : kc)[row * (HD / 2) + lane] = (uint8_t)code;
   if (lane == 0) {
     (is_v ? vs : ks)[row] = p.s16;
@@ -436,8 +438,8 @@ hipError_t launch_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F, 
   return hipGetLastError();
 }
 
-hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq,
-                                 int64_t Hkv, const int32_t* positions, double rope_base,
+hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t T,
+                                 int64_t Hq, int64_t Hkv, const int32_t* positions, double rope_base,
                                  bool k_had, bool v_had, uint16_t* q_out, uint8_t* kc,
                                  uint16_t* ks, int16_t* kz, uint8_t* vc, uint16_t* vs,
                                  int16_t* vz, int64_t s_cap, float* k_dbg, float* v_dbg,
@@ -447,7 +449,7 @@ hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, in
     tab.inv_freq[i] = (float)__builtin_pow(rope_base, -2.0 * i / (double)HD);
   const int64_t waves = M * (Hq + 2 * Hkv);
   hipLaunchKernelGGL(rope_kv_append_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0,
-                     stream, qkv, ldq, (int)M, (int)Hq, (int)Hkv, positions, tab, k_had ? 1 : 0,
+                     stream, qkv, ldq, (int)M, (int)T, (int)Hq, (int)Hkv, positions, tab, k_had ? 1 : 0,
                      v_had ? 1 : 0, q_out, kc, ks, kz, vc, vs, vz, s_cap, k_dbg, v_dbg);
   return hipGetLastError();
 }

@@ -332,13 +332,17 @@ offq_status_t offq_swiglu(const uint16_t* gu, int64_t ldg, int64_t M, int64_t F,
   return launched(offq::launch_swiglu(gu, ldg, M, F, out, ldo, (hipStream_t)stream), "swiglu");
 }
 
-offq_status_t offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq, int64_t Hkv,
-                        int32_t head_dim, const int32_t* positions, double rope_base,
-                        int32_t k_hadamard, int32_t v_hadamard, uint16_t* q_out,
-                        uint8_t* k_codes, uint16_t* k_scale, int16_t* k_zero, uint8_t* v_codes,
-                        uint16_t* v_scale, int16_t* v_zero, int64_t s_cap, float* k_y_debug,
-                        float* v_y_debug, void* stream) {
-  if (M < 0 || Hq <= 0 || Hkv <= 0) return fail(OFFQ_ERR_INVALID, "need M >= 0, Hq, Hkv > 0");
+namespace {
+// Shared by the decode (T = 1) and prefill forms: M = B T rows, row m of
+// sequence m / T.
+offq_status_t rope_kv(const uint16_t* qkv, int64_t ldq, int64_t B, int64_t T, int64_t Hq,
+                      int64_t Hkv, int32_t head_dim, const int32_t* positions, double rope_base,
+                      int32_t k_hadamard, int32_t v_hadamard, uint16_t* q_out, uint8_t* k_codes,
+                      uint16_t* k_scale, int16_t* k_zero, uint8_t* v_codes, uint16_t* v_scale,
+                      int16_t* v_zero, int64_t s_cap, float* k_y_debug, float* v_y_debug,
+                      void* stream, const char* what) {
+  if (B < 0 || T < 1 || Hq <= 0 || Hkv <= 0)
+    return fail(OFFQ_ERR_INVALID, "need rows >= 0, T >= 1, Hq, Hkv > 0");
   if (head_dim != 128) return fail(OFFQ_ERR_UNSUPPORTED, "head_dim = %d (only 128)", head_dim);
   if (ldq < (Hq + 2 * Hkv) * 128 || ldq % 2)
     return fail(OFFQ_ERR_INVALID, "ldq must be >= (Hq + 2 Hkv) * 128 and even");
@@ -346,8 +350,11 @@ offq_status_t offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, i
   if (!(rope_base > 1.0) || rope_base > 1e30) return fail(OFFQ_ERR_INVALID, "rope_base must be > 1");
   if ((k_hadamard != 0 && k_hadamard != 1) || (v_hadamard != 0 && v_hadamard != 1))
     return fail(OFFQ_ERR_INVALID, "k_hadamard / v_hadamard must be 0 or 1");
+  if (T > (int64_t(1) << 31) || B > (int64_t(1) << 32) / T)
+    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
+  const int64_t M = B * T;
   if (M * (Hq + 2 * Hkv) > (int64_t(1) << 32) || Hq + 2 * Hkv > (1 << 20) ||
-      s_cap > (int64_t(1) << 40) / (M > 0 ? M * Hkv : 1))
+      s_cap > (int64_t(1) << 40) / (B > 0 ? B * Hkv : 1))
     return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
   if (!qkv || !positions || !q_out || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale ||
       !v_zero)
@@ -358,11 +365,72 @@ offq_status_t offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, i
     return fail(OFFQ_ERR_INVALID, "misaligned pointer (qkv, q_out, positions: 4 B; debug: 8 B)");
   if (M == 0) return ok();
   if (offq_status_t st = check_device()) return st;
-  return launched(offq::launch_rope_kv_append(qkv, ldq, M, Hq, Hkv, positions, rope_base,
+  return launched(offq::launch_rope_kv_append(qkv, ldq, M, T, Hq, Hkv, positions, rope_base,
                                               k_hadamard != 0, v_hadamard != 0, q_out, k_codes,
                                               k_scale, k_zero, v_codes, v_scale, v_zero, s_cap,
                                               k_y_debug, v_y_debug, (hipStream_t)stream),
-                  "rope_kv_append");
+                  what);
+}
+}  // namespace
+
+offq_status_t offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq, int64_t Hkv,
+                        int32_t head_dim, const int32_t* positions, double rope_base,
+                        int32_t k_hadamard, int32_t v_hadamard, uint16_t* q_out,
+                        uint8_t* k_codes, uint16_t* k_scale, int16_t* k_zero, uint8_t* v_codes,
+                        uint16_t* v_scale, int16_t* v_zero, int64_t s_cap, float* k_y_debug,
+                        float* v_y_debug, void* stream) {
+  return rope_kv(qkv, ldq, M, 1, Hq, Hkv, head_dim, positions, rope_base, k_hadamard, v_hadamard,
+                 q_out, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, s_cap, k_y_debug,
+                 v_y_debug, stream, "rope_kv_append");
+}
+
+offq_status_t offq_rope_kv_prefill(const uint16_t* qkv, int64_t ldq, int64_t B, int64_t T,
+                        int64_t Hq, int64_t Hkv, int32_t head_dim, const int32_t* positions,
+                        double rope_base, int32_t k_hadamard, int32_t v_hadamard,
+                        uint16_t* q_out, uint8_t* k_codes, uint16_t* k_scale, int16_t* k_zero,
+                        uint8_t* v_codes, uint16_t* v_scale, int16_t* v_zero, int64_t s_cap,
+                        float* k_y_debug, float* v_y_debug, void* stream) {
+  return rope_kv(qkv, ldq, B, T, Hq, Hkv, head_dim, positions, rope_base, k_hadamard, v_hadamard,
+                 q_out, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, s_cap, k_y_debug,
+                 v_y_debug, stream, "rope_kv_prefill");
+}
+
+offq_status_t offq_kv_attention_prefill(const uint16_t* q, int64_t B, int64_t T, int64_t Hq,
+                        int64_t Hkv, int32_t head_dim, int64_t past, const uint8_t* k_codes,
+                        const uint16_t* k_scale, const int16_t* k_zero, const uint8_t* v_codes,
+                        const uint16_t* v_scale, const int16_t* v_zero, int64_t s_cap,
+                        float sm_scale, int32_t v_hadamard, uint16_t* out, void* stream) {
+  if (B < 0 || T < 0 || Hq <= 0 || Hkv <= 0 || past < 0)
+    return fail(OFFQ_ERR_INVALID, "need B, T, past >= 0 and Hq, Hkv > 0");
+  if (head_dim != 128) return fail(OFFQ_ERR_UNSUPPORTED, "head_dim = %d (only 128)", head_dim);
+  if (Hq % Hkv) return fail(OFFQ_ERR_INVALID, "Hq = %lld is not a multiple of Hkv = %lld",
+                            (long long)Hq, (long long)Hkv);
+  const int64_t G = Hq / Hkv;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(OFFQ_ERR_UNSUPPORTED, "Hq / Hkv = %lld (supported: 1, 2, 4, 8)", (long long)G);
+  if (past + T > s_cap) return fail(OFFQ_ERR_INVALID, "past + T exceeds s_cap");
+  if (v_hadamard != 0 && v_hadamard != 1) return fail(OFFQ_ERR_INVALID, "v_hadamard must be 0 or 1");
+  if (!(sm_scale > 0.0f) || sm_scale > 1e30f) return fail(OFFQ_ERR_INVALID, "sm_scale must be > 0");
+  if (T > (int64_t(1) << 30) || past > (int64_t(1) << 30) || Hq > (1 << 16) ||
+      B * T > (int64_t(1) << 31) / Hq || B * Hkv * ((T + 31) / 32) > (int64_t(1) << 31) ||
+      s_cap > (int64_t(1) << 40) / (B > 0 ? B * Hkv : 1))
+    return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");
+  if (B == 0 || T == 0) return ok();
+  if (!q || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale || !v_zero || !out)
+    return fail(OFFQ_ERR_INVALID, "null pointer argument");
+  if (!aligned(q, 16) || !aligned(out, 16) || !aligned(k_codes, 16) || !aligned(v_codes, 16) ||
+      !aligned(k_scale, 2) || !aligned(k_zero, 2) || !aligned(v_scale, 2) || !aligned(v_zero, 2))
+    return fail(OFFQ_ERR_INVALID, "misaligned pointer (q, out, codes: 16 B; scales: 2 B)");
+  const int64_t n = B * T * Hq * 128 * 2;
+  const uintptr_t qa = (uintptr_t)q, oa = (uintptr_t)out;
+  if (n > 0 && qa < oa + (uintptr_t)n && oa < qa + (uintptr_t)n)
+    return fail(OFFQ_ERR_INVALID, "out overlaps q");
+  if (offq_status_t st = check_device()) return st;
+  return launched(offq::launch_kv_attention_prefill(q, B, T, Hq, Hkv, past, k_codes, k_scale,
+                                                    k_zero, v_codes, v_scale, v_zero, s_cap,
+                                                    sm_scale, v_hadamard != 0, out,
+                                                    (hipStream_t)stream),
+                  "kv_attention_prefill");
 }
 
 int64_t offq_top1_workspace_bytes(int64_t n_seq, int64_t seq_len) {
