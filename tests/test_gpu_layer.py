@@ -1,8 +1,8 @@
 """GPU parity: the decoder-layer steps (offq_add_rmsnorm, offq_swiglu,
 offq_rope_kv_append, grouped-query offq_kv_attention_decode) against
-oracle/layer.py, and one whole decode step of a Llama-3-8B-shaped layer
-(D 4096, 32 query / 8 key-value heads, MLP 14336, g = 128) against the oracle
-chain.
+oracle/layer.py, and one whole decode step and one whole prefill of a
+Llama-3-8B-shaped layer (D 4096, 32 query / 8 key-value heads, MLP 14336,
+g = 128) against the oracle chain.
 
 Bars: the residual sum h = bf16(fl32(x + r)) is bit-exact; bf16 outputs of
 fp32 arithmetic (RMSNorm, SwiGLU, RoPE) are within one bf16 ulp of the
@@ -224,11 +224,13 @@ def _llama_layer(M, ctx, seed=0, D=4096, Hq=32, Hkv=8, F=14336, g=128):
     return x, wf, cache, np.full(M, ctx, np.int32), ctx + 1, cfg
 
 
-def run_gpu_layer(x, wpk, cache, pos, seq_len, cfg, debug=False, fused=False):
+def run_gpu_layer(x, wpk, cache, pos, seq_len, cfg, debug=False, fused=False, prefill=None):
     """One decode step through the C ABI: the sequence of library calls a
     serving loop makes for a layer (fused: the norm steps and the SwiGLU step
     each merged with the quantizer that follows them).  With debug, also the
-    rows the quantizers saw (the rotated MLP down input, the new K/V rows)."""
+    rows the quantizers saw (the rotated MLP down input, the new K/V rows).
+    With prefill = (B, past): the prefill of T = rows / B tokens per
+    sequence instead (row b T + t at position past + t; seq_len unused)."""
     Hq, Hkv, g, eps = cfg["Hq"], cfg["Hkv"], cfg["g"], cfg["eps"]
     M = x.shape[0]
     if fused:
@@ -237,10 +239,17 @@ def run_gpu_layer(x, wpk, cache, pos, seq_len, cfg, debug=False, fused=False):
         _, y0 = offq.offq_add_rmsnorm(x, None, eps, want_h=False)
         c, s, z, _ = offq.offq_rotate_quantize(y0, g, apply_hadamard=False)
     qkv, _ = offq.offq_w4a4_gemm(c, s, z, *wpk["qkv"], g)
-    q, ky, vy = offq.offq_rope_kv_append(qkv, Hq, Hkv, pos, cache, rope_base=cfg["rope_base"],
-                                         debug=debug)
-    o = offq.offq_kv_attention_decode(q, cache["k_codes"], cache["k_scale"], cache["k_zero"],
-                                      cache["v_codes"], cache["v_scale"], cache["v_zero"], seq_len)
+    if prefill is None:
+        q, ky, vy = offq.offq_rope_kv_append(qkv, Hq, Hkv, pos, cache, rope_base=cfg["rope_base"],
+                                             debug=debug)
+        o = offq.offq_kv_attention_decode(q, cache["k_codes"], cache["k_scale"], cache["k_zero"],
+                                          cache["v_codes"], cache["v_scale"], cache["v_zero"],
+                                          seq_len)
+    else:
+        B, past = prefill
+        q, ky, vy = offq.offq_rope_kv_prefill(qkv, B, Hq, Hkv, pos, cache,
+                                              rope_base=cfg["rope_base"], debug=debug)
+        o = offq.offq_kv_attention_prefill(q.view(B, M // B, Hq, 128), cache, past).view(M, Hq, 128)
     c, s, z, _ = offq.offq_rotate_quantize(o.reshape(M, Hq * 128), g, apply_hadamard=False)
     attn_out, _ = offq.offq_w4a4_gemm(c, s, z, *wpk["o"], g)
     if fused:
@@ -332,5 +341,75 @@ def test_decode_layer_chain(M, ctx, fused):
     # them (measured: 0.05 % at the attention output, 10 % on the MLP down
     # output, ~1 % on the residual stream); the bar bounds the residual stream
     ref, _, _ = OL.decode_layer(x, weights, cache, pos, seq_len, cfg)
+    rel = np.linalg.norm(P.host(out.float()) - ref) / np.linalg.norm(ref)
+    assert rel < 5e-2, rel
+
+
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("B,T,past", [(2, 40, 30), (1, 96, 0)])
+def test_prefill_layer_chain(B, T, past, fused):
+    """The prefill of T tokens per sequence through a Llama-3-8B-shaped layer
+    (the QKV/O/up/down projections at B T rows): each GPU step meets its bar
+    against the oracle step fed the previous GPU step's output; the new cache
+    rows are the oracle quantizer's of the GPU's rows; the attention meets
+    the prefill attention bar over the cache the GPU wrote; end to end the
+    output stays close to the oracle's prefill layer from the same inputs."""
+    from tests.test_gpu_prefill import _magnitude
+    M, D, Hq, Hkv, F, g = B * T, 4096, 32, 8, 14336, 128
+    rng = np.random.default_rng(B * T + past)
+    x = inputs.round_to_bf16(rng.standard_normal((M, D)).astype(np.float32))
+    shapes = {"qkv": ((Hq + 2 * Hkv) * 128, D), "o": (D, Hq * 128), "ug": (2 * F, D), "down": (D, F)}
+    wf = {k: inputs.weights(*s, seed=past + i, std=1.0 / math.sqrt(s[1]))
+          for i, (k, s) in enumerate(shapes.items())}
+    s_cap = past + T + 3
+    kc, ks, kz = inputs.kv4_cache(B, Hkv, s_cap, 128, seed=T)
+    vc, vs, vz = inputs.kv4_cache(B, Hkv, s_cap, 128, seed=T + 1)
+    cache = dict(k_codes=kc, k_scale=ks, k_zero=kz, v_codes=vc, v_scale=vs, v_zero=vz)
+    cfg = dict(Hq=Hq, Hkv=Hkv, g=g, eps=1e-5, rope_base=500000.0)
+    weights = {k: OQ.quantize_weights(w) for k, w in wf.items()}
+    wpk = {k: offq.offq_pack_weights(torch.from_numpy(w).to(P.DEV), g) for k, w in wf.items()}
+    dcache = {k: torch.from_numpy(np.ascontiguousarray(v)).to(P.DEV) for k, v in cache.items()}
+    pos = (past + np.tile(np.arange(T), B)).astype(np.int32)
+    out, it = run_gpu_layer(_bf16_dev(x), wpk, dcache, torch.from_numpy(pos).to(P.DEV), None, cfg,
+                            debug=True, fused=fused, prefill=(B, past))
+    torch.cuda.synchronize()
+    H = {k: (P.host(v.float()) if v.dtype == torch.bfloat16 else P.host(v))
+         for k, v in it.items() if v is not None}
+    if fused:
+        H["a"] = OL.bf16(OL.swiglu(H["gu"]))
+    _within_ulp(H["y0"], OL.add_rmsnorm(x, None, 1e-5)[1])
+    h1_ref, y1_ref = OL.add_rmsnorm(x, H["attn_out"], 1e-5)
+    assert np.array_equal(H["h1"], h1_ref)
+    _within_ulp(H["y1"], y1_ref)
+    assert np.array_equal(P.host(out.float()), OL.add_rmsnorm(H["h1"], H["down"], 1e-5)[0])
+    _gemm_bar(H["qkv"], H["y0"], weights["qkv"], g)
+    _gemm_bar(H["attn_out"], H["o"].reshape(M, -1), weights["o"], g)
+    _gemm_bar(H["gu"], H["y1"], weights["ug"], g)
+    from oracle import hadamard as OH
+    flips = OG.bf16_ulp(H["a"]).reshape(M, -1, g).sum(-1).repeat(g, -1) if fused else 0.0
+    assert np.all(np.abs(H["a_rot"] - OH.rotate(H["a"], g)) <=
+                  (9 * 2.0 ** -24 * np.abs(H["a"]).reshape(M, -1, g).sum(-1).repeat(g, -1) + flips)
+                  / math.sqrt(g))
+    _gemm_bar(H["down"], H["a"], weights["down"], g, y_rot=H["a_rot"])
+    # RoPE + the new cache rows, at positions past .. past + T - 1 of each sequence
+    q_ref, _, vy_ref = OL.kv_rows(H["qkv"], Hq, Hkv, pos, cfg["rope_base"])
+    _within_ulp(H["q"], OL.bf16(q_ref), atol=1e-6 * np.abs(q_ref).max())
+    assert np.array_equal(H["v_y"], vy_ref)
+    for name in ("k", "v"):
+        codes, _, _ = OKV.kv_quantize(H[name + "_y"].reshape(-1, 128))
+        got = P.host(dcache[name + "_codes"])[:, :, past:past + T]
+        want = OQ.pack_nibbles(codes).reshape(B, T, Hkv, 64).transpose(0, 2, 1, 3)
+        assert np.array_equal(got, want), name
+    # causal attention over the cache the GPU wrote, with the GPU's queries
+    hc = {k: P.host(v) for k, v in dcache.items()}
+    c6 = (hc["k_codes"], hc["k_scale"], hc["k_zero"], hc["v_codes"], hc["v_scale"], hc["v_zero"])
+    qg = H["q"].reshape(B, T, Hq, 128)
+    o_ref = OA.prefill_attention(qg, *c6, past, 1 / math.sqrt(128))
+    mag = _magnitude(qg, *c6, past, 1 / math.sqrt(128), list(range(T)))
+    o_got = H["o"].reshape(B, T, Hq, 128)
+    assert np.all(np.abs(o_got - o_ref) <= 2.0 ** -8 * (1 + 2.0 ** -5) * np.abs(o_ref) + 2.0 ** -11 * mag)
+    # end to end (the decode chain's bar: 4-bit decisions flip downstream of
+    # rounding-order differences and each quantized layer amplifies them)
+    ref, _, _ = OL.prefill_layer(x, weights, cache, past, cfg)
     rel = np.linalg.norm(P.host(out.float()) - ref) / np.linalg.norm(ref)
     assert rel < 5e-2, rel
