@@ -48,6 +48,7 @@ sys.path.insert(0, ROOT)
 METRIC = "W4A4 offset-GEMM int TOPS (prefill) + quantize/decode HBM GB/s vs peak"
 PEAK_INT8_TOPS = 5000.0     # MI355X dense int8 MFMA, 5.0 POP/s
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, 8 TB/s
+PEAK_FP16_TFLOPS = 2500.0   # MI355X dense fp16 / bf16 MFMA, 2.5 PFLOP/s
 LLC_BYTES = 256 << 20       # MI355X Infinity Cache
 
 
@@ -58,7 +59,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="mlp_prefill",
                    choices=["attn_proj_prefill", "mlp_prefill", "decode", "kv_chain",
-                            "kv_decode_attention", "decode_layer", "calibration"])
+                            "kv_decode_attention", "decode_layer", "prefill_layer",
+                            "calibration"])
     p.add_argument("--decode-m", type=int, default=16)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-components", action="store_true",
@@ -446,6 +448,49 @@ def main():
                   "output quantized in its combine pass, O GEMV, add + RMSNorm + quantize, "
                   "up/gate GEMV, SwiGLU + H4 + quantize, down GEMV (its residual add is the next "
                   "layer's first add)", "input_sets": lsets.n}
+    elif wl == "prefill_layer":
+        lc = inputs.WORKLOADS["prefill_layer"]
+        Bp, Tp, past = lc["B"], lc["T"], lc["past"]
+        M, D, Hq, Hkv, F, g = Bp * Tp, lc["D"], lc["Hq"], lc["Hkv"], lc["F"], lc["g"]
+        s_cap = past + Tp
+        NQKV = (Hq + 2 * Hkv) * 128
+        lshapes = {"qkv": (NQKV, D), "o": (D, Hq * 128), "ug": (2 * F, D), "down": (D, F)}
+        bf, u8, f16, i16 = torch.bfloat16, torch.uint8, torch.float16, torch.int16
+
+        def make_prefill(i):
+            sd = lc["seed"] + 100 * i
+            gen = torch.Generator(device="cuda")
+            gen.manual_seed(sd)
+            st = {"x": torch.randn((M, D), generator=gen, device="cuda").to(bf)}
+            for j, (k, (n_, k_)) in enumerate(lshapes.items()):
+                w = inputs.weights_device(n_, k_, seed=sd + j, device="cuda", std=1.0 / k_ ** 0.5)
+                st["w_" + k] = offq.offq_pack_weights(w, g)
+                del w
+            kc_, ks_, kz_ = inputs.kv4_cache_device(Bp, Hkv, s_cap, 128, seed=sd, device="cuda")
+            vc_, vs_, vz_ = inputs.kv4_cache_device(Bp, Hkv, s_cap, 128, seed=sd + 1, device="cuda")
+            st.update(kc=kc_, ks=ks_, kz=kz_, vc=vc_, vs=vs_, vz=vz_,
+                      pos=(past + torch.arange(Tp, dtype=torch.int32, device="cuda")).repeat(Bp))
+            e = lambda *sh, dt=bf: torch.empty(sh, dtype=dt, device="cuda")
+            st.update(qkv=e(M, NQKV), q=e(M, Hq, 128), o=e(M, Hq, 128), ao=e(M, D), h0=e(M, D),
+                      h1=e(M, D), gu=e(M, 2 * F), dn=torch.zeros((M, D), dtype=bf, device="cuda"))
+            for name, K_ in (("c_in", D), ("c_o", Hq * 128), ("c_d", F)):
+                st[name] = (e(M, K_ // 2, dt=u8), e(M, K_ // g, dt=f16), e(M, K_ // g, dt=i16))
+            return st
+
+        lbytes = sum(weight_bytes(n_, k_, g) for n_, k_ in lshapes.values())
+        lsets = Sets(make_prefill, lbytes + M * (D * 2 * 8 + NQKV * 2 + F * 6))
+        layers = []
+        gemm_shapes = {"w4a4_gemm_qkv": (NQKV, D), "w4a4_gemm_o": (D, Hq * 128),
+                       "w4a4_gemm_upgate": (2 * F, D), "w4a4_gemm_down": (D, F)}
+        work_ops = sum(2.0 * M * n_ * k_ for n_, k_ in gemm_shapes.values())
+        # causal attention: 2 * 128 multiply-adds per (query, attended key) for
+        # the scores and as many for the values
+        attn_flops = 4.0 * 128 * Bp * Hq * (Tp * past + Tp * (Tp + 1) / 2)
+        config = {"workload": wl, "B": Bp, "T": Tp, "past": past, "D": D, "heads": [Hq, Hkv],
+                  "mlp": F, "g": g, "step": "add (the previous layer's residual) + RMSNorm + "
+                  "quantize, QKV GEMM, RoPE + H3 + KV4 write of the T tokens, causal attention "
+                  "over the 4-bit cache, quantize, O GEMM, add + RMSNorm + quantize, up/gate GEMM, "
+                  "SwiGLU + H4 + quantize, down GEMM", "input_sets": lsets.n}
     else:  # decode
         up = regroup(inputs.WORKLOADS["decode_up"])
         dn = regroup(inputs.WORKLOADS["decode_down"])
@@ -549,6 +594,63 @@ def main():
             return gemm(st, "c_d", F, D, "w_down", st["dn"])
         # the whole layer is one phase: its kernels depend on each other
         phases.append(("decode_layer", step_layer))
+    if wl == "prefill_layer":
+        eps, base, sm = 1e-5, 500000.0, 1.0 / 128 ** 0.5
+        P_ = lambda t: t.data_ptr()
+
+        def pgemm(name, cname, K_, N_, wname, dst):
+            def f(i):
+                st = lsets[i]
+                c_, s_, z_ = st[cname]
+                wc_, ws_, wcs_ = st[wname]
+                return _lib.offq_w4a4_gemm_raw(P_(c_), P_(s_), P_(z_), P_(wc_), P_(ws_), P_(wcs_),
+                                               M, N_, K_, g, P_(st[dst]), N_, None, sp)
+            return (name, f)
+
+        def pnorm(name, xname, rname, hname):
+            def f(i):
+                st = lsets[i]
+                c_, s_, z_ = st["c_in"]
+                return _lib.offq_add_rmsnorm_quantize_raw(
+                    P_(st[xname]), D, P_(st[rname]), D, M, D, eps, g, P_(st[hname]), D, P_(c_),
+                    P_(s_), P_(z_), None, 0, sp)
+            return (name, f)
+
+        def p_rope(i):
+            st = lsets[i]
+            return _lib.offq_rope_kv_prefill_raw(
+                P_(st["qkv"]), NQKV, Bp, Tp, Hq, Hkv, 128, P_(st["pos"]), base, 1, 0, P_(st["q"]),
+                P_(st["kc"]), P_(st["ks"]), P_(st["kz"]), P_(st["vc"]), P_(st["vs"]), P_(st["vz"]),
+                s_cap, None, None, sp)
+
+        def p_attn(i):
+            st = lsets[i]
+            return _lib.offq_kv_attention_prefill_raw(
+                P_(st["q"]), Bp, Tp, Hq, Hkv, 128, past, P_(st["kc"]), P_(st["ks"]), P_(st["kz"]),
+                P_(st["vc"]), P_(st["vs"]), P_(st["vz"]), s_cap, sm, 0, P_(st["o"]), sp)
+
+        def p_quant_o(i):
+            st = lsets[i]
+            c_, s_, z_ = st["c_o"]
+            return _lib.offq_rotate_quantize_raw(P_(st["o"]), M, Hq * 128, Hq * 128, g, 0, P_(c_),
+                                                 P_(s_), P_(z_), None, sp)
+
+        def p_swiglu(i):
+            st = lsets[i]
+            c_, s_, z_ = st["c_d"]
+            return _lib.offq_swiglu_rotate_quantize_raw(P_(st["gu"]), 2 * F, M, F, P_(c_), P_(s_),
+                                                        P_(z_), None, sp)
+        # steady state as in the decode layer: the previous layer's residual
+        # add (x + dn) is this layer's first step
+        phases += [pnorm("add_rmsnorm_quantize_in", "x", "dn", "h0"),
+                   pgemm("w4a4_gemm_qkv", "c_in", D, NQKV, "w_qkv", "qkv"),
+                   ("rope_kv_prefill", p_rope), ("kv_attention_prefill", p_attn),
+                   ("rotate_quantize_o", p_quant_o),
+                   pgemm("w4a4_gemm_o", "c_o", Hq * 128, D, "w_o", "ao"),
+                   pnorm("add_rmsnorm_quantize_post", "h0", "ao", "h1"),
+                   pgemm("w4a4_gemm_upgate", "c_in", D, 2 * F, "w_ug", "gu"),
+                   ("swiglu_rotate_quantize", p_swiglu),
+                   pgemm("w4a4_gemm_down", "c_d", F, D, "w_down", "dn")]
     if wl == "kv_decode_attention":
         def run_attn(i):
             a_ = asets[i]
@@ -616,6 +718,19 @@ def main():
         value = comp[name]["GBs"]
         unit = "GB/s"
         roof = hbm_roof(comp, name, None)
+    elif wl == "prefill_layer":
+        for name, (n_, k_) in gemm_shapes.items():
+            ann_mm(comp[name], M, n_, k_)
+        ca = comp["kv_attention_prefill"]
+        ca["alg_flops"] = attn_flops
+        ca["TFLOPs"] = round(attn_flops / (ca["us"] * 1e-6) / 1e12, 1)
+        ca["frac_fp16_peak"] = round(ca["TFLOPs"] / PEAK_FP16_TFLOPS, 4)
+        if "median_us" in ca:
+            ca["TFLOPs_median"] = round(attn_flops / (ca["median_us"] * 1e-6) / 1e12, 1)
+        value = work_ops / (ms * 1e-3) / 1e12
+        unit = "TOPS"
+        config["tokens_per_s"] = round(M / (ms * 1e-3), 1)
+        roof = mfma_roof(comp, "w4a4_gemm_upgate", None)
     elif wl == "kv_decode_attention":
         name = "kv_attention_decode"
         ann_bytes(comp[name], attn_bytes(B * H, S, Dh))

@@ -240,6 +240,22 @@ def offq_rope_kv_append_raw(qkv, ldq, M, Hq, Hkv, head_dim, positions, rope_base
                                    v_zero, s_cap, k_y_debug, v_y_debug, stream)
 
 
+def offq_rope_kv_prefill_raw(qkv, ldq, B, T, Hq, Hkv, head_dim, positions, rope_base, k_hadamard,
+                             v_hadamard, q_out, k_codes, k_scale, k_zero, v_codes, v_scale,
+                             v_zero, s_cap, k_y_debug, v_y_debug, stream):
+    return lib.offq_rope_kv_prefill(qkv, ldq, B, T, Hq, Hkv, head_dim, positions, rope_base,
+                                    k_hadamard, v_hadamard, q_out, k_codes, k_scale, k_zero,
+                                    v_codes, v_scale, v_zero, s_cap, k_y_debug, v_y_debug, stream)
+
+
+def offq_kv_attention_prefill_raw(q, B, T, Hq, Hkv, head_dim, past, k_codes, k_scale, k_zero,
+                                  v_codes, v_scale, v_zero, s_cap, sm_scale, v_hadamard, out,
+                                  stream):
+    return lib.offq_kv_attention_prefill(q, B, T, Hq, Hkv, head_dim, past, k_codes, k_scale,
+                                         k_zero, v_codes, v_scale, v_zero, s_cap, sm_scale,
+                                         v_hadamard, out, stream)
+
+
 # ------------------------------------------------------------ tensor wrappers
 def _torch():
     import torch

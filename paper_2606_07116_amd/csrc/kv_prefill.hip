@@ -25,7 +25,8 @@
 // * per-key parameters (score slope and offset, sv, zv) reach the lane that
 //   needs them through DPP row_newbcast, folded into the arithmetic
 //   instruction that uses them;
-// * V is transposed once per workgroup into LDS as fp16 code values (keys
+// * K and V are unpacked once per workgroup into LDS as fp16 code values,
+//   K in the operand order of the score product, V transposed (keys
 //   permuted to match the accumulator rows of S^T), shared by all waves.
 //
 // Organisation: one workgroup per (sequence b, kv head, 32 NW / G query
@@ -34,6 +35,8 @@
 // positions of sub-tile w / G.  Keys stream in blocks of 64 through a double-buffered LDS stage;
 // a wave skips the blocks past its last query and masks the diagonal ones.
 // Workgroups with the most keys launch first.
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -42,18 +45,20 @@ namespace {
 
 constexpr int PD = 128;     // head dimension
 constexpr int KB = 64;      // keys per block
-constexpr int KROW = 80;    // LDS bytes per key row of codes (64 + 16 padding)
+constexpr int KROW = 272;   // LDS bytes per key row: 128 fp16 code values + 16 padding
 constexpr int VROW = 144;   // LDS bytes per dimension row of V^T (64 fp16 + 16 padding)
 constexpr float PLOG2E = 1.4426950408889634f;
+constexpr float TAU = 8.0f;  // lazy rescaling: a reference maximum may lag by up to 2^8
 
 typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
 typedef float f16v_t __attribute__((ext_vector_type(16)));
 
 struct Stage {
-  uint8_t k[KB * KROW];   // key codes, one padded row per key
+  uint8_t k[KB * KROW];   // key codes as fp16 c 2^-24 (16 c 2^-24), operand order
   uint8_t vt[PD * VROW];  // V^T: per dimension, the 64 keys' codes as fp16 c 2^-24
   float4 sc[KB];          // per key: (score slope, score offset / sum q, sv, zv)
+  float tau;              // how far a row maximum may pass its reference unrescaled
 };
 
 __device__ __forceinline__ uint32_t pk_f16(float a, float b) {
@@ -196,7 +201,16 @@ __global__ __launch_bounds__(G < 4 ? 256 : 64 * G, G < 8 ? 2 : 1) void kv_prefil
   };
   auto store = [&](int kb, Stage& S) {
     if (tid < 256) {
-      *reinterpret_cast<uint4*>(S.k + (tid >> 2) * KROW + 16 * (tid & 3)) = kreg;
+      // code word i of the key row (8 dims) -> the 8 fp16 operand values of
+      // one k-step: (d0, d4), (16 d1, 16 d5), (d2, d6), (16 d3, 16 d7)
+      uint4* kd = reinterpret_cast<uint4*>(S.k + (tid >> 2) * KROW + 64 * (tid & 3));
+      const uint32_t kw4[4] = {kreg.x, kreg.y, kreg.z, kreg.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t u = kw4[i];
+        kd[i] = make_uint4(u & 0x000F000Fu, u & 0x00F000F0u, (u >> 8) & 0x000F000Fu,
+                           (u >> 8) & 0x00F000F0u);
+      }
       const int kp = tid & 31, dc = tid >> 5;
       uint32_t* vt = reinterpret_cast<uint32_t*>(S.vt + 16 * dc * VROW + 2 * vt_pos(2 * kp));
 #pragma unroll
@@ -216,9 +230,15 @@ __global__ __launch_bounds__(G < 4 ? 256 : 64 * G, G < 8 ? 2 : 1) void kv_prefil
         // log2-domain score = a dot + b sum(q_r), dot = 2^(-9-e) sum q_r c
         const bool valid = kb * KB + tid < nk;
         const float skm = sm2 * fp16_bits_to_f32(r_ks);
+        const float svf = valid ? fp16_bits_to_f32(r_vs) : 0.0f;
         S.sc[tid] = valid ? make_float4(__builtin_amdgcn_ldexpf(skm, 9 + e), -skm * (float)r_kz,
-                                        fp16_bits_to_f32(r_vs), (float)r_vz)
+                                        svf, (float)r_vz)
                           : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        // a weight p sv with p <= 2^tau stays below 65000 (finite in fp16)
+        float mx = fabsf(svf);
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+        if (tid == 0) S.tau = fminf(TAU, mx > 0.0f ? __builtin_log2f(65000.0f / mx) : TAU);
       }
     }
   };
@@ -243,103 +263,96 @@ __global__ __launch_bounds__(G < 4 ? 256 : 64 * G, G < 8 ? 2 : 1) void kv_prefil
     if (live && kb * KB <= pmax) {
       // ---- S^T = K Q^T: two 32-key tiles ---------------------------------
       f16v_t sacc[2];
-      uint4 kw[2][2];
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt) {
-        const uint4* kr = reinterpret_cast<const uint4*>(S.k + (32 * tt + ql) * KROW + 32 * h);
-        kw[tt][0] = kr[0];
-        kw[tt][1] = kr[1];
+      for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[tt][r] = 0.0f;
-      }
+      // tile 0's chain first, then tile 1's: tile 0's softmax can start
+      // while tile 1's products are still on the matrix cores
 #pragma unroll
-      for (int s = 0; s < 8; ++s)
+      for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int tt = 0; tt < 2; ++tt) {
-          const uint4 kv = kw[tt][s >> 2];
-          const uint32_t u = (s & 3) == 0 ? kv.x : (s & 3) == 1 ? kv.y : (s & 3) == 2 ? kv.z : kv.w;
-          const uint32_t a4[4] = {u & 0x000F000Fu, u & 0x00F000F0u, (u >> 8) & 0x000F000Fu,
-                                  (u >> 8) & 0x00F000F0u};
+        for (int s = 0; s < 8; ++s) {
+          // lane (key, half h), k-step s: code word 8 h + s of the key row
+          const uint4 a = *reinterpret_cast<const uint4*>(S.k + (32 * tt + ql) * KROW +
+                                                          16 * (8 * h + s));
           const uint32_t b4[4] = {qb[s][0], qb[s][1], qb[s][2], qb[s][3]};
-          sacc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8_t, a4),
+          sacc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8_t, a),
                                                             __builtin_bit_cast(h8_t, b4),
                                                             sacc[tt], 0, 0, 0);
         }
 
-      // ---- scores, causal mask, running max -------------------------------
-      const float4 sc0 = S.sc[kap], sc1 = S.sc[32 + kap];
-      float sv[2][16];
-#define PF_SCORE(R)                                                               \
-  sv[0][R] = __builtin_fmaf(bcast<R>(sc0.x), sacc[0][R], bcast<R>(sc0.y) * qsum); \
-  sv[1][R] = __builtin_fmaf(bcast<R>(sc1.x), sacc[1][R], bcast<R>(sc1.y) * qsum);
-      PF_FOR16(PF_SCORE)
+      // One 32-key tile: scores, causal mask, running maximum, the weights
+      // w = fp16(p sv) as the B operand of O^T += V^T W^T and that product.
+      // Tile by tile, so that one tile's VALU work overlaps the other's MFMAs.
+      auto tile = [&](auto tile_c) {
+        constexpr int TT = decltype(tile_c)::value;
+        const float4 sc = S.sc[32 * TT + kap];
+        float sv[16];
+#define PF_SCORE(R) sv[R] = __builtin_fmaf(bcast<R>(sc.x), sacc[TT][R], bcast<R>(sc.y) * qsum);
+        PF_FOR16(PF_SCORE)
 #undef PF_SCORE
-      if (kb * KB + KB - 1 > pmin) {
-        const int kbase = kb * KB + 4 * h - pq;  // key - pq = kbase + 32 tt + 8 (r / 4) + r % 4
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
+        if (kb * KB + 32 * TT + 31 > pmin) {
+          const int kbase = kb * KB + 32 * TT + 4 * h - pq;  // key - pq = kbase + 8 (r / 4) + r % 4
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            if (kbase + 32 * tt + 8 * (r >> 2) + (r & 3) > 0) sv[tt][r] = -__builtin_inff();
-      }
-      float bm = sv[0][0];
+            if (kbase + 8 * (r >> 2) + (r & 3) > 0) sv[r] = -__builtin_inff();
+        }
+        float bm = sv[0];
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
+        for (int r = 1; r < 16; ++r) bm = fmaxf(bm, sv[r]);
+        bm = fmaxf(bm, __shfl_xor(bm, 32));
+        // The reference m of a row only moves when the tile's maximum passes
+        // it by more than tau (then every row moves to its own maximum): the
+        // weights stay below 2^tau (finite in fp16 by the choice of tau),
+        // their relative rounding is unchanged, and the O rescale runs rarely.
+        if (__builtin_amdgcn_ballot_w64(bm > m + fmaxf(S.tau, 0.0f))) {
+          const float mn = fmaxf(m, bm);
+          const float f = __builtin_amdgcn_exp2f(m - mn);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) bm = fmaxf(bm, sv[tt][r]);
-      bm = fmaxf(bm, __shfl_xor(bm, 32));
-      const float mn = fmaxf(m, bm);
-      if (__builtin_amdgcn_ballot_w64(mn > m)) {
-        const float f = __builtin_amdgcn_exp2f(m - mn);
+          for (int d = 0; d < 4; ++d)
 #pragma unroll
-        for (int d = 0; d < 4; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[d][r] *= f;
-        l *= f;
-        zs *= f;
-        m = mn;
-      }
-
-      // ---- weights w = fp16(p sv) as the B operand of O^T = V^T W^T -------
-      uint32_t wb[4][4];
+            for (int r = 0; r < 16; ++r) oacc[d][r] *= f;
+          l *= f;
+          zs *= f;
+          m = mn;
+        }
 #define PF_WEIGHT(R)                                                          \
   {                                                                           \
-    const float p0 = __builtin_amdgcn_exp2f(sv[0][R] - m);                    \
-    const float p1 = __builtin_amdgcn_exp2f(sv[1][R] - m);                    \
-    l += p0 + p1;                                                             \
-    sv[0][R] = p0 * bcast<R>(sc0.z);                                          \
-    sv[1][R] = p1 * bcast<R>(sc1.z);                                          \
+    const float p = __builtin_amdgcn_exp2f(sv[R] - m);                        \
+    l += p;                                                                   \
+    float w = bcast<R>(sc.z) * p;                                             \
+    asm volatile("" : "+v"(w)); /* keep the DPP multiply */                   \
+    sv[R] = w;                                                                \
   }
-      PF_FOR16(PF_WEIGHT)
+        PF_FOR16(PF_WEIGHT)
 #undef PF_WEIGHT
+        uint32_t wb[2][4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int tt = k >> 1, r0 = 8 * (k & 1);
+        for (int k = 0; k < 2; ++k)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) wb[k][j] = pk_f16(sv[tt][r0 + 2 * j], sv[tt][r0 + 2 * j + 1]);
-      }
-      // the zero-point term with the rounded weights
-#define PF_ZSUM(R)                                                                                 \
-  {                                                                                                \
-    const h2_t w0 = __builtin_bit_cast(h2_t, wb[(R) >> 3][((R) & 7) >> 1]);                        \
-    const h2_t w1 = __builtin_bit_cast(h2_t, wb[2 + ((R) >> 3)][((R) & 7) >> 1]);                  \
-    zs = __builtin_fmaf((float)((R) & 1 ? w0.y : w0.x), bcast<R>(sc0.w), zs);                      \
-    zs = __builtin_fmaf((float)((R) & 1 ? w1.y : w1.x), bcast<R>(sc1.w), zs);                      \
+          for (int j = 0; j < 4; ++j) wb[k][j] = pk_f16(sv[8 * k + 2 * j], sv[8 * k + 2 * j + 1]);
+        // the zero-point term with the rounded weights
+#define PF_ZSUM(R)                                                                    \
+  {                                                                                   \
+    const h2_t w2 = __builtin_bit_cast(h2_t, wb[(R) >> 3][((R) & 7) >> 1]);           \
+    zs = __builtin_fmaf((float)((R) & 1 ? w2.y : w2.x), bcast<R>(sc.w), zs);          \
   }
-      PF_FOR16(PF_ZSUM)
+        PF_FOR16(PF_ZSUM)
 #undef PF_ZSUM
-
-      // ---- O^T += V^T W^T -------------------------------------------------
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
+        for (int k = 0; k < 2; ++k)
 #pragma unroll
-        for (int d = 0; d < 4; ++d) {
-          const uint4 v = *reinterpret_cast<const uint4*>(S.vt + (32 * d + ql) * VROW +
-                                                          2 * (16 * k + 8 * h));
-          oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8_t, v),
-                                                           __builtin_bit_cast(h8_t, wb[k]),
-                                                           oacc[d], 0, 0, 0);
-        }
+          for (int d = 0; d < 4; ++d) {
+            const uint4 v = *reinterpret_cast<const uint4*>(S.vt + (32 * d + ql) * VROW +
+                                                            2 * (16 * (2 * TT + k) + 8 * h));
+            oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8_t, v),
+                                                             __builtin_bit_cast(h8_t, wb[k]),
+                                                             oacc[d], 0, 0, 0);
+          }
+      };
+      tile(std::integral_constant<int, 0>{});
+      tile(std::integral_constant<int, 1>{});
     }
     if (kb + 1 < nb) store(kb + 1, st[(kb + 1) & 1]);
     __syncthreads();
@@ -350,11 +363,12 @@ __global__ __launch_bounds__(G < 4 ? 256 : 64 * G, G < 8 ? 2 : 1) void kv_prefil
   l += __shfl_xor(l, 32);
   zs += __shfl_xor(zs, 32);
   float y[64];  // y[16 d + r]: dim 32 d + 8 (r / 4) + 4 h + r % 4
+  const float il = 1.0f / l;
 #pragma unroll
   for (int d = 0; d < 4; ++d)
 #pragma unroll
     for (int r = 0; r < 16; ++r)
-      y[16 * d + r] = (__builtin_amdgcn_ldexpf(oacc[d][r], 24) - zs) / l;
+      y[16 * d + r] = (__builtin_amdgcn_ldexpf(oacc[d][r], 24) - zs) * il;
   if (v_had) {
 #pragma unroll
     for (int s = 1; s < 64; s <<= 1)

@@ -129,9 +129,10 @@ struct RopeTable {
   float inv_freq[HD / 2];  // fl32(base^(-2i/128)), computed on the host in double
 };
 
-// One wave per (token m, head slot j): j < Hq query heads, then Hkv key heads,
-// then Hkv value heads of the projection row qkv[m].  Lane l holds dims 2l,
-// 2l + 1.  RoPE pairs dims (i, i + 64) (rotation of the two halves):
+// One wave per (token m, SPW consecutive head slots j): j < Hq query heads,
+// then Hkv key heads, then Hkv value heads of the projection row qkv[m]; the
+// wave computes the token's RoPE angles once for its slots.  Lane l holds
+// dims 2l, 2l + 1.  RoPE pairs dims (i, i + 64) (rotation of the two halves):
 //   x'[i] = x[i] cos(a_i) - x[i + 64] sin(a_i),  x'[i + 64] = x[i + 64] cos(a_i) + x[i] sin(a_i)
 // with a_i = fl32(pos * inv_freq[i]).  Queries are stored as bf16; keys are
 // rounded to bf16, rotated by c H (optional) and quantized; values are
@@ -140,7 +141,7 @@ struct RopeTable {
 // for kv head h is ((m / T) * Hkv + h) * s_cap + pos[m]; positions outside
 // [0, s_cap) write nothing.
 __global__ __launch_bounds__(256) void rope_kv_append_kernel(
-    const uint16_t* __restrict__ qkv, int64_t ldq, int M, int T, int Hq, int Hkv,
+    const uint16_t* __restrict__ qkv, int64_t ldq, int M, int T, int Hq, int Hkv, int spw,
     const int32_t* __restrict__ positions, RopeTable tab, int k_had, int v_had,
     uint16_t* __restrict__ q_out, uint8_t* __restrict__ kc, uint16_t* __restrict__ ks,
     int16_t* __restrict__ kz, uint8_t* __restrict__ vc, uint16_t* __restrict__ vs,
@@ -150,60 +151,67 @@ __global__ __launch_bounds__(256) void rope_kv_append_kernel(
   const int64_t wid = (int64_t)__builtin_amdgcn_workgroup_id_x() * 4 +
                       ((int)__builtin_amdgcn_workitem_id_x() >> 6);
   const int slots = Hq + 2 * Hkv;
-  if (wid >= (int64_t)M * slots) return;
-  const int m = (int)(wid / slots), j = (int)(wid - (int64_t)m * slots);
-  const uint32_t w = reinterpret_cast<const uint32_t*>(qkv + (int64_t)m * ldq + (int64_t)j * HD)[lane];
-  float x0 = bf16_lo(w), x1 = bf16_hi(w);
+  const int per_tok = (slots + spw - 1) / spw;
+  if (wid >= (int64_t)M * per_tok) return;
+  const int m = (int)(wid / per_tok);
+  const int j0 = (int)(wid - (int64_t)m * per_tok) * spw, j1 = min(j0 + spw, slots);
   const int pos = positions[m];
-  const bool is_v = j >= Hq + Hkv;
-  if (!is_v) {
-    const float p0 = __shfl_xor(x0, 32), p1 = __shfl_xor(x1, 32);
+  const uint32_t* row = reinterpret_cast<const uint32_t*>(qkv + (int64_t)m * ldq);
+  float s0 = 0.0f, c0 = 1.0f, s1 = 0.0f, c1 = 1.0f;
+  if (j0 < Hq + Hkv) {
     const int i0 = (2 * lane) & 63;
-    float s0, c0, s1, c1;
     sincosf((float)pos * tab.inv_freq[i0], &s0, &c0);
     sincosf((float)pos * tab.inv_freq[i0 + 1], &s1, &c1);
-    if (lane < 32) {
-      x0 = x0 * c0 - p0 * s0;
-      x1 = x1 * c1 - p1 * s1;
-    } else {
-      x0 = x0 * c0 + p0 * s0;
-      x1 = x1 * c1 + p1 * s1;
-    }
-    if (j < Hq) {
-      reinterpret_cast<uint32_t*>(q_out + ((int64_t)m * Hq + j) * HD)[lane] = bf16x2_rne(x0, x1);
-      return;
-    }
-    // the key after RoPE is a bf16 activation
-    x0 = bf16_lo(f32_to_bf16_rne(x0));
-    x1 = bf16_lo(f32_to_bf16_rne(x1));
   }
-  const int h = is_v ? j - Hq - Hkv : j - Hq;
-  if (is_v ? v_had : k_had) {
-    // 128-point FWHT: dim bit 0 inside the lane, bits 1..6 across lanes
-    float a = x0 + x1, b = x0 - x1;
+  for (int j = j0; j < j1; ++j) {
+    const uint32_t w = row[(int64_t)j * (HD / 2) + lane];
+    float x0 = bf16_lo(w), x1 = bf16_hi(w);
+    const bool is_v = j >= Hq + Hkv;
+    if (!is_v) {
+      const float p0 = __shfl_xor(x0, 32), p1 = __shfl_xor(x1, 32);
+      if (lane < 32) {
+        x0 = x0 * c0 - p0 * s0;
+        x1 = x1 * c1 - p1 * s1;
+      } else {
+        x0 = x0 * c0 + p0 * s0;
+        x1 = x1 * c1 + p1 * s1;
+      }
+      if (j < Hq) {
+        reinterpret_cast<uint32_t*>(q_out + ((int64_t)m * Hq + j) * HD)[lane] = bf16x2_rne(x0, x1);
+        continue;
+      }
+      // the key after RoPE is a bf16 activation
+      x0 = bf16_lo(f32_to_bf16_rne(x0));
+      x1 = bf16_lo(f32_to_bf16_rne(x1));
+    }
+    const int h = is_v ? j - Hq - Hkv : j - Hq;
+    if (is_v ? v_had : k_had) {
+      // 128-point FWHT: dim bit 0 inside the lane, bits 1..6 across lanes
+      float a = x0 + x1, b = x0 - x1;
 #pragma unroll
-    for (int s = 0; s < 6; ++s) {
-      const float ya = __shfl_xor(a, 1 << s), yb = __shfl_xor(b, 1 << s);
-      const bool up = (lane >> s) & 1;
-      a = up ? ya - a : a + ya;
-      b = up ? yb - b : b + yb;
+      for (int s = 0; s < 6; ++s) {
+        const float ya = __shfl_xor(a, 1 << s), yb = __shfl_xor(b, 1 << s);
+        const bool up = (lane >> s) & 1;
+        a = up ? ya - a : a + ya;
+        b = up ? yb - b : b + yb;
+      }
+      const float c = 0.08838834764831845f;  // fl32(1 / sqrt(128))
+      x0 = a * c;
+      x1 = b * c;
     }
-    const float c = 0.08838834764831845f;  // fl32(1 / sqrt(128))
-    x0 = a * c;
-    x1 = b * c;
-  }
-  float* dbg = is_v ? v_dbg : k_dbg;
-  if (dbg) reinterpret_cast<float2*>(dbg + ((int64_t)m * Hkv + h) * HD)[lane] = make_float2(x0, x1);
-  const float mx = wmax(fmaxf(x0, x1)), mn = wmin(fminf(x0, x1));
-  const QParams p = quant_params(mx, mn);
-  const uint32_t lo = __float_as_uint(p.lo);
-  const uint32_t code = (quant_bits(x0, p) - lo) | ((quant_bits(x1, p) - lo) << 4);
-  if (pos < 0 || (int64_t)pos >= s_cap) return;
-  const int64_t row = ((int64_t)(m / T) * Hkv + h) * s_cap + pos;
-  (is_v ? vc : kc)[row * (HD / 2) + lane] = (uint8_t)code;
-  if (lane == 0) {
-    (is_v ? vs : ks)[row] = p.s16;
-    (is_v ? vz : kz)[row] = p.z;
+    float* dbg = is_v ? v_dbg : k_dbg;
+    if (dbg) reinterpret_cast<float2*>(dbg + ((int64_t)m * Hkv + h) * HD)[lane] = make_float2(x0, x1);
+    const float mx = wmax(fmaxf(x0, x1)), mn = wmin(fminf(x0, x1));
+    const QParams p = quant_params(mx, mn);
+    const uint32_t lo = __float_as_uint(p.lo);
+    const uint32_t code = (quant_bits(x0, p) - lo) | ((quant_bits(x1, p) - lo) << 4);
+    if (pos < 0 || (int64_t)pos >= s_cap) continue;
+    const int64_t crow = ((int64_t)(m / T) * Hkv + h) * s_cap + pos;
+    (is_v ? vc : kc)[crow * (HD / 2) + lane] = (uint8_t)code;
+    if (lane == 0) {
+      (is_v ? vs : ks)[crow] = p.s16;
+      (is_v ? vz : kz)[crow] = p.z;
+    }
   }
 }
 
@@ -447,9 +455,12 @@ hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, in
   RopeTable tab;
   for (int i = 0; i < HD / 2; ++i)
     tab.inv_freq[i] = (float)__builtin_pow(rope_base, -2.0 * i / (double)HD);
-  const int64_t waves = M * (Hq + 2 * Hkv);
+  // many tokens: a wave takes 8 head slots of a token (one set of angles for
+  // them); few tokens: one slot per wave, for parallelism
+  const int spw = M >= 256 ? 8 : 1;
+  const int64_t waves = M * ((Hq + 2 * Hkv + spw - 1) / spw);
   hipLaunchKernelGGL(rope_kv_append_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0,
-                     stream, qkv, ldq, (int)M, (int)T, (int)Hq, (int)Hkv, positions, tab, k_had ? 1 : 0,
+                     stream, qkv, ldq, (int)M, (int)T, (int)Hq, (int)Hkv, spw, positions, tab, k_had ? 1 : 0,
                      v_had ? 1 : 0, q_out, kc, ks, kz, vc, vs, vz, s_cap, k_dbg, v_dbg);
   return hipGetLastError();
 }

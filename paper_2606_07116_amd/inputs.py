@@ -53,6 +53,9 @@ WORKLOADS = {
     "kv_decode_attention": dict(B=8, H=32, S=32768, Dh=128, seed=6),
     # one decode step of a Llama-3-8B-shaped layer: 16 sequences at context 4096
     "decode_layer": dict(M=16, D=4096, Hq=32, Hkv=8, F=14336, g=128, ctx=4096, seed=7),
+    # the prefill of the same layer: 2 sequences of 2048 tokens (4096 rows
+    # through the projections), causal attention over the tokens just written
+    "prefill_layer": dict(B=2, T=2048, past=0, D=4096, Hq=32, Hkv=8, F=14336, g=128, seed=9),
     # offline calibration of one 4096-channel layer input (U1 P1 H1): 128
     # calibration sequences of 2048 tokens; the rotation fused into the QKV
     # and up/gate weights of a Llama-3-8B-shaped layer

@@ -21,6 +21,7 @@ import torch
 
 import paper_2606_07116_amd as offq
 from oracle import attention as OA
+from oracle import gemm as OG
 from oracle import kv as OKV
 from oracle import layer as OL
 from oracle import quantizer as OQ
@@ -151,6 +152,19 @@ def test_prefill_attention_large_zero_points(case):
     _run(B, T, 8, Hkv, past, S=S, seed=25, sm=sm, cache=(kc, ks, kz, vc, vs, vz))
 
 
+@pytest.mark.parametrize("sm", [0.05, 1.0])
+def test_prefill_attention_large_value_scales(sm):
+    """Value scales up to 60000 (fp16's top binade): a weight p sv must stay
+    finite in fp16, so the reference maximum of a row may lag its true
+    maximum by less there (sm = 1: peaked rows whose maximum keeps moving)."""
+    B, Hkv, T, past = 1, 2, 200, 30
+    S = past + T
+    rng = np.random.default_rng(int(sm * 100))
+    kc, ks, kz, vc, _, vz = _host_cache(B, Hkv, S, 31)
+    vs = rng.uniform(2000.0, 60000.0, size=(B, Hkv, S)).astype(np.float16)
+    _run(B, T, 8, Hkv, past, S=S, seed=32, sm=sm, cache=(kc, ks, kz, vc, vs, vz))
+
+
 def test_prefill_attention_deterministic_and_out_buffer():
     B, T, Hq, Hkv, past = 1, 80, 4, 1, 10
     q = inputs.queries(B * T, Hq, 128, seed=3).reshape(B, T, Hq, 128)
@@ -186,7 +200,8 @@ def _zero_cache(B, Hkv, s_cap, fill):
                 k_zero=z(B, Hkv, s_cap, dt=torch.int16), v_zero=z(B, Hkv, s_cap, dt=torch.int16))
 
 
-@pytest.mark.parametrize("B,T,Hq,Hkv,past,s_cap", [(2, 37, 8, 2, 5, 50), (1, 300, 32, 8, 0, 300)])
+@pytest.mark.parametrize("B,T,Hq,Hkv,past,s_cap", [(2, 37, 8, 2, 5, 50), (1, 300, 32, 8, 0, 300),
+                                                  (2, 150, 5, 1, 20, 170)])
 def test_rope_kv_prefill(B, T, Hq, Hkv, past, s_cap):
     """Row b T + t lands at position past + t of sequence b's cache, as the
     oracle's RoPE + H3 + KV quantizer writes it; nothing else changes."""
@@ -203,8 +218,18 @@ def test_rope_kv_prefill(B, T, Hq, Hkv, past, s_cap):
                                             debug=True)
     torch.cuda.synchronize()
     assert torch.equal(q, q1) and torch.equal(ky, ky1) and torch.equal(vy, vy1)
-    q_ref, _, vy_ref = OL.kv_rows(qkv, Hq, Hkv, pos, 500000.0)
+    q_ref, ky_ref, vy_ref = OL.kv_rows(qkv, Hq, Hkv, pos, 500000.0)
     assert np.array_equal(P.host(vy), vy_ref)
+    # the query within one bf16 ulp of the oracle's RoPE; the key rows within
+    # the rotation bound of the decode form's test (fp32 RoPE, a bf16 rounding
+    # of the key before H3, the 7-stage fp32 butterfly)
+    qg = P.host(q.float()).astype(np.float64)
+    qr = OL.bf16(q_ref)
+    assert np.all(np.abs(qg - qr) <= OG.bf16_ulp(qr) * (1 + 1e-9) + 1e-6 * np.abs(q_ref).max())
+    k_in = OL.bf16(OL.rope(qkv.reshape(M, Hq + 2 * Hkv, 128)[:, Hq:Hq + Hkv], pos[:, None], 500000.0))
+    kb = (7 + 2) * 2.0 ** -24 * np.abs(k_in).sum(-1, keepdims=True) / math.sqrt(128) + \
+        OG.bf16_ulp(k_in).sum(-1, keepdims=True) / math.sqrt(128) + 1e-5 * np.abs(k_in).max(-1, keepdims=True)
+    assert np.all(np.abs(P.host(ky) - ky_ref) <= kb)
     for name, rows in (("k", P.host(ky)), ("v", P.host(vy))):
         codes, s, z = OKV.kv_quantize(rows.reshape(-1, 128))
         packed = OQ.pack_nibbles(codes).reshape(B, T, Hkv, 64).transpose(0, 2, 1, 3)
