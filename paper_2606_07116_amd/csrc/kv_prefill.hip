@@ -29,10 +29,11 @@
 //   K in the operand order of the score product, V transposed (keys
 //   permuted to match the accumulator rows of S^T), shared by all waves.
 //
-// Organisation: one workgroup per (sequence b, kv head, 32 NW / G query
-// positions), NW = 4 waves for G <= 4 and G waves for G = 8; wave w takes
-// query head w % G of the kv head (grouped-query attention) at the 32
-// positions of sub-tile w / G.  Keys stream in blocks of 64 through a double-buffered LDS stage;
+// Organisation: one workgroup of 8 waves per (sequence b, kv head, 256 / G
+// query positions); wave w takes query head w % G of the kv head
+// (grouped-query attention) at the 32 positions of sub-tile w / G, so a
+// staged key block serves 256 queries and its staging work is split over
+// 512 threads (keys in one half, values in the other).  Keys stream in blocks of 64 through a double-buffered LDS stage;
 // a wave skips the blocks past its last query and masks the diagonal ones.
 // Workgroups with the most keys launch first.
 #include <type_traits>
@@ -84,13 +85,13 @@ __device__ __forceinline__ int vt_pos(int k) {
 #define PF_FOR16(X) X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15)
 
 template <int G>
-__global__ __launch_bounds__(G < 4 ? 256 : 64 * G, G < 8 ? 2 : 1) void kv_prefill_kernel(
+__global__ __launch_bounds__(512, 1) void kv_prefill_kernel(
     const uint16_t* __restrict__ q, int B, int T, int Hq, int Hkv, int past,
     const uint8_t* __restrict__ kc, const uint16_t* __restrict__ ks,
     const int16_t* __restrict__ kz, const uint8_t* __restrict__ vc,
     const uint16_t* __restrict__ vs, const int16_t* __restrict__ vz, int64_t s_cap, float sm2,
     float cnorm, int v_had, uint16_t* __restrict__ out) {
-  constexpr int NW = G < 4 ? 4 : G;
+  constexpr int NW = 8;
   constexpr int TP = 32 * NW / G;  // query positions per workgroup
   __shared__ Stage st[2];
   __shared__ float red[NW];
@@ -173,7 +174,7 @@ __global__ __launch_bounds__(G < 4 ? 256 : 64 * G, G < 8 ? 2 : 1) void kv_prefil
     qb[s][3] = pk_f16(__builtin_amdgcn_ldexpf(v[3], 11 - e), __builtin_amdgcn_ldexpf(v[7], 11 - e));
   }
 
-  // ---- staging of one key block (threads 0..255) --------------------------
+  // ---- staging of one key block: keys by threads 0..255, values by 256..511 -
   const int64_t rowbase = (int64_t)bh * s_cap;
   const uint8_t* kcb = kc + rowbase * (PD / 2);
   const uint8_t* vcb = vc + rowbase * (PD / 2);
@@ -181,15 +182,17 @@ __global__ __launch_bounds__(G < 4 ? 256 : 64 * G, G < 8 ? 2 : 1) void kv_prefil
   uint2 va = make_uint2(0, 0), vb = make_uint2(0, 0);
   uint16_t r_ks = 0, r_vs = 0;
   int16_t r_kz = 0, r_vz = 0;
+  const int vid = tid - 256;  // value-staging thread index (0..255 for waves 4..7)
   auto load = [&](int kb) {
-    if (tid < 256) {
-      const int k0 = kb * KB;
-      const int key = min(k0 + (tid >> 2), nk - 1);
-      kreg = *reinterpret_cast<const uint4*>(kcb + (int64_t)key * (PD / 2) + 16 * (tid & 3));
-      const int kp = tid & 31, dc = tid >> 5;
+    const int k0 = kb * KB;
+    if (tid >= 256) {
+      const int kp = vid & 31, dc = vid >> 5;
       const int ka = min(k0 + 2 * kp, nk - 1), kb1 = min(k0 + 2 * kp + 1, nk - 1);
       va = *reinterpret_cast<const uint2*>(vcb + (int64_t)ka * (PD / 2) + 8 * dc);
       vb = *reinterpret_cast<const uint2*>(vcb + (int64_t)kb1 * (PD / 2) + 8 * dc);
+    } else {
+      const int key = min(k0 + (tid >> 2), nk - 1);
+      kreg = *reinterpret_cast<const uint4*>(kcb + (int64_t)key * (PD / 2) + 16 * (tid & 3));
       if (tid < KB) {
         const int64_t r = rowbase + min(k0 + tid, nk - 1);
         r_ks = ks[r];
@@ -200,18 +203,8 @@ __global__ __launch_bounds__(G < 4 ? 256 : 64 * G, G < 8 ? 2 : 1) void kv_prefil
     }
   };
   auto store = [&](int kb, Stage& S) {
-    if (tid < 256) {
-      // code word i of the key row (8 dims) -> the 8 fp16 operand values of
-      // one k-step: (d0, d4), (16 d1, 16 d5), (d2, d6), (16 d3, 16 d7)
-      uint4* kd = reinterpret_cast<uint4*>(S.k + (tid >> 2) * KROW + 64 * (tid & 3));
-      const uint32_t kw4[4] = {kreg.x, kreg.y, kreg.z, kreg.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t u = kw4[i];
-        kd[i] = make_uint4(u & 0x000F000Fu, u & 0x00F000F0u, (u >> 8) & 0x000F000Fu,
-                           (u >> 8) & 0x00F000F0u);
-      }
-      const int kp = tid & 31, dc = tid >> 5;
+    if (tid >= 256) {
+      const int kp = vid & 31, dc = vid >> 5;
       uint32_t* vt = reinterpret_cast<uint32_t*>(S.vt + 16 * dc * VROW + 2 * vt_pos(2 * kp));
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
@@ -225,6 +218,17 @@ __global__ __launch_bounds__(G < 4 ? 256 : 64 * G, G < 8 ? 2 : 1) void kv_prefil
           vt[(8 * u + m) * (VROW / 4)] = (t0 >> (4 * m)) & 0x000F000Fu;
           vt[(8 * u + 4 + m) * (VROW / 4)] = (t1 >> (4 * m)) & 0x000F000Fu;
         }
+      }
+    } else {
+      // code word i of the key row (8 dims) -> the 8 fp16 operand values of
+      // one k-step: (d0, d4), (16 d1, 16 d5), (d2, d6), (16 d3, 16 d7)
+      uint4* kd = reinterpret_cast<uint4*>(S.k + (tid >> 2) * KROW + 64 * (tid & 3));
+      const uint32_t kw4[4] = {kreg.x, kreg.y, kreg.z, kreg.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t u = kw4[i];
+        kd[i] = make_uint4(u & 0x000F000Fu, u & 0x00F000F0u, (u >> 8) & 0x000F000Fu,
+                           (u >> 8) & 0x00F000F0u);
       }
       if (tid < KB) {
         // log2-domain score = a dot + b sum(q_r), dot = 2^(-9-e) sum q_r c
@@ -411,7 +415,7 @@ hipError_t launch_kv_attention_prefill(const uint16_t* q, int64_t B, int64_t T, 
   const int G = (int)(Hq / Hkv);
   const float sm2 = sm_scale * PLOG2E;
   const float cnorm = (float)(1.0 / __builtin_sqrt((double)PD));
-  const int NW = G < 4 ? 4 : G;
+  const int NW = 8;
   const int64_t TP = 32 * NW / G;
   const int64_t grid = B * Hkv * ((T + TP - 1) / TP);
 #define PF_LAUNCH(GG)                                                                          \

@@ -94,10 +94,11 @@ def _run(B, T, Hq, Hkv, past, S=None, v_had=False, seed=0, rows=None, sm=SM, cac
 
 @pytest.mark.parametrize("B,T,Hq,Hkv,past", [
     (1, 1, 4, 1, 0), (1, 1, 4, 1, 37),        # one token, with and without context
-    (2, 37, 4, 1, 0), (1, 64, 4, 1, 0),       # one ragged and one whole 32-row tile pair
-    (1, 100, 8, 2, 5),                        # four tiles, ragged, a short context
-    (2, 65, 2, 2, 0), (1, 130, 4, 2, 3),      # G = 1 (128 positions per workgroup), G = 2
-    (1, 40, 8, 1, 0), (1, 33, 16, 2, 70),     # G = 8 (eight waves)
+    (2, 37, 4, 1, 0), (1, 64, 4, 1, 0),       # a ragged and a whole 64-position workgroup
+    (1, 100, 8, 2, 5),                        # two workgroups, ragged, a short context
+    (2, 65, 2, 2, 0), (1, 300, 2, 2, 0),      # G = 1 (256 positions per workgroup)
+    (1, 130, 4, 2, 3),                        # G = 2 (128 positions per workgroup)
+    (1, 40, 8, 1, 0), (1, 33, 16, 2, 70),     # G = 8 (32 positions per workgroup)
     (2, 300, 8, 2, 200),                      # many key blocks, a context longer than a block
 ])
 def test_prefill_attention_shapes(B, T, Hq, Hkv, past):
