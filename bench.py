@@ -247,6 +247,53 @@ def cpu_baseline(layers, sample_rows, min_s=10.0, per_config=None):
     return out
 
 
+def cpu_prefill_layer(lc, tokens, min_s=10.0):
+    """The oracle's prefill of the layer (oracle.layer.prefill_layer: every
+    stage, the causal attention over the 4-bit cache included) on a bounded
+    sample: the first ``tokens`` tokens of one sequence with the full-width
+    weights, repeated until ``min_s`` seconds; the rate in the metric's unit
+    (integer TOP/s of the sampled projections) and in tokens per second.  The
+    weight quantization is setup, not timed."""
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    from oracle import layer as OL
+    from oracle import quantizer as OQ
+    from paper_2606_07116_amd import inputs
+
+    D, Hq, Hkv, F, g = lc["D"], lc["Hq"], lc["Hkv"], lc["F"], lc["g"]
+    shapes = {"qkv": ((Hq + 2 * Hkv) * 128, D), "o": (D, Hq * 128), "ug": (2 * F, D), "down": (D, F)}
+    ncpu = len(os.sched_getaffinity(0))
+    with threadpool_limits(limits=ncpu):
+        weights = {k: OQ.quantize_weights(inputs.weights(n, k_, seed=lc["seed"] + j,
+                                                         std=1.0 / k_ ** 0.5))
+                   for j, (k, (n, k_)) in enumerate(shapes.items())}
+        rng = np.random.default_rng(lc["seed"])
+        x = inputs.round_to_bf16(rng.standard_normal((tokens, D)).astype(np.float32))
+        kc, ks, kz = inputs.kv4_cache(1, Hkv, tokens, 128, seed=lc["seed"])
+        vc, vs, vz = inputs.kv4_cache(1, Hkv, tokens, 128, seed=lc["seed"] + 1)
+        cache = dict(k_codes=kc, k_scale=ks, k_zero=kz, v_codes=vc, v_scale=vs, v_zero=vz)
+        cfg = dict(Hq=Hq, Hkv=Hkv, g=g, eps=1e-5, rope_base=500000.0)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            OL.prefill_layer(x, weights, cache, 0, cfg)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= min_s or reps >= 50:
+                break
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    ops = sum(2.0 * tokens * n * k_ for n, k_ in shapes.values()) * reps
+    return {"value": round(ops / el / 1e12, 4), "unit": "TOPS", "cores": int(threads),
+            "kind": "oracle", "tokens_per_s": round(tokens * reps / el, 2),
+            "sample": f"the first {tokens} tokens of one sequence through the whole layer "
+                      f"(D {D}, {Hq}/{Hkv} heads, MLP {F}, g = {g}, causal attention over the "
+                      f"{tokens} cached positions), {reps} time(s) in {el:.1f} s; rate = "
+                      "projection int ops / s",
+            "cpu_model": _cpu_model(), "host_cpus": ncpu,
+            "threads_note": "BLAS (the integer GEMMs via fp64 matmul) uses the threads above; "
+                            "the other stages are numpy"}
+
+
 def _cpu_layer_config(layers, rows, n_cols=None, unit="TOPS"):
     """One oracle pass over each layer of a workload on its first ``rows``
     rows (and first ``n_cols`` output channels when given), per-stage
@@ -793,6 +840,8 @@ def main():
                 "kv_quantize": _cpu_kv_config(1 << 16),
             }
         out["cpu_baseline"] = cpu_baseline(lay, 256, 10.0, per_config)
+    elif not args.no_cpu_baseline and wl == "prefill_layer":
+        out["cpu_baseline"] = cpu_prefill_layer(inputs.WORKLOADS["prefill_layer"], 64, 10.0)
     elif not args.no_cpu_baseline and wl == "attn_proj_prefill":
         out["cpu_baseline"] = cpu_baseline([("proj", M, K, N, g, spec, cfg["seed"], None)], 512, 10.0)
     print(json.dumps(out), flush=True)
