@@ -411,7 +411,7 @@ offq_status_t offq_kv_attention_prefill(const uint16_t* q, int64_t B, int64_t T,
   if (past + T > s_cap) return fail(OFFQ_ERR_INVALID, "past + T exceeds s_cap");
   if (v_hadamard != 0 && v_hadamard != 1) return fail(OFFQ_ERR_INVALID, "v_hadamard must be 0 or 1");
   if (!(sm_scale > 0.0f) || sm_scale > 1e30f) return fail(OFFQ_ERR_INVALID, "sm_scale must be > 0");
-  if (T > (int64_t(1) << 30) || past > (int64_t(1) << 30) || Hq > (1 << 16) ||
+  if (past + T > (int64_t(1) << 30) || Hq > (1 << 16) ||
       B * T > (int64_t(1) << 31) / Hq || B * Hkv * ((T + 31) / 32) > (int64_t(1) << 31) ||
       s_cap > (int64_t(1) << 40) / (B > 0 ? B * Hkv : 1))
     return fail(OFFQ_ERR_UNSUPPORTED, "sizes too large");

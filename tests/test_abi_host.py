@@ -209,3 +209,49 @@ def test_package_import_does_not_load_the_library():
             "assert 'paper_2606_07116_amd._lib' not in sys.modules")
     r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+@pytest.mark.parametrize("change,expect", [
+    ({}, None),                                             # valid: reaches the device check
+    ({"head_dim": 64}, _lib.OFFQ_ERR_UNSUPPORTED),
+    ({"Hq": 12, "Hkv": 4}, _lib.OFFQ_ERR_UNSUPPORTED),      # group of 3
+    ({"Hq": 6, "Hkv": 4}, _lib.OFFQ_ERR_INVALID),           # not a multiple
+    ({"past": 70}, _lib.OFFQ_ERR_INVALID),                  # past + T > s_cap
+    ({"T": -1}, _lib.OFFQ_ERR_INVALID),
+    ({"v_had": 2}, _lib.OFFQ_ERR_INVALID),
+    ({"sm": 0.0}, _lib.OFFQ_ERR_INVALID),
+    ({"q": None}, _lib.OFFQ_ERR_INVALID),
+    ({"out": P + 8}, _lib.OFFQ_ERR_INVALID),                # misaligned (16 B)
+    ({"out": P + 64}, _lib.OFFQ_ERR_INVALID),               # overlaps q
+    ({"past": (1 << 30) - 10, "s_cap": 1 << 31}, _lib.OFFQ_ERR_UNSUPPORTED),
+    ({"T": 0, "q": None, "out": None}, _lib.OFFQ_OK),       # empty: nothing to do
+])
+def test_kv_attention_prefill_validation(change, expect):
+    names = ["q", "B", "T", "Hq", "Hkv", "head_dim", "past", "kc", "ks", "kz", "vc", "vs", "vz",
+             "s_cap", "sm", "v_had", "out", "stream"]
+    a = dict(zip(names, [P, 2, 64, 8, 2, 128, 0, P, P, P, P, P, P, 100, 0.1, 0, P + (1 << 24),
+                         None]))
+    a.update(change)
+    st = _lib.offq_kv_attention_prefill_raw(*[a[n] for n in names])
+    import torch
+    if expect is None:
+        if torch.cuda.is_available():
+            pytest.skip("a GPU is present")
+        expect = _lib.OFFQ_ERR_HIP
+    assert st == expect, _lib.last_error()
+
+
+def test_rope_kv_prefill_validation():
+    L = _lib
+    # qkv, ldq, B, T, Hq, Hkv, head_dim, positions, base, k_had, v_had, q_out,
+    # 6 cache arrays, s_cap, k_dbg, v_dbg, stream
+    args = [P, 768, 2, 3, 2, 2, 128, P, 500000.0, 1, 0, P, P, P, P, P, P, P, 100, None, None, None]
+    for i, bad, expect in ((6, 64, L.OFFQ_ERR_UNSUPPORTED), (3, 0, L.OFFQ_ERR_INVALID),
+                           (9, 2, L.OFFQ_ERR_INVALID), (1, 700, L.OFFQ_ERR_INVALID),
+                           (7, None, L.OFFQ_ERR_INVALID)):
+        a = list(args)
+        a[i] = bad
+        assert L.offq_rope_kv_prefill_raw(*a) == expect, (i, L.last_error())
+    a = list(args)
+    a[2] = 0  # no sequences: nothing to do
+    assert L.offq_rope_kv_prefill_raw(*a) == L.OFFQ_OK
