@@ -33,9 +33,14 @@
 // query positions); wave w takes query head w % G of the kv head
 // (grouped-query attention) at the 32 positions of sub-tile w / G, so a
 // staged key block serves 256 queries and its staging work is split over
-// 512 threads (keys in one half, values in the other).  Keys stream in blocks of 64 through a double-buffered LDS stage;
-// a wave skips the blocks past its last query and masks the diagonal ones.
-// Workgroups with the most keys launch first.
+// 512 threads (keys in one half, values in the other).  Keys stream in
+// blocks of 64 through a double-buffered LDS stage; a wave skips the blocks
+// past its last query and masks the diagonal ones, and takes a block's two
+// 32-key tiles one after the other (the first tile's softmax runs while the
+// second tile's score products are on the matrix cores).  The output rescale
+// is lazy: a row's reference maximum moves only when a tile's maximum passes
+// it by more than tau (at most 8, and small enough that every weight p sv
+// stays finite in fp16).  Workgroups with the most keys launch first.
 #include <type_traits>
 
 #include "common.h"
