@@ -316,11 +316,15 @@ __global__ __launch_bounds__(RN_THREADS) void add_rmsnorm_quant_kernel(
 }
 
 // SwiGLU + the online 128-point Hadamard H4 + the quantizer (g = 128) for
-// the down-projection input: a = bf16(fl32(silu(gate) * up)) as swiglu_kernel,
-// then y = c H a per group of 128 (fp32 butterflies, c = fl32(1/sqrt(128))
+// the down-projection input: a = bf16(fl32(silu(gate) * up)) with silu from
+// the hardware exp2 and reciprocal (swiglu_kernel divides exactly; the two
+// can differ by one bf16 ulp next to a rounding midpoint), then y = c H a
+// per group of 128 (fp32 butterflies, c = fl32(1/sqrt(128))
 // after them) and the codes of Eq. 1.  A group is 16 lanes x 8 channels:
 // butterfly stages over channel bits 0..2 inside the lane, bits 3..6 across
 // the lanes.  Workgroup: 16 groups of one row.
+constexpr float SW_LOG2E = 1.4426950408889634f;
+
 __global__ __launch_bounds__(256) void swiglu_rq_kernel(const uint16_t* __restrict__ gu,
                                                         int64_t ldg, int F,
                                                         uint8_t* __restrict__ codes,
@@ -342,7 +346,11 @@ __global__ __launch_bounds__(256) void swiglu_rq_kernel(const uint16_t* __restri
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const float g0 = bf16_lo(gw[k]), g1 = bf16_hi(gw[k]);
-    const float a0 = g0 / (1.0f + expf(-g0)), a1 = g1 / (1.0f + expf(-g1));
+    // silu with the hardware exp2 and reciprocal (about 1 ulp each): the
+    // product rounds to bf16, so an error of a few fp32 ulps can only move a
+    // value that lies next to a rounding midpoint to the other neighbour
+    const float a0 = g0 * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(g0 * -SW_LOG2E));
+    const float a1 = g1 * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(g1 * -SW_LOG2E));
     const uint32_t ab = bf16x2_rne(a0 * bf16_lo(uw[k]), a1 * bf16_hi(uw[k]));
     v[2 * k] = bf16_lo(ab);
     v[2 * k + 1] = bf16_hi(ab);
