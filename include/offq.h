@@ -333,20 +333,21 @@ offq_status_t offq_swiglu_rotate_quantize(const uint16_t* gu, int64_t ldg, int64
  * per-head online Hadamard H3 on the key (sec. 3.3 step 2(3)) and the KV4
  * quantizer (as offq_kv_quantize, group = head dim) writing position
  * positions[m] of sequence m into the cache:
- *   qkv [M, (Hq + 2 Hkv) * 128] (ldq >= that, even): query heads, then key
- *     heads, then value heads of the QKV projection of token m;
+ *   qkv [M, (Hq + 2 Hkv) * 128] (ldq >= that, a multiple of 8; qkv 16-byte
+ *     aligned): query heads, then key heads, then value heads of the QKV
+ *     projection of token m;
  *   positions int32 [M] (device): the position of token m in its sequence;
  *     a position outside [0, s_cap) writes nothing to the cache;
  *   rope_base: RoPE's base (theta); dims (i, i + 64) rotate by angle
  *     fl32(pos * fl32(base^(-2i/128))), computed in fp32;
  *   k_hadamard / v_hadamard (0 or 1): c H on the key (after RoPE and a bf16
  *     rounding) / on the value before quantization (paper: 1 / 0);
- *   q_out [M, Hq, 128]: the query after RoPE;
+ *   q_out [M, Hq, 128] (16-byte aligned): the query after RoPE;
  *   k_codes, v_codes uint8 [M, Hkv, s_cap, 64]; k_scale, v_scale fp16 and
  *     k_zero, v_zero int16 [M, Hkv, s_cap] (the layout the decode attention
  *     reads);
- *   k_y_debug, v_y_debug fp32 [M, Hkv, 128] or NULL: the rows that were
- *     quantized.
+ *   k_y_debug, v_y_debug fp32 [M, Hkv, 128] (16-byte aligned) or NULL: the
+ *     rows that were quantized.
  * head_dim must be 128.
  */
 offq_status_t offq_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, int64_t Hq, int64_t Hkv,

@@ -129,86 +129,126 @@ struct RopeTable {
   float inv_freq[HD / 2];  // fl32(base^(-2i/128)), computed on the host in double
 };
 
-// One wave per (token m, SPW consecutive head slots j): j < Hq query heads,
-// then Hkv key heads, then Hkv value heads of the projection row qkv[m]; the
-// wave computes the token's RoPE angles once for its slots.  Lane l holds
-// dims 2l, 2l + 1.  RoPE pairs dims (i, i + 64) (rotation of the two halves):
+// One workgroup (4 waves) per token m; each group of 16 lanes takes one head
+// slot j at a time (j < Hq query heads, then Hkv key heads, then Hkv value
+// heads of the projection row qkv[m]; slots gg, gg + 16, ... for group gg),
+// lane l of a group holding dims 8 l .. 8 l + 7.  The token's 64 RoPE angles
+// a_i = fl32(pos * inv_freq[i]) are computed once into LDS.  RoPE pairs dims
+// (i, i + 64), which sit in lanes l and l + 8 of the group:
 //   x'[i] = x[i] cos(a_i) - x[i + 64] sin(a_i),  x'[i + 64] = x[i + 64] cos(a_i) + x[i] sin(a_i)
-// with a_i = fl32(pos * inv_freq[i]).  Queries are stored as bf16; keys are
-// rounded to bf16, rotated by c H (optional) and quantized; values are
-// quantized (optionally after c H).  Token m belongs to sequence m / T (T = 1
-// for a decode step, T new tokens per sequence for a prefill); its cache row
-// for kv head h is ((m / T) * Hkv + h) * s_cap + pos[m]; positions outside
-// [0, s_cap) write nothing.
+// Queries are stored as bf16; keys are rounded to bf16, rotated by c H
+// (optional: butterflies over dim bits 0..2 in the lane, 3..6 across the
+// group) and quantized; values are quantized (optionally after c H).  Token m
+// belongs to sequence m / T (T = 1 for a decode step, T new tokens per
+// sequence for a prefill); its cache row for kv head h is
+// ((m / T) * Hkv + h) * s_cap + pos[m]; positions outside [0, s_cap) write
+// nothing.
 __global__ __launch_bounds__(256) void rope_kv_append_kernel(
-    const uint16_t* __restrict__ qkv, int64_t ldq, int M, int T, int Hq, int Hkv, int spw,
+    const uint16_t* __restrict__ qkv, int64_t ldq, int M, int T, int Hq, int Hkv,
     const int32_t* __restrict__ positions, RopeTable tab, int k_had, int v_had,
     uint16_t* __restrict__ q_out, uint8_t* __restrict__ kc, uint16_t* __restrict__ ks,
     int16_t* __restrict__ kz, uint8_t* __restrict__ vc, uint16_t* __restrict__ vs,
     int16_t* __restrict__ vz, int64_t s_cap, float* __restrict__ k_dbg,
     float* __restrict__ v_dbg) {
-  const int lane = (int)__builtin_amdgcn_workitem_id_x() & 63;
-  const int64_t wid = (int64_t)__builtin_amdgcn_workgroup_id_x() * 4 +
-                      ((int)__builtin_amdgcn_workitem_id_x() >> 6);
+  __shared__ float2 s_cs[HD / 2];  // (cos, sin) of the token's angles
+  const int tid = (int)__builtin_amdgcn_workitem_id_x();
+  const int m = (int)__builtin_amdgcn_workgroup_id_x();
+  const int l16 = tid & 15, gg = tid >> 4;
   const int slots = Hq + 2 * Hkv;
-  const int per_tok = (slots + spw - 1) / spw;
-  if (wid >= (int64_t)M * per_tok) return;
-  const int m = (int)(wid / per_tok);
-  const int j0 = (int)(wid - (int64_t)m * per_tok) * spw, j1 = min(j0 + spw, slots);
   const int pos = positions[m];
-  const uint32_t* row = reinterpret_cast<const uint32_t*>(qkv + (int64_t)m * ldq);
-  float s0 = 0.0f, c0 = 1.0f, s1 = 0.0f, c1 = 1.0f;
-  if (j0 < Hq + Hkv) {
-    const int i0 = (2 * lane) & 63;
-    sincosf((float)pos * tab.inv_freq[i0], &s0, &c0);
-    sincosf((float)pos * tab.inv_freq[i0 + 1], &s1, &c1);
+  if (tid < HD / 2) {
+    float sn, cs;
+    sincosf((float)pos * tab.inv_freq[tid], &sn, &cs);
+    s_cs[tid] = make_float2(cs, sn);
   }
-  for (int j = j0; j < j1; ++j) {
-    const uint32_t w = row[(int64_t)j * (HD / 2) + lane];
-    float x0 = bf16_lo(w), x1 = bf16_hi(w);
+  __syncthreads();
+  // this lane's angles: pair indices 8 (l16 mod 8) .. + 7
+  float cs8[8], sn8[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float2 v = s_cs[8 * (l16 & 7) + i];
+    cs8[i] = v.x;
+    sn8[i] = v.y;
+  }
+  const bool upper = l16 >= 8;  // holds dims 64 .. 127
+  const uint16_t* row = qkv + (int64_t)m * ldq + 8 * l16;
+  for (int j = gg; j < slots; j += 16) {
+    const uint4 w4 = *reinterpret_cast<const uint4*>(row + (int64_t)j * HD);
+    const uint32_t wv[4] = {w4.x, w4.y, w4.z, w4.w};
+    float x[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x[2 * k] = bf16_lo(wv[k]);
+      x[2 * k + 1] = bf16_hi(wv[k]);
+    }
     const bool is_v = j >= Hq + Hkv;
     if (!is_v) {
-      const float p0 = __shfl_xor(x0, 32), p1 = __shfl_xor(x1, 32);
-      if (lane < 32) {
-        x0 = x0 * c0 - p0 * s0;
-        x1 = x1 * c1 - p1 * s1;
-      } else {
-        x0 = x0 * c0 + p0 * s0;
-        x1 = x1 * c1 + p1 * s1;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float p = __shfl_xor(x[i], 8);
+        x[i] = upper ? x[i] * cs8[i] + p * sn8[i] : x[i] * cs8[i] - p * sn8[i];
       }
       if (j < Hq) {
-        reinterpret_cast<uint32_t*>(q_out + ((int64_t)m * Hq + j) * HD)[lane] = bf16x2_rne(x0, x1);
+        *reinterpret_cast<uint4*>(q_out + ((int64_t)m * Hq + j) * HD + 8 * l16) =
+            make_uint4(bf16x2_rne(x[0], x[1]), bf16x2_rne(x[2], x[3]), bf16x2_rne(x[4], x[5]),
+                       bf16x2_rne(x[6], x[7]));
         continue;
       }
       // the key after RoPE is a bf16 activation
-      x0 = bf16_lo(f32_to_bf16_rne(x0));
-      x1 = bf16_lo(f32_to_bf16_rne(x1));
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] = bf16_lo(f32_to_bf16_rne(x[i]));
     }
     const int h = is_v ? j - Hq - Hkv : j - Hq;
     if (is_v ? v_had : k_had) {
-      // 128-point FWHT: dim bit 0 inside the lane, bits 1..6 across lanes
-      float a = x0 + x1, b = x0 - x1;
+      // 128-point FWHT: dim bits 0..2 inside the lane, bits 3..6 across the group
 #pragma unroll
-      for (int s = 0; s < 6; ++s) {
-        const float ya = __shfl_xor(a, 1 << s), yb = __shfl_xor(b, 1 << s);
-        const bool up = (lane >> s) & 1;
-        a = up ? ya - a : a + ya;
-        b = up ? yb - b : b + yb;
+      for (int st = 1; st < 8; st <<= 1)
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (!(i & st)) {
+            const float a = x[i], b = x[i + st];
+            x[i] = a + b;
+            x[i + st] = a - b;
+          }
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        const bool up = (l16 >> st) & 1;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float o = __shfl_xor(x[i], 1 << st);
+          x[i] = up ? o - x[i] : x[i] + o;
+        }
       }
       const float c = 0.08838834764831845f;  // fl32(1 / sqrt(128))
-      x0 = a * c;
-      x1 = b * c;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] *= c;
     }
     float* dbg = is_v ? v_dbg : k_dbg;
-    if (dbg) reinterpret_cast<float2*>(dbg + ((int64_t)m * Hkv + h) * HD)[lane] = make_float2(x0, x1);
-    const float mx = wmax(fmaxf(x0, x1)), mn = wmin(fminf(x0, x1));
+    if (dbg) {
+      float4* d4 = reinterpret_cast<float4*>(dbg + ((int64_t)m * Hkv + h) * HD + 8 * l16);
+      d4[0] = make_float4(x[0], x[1], x[2], x[3]);
+      d4[1] = make_float4(x[4], x[5], x[6], x[7]);
+    }
+    float mx = x[0], mn = x[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) {
+      mx = fmaxf(mx, x[i]);
+      mn = fminf(mn, x[i]);
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      mx = fmaxf(mx, __shfl_xor(mx, o));
+      mn = fminf(mn, __shfl_xor(mn, o));
+    }
     const QParams p = quant_params(mx, mn);
     const uint32_t lo = __float_as_uint(p.lo);
-    const uint32_t code = (quant_bits(x0, p) - lo) | ((quant_bits(x1, p) - lo) << 4);
+    uint32_t code = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) code |= (quant_bits(x[k], p) - lo) << (4 * k);
     if (pos < 0 || (int64_t)pos >= s_cap) continue;
     const int64_t crow = ((int64_t)(m / T) * Hkv + h) * s_cap + pos;
-    (is_v ? vc : kc)[crow * (HD / 2) + lane] = (uint8_t)code;
-    if (lane == 0) {
+    reinterpret_cast<uint32_t*>((is_v ? vc : kc) + crow * (HD / 2))[l16] = code;
+    if (l16 == 0) {
       (is_v ? vs : ks)[crow] = p.s16;
       (is_v ? vz : kz)[crow] = p.z;
     }
@@ -463,12 +503,8 @@ hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, in
   RopeTable tab;
   for (int i = 0; i < HD / 2; ++i)
     tab.inv_freq[i] = (float)__builtin_pow(rope_base, -2.0 * i / (double)HD);
-  // many tokens: a wave takes 8 head slots of a token (one set of angles for
-  // them); few tokens: one slot per wave, for parallelism
-  const int spw = M >= 256 ? 8 : 1;
-  const int64_t waves = M * ((Hq + 2 * Hkv + spw - 1) / spw);
-  hipLaunchKernelGGL(rope_kv_append_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0,
-                     stream, qkv, ldq, (int)M, (int)T, (int)Hq, (int)Hkv, spw, positions, tab, k_had ? 1 : 0,
+  hipLaunchKernelGGL(rope_kv_append_kernel, dim3((unsigned)M), dim3(256), 0, stream, qkv, ldq,
+                     (int)M, (int)T, (int)Hq, (int)Hkv, positions, tab, k_had ? 1 : 0,
                      v_had ? 1 : 0, q_out, kc, ks, kz, vc, vs, vz, s_cap, k_dbg, v_dbg);
   return hipGetLastError();
 }

@@ -344,8 +344,8 @@ offq_status_t rope_kv(const uint16_t* qkv, int64_t ldq, int64_t B, int64_t T, in
   if (B < 0 || T < 1 || Hq <= 0 || Hkv <= 0)
     return fail(OFFQ_ERR_INVALID, "need rows >= 0, T >= 1, Hq, Hkv > 0");
   if (head_dim != 128) return fail(OFFQ_ERR_UNSUPPORTED, "head_dim = %d (only 128)", head_dim);
-  if (ldq < (Hq + 2 * Hkv) * 128 || ldq % 2)
-    return fail(OFFQ_ERR_INVALID, "ldq must be >= (Hq + 2 Hkv) * 128 and even");
+  if (ldq < (Hq + 2 * Hkv) * 128 || ldq % 8)
+    return fail(OFFQ_ERR_INVALID, "ldq must be >= (Hq + 2 Hkv) * 128 and a multiple of 8");
   if (s_cap < 1) return fail(OFFQ_ERR_INVALID, "s_cap must be >= 1");
   if (!(rope_base > 1.0) || rope_base > 1e30) return fail(OFFQ_ERR_INVALID, "rope_base must be > 1");
   if ((k_hadamard != 0 && k_hadamard != 1) || (v_hadamard != 0 && v_hadamard != 1))
@@ -359,10 +359,12 @@ offq_status_t rope_kv(const uint16_t* qkv, int64_t ldq, int64_t B, int64_t T, in
   if (!qkv || !positions || !q_out || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale ||
       !v_zero)
     return fail(OFFQ_ERR_INVALID, "null pointer argument");
-  if (!aligned(qkv, 4) || !aligned(positions, 4) || !aligned(q_out, 4) || !aligned(k_scale, 2) ||
+  if (!aligned(qkv, 16) || !aligned(positions, 4) || !aligned(q_out, 16) ||
+      !aligned(k_codes, 4) || !aligned(v_codes, 4) || !aligned(k_scale, 2) ||
       !aligned(k_zero, 2) || !aligned(v_scale, 2) || !aligned(v_zero, 2) ||
-      (k_y_debug && !aligned(k_y_debug, 8)) || (v_y_debug && !aligned(v_y_debug, 8)))
-    return fail(OFFQ_ERR_INVALID, "misaligned pointer (qkv, q_out, positions: 4 B; debug: 8 B)");
+      (k_y_debug && !aligned(k_y_debug, 16)) || (v_y_debug && !aligned(v_y_debug, 16)))
+    return fail(OFFQ_ERR_INVALID,
+                "misaligned pointer (qkv, q_out, debug: 16 B; codes, positions: 4 B)");
   if (M == 0) return ok();
   if (offq_status_t st = check_device()) return st;
   return launched(offq::launch_rope_kv_append(qkv, ldq, M, T, Hq, Hkv, positions, rope_base,
