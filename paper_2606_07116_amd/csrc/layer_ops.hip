@@ -129,11 +129,12 @@ struct RopeTable {
   float inv_freq[HD / 2];  // fl32(base^(-2i/128)), computed on the host in double
 };
 
-// One workgroup (4 waves) per token m; each group of 16 lanes takes one head
-// slot j at a time (j < Hq query heads, then Hkv key heads, then Hkv value
-// heads of the projection row qkv[m]; slots gg, gg + 16, ... for group gg),
-// lane l of a group holding dims 8 l .. 8 l + 7.  The token's 64 RoPE angles
-// a_i = fl32(pos * inv_freq[i]) are computed once into LDS.  RoPE pairs dims
+// One workgroup per (token m, GPW head slots): 16 slots (4 waves) when the
+// step has many tokens, 4 (one wave) for a few tokens, so that a decode step
+// still has enough workgroups; each group of 16 lanes takes one head slot j (j < Hq query heads, then Hkv key heads, then
+// Hkv value heads of the projection row qkv[m]), lane l of a group holding
+// dims 8 l .. 8 l + 7.  The token's 64 RoPE angles a_i = fl32(pos *
+// inv_freq[i]) are computed once per workgroup into LDS.  RoPE pairs dims
 // (i, i + 64), which sit in lanes l and l + 8 of the group:
 //   x'[i] = x[i] cos(a_i) - x[i + 64] sin(a_i),  x'[i + 64] = x[i + 64] cos(a_i) + x[i] sin(a_i)
 // Queries are stored as bf16; keys are rounded to bf16, rotated by c H
@@ -143,7 +144,8 @@ struct RopeTable {
 // sequence for a prefill); its cache row for kv head h is
 // ((m / T) * Hkv + h) * s_cap + pos[m]; positions outside [0, s_cap) write
 // nothing.
-__global__ __launch_bounds__(256) void rope_kv_append_kernel(
+template <int GPW>
+__global__ __launch_bounds__(16 * GPW) void rope_kv_append_kernel(
     const uint16_t* __restrict__ qkv, int64_t ldq, int M, int T, int Hq, int Hkv,
     const int32_t* __restrict__ positions, RopeTable tab, int k_had, int v_had,
     uint16_t* __restrict__ q_out, uint8_t* __restrict__ kc, uint16_t* __restrict__ ks,
@@ -152,9 +154,11 @@ __global__ __launch_bounds__(256) void rope_kv_append_kernel(
     float* __restrict__ v_dbg) {
   __shared__ float2 s_cs[HD / 2];  // (cos, sin) of the token's angles
   const int tid = (int)__builtin_amdgcn_workitem_id_x();
-  const int m = (int)__builtin_amdgcn_workgroup_id_x();
-  const int l16 = tid & 15, gg = tid >> 4;
   const int slots = Hq + 2 * Hkv;
+  const int nchunk = (slots + GPW - 1) / GPW;
+  const int bid = (int)__builtin_amdgcn_workgroup_id_x();
+  const int m = bid / nchunk;
+  const int l16 = tid & 15, j = (bid - m * nchunk) * GPW + (tid >> 4);
   const int pos = positions[m];
   if (tid < HD / 2) {
     float sn, cs;
@@ -172,7 +176,7 @@ __global__ __launch_bounds__(256) void rope_kv_append_kernel(
   }
   const bool upper = l16 >= 8;  // holds dims 64 .. 127
   const uint16_t* row = qkv + (int64_t)m * ldq + 8 * l16;
-  for (int j = gg; j < slots; j += 16) {
+  if (j < slots) {  // whole groups of 16 lanes leave together
     const uint4 w4 = *reinterpret_cast<const uint4*>(row + (int64_t)j * HD);
     const uint32_t wv[4] = {w4.x, w4.y, w4.z, w4.w};
     float x[8];
@@ -192,7 +196,7 @@ __global__ __launch_bounds__(256) void rope_kv_append_kernel(
         *reinterpret_cast<uint4*>(q_out + ((int64_t)m * Hq + j) * HD + 8 * l16) =
             make_uint4(bf16x2_rne(x[0], x[1]), bf16x2_rne(x[2], x[3]), bf16x2_rne(x[4], x[5]),
                        bf16x2_rne(x[6], x[7]));
-        continue;
+        return;
       }
       // the key after RoPE is a bf16 activation
 #pragma unroll
@@ -245,7 +249,7 @@ __global__ __launch_bounds__(256) void rope_kv_append_kernel(
     uint32_t code = 0;
 #pragma unroll
     for (int k = 0; k < 8; ++k) code |= (quant_bits(x[k], p) - lo) << (4 * k);
-    if (pos < 0 || (int64_t)pos >= s_cap) continue;
+    if (pos < 0 || (int64_t)pos >= s_cap) return;
     const int64_t crow = ((int64_t)(m / T) * Hkv + h) * s_cap + pos;
     reinterpret_cast<uint32_t*>((is_v ? vc : kc) + crow * (HD / 2))[l16] = code;
     if (l16 == 0) {
@@ -503,9 +507,13 @@ hipError_t launch_rope_kv_append(const uint16_t* qkv, int64_t ldq, int64_t M, in
   RopeTable tab;
   for (int i = 0; i < HD / 2; ++i)
     tab.inv_freq[i] = (float)__builtin_pow(rope_base, -2.0 * i / (double)HD);
-  hipLaunchKernelGGL(rope_kv_append_kernel, dim3((unsigned)M), dim3(256), 0, stream, qkv, ldq,
-                     (int)M, (int)T, (int)Hq, (int)Hkv, positions, tab, k_had ? 1 : 0,
-                     v_had ? 1 : 0, q_out, kc, ks, kz, vc, vs, vz, s_cap, k_dbg, v_dbg);
+  // 16 head slots per workgroup with many tokens, 4 with few
+  const int gpw = M >= 256 ? 16 : 4;
+  const int64_t nchunk = (Hq + 2 * Hkv + gpw - 1) / gpw;
+  hipLaunchKernelGGL(gpw == 16 ? rope_kv_append_kernel<16> : rope_kv_append_kernel<4>,
+                     dim3((unsigned)(M * nchunk)), dim3(16 * gpw), 0, stream, qkv, ldq, (int)M,
+                     (int)T, (int)Hq, (int)Hkv, positions, tab, k_had ? 1 : 0, v_had ? 1 : 0,
+                     q_out, kc, ks, kz, vc, vs, vz, s_cap, k_dbg, v_dbg);
   return hipGetLastError();
 }
 
