@@ -243,20 +243,23 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
 // K in eighths with two tiles per wave from 6144 channels, one below, where K
 // splits into eighths of whole batches (from K = 16384 with two tiles: K in
 // sixteenths, batches of two steps: 26.7-27.8 against 29.9-31.4 us at
-// 28672 -> 8192); else one tile per wave and K in quarters (e.g. K = 14336).  A K that is not a whole number of such batches
-// (short rows, e.g. K = 256) takes one tile per wave, batches of one step and
-// K in as many parts (4, 2, 1) as it divides into.
+// 28672 -> 8192); a K that is a multiple of 2048 but not of 4096 (14336,
+// 6144, 2048) one tile per wave, K in sixteenths and batches of one step
+// (4096 <- 14336 at g = 128: 15.0 -> 11.0 us against quarters in batches of
+// four; 7.9 against 12.3 us at M = 1).  A K that is not a whole number of
+// such batches (short rows, e.g. K = 256) takes one tile per wave, batches
+// of one step and K in as many parts (4, 2, 1) as it divides into.
 static void gemv_shape(int64_t N, int64_t K, int& T, int& P, int& B) {
   if (N >= 16384) {
-    T = 4, P = 4;
+    T = 4, P = 4, B = 2;
   } else if (K % 4096 == 0) {
     T = N >= 6144 ? 2 : 1, P = T == 2 && K >= 16384 ? 16 : 8;
+    B = P == 16 ? 2 : 4;
   } else if (K % 2048 == 0) {
-    T = 1, P = 4;
+    T = 1, P = 16, B = 1;
   } else {
-    T = 4, P = 4;
+    T = 4, P = 4, B = 2;
   }
-  B = T >= 4 || P == 16 ? 2 : 4;
   if (K % ((int64_t)P * KSTEP * B) != 0) {
     T = 1, B = 1;
     P = K % (4 * KSTEP) == 0 ? 4 : K % (2 * KSTEP) == 0 ? 2 : 1;
@@ -313,6 +316,7 @@ hipError_t launch_w4a4_gemv_mfma(const uint8_t* a_codes, const uint16_t* a_scale
   return launch_gv<T, P, B>(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, log2g, \
                             y, ldy, acc_debug, stream)
   if (B == 1) {
+    if (P == 16) OFFQ_GV(1, 16, 1);
     if (P == 4) OFFQ_GV(1, 4, 1);
     if (P == 2) OFFQ_GV(1, 2, 1);
     OFFQ_GV(1, 1, 1);
