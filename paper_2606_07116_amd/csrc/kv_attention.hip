@@ -623,7 +623,21 @@ __global__ __launch_bounds__(THREADS) void kv_attention_gqa_kernel(
   __shared__ GqaSmem<G> S;
   const int unit = (int)__builtin_amdgcn_workgroup_id_x();
   if (unit >= units) return;
-  const int kvh = unit / nchunk, chunk = unit - kvh * nchunk;
+  // The full chunks of every key/value head take the low ids and the short
+  // final chunks (seq_len not a multiple of CHG) the last ones: workgroups
+  // start in id order, so when the full chunks just fill the resident slots
+  // (context 4096 + 1 at 128 key/value heads: 1024 full, 128 one-position
+  // chunks) no full chunk waits for a second round behind the short ones.
+  const int nfull = seq_len / CHG;
+  const int nkv = units / nchunk;
+  int kvh, chunk;
+  if (unit < nkv * nfull) {
+    kvh = unit / nfull;
+    chunk = unit - kvh * nfull;
+  } else {
+    kvh = unit - nkv * nfull;
+    chunk = nfull;
+  }
   const int j0 = chunk * CHG;
   const int n = min(CHG, seq_len - j0);
   const int64_t row0 = (int64_t)kvh * S_cap + j0;
