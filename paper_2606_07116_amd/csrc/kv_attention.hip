@@ -339,16 +339,19 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
 // ---------------------------------------------------------------------------
 // Grouped heads together: one workgroup per (key/value head, chunk) serves
 // the G query heads that share it, so each code word is loaded and unpacked
-// once for all of them.  Scores: as above, with G sets of query pairs (each
-// query scaled by its own power of two); every lane of a quad ends with the
-// G dot products of its position and lane qd stores query qd's score to LDS.
-// Weights: per pair of adjacent positions and query, fp16 pairs in LDS.
-// Values: a lane (word dg = lane & 15 of the row, position pair pg =
-// lane >> 4) takes 4 code bytes (8 dimensions) of two adjacent positions per
-// step; the interleave and the masks are shared by the G queries' dots.
+// once for all of them.  Scores: on the matrix cores, one 16x16x32 fp16
+// product per 16 positions and 32 dims, the key codes as fp16 subnormals
+// (the same exact products as the dot2 path above, each query scaled by its
+// own power of two), the G queries as columns of the other operand (the
+// remaining columns zero: the matrix cores still take far fewer cycles than
+// the G dot2 chains).  Weights: per pair of adjacent positions and query,
+// fp16 pairs in LDS.  Values: a lane (word dg = lane & 15 of the row,
+// position pair pg = lane >> 4) takes 4 code bytes (8 dimensions) of two
+// adjacent positions per step; the interleave and the masks are shared by
+// the G queries' dots.
 constexpr int CHG = 512;        // positions per grouped-head workgroup
 constexpr int GROWS = CHG / WAVES;
-constexpr int GNIT = GROWS / 32;
+constexpr int GNK = GROWS / 16;  // groups of 16 positions per wave
 
 // Workgroup barrier for LDS traffic only: global loads still in flight stay
 // in flight (a full barrier would first wait for them).
@@ -358,8 +361,11 @@ __device__ __forceinline__ void lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+typedef _Float16 h8v_t __attribute__((ext_vector_type(8)));
+typedef float f4v_t __attribute__((ext_vector_type(4)));
+
 template <int G>
-struct GqaSmem {
+struct alignas(16) GqaSmem {
   float qf[G][DH];
   uint32_t qp[G][DH / 2];
   float qsum[G], qexp[G];
@@ -384,28 +390,60 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
   const int tid = (int)__builtin_amdgcn_workitem_id_x();
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qd = lane & 3, rg = lane >> 2;
-  const int nact = FULL ? GNIT : min(GNIT, max(0, (n - wave * GROWS + 31) / 32));
-  auto row = [&](int it, int h) {
-    const int r = wave * GROWS + it * 32 + h * 16 + rg;
-    return FULL ? r : min(r, n - 1);
-  };
+  const int pr = lane & 15, kq = lane >> 4;
+  const int nact = FULL ? GNK : min(GNK, max(0, (n - wave * GROWS + 15) / 16));
 
-  // ---- key codes ------------------------------------------------------------
+  // ---- first the small loads: the query (waves < G) and the scale and
+  // zero-point of two positions per thread.  Loads complete in issue order,
+  // so their uses below wait for them alone while the code words requested
+  // after them are still in flight.
+  // (every wave loads a query, waves past G a copy, so that no branch
+  // holds the load and its first use together)
+  const uint16_t* qh = q + ((int64_t)kvh * G + wave % G) * DH;
+  const uint32_t qlo = qh[2 * lane], qhi = qh[2 * lane + 1];
+  constexpr int PPT = CHG / THREADS;  // positions per thread for the parameters
+  uint16_t ksr[PPT], vsr[PPT];
+  int16_t kzr[PPT], vzr[PPT];
+#pragma unroll
+  for (int t = 0; t < PPT; ++t) {
+    const int r = tid * PPT + t;
+    const int64_t rr = row0 + (FULL ? r : min(r, n - 1));
+    ksr[t] = ks[rr];
+    kzr[t] = kz[rr];
+    vsr[t] = vs[rr];
+    vzr[t] = vz[rr];
+  }
+
+  // ---- key codes: lane (position pr of a group of 16, quarter kq of its row)
   const uint8_t* kbase = kc + row0 * (DH / 2);
-  uint4 kd[GNIT][2];
+  uint4 kd[GNK];
 #pragma unroll
-  for (int it = 0; it < GNIT; ++it)
-    if (FULL || it < nact)
+  for (int gi = 0; gi < GNK; ++gi)
+    if (FULL || gi < nact) {
+      const int r = wave * GROWS + gi * 16 + pr;
+      kd[gi] = *reinterpret_cast<const uint4*>(kbase + (uint32_t)((FULL ? r : min(r, n - 1)) *
+                                                                  (DH / 2) + kq * 16));
+    }
+
+  // ---- value codes: lane (word dg, position pair pg) -------------------------
+  // Requested with the key codes, so that they arrive while the scores are
+  // formed.  Rows past the chunk's end read the last row (their weights are
+  // zero).
+  const int dg = lane & 15, pg = lane >> 4;
+  const uint32_t* vrow = reinterpret_cast<const uint32_t*>(vc + row0 * (DH / 2)) + dg;
+  constexpr int VIT = GROWS / 8;  // steps of 8 positions (4 pairs) per wave
+  uint32_t va[VIT], vb[VIT];
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
-        kd[it][h] =
-            *reinterpret_cast<const uint4*>(kbase + (uint32_t)(row(it, h) * (DH / 2) + qd * 16));
+  for (int t = 0; t < VIT; ++t) {
+    const int ra = wave * GROWS + t * 8 + 2 * pg;
+    const int rA = FULL ? ra : min(ra, n - 1), rB = FULL ? ra + 1 : min(ra + 1, n - 1);
+    va[t] = vrow[(int64_t)rA * (DH / 8)];
+    vb[t] = vrow[(int64_t)rB * (DH / 8)];
+  }
 
   // ---- queries: wave w rotates query w --------------------------------------
   if (wave < G) {
-    const uint16_t* qh = q + ((int64_t)kvh * G + wave) * DH;
-    const float a = bf16_lo(qh[2 * lane]), b = bf16_lo(qh[2 * lane + 1]);
+    const float a = bf16_lo(qlo), b = bf16_lo(qhi);
     float x0 = a + b, x1 = a - b;
 #pragma unroll
     for (int s = 0; s < 6; ++s) {
@@ -426,7 +464,7 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
       S.qexp[wave] = (float)e;
     }
   }
-  __syncthreads();
+  lds_sync();
   if (tid < 64 * G) {
     const int gq = tid >> 6, p = tid & 63;
     const int i = p >> 2, j = p & 3;
@@ -434,94 +472,68 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
     S.qp[gq][p] = pack_f16(S.qf[gq][8 * i + j] * f, S.qf[gq][8 * i + j + 4] * f);
   }
 #pragma unroll
-  for (int t = 0; t < CHG / THREADS; ++t) {
-    const int r = tid * (CHG / THREADS) + t;
-    const int64_t rr = row0 + (FULL ? r : min(r, n - 1));
-    const float skm = sm2 * fp16_bits_to_f32(ks[rr]);
-    S.kab[r] = make_float2(skm, -skm * (float)kz[rr]);
-    S.vsz[r] = (FULL || r < n) ? make_float2(fp16_bits_to_f32(vs[rr]), (float)vz[rr])
+  for (int t = 0; t < PPT; ++t) {
+    const int r = tid * PPT + t;
+    const float skm = sm2 * fp16_bits_to_f32(ksr[t]);
+    S.kab[r] = make_float2(skm, -skm * (float)kzr[t]);
+    S.vsz[r] = (FULL || r < n) ? make_float2(fp16_bits_to_f32(vsr[t]), (float)vzr[t])
                                : make_float2(0.0f, 0.0f);
   }
-  __syncthreads();
+  lds_sync();
 
-  uint32_t qp[G][4][4];
-  float cq[G], qs[G];
+  // ---- scores on the matrix cores --------------------------------------------
+  // A 16x16x32 fp16 product per group of 16 positions and word j of each
+  // row quarter: A = the key codes (row = position pr, the 8 dims of word j
+  // of quarter kq, unpacked by masks into fp16 subnormals c 2^-24 in the
+  // order d0 d4 16d1 16d5 d2 d6 16d3 16d7), B = the queries in the same
+  // order (column = query, zero past G; the odd dims pre-scaled by 1/16 in
+  // qp).  Lane (pr, kq) ends with query pr's dots of positions 4 kq .. 4 kq + 3
+  // of the group; every product is exact in fp32, as in the dot2 path.
+  h8v_t qb[4];
+  float cq = 0.0f, qs = 0.0f;
 #pragma unroll
-  for (int gq = 0; gq < G; ++gq) {
+  for (int j = 0; j < 4; ++j) qb[j] = h8v_t{};
+  if (pr < G) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) qp[gq][u][j] = S.qp[gq][16 * qd + 4 * u + j];
-    cq[gq] = __builtin_amdgcn_ldexpf(1.0f, 9 + (int)S.qexp[gq]);  // dot = 2^-24 sum q' c
-    qs[gq] = S.qsum[gq];
+    for (int j = 0; j < 4; ++j)
+      qb[j] = __builtin_bit_cast(h8v_t, *reinterpret_cast<const uint4*>(&S.qp[pr][16 * kq + 4 * j]));
+    cq = __builtin_amdgcn_ldexpf(1.0f, 9 + (int)S.qexp[pr]);  // dot = 2^-24 sum q' c
+    qs = S.qsum[pr];
   }
-
-  // ---- scores ---------------------------------------------------------------
-  float mloc[G];
+  float mloc = -__builtin_inff();
 #pragma unroll
-  for (int gq = 0; gq < G; ++gq) mloc[gq] = -__builtin_inff();
-#pragma unroll
-  for (int it = 0; it < GNIT; ++it) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int r = wave * GROWS + it * 32 + h * 16 + rg;
-      if (!FULL && it >= nact) {
-        if (qd < G) S.sc[qd][r] = -__builtin_inff();
-        continue;
-      }
-      const uint32_t w4[4] = {kd[it][h].x, kd[it][h].y, kd[it][h].z, kd[it][h].w};
-      float d[G];
-#pragma unroll
-      for (int gq = 0; gq < G; ++gq) d[gq] = 0.0f;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint32_t w = w4[u], w8 = w >> 8;
-        const uint32_t t0 = w & 0x000F000Fu, t1 = w & 0x00F000F0u;
-        const uint32_t t2 = w8 & 0x000F000Fu, t3 = w8 & 0x00F000F0u;
-#pragma unroll
-        for (int gq = 0; gq < G; ++gq) {
-          d[gq] = dot2_f16(qp[gq][u][0], t0, d[gq]);
-          d[gq] = dot2_f16(qp[gq][u][1], t1, d[gq]);
-          d[gq] = dot2_f16(qp[gq][u][2], t2, d[gq]);
-          d[gq] = dot2_f16(qp[gq][u][3], t3, d[gq]);
-        }
-      }
-      const float2 ab = S.kab[r];
-      float mine = -__builtin_inff();
-#pragma unroll
-      for (int gq = 0; gq < G; ++gq) {
-        d[gq] += dpp<0xB1>(d[gq]);
-        d[gq] += dpp<0x4E>(d[gq]);
-        float sg = __builtin_fmaf(ab.x * cq[gq], d[gq], ab.y * qs[gq]);
-        if (!FULL && r >= n) sg = -__builtin_inff();
-        mloc[gq] = fmaxf(mloc[gq], sg);
-        if (qd == gq) mine = sg;
-      }
-      if (qd < G) S.sc[qd][r] = mine;
+  for (int gi = 0; gi < GNK; ++gi) {
+    const int rb = wave * GROWS + gi * 16 + 4 * kq;  // this lane's first position
+    if (!FULL && gi >= nact) {
+      if (pr < G)
+        *reinterpret_cast<float4*>(&S.sc[pr][rb]) =
+            make_float4(-__builtin_inff(), -__builtin_inff(), -__builtin_inff(), -__builtin_inff());
+      continue;
     }
-  }
+    const uint32_t w4[4] = {kd[gi].x, kd[gi].y, kd[gi].z, kd[gi].w};
+    f4v_t d = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-  for (int gq = 0; gq < G; ++gq) {
-    const float m = wave_max(mloc[gq]);
-    if (lane == 0) S.red[0][gq][wave] = m;
-  }
-
-  // ---- value codes: lane (word dg, position pair pg) -------------------------
-  // All of the wave's value words are requested here, into the registers the
-  // key codes held: their latency runs under the softmax below instead of
-  // after it.  Rows past the chunk's end read the last row (their weights
-  // are zero).
-  const int dg = lane & 15, pg = lane >> 4;
-  const uint32_t* vrow = reinterpret_cast<const uint32_t*>(vc + row0 * (DH / 2)) + dg;
-  constexpr int VIT = GROWS / 8;  // steps of 8 positions (4 pairs) per wave
-  uint32_t va[VIT], vb[VIT];
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t w = w4[j], w8 = w >> 8;
+      const uint4 a = make_uint4(w & 0x000F000Fu, w & 0x00F000F0u, w8 & 0x000F000Fu,
+                                 w8 & 0x00F000F0u);
+      d = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v_t, a), qb[j], d, 0, 0, 0);
+    }
+    const float4 ab01 = *reinterpret_cast<const float4*>(&S.kab[rb]);
+    const float4 ab23 = *reinterpret_cast<const float4*>(&S.kab[rb + 2]);
+    const float ax[4] = {ab01.x, ab01.z, ab23.x, ab23.z}, ay[4] = {ab01.y, ab01.w, ab23.y, ab23.w};
+    float sg[4];
 #pragma unroll
-  for (int t = 0; t < VIT; ++t) {
-    const int ra = wave * GROWS + t * 8 + 2 * pg;
-    const int rA = FULL ? ra : min(ra, n - 1), rB = FULL ? ra + 1 : min(ra + 1, n - 1);
-    va[t] = vrow[(int64_t)rA * (DH / 8)];
-    vb[t] = vrow[(int64_t)rB * (DH / 8)];
+    for (int r = 0; r < 4; ++r) {
+      sg[r] = __builtin_fmaf(ax[r] * cq, d[r], ay[r] * qs);
+      if (!FULL && rb + r >= n) sg[r] = -__builtin_inff();
+      mloc = fmaxf(mloc, sg[r]);
+    }
+    if (pr < G) *reinterpret_cast<float4*>(&S.sc[pr][rb]) = make_float4(sg[0], sg[1], sg[2], sg[3]);
   }
+  mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+  mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+  if (lane < G) S.red[0][lane][wave] = mloc;
   lds_sync();
 
   // ---- weights: fp16 pairs per (position pair, query) ------------------------
