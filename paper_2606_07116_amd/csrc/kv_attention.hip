@@ -345,10 +345,9 @@ __device__ __forceinline__ void attention_chunk(ChunkSmem& S, const uint16_t* __
 // own power of two), the G queries as columns of the other operand (the
 // remaining columns zero: the matrix cores still take far fewer cycles than
 // the G dot2 chains).  Weights: per pair of adjacent positions and query,
-// fp16 pairs in LDS.  Values: a lane (word dg = lane & 15 of the row,
-// position pair pg = lane >> 4) takes 4 code bytes (8 dimensions) of two
-// adjacent positions per step; the interleave and the masks are shared by
-// the G queries' dots.
+// fp16 pairs in LDS.  Values: on the matrix cores too, the weights as the
+// row operand and the value codes of 8 positions per lane (two rows'
+// bytes interleaved by a permute, then masked) as the column operand.
 constexpr int CHG = 512;        // positions per grouped-head workgroup
 constexpr int GROWS = CHG / WAVES;
 constexpr int GNK = GROWS / 16;  // groups of 16 positions per wave
@@ -425,21 +424,23 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
                                                                   (DH / 2) + kq * 16));
     }
 
-  // ---- value codes: lane (word dg, position pair pg) -------------------------
+  // ---- value codes: lane (word dg = pr of the row, positions 8 kq .. 8 kq + 7
+  // of each block of 32) -----------------------------------------------------
   // Requested with the key codes, so that they arrive while the scores are
   // formed.  Rows past the chunk's end read the last row (their weights are
-  // zero).
-  const int dg = lane & 15, pg = lane >> 4;
-  const uint32_t* vrow = reinterpret_cast<const uint32_t*>(vc + row0 * (DH / 2)) + dg;
-  constexpr int VIT = GROWS / 8;  // steps of 8 positions (4 pairs) per wave
-  uint32_t va[VIT], vb[VIT];
+  // zero); blocks wholly past it are skipped.
+  constexpr int VB = GROWS / 32;  // blocks of 32 positions per wave
+  const int nvb = FULL ? VB : min(VB, max(0, (n - wave * GROWS + 31) / 32));
+  const uint32_t* vrow = reinterpret_cast<const uint32_t*>(vc + row0 * (DH / 2)) + pr;
+  uint32_t vv[VB][8];
 #pragma unroll
-  for (int t = 0; t < VIT; ++t) {
-    const int ra = wave * GROWS + t * 8 + 2 * pg;
-    const int rA = FULL ? ra : min(ra, n - 1), rB = FULL ? ra + 1 : min(ra + 1, n - 1);
-    va[t] = vrow[(int64_t)rA * (DH / 8)];
-    vb[t] = vrow[(int64_t)rB * (DH / 8)];
-  }
+  for (int bk = 0; bk < VB; ++bk)
+    if (FULL || bk < nvb)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int r = wave * GROWS + bk * 32 + 8 * kq + i;
+        vv[bk][i] = vrow[(int64_t)(FULL ? r : min(r, n - 1)) * (DH / 8)];
+      }
 
   // ---- queries: wave w rotates query w --------------------------------------
   if (wave < G) {
@@ -570,45 +571,51 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
   }
   lds_sync();
 
-  // ---- values ---------------------------------------------------------------
-  float acc[G][8];
+  // ---- values on the matrix cores -------------------------------------------
+  // O[q][8 dg + m] = sum over positions of W[q][pos] V[pos][8 dg + m]: one
+  // 16x16x32 fp16 product per block of 32 positions and nibble m of the code
+  // words.  A = the weights (row = query pr, zero past G; positions
+  // 8 kq .. 8 kq + 7 of the block, the fp16 pairs of wp), B = the value codes
+  // (column = word dg = pr, the same positions in pairs: the bytes of two
+  // rows interleaved by a permute, nibble m masked out as fp16 subnormals,
+  // 16 times the code for odd m).  Lanes 0..15 end with dims 8 dg + m of the
+  // queries 0..3 (their rows of the product).
+  f4v_t oacc[8];
 #pragma unroll
-  for (int gq = 0; gq < G; ++gq)
+  for (int m = 0; m < 8; ++m) oacc[m] = f4v_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int k = 0; k < 8; ++k) acc[gq][k] = 0.0f;
-  {
+  for (int bk = 0; bk < VB; ++bk) {
+    if (!FULL && bk >= nvb) continue;
+    const int p0 = wave * GROWS + bk * 32 + 8 * kq;
+    h8v_t aw = h8v_t{};
+    if (pr < G) aw = __builtin_bit_cast(h8v_t, *reinterpret_cast<const uint4*>(&S.wp[pr][p0 / 2]));
+    uint32_t xs[4][4];  // per position pair: bytes 0-1 of both rows, >> 8, bytes 2-3, >> 8
 #pragma unroll
-    for (int t = 0; t < VIT; ++t) {
-      const int pair = (wave * GROWS + t * 8) / 2 + pg;
-      const uint32_t x0 = __builtin_amdgcn_perm(vb[t], va[t], 0x05040100u);
-      const uint32_t x1 = __builtin_amdgcn_perm(vb[t], va[t], 0x07060302u);
-      const uint32_t x08 = x0 >> 8, x18 = x1 >> 8;
-      const uint32_t c[8] = {x0 & 0x000F000Fu,  x0 & 0x00F000F0u, x08 & 0x000F000Fu,
-                             x08 & 0x00F000F0u, x1 & 0x000F000Fu, x1 & 0x00F000F0u,
-                             x18 & 0x000F000Fu, x18 & 0x00F000F0u};
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t x0 = __builtin_amdgcn_perm(vv[bk][2 * i + 1], vv[bk][2 * i], 0x05040100u);
+      const uint32_t x1 = __builtin_amdgcn_perm(vv[bk][2 * i + 1], vv[bk][2 * i], 0x07060302u);
+      xs[i][0] = x0;
+      xs[i][1] = x0 >> 8;
+      xs[i][2] = x1;
+      xs[i][3] = x1 >> 8;
+    }
 #pragma unroll
-      for (int gq = 0; gq < G; ++gq) {
-        const uint32_t w = S.wp[gq][pair];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) acc[gq][k] = dot2_f16(w, c[k], acc[gq][k]);
-      }
+    for (int m = 0; m < 8; ++m) {
+      const uint32_t mask = (m & 1) ? 0x00F000F0u : 0x000F000Fu;
+      const uint4 bv = make_uint4(xs[0][m >> 1] & mask, xs[1][m >> 1] & mask,
+                                  xs[2][m >> 1] & mask, xs[3][m >> 1] & mask);
+      oacc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aw, __builtin_bit_cast(h8v_t, bv), oacc[m],
+                                                       0, 0, 0);
     }
   }
-  // sum over the 4 position-pair lanes of each word, then over the waves
-#pragma unroll
-  for (int gq = 0; gq < G; ++gq)
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      acc[gq][k] += __shfl_xor(acc[gq][k], 16);
-      acc[gq][k] += __shfl_xor(acc[gq][k], 32);
-    }
-  if (pg == 0) {
+  if (lane < 16) {
 #pragma unroll
     for (int gq = 0; gq < G; ++gq) {
-      float* dst = &S.o[wave][gq][8 * dg];
-      *reinterpret_cast<float4*>(dst) = make_float4(acc[gq][0], acc[gq][1], acc[gq][2], acc[gq][3]);
+      float* dst = &S.o[wave][gq][8 * pr];
+      *reinterpret_cast<float4*>(dst) =
+          make_float4(oacc[0][gq], oacc[1][gq], oacc[2][gq], oacc[3][gq]);
       *reinterpret_cast<float4*>(dst + 4) =
-          make_float4(acc[gq][4], acc[gq][5], acc[gq][6], acc[gq][7]);
+          make_float4(oacc[4][gq], oacc[5][gq], oacc[6][gq], oacc[7][gq]);
     }
   }
   __syncthreads();
@@ -627,7 +634,7 @@ __device__ __forceinline__ void gqa_chunk(GqaSmem<G>& S, const uint16_t* __restr
 }
 
 template <int G>
-__global__ __launch_bounds__(THREADS) void kv_attention_gqa_kernel(
+__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(4))) void kv_attention_gqa_kernel(
     const uint16_t* __restrict__ q, const uint8_t* __restrict__ kc, const uint16_t* __restrict__ ks,
     const int16_t* __restrict__ kz, const uint8_t* __restrict__ vc, const uint16_t* __restrict__ vs,
     const int16_t* __restrict__ vz, int64_t S_cap, int seq_len, int nchunk, int units, float sm2,
