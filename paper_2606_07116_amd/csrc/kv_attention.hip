@@ -642,20 +642,22 @@ __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(4))) vo
   __shared__ GqaSmem<G> S;
   const int unit = (int)__builtin_amdgcn_workgroup_id_x();
   if (unit >= units) return;
-  // The full chunks of every key/value head take the low ids and the short
-  // final chunks (seq_len not a multiple of CHG) the last ones: workgroups
-  // start in id order, so when the full chunks just fill the resident slots
-  // (context 4096 + 1 at 128 key/value heads: 1024 full, 128 one-position
-  // chunks) no full chunk waits for a second round behind the short ones.
+  // The short final chunks (seq_len not a multiple of CHG) take the lowest
+  // ids, then the full chunks of every key/value head.  Workgroups start in
+  // id order: the short ones finish within a few microseconds and free their
+  // slots early, instead of running as a tail after the full ones (context
+  // 4096 + 1 at 128 key/value heads: 128 one-position chunks, then 1024 full
+  // ones, four resident per CU).
   const int nfull = seq_len / CHG;
   const int nkv = units / nchunk;
+  const int nshort = units - nkv * nfull;  // nkv or 0
   int kvh, chunk;
-  if (unit < nkv * nfull) {
-    kvh = unit / nfull;
-    chunk = unit - kvh * nfull;
-  } else {
-    kvh = unit - nkv * nfull;
+  if (unit < nshort) {
+    kvh = unit;
     chunk = nfull;
+  } else {
+    kvh = (unit - nshort) / nfull;
+    chunk = unit - nshort - kvh * nfull;
   }
   const int j0 = chunk * CHG;
   const int n = min(CHG, seq_len - j0);
