@@ -188,11 +188,12 @@ def test_rope_kv_append_position_outside_cache_writes_nothing():
                                                 (3, 4, 1, 64, 50), (2, 16, 8, 700, 650),
                                                 (1, 4, 2, 2048, 2048), (1, 16, 2, 1300, 1300),
                                                 (2, 8, 2, 3000, 1),
-                                                # a final chunk of 64 positions joins the
-                                                # chunk before it, one of 65 does not; with
-                                                # 576 one workgroup per head takes both
+                                                # final chunks of 64 and 65 positions, and of
+                                                # 16, 48 and 33 (whole and partial groups of
+                                                # 16 keys and blocks of 32 values in a wave)
                                                 (1, 8, 2, 1100, 1088), (1, 8, 4, 1100, 1089),
-                                                (2, 4, 2, 600, 576)])
+                                                (2, 4, 2, 600, 576), (1, 8, 2, 600, 528),
+                                                (2, 4, 2, 600, 560), (1, 8, 2, 600, 545)])
 def test_gqa_attention(B, Hq, Hkv, S, seq_len):
     q = inputs.queries(B, Hq, 128, seed=S)
     kc, ks, kz = inputs.kv4_cache(B, Hkv, S, 128, seed=S)
