@@ -30,7 +30,9 @@
 //   dimension, dotted with the fp16 pair of their weights p sv.
 //
 // Grouped-query attention: query head h of batch b reads the cache of
-// key/value head h / group (group = Hq / Hkv; 1 for plain multi-head).
+// key/value head h / group (group = Hq / Hkv; 1 for plain multi-head).  For
+// group 2 and 4 one workgroup serves the group's query heads together and
+// forms both products on the matrix cores instead (below).
 //
 // Organisation (split over the sequence, as in flash decoding)
 // * Pass 1: one workgroup of 4 waves per (b, h, chunk of 1024 positions);
