@@ -114,7 +114,9 @@ offq_status_t offq_rotate_quantize(const uint16_t* x, int64_t M, int64_t K, int6
  *
  *   a_codes  uint8 [M, K/2] (from offq_rotate_quantize), 16-byte aligned.
  *   a_scale  fp16  [M, K/g];  a_zero int16 [M, K/g].
- *   w_codes  uint8 [N, K/2] two's-complement int4, 16-byte aligned.
+ *   w_codes  two's-complement int4 codes in the blocked layout written by
+ *            offq_pack_weights (offq_weight_codes_bytes(N, K) bytes),
+ *            16-byte aligned.
  *   w_scale  fp16  [N] per-output-channel symmetric scale sw.
  *   w_colsum int32 [K/g, N]: colsum[b, n] = sum_{k in group b} q_w[n, k].
  *   M, N, K  K % g == 0; g power of two, 64 <= g <= 8192.
@@ -157,11 +159,28 @@ offq_status_t offq_kv_quantize(const uint16_t* kv, int64_t rows, int32_t head_di
  *
  *   w        fp32 [N, K] contiguous, 16-byte aligned.
  *   g        group size the activations will use (power of two, 64..8192, K % g == 0).
- *   w_codes  uint8 [N, K/2]; w_scale fp16 [N]; w_colsum int32 [K/g, N].
+ *   w_codes  offq_weight_codes_bytes(N, K) bytes, 16-byte aligned, in the
+ *            blocked layout below; w_scale fp16 [N]; w_colsum int32 [K/g, N].
+ *
+ *   Blocked layout of w_codes: the codes of 16 output rows x 128 k form a
+ *   1 KB block, 16 rows of 64 bytes (byte j of a block row holds k = 2j in
+ *   its low nibble and k = 2j + 1 in its high nibble); the blocks of a band of
+ *   16 rows follow in k order, the bands in row order.  Byte kk of row n sits
+ *   at ((n / 16) * KB + kk / 64) * 1024 + (n % 16) * 64 + kk % 64 with
+ *   KB = ceil(K / 128).  Rows past N up to a multiple of 16 and k past K up
+ *   to a multiple of 128 hold zero codes.  (One wave's 16-byte-per-lane load
+ *   of a block then reads 1 KB of contiguous memory in the decode GEMV.)
  */
 offq_status_t offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g,
                       uint8_t* w_codes, uint16_t* w_scale, int32_t* w_colsum,
                       void* stream);
+
+/*
+ * offq_weight_codes_bytes -- size of w_codes for an [N, K] weight:
+ * ceil(N / 16) * ceil(K / 128) * 1024 bytes; 0 for N or K outside
+ * [1, 2^30].
+ */
+int64_t offq_weight_codes_bytes(int64_t N, int64_t K);
 
 /*
  * offq_kv_attention_decode -- one decode step of attention over the 4-bit KV

@@ -6,7 +6,9 @@ arguments.  Entry points (same names as ``include/offq.h``):
     offq_rotate_quantize(x, g, apply_hadamard=True, debug=False)
     offq_w4a4_gemm(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, g, debug=False)
     offq_kv_quantize(kv, apply_hadamard=True, debug=False)
-    offq_pack_weights(w, g)
+    offq_pack_weights(w, g)          (w_codes in the blocked operand layout;
+                                      blocked_weight_codes / row_major_weight_codes
+                                      convert from / to row-major [N, K/2] codes)
     offq_kv_attention_decode(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, seq_len, ...)
     offq_add_rmsnorm(x, res=None, eps=1e-5)
     offq_swiglu(gu)
@@ -50,6 +52,10 @@ _EXPORTS = frozenset((
     "offq_pack_weights",
     "offq_rotate_quantize",
     "offq_w4a4_gemm",
+    "offq_weight_codes_bytes",
+    "weight_codes_shape",
+    "blocked_weight_codes",
+    "row_major_weight_codes",
     "status_name",
 ))
 

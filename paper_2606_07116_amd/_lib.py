@@ -28,6 +28,7 @@ EXPORTED = (
     "offq_w4a4_gemm",
     "offq_kv_quantize",
     "offq_pack_weights",
+    "offq_weight_codes_bytes",
     "offq_kv_attention_decode",
     "offq_kv_attention_workspace_bytes",
     "offq_kv_attention_decode_gqa",
@@ -85,6 +86,8 @@ def _load():
     lib.offq_kv_quantize.argtypes = [vp, i64, i32, i64, i32, vp, vp, vp, vp, vp]
     lib.offq_pack_weights.restype = ctypes.c_int
     lib.offq_pack_weights.argtypes = [vp, i64, i64, i32, vp, vp, vp, vp]
+    lib.offq_weight_codes_bytes.restype = i64
+    lib.offq_weight_codes_bytes.argtypes = [i64, i64]
     lib.offq_kv_attention_decode.restype = ctypes.c_int
     lib.offq_kv_attention_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i32,
                                              ctypes.c_float, i32, vp, vp, i64, vp]
@@ -186,6 +189,39 @@ def offq_kv_attention_decode_raw(q, k_codes, k_scale, k_zero, v_codes, v_scale, 
 
 def offq_kv_attention_workspace_bytes(B, H, seq_len):
     return lib.offq_kv_attention_workspace_bytes(B, H, seq_len)
+
+
+def offq_weight_codes_bytes(N, K):
+    return lib.offq_weight_codes_bytes(N, K)
+
+
+def weight_codes_shape(N, K):
+    """Shape of the w_codes tensor offq_pack_weights returns: [bands of 16
+    rows, blocks of 128 k, 16 rows, 64 bytes] (the blocked operand layout)."""
+    return ((N + 15) // 16, (K + 127) // 128, 16, 64)
+
+
+def blocked_weight_codes(rows):
+    """Row-major packed weight codes [N, K/2] (uint8, numpy or torch) in the
+    blocked operand layout, zero padded: a layout conversion for weights
+    packed elsewhere."""
+    N, Kh = rows.shape
+    nb, kb, _, _ = weight_codes_shape(N, 2 * Kh)
+    if hasattr(rows, "new_zeros"):
+        pad = rows.new_zeros((16 * nb, 64 * kb))
+    else:
+        import numpy as np
+        pad = np.zeros((16 * nb, 64 * kb), dtype=rows.dtype)
+    pad[:N, :Kh] = rows
+    out = pad.reshape(nb, 16, kb, 64).swapaxes(1, 2)
+    return out.contiguous() if hasattr(out, "contiguous") else out.copy()
+
+
+def row_major_weight_codes(blocked, N, K):
+    """The inverse of blocked_weight_codes: [N, K/2] row-major codes."""
+    nb, kb, _, _ = weight_codes_shape(N, K)
+    rows = blocked.reshape(nb, kb, 16, 64).swapaxes(1, 2).reshape(16 * nb, 64 * kb)
+    return rows[:N, :K // 2]
 
 
 def offq_kv_attention_decode_gqa_raw(q, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, B, Hq,
@@ -308,7 +344,7 @@ def offq_w4a4_gemm(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, g, debu
     _need(a_codes, torch.uint8, "a_codes", 2)
     _need(a_scale, torch.float16, "a_scale", 2)
     _need(a_zero, torch.int16, "a_zero", 2)
-    _need(w_codes, torch.uint8, "w_codes", 2)
+    _need(w_codes, torch.uint8, "w_codes")
     _need(w_scale, torch.float16, "w_scale", 1)
     _need(w_colsum, torch.int32, "w_colsum", 2)
     for t, n in ((a_codes, "a_codes"), (a_scale, "a_scale"), (a_zero, "a_zero"), (w_codes, "w_codes"),
@@ -316,10 +352,10 @@ def offq_w4a4_gemm(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, g, debu
         if not t.is_contiguous():
             raise ValueError(f"{n} must be contiguous")
     M, Kh = a_codes.shape
-    N = w_codes.shape[0]
+    N = w_scale.shape[0]
     K = 2 * Kh
-    if w_codes.shape[1] != Kh or a_scale.shape != (M, K // g) or a_zero.shape != (M, K // g) \
-            or w_scale.shape != (N,) or w_colsum.shape != (K // g, N):
+    if w_codes.numel() != lib.offq_weight_codes_bytes(N, K) or a_scale.shape != (M, K // g) \
+            or a_zero.shape != (M, K // g) or w_colsum.shape != (K // g, N):
         raise ValueError("operand shapes do not match")
     dev = a_codes.device
     y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=dev)
@@ -357,15 +393,16 @@ def offq_kv_quantize(kv, apply_hadamard=True, debug=False):
 
 
 def offq_pack_weights(w, g):
-    """w: fp32 [N, K] contiguous.  Returns (w_codes u8 [N, K/2], w_scale fp16 [N],
-    w_colsum int32 [K/g, N])."""
+    """w: fp32 [N, K] contiguous.  Returns (w_codes u8 in the blocked operand
+    layout, shape weight_codes_shape(N, K), w_scale fp16 [N], w_colsum int32
+    [K/g, N])."""
     torch = _torch()
     _need(w, torch.float32, "w", 2)
     if not w.is_contiguous():
         raise ValueError("w must be contiguous")
     N, K = w.shape
     dev = w.device
-    wc = torch.empty((N, K // 2), dtype=torch.uint8, device=dev)
+    wc = torch.empty(weight_codes_shape(N, K), dtype=torch.uint8, device=dev)
     ws = torch.empty((N,), dtype=torch.float16, device=dev)
     cs = torch.empty((K // g, N), dtype=torch.int32, device=dev)
     _check(lib.offq_pack_weights(_ptr(w), N, K, int(g), _ptr(wc), _ptr(ws), _ptr(cs), _stream()),

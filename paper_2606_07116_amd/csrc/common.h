@@ -6,6 +6,21 @@
 
 namespace offq {
 
+// Weight operand layout (written by offq_pack_weights, read by the GEMM and
+// GEMV kernels): the packed codes of 16 output rows x 128 k form a 1 KB block
+// (16 rows of 64 bytes); the blocks of a band of 16 rows follow in k order and
+// the bands in row order.  Rows past N up to a multiple of 16, and k past K up
+// to a multiple of 128, hold zero codes.  A wave that loads 16 bytes per lane
+// of one block reads 1 KB of contiguous memory.
+__host__ __device__ constexpr int64_t wblk_kblocks(int64_t K) { return (K + 127) >> 7; }
+__host__ __device__ constexpr int64_t wblk_bytes(int64_t N, int64_t K) {
+  return ((N + 15) >> 4) * wblk_kblocks(K) * 1024;
+}
+// byte offset of code byte kk (codes 2 kk, 2 kk + 1) of row n; KB = wblk_kblocks(K)
+__host__ __device__ inline int64_t wblk_off(int64_t n, int64_t kk, int64_t KB) {
+  return ((((n >> 4) * KB + (kk >> 6)) << 10) | ((n & 15) << 6) | (kk & 63));
+}
+
 // bf16 bit pattern -> fp32 (exact).
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include "../../include/offq.h"
+#include "common.h"
 #include "internal.h"
 
 namespace {
@@ -160,6 +161,11 @@ offq_status_t offq_w4a4_gemm(const uint8_t* a_codes, const uint16_t* a_scale, co
     e = offq::launch_w4a4_gemm(a_codes, a_scale, a_zero, w_codes, w_scale, w_colsum, M, N, K, lg,
                                y, ldy, acc_debug, (hipStream_t)stream);
   return launched(e, M <= 16 ? "w4a4_gemv" : "w4a4_gemm");
+}
+
+int64_t offq_weight_codes_bytes(int64_t N, int64_t K) {
+  if (N <= 0 || K <= 0 || N > (1 << 30) || K > (1 << 30)) return 0;
+  return offq::wblk_bytes(N, K);
 }
 
 offq_status_t offq_pack_weights(const float* w, int64_t N, int64_t K, int32_t g, uint8_t* w_codes,

@@ -1,7 +1,8 @@
 // Offline weight packing: per-output-channel symmetric 4-bit quantization
 // (sec. 4, implementation: weights per-channel symmetric) into the operand
 // format of the W4A4 GEMM, plus the per-group column sums the epilogue uses
-// for the zero-point correction.
+// for the zero-point correction.  The codes go to the blocked operand layout
+// (1 KB blocks of 16 rows x 128 k; padding rows and k written as zero codes).
 //
 //   sw[n]   = fp16_rne(clamp(max_k |w[n,k]| / 7, 2^-24, 65504))   (1 for a zero row)
 //   q[n,k]  = clamp(rne(w[n,k] / sw[n]), -8, 7)       (quotient evaluated in fp64;
@@ -23,6 +24,15 @@ __global__ __launch_bounds__(PW_THREADS) void pack_weights_kernel(
   __shared__ int gsum[PW_MAX_GROUPS];
   const int64_t n = blockIdx.x;
   const int tid = threadIdx.x;
+  const int64_t KB = wblk_kblocks(K);
+  if (n >= N) {  // padding rows of the last band: zero codes
+    for (int64_t kk = tid * 4; kk < KB * 64; kk += PW_THREADS * 4)
+      *reinterpret_cast<uint32_t*>(wc + wblk_off(n, kk, KB)) = 0u;
+    return;
+  }
+  // padding k of the row's last block
+  for (int64_t kk = (K >> 1) + tid * 4; kk < KB * 64; kk += PW_THREADS * 4)
+    *reinterpret_cast<uint32_t*>(wc + wblk_off(n, kk, KB)) = 0u;
   const float* row = w + n * K;
   const int G = (int)(K >> log2g);
 
@@ -63,7 +73,7 @@ __global__ __launch_bounds__(PW_THREADS) void pack_weights_kernel(
       sum += qi;
       packed |= ((uint32_t)qi & 0xfu) << (4 * j);
     }
-    *reinterpret_cast<uint32_t*>(wc + n * (K >> 1) + (k >> 1)) = packed;
+    *reinterpret_cast<uint32_t*>(wc + wblk_off(n, k >> 1, KB)) = packed;
     atomicAdd(&gsum[(int)(k >> log2g)], sum);
   }
   __syncthreads();
@@ -76,7 +86,7 @@ hipError_t launch_pack_weights(const float* w, int64_t N, int64_t K, int log2g,
                                uint8_t* w_codes, uint16_t* w_scale,
                                int32_t* w_colsum, hipStream_t stream) {
   if ((K >> log2g) > PW_MAX_GROUPS) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(pack_weights_kernel, dim3((unsigned)N), dim3(PW_THREADS), 0, stream, w,
+  hipLaunchKernelGGL(pack_weights_kernel, dim3((unsigned)((N + 15) / 16 * 16)), dim3(PW_THREADS), 0, stream, w,
                      N, K, log2g, w_codes, w_scale, w_colsum);
   return hipGetLastError();
 }

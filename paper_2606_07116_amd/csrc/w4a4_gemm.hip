@@ -82,7 +82,10 @@ __global__ __launch_bounds__(256) void w4a4_gemm_kernel(
   const bool a_ok = tm + lrow < M;
   const bool b_ok = tn + lrow < N;
   const uint8_t* a_src = A + (int64_t)(a_ok ? tm + lrow : 0) * ldk + lhalf * 16;
-  const uint8_t* b_src = W + (int64_t)(b_ok ? tn + lrow : 0) * ldk + lhalf * 16;
+  // weights in the blocked layout: k-step kit of row r is bytes 32 kit + 16 lhalf
+  const int64_t KB = wblk_kblocks(K);
+  const int64_t b_row = b_ok ? tn + lrow : 0;
+  auto b_src = [&](int kit) { return W + wblk_off(b_row, 32 * kit + 16 * lhalf, KB); };
   const int st = slot(lrow, lhalf);
 
   const int fr = lane & 31, fh = lane >> 5;
@@ -100,7 +103,7 @@ __global__ __launch_bounds__(256) void w4a4_gemm_kernel(
 
   const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
   uint4 ra = a_ok ? *reinterpret_cast<const uint4*>(a_src) : z4;
-  uint4 rb = b_ok ? *reinterpret_cast<const uint4*>(b_src) : z4;
+  uint4 rb = b_ok ? *reinterpret_cast<const uint4*>(b_src(0)) : z4;
   As[0][st] = ra;
   Bs[0][st] = rb;
   __syncthreads();
@@ -109,7 +112,7 @@ __global__ __launch_bounds__(256) void w4a4_gemm_kernel(
     const int buf = kit & 1;
     if (kit + 1 < nk) {
       ra = a_ok ? *reinterpret_cast<const uint4*>(a_src + (int64_t)(kit + 1) * 32) : z4;
-      rb = b_ok ? *reinterpret_cast<const uint4*>(b_src + (int64_t)(kit + 1) * 32) : z4;
+      rb = b_ok ? *reinterpret_cast<const uint4*>(b_src(kit + 1)) : z4;
     }
     v4i alo[2], ahi[2], blo[2], bhi[2];
 #pragma unroll
@@ -217,7 +220,7 @@ __global__ __launch_bounds__(256) void w4a4_gemv_kernel(
   if (n >= N) return;  // wave-uniform
   const int64_t ldk = K >> 1;
   const int G = K >> log2g;
-  const uint8_t* wrow = W + (int64_t)n * ldk;
+  const int64_t KB = wblk_kblocks(K);               // weights in the blocked layout
   const int nchunks = (int)(ldk >> 4);            // 16-byte chunks (32 k) per row
   const int seg = 1 << min(log2g - 5, 6);        // lanes of one group in one pass
   const int passes = (nchunks + 63) >> 6;
@@ -232,7 +235,7 @@ __global__ __launch_bounds__(256) void w4a4_gemv_kernel(
   for (int p = 0; p < passes; ++p) {
     const int c = (p << 6) + lane;
     const bool live = c < nchunks;  // a dead lane's zero weights add nothing
-    const uint4 w = live ? *reinterpret_cast<const uint4*>(wrow + (int64_t)c * 16) : z4;
+    const uint4 w = live ? *reinterpret_cast<const uint4*>(W + wblk_off(n, (int64_t)c * 16, KB)) : z4;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       if (m < M) {

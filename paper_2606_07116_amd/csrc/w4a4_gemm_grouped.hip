@@ -156,7 +156,10 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   // s % 4 (16 bytes = 32 k); rows past M (N) read as zero.
   const uint8_t* pbase = XW ? A + (int64_t)tm * ldk : W + (int64_t)tn * ldk;
   const uint8_t* xbase = XW ? W + (int64_t)tn * ldk : A + (int64_t)tm * ldk;
-  const int prows = XW ? M - tm : N - tn, xrows = XW ? N - tn : M - tm;
+  // (weights: bands of 16 rows of the blocked layout, K a multiple of 128, so a
+  // band is 16 ldk bytes; the padding rows of the last band hold zero codes)
+  const int wrows = (N - tn + 15) & ~15;
+  const int prows = XW ? M - tm : wrows, xrows = XW ? wrows : M - tm;
   const __amdgpu_buffer_rsrc_t prsrc = __builtin_amdgcn_make_buffer_rsrc(
       (void*)pbase, 0, (int)((int64_t)prows * ldk), 0x00020000);
   const __amdgpu_buffer_rsrc_t xrsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -165,8 +168,10 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   const __amdgpu_buffer_rsrc_t prsrc0 = __builtin_amdgcn_make_buffer_rsrc((void*)pbase, 0, 0, 0x00020000);
   const __amdgpu_buffer_rsrc_t xrsrc0 = __builtin_amdgcn_make_buffer_rsrc((void*)xbase, 0, 0, 0x00020000);
   const int crow = tid >> 2, cch = tid & 3;
-  const int voff = crow * (int)ldk + cch * 16;
-  const int vstep = (C::THREADS / 4) * (int)ldk;  // 128 rows
+  const int voff_a = crow * (int)ldk + cch * 16;
+  const int voff_w = (crow >> 4) * 16 * (int)ldk + (crow & 15) * 64 + cch * 16;
+  const int pvoff = XW ? voff_a : voff_w, xvoff = XW ? voff_w : voff_a;
+  const int vstep = (C::THREADS / 4) * (int)ldk;  // 128 rows (8 weight bands)
   constexpr int NLD = C::P_LD + C::X_LD;
   v4i rgb[C::NRB][NLD];   // stages in flight
   v4i ra[NLD], rb[NLD];    // stages 0 and 1 in the prologue
@@ -174,13 +179,15 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   auto gload = [&](int st, v4i (&rg)[NLD]) __attribute__((always_inline)) {
     const bool ok = st < nst;
     const __amdgpu_buffer_rsrc_t pr = ok ? prsrc : prsrc0, xr = ok ? xrsrc : xrsrc0;
+    // a stage is 64 bytes of an activation row, one 1 KB block of a weight band
     const int soff = ok ? st * (C::KSTAGE / 2) : 0;
+    const int psoff = XW ? soff : 16 * soff, xsoff = XW ? 16 * soff : soff;
 #pragma unroll
     for (int i = 0; i < C::P_LD; ++i)
-      rg[i] = __builtin_amdgcn_raw_buffer_load_b128(pr, voff + i * vstep, soff, 0);
+      rg[i] = __builtin_amdgcn_raw_buffer_load_b128(pr, pvoff + i * vstep, psoff, 0);
 #pragma unroll
     for (int i = 0; i < C::X_LD; ++i)
-      rg[C::P_LD + i] = __builtin_amdgcn_raw_buffer_load_b128(xr, voff + i * vstep, soff, 0);
+      rg[C::P_LD + i] = __builtin_amdgcn_raw_buffer_load_b128(xr, xvoff + i * vstep, xsoff, 0);
   };
   // element index of this thread's chunk in slot 0 (row crow + 128 i adds
   // 512 i packed / 1024 i unpacked slots: the swizzles repeat every 128 rows)

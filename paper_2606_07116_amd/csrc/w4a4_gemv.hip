@@ -74,14 +74,17 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
 
 
   // rows past N (weights) and past M (tokens) read as zero
+  // (weights: the tile's bands of the blocked layout, K a multiple of 128, so a
+  // band is 16 ldk bytes; the padding rows of the last band hold zero codes)
   const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(W + (int64_t)n0 * ldk), 0, (int)((int64_t)min(16 * T, N - n0) * ldk), 0x00020000);
+      (void*)(W + (int64_t)n0 * ldk), 0, (int)((int64_t)((min(16 * T, N - n0) + 15) & ~15) * ldk),
+      0x00020000);
   const __amdgpu_buffer_rsrc_t arsrc =
       __builtin_amdgcn_make_buffer_rsrc((void*)A, 0, M * ldk, 0x00020000);
   const int a_off = r16 * ldk + (k0 >> 1) + 16 * kb;
   int w_off[T];
 #pragma unroll
-  for (int t = 0; t < T; ++t) w_off[t] = (16 * t + r16) * ldk + (k0 >> 1) + 16 * kb;
+  for (int t = 0; t < T; ++t) w_off[t] = (t * (K >> 7) + (k0 >> 7)) * 1024 + r16 * 64 + 16 * kb;
 
   v4i acc[T];
   float F[T][4];
@@ -131,7 +134,7 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
       aa[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(arsrc, a_off, so, 0));
 #pragma unroll
       for (int t = 0; t < T; ++t)
-        wa[u][t] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wrsrc, w_off[t], so, 0));
+        wa[u][t] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wrsrc, w_off[t], 16 * so, 0));
     }
   };
   const int gmask = (1 << (log2g - 7)) - 1;  // steps per group - 1
@@ -237,9 +240,13 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
 }  // namespace
 
 // Launch shape (T row tiles per wave, K in P parts, BATCH steps per load
-// batch), as measured at M = 16 (g = 128 ... 8192): wide layers (>= 16384
-// channels) take four row tiles per wave (one activation load serves four
-// weight loads) and K in quarters; narrower ones need more waves in flight:
+// batch), as measured at M = 16 (g = 128 ... 8192) on the blocked weight
+// layout: wide layers (>= 16384 channels) take two row tiles per wave and K
+// in eighths, batches of two steps (8192 -> 28672: 27.0 -> 25.1 us at
+// M = 16, 27.0 -> 22.8 at M = 1, against four tiles and K in quarters, the
+// best shape of the row-major layout; the same at 4096 -> 28672), or four
+// tiles and K in quarters when K is not a multiple of 2048; narrower ones
+// need more waves in flight:
 // K in eighths with two tiles per wave from 6144 channels, one below, where K
 // splits into eighths of whole batches (from K = 16384 with two tiles: K in
 // sixteenths, batches of two steps: 26.7-27.8 against 29.9-31.4 us at
@@ -251,7 +258,8 @@ __global__ __launch_bounds__(64 * P) void w4a4_gemv_kernel(
 // of one step and K in as many parts (4, 2, 1) as it divides into.
 static void gemv_shape(int64_t N, int64_t K, int& T, int& P, int& B) {
   if (N >= 16384) {
-    T = 4, P = 4, B = 2;
+    if (K % 2048 == 0) T = 2, P = 8, B = 2;
+    else T = 4, P = 4, B = 2;
   } else if (K % 4096 == 0) {
     T = N >= 6144 ? 2 : 1, P = T == 2 && K >= 16384 ? 16 : 8;
     B = P == 16 ? 2 : 4;
@@ -323,6 +331,7 @@ hipError_t launch_w4a4_gemv_mfma(const uint8_t* a_codes, const uint16_t* a_scale
   }
   if (T == 4) OFFQ_GV(4, 4, 2);
   if (T == 2 && P == 16) OFFQ_GV(2, 16, 2);
+  if (T == 2 && B == 2) OFFQ_GV(2, 8, 2);
   if (T == 2) OFFQ_GV(2, 8, 4);
   if (P == 8) OFFQ_GV(1, 8, 4);
   OFFQ_GV(1, 4, 4);

@@ -96,7 +96,9 @@ def oracle_weights(w, g):
 
 
 def upload_weights(packed, sw, cs):
-    return (torch.from_numpy(packed).to(DEV), torch.from_numpy(sw).to(DEV),
+    """Row-major oracle codes [N, K/2] uploaded in the blocked operand layout."""
+    from paper_2606_07116_amd import _lib
+    return (torch.from_numpy(_lib.blocked_weight_codes(packed)).to(DEV), torch.from_numpy(sw).to(DEV),
             torch.from_numpy(cs).to(DEV))
 
 

@@ -4,7 +4,9 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
+import torch
 
 from paper_2606_07116_amd import _lib
 
@@ -255,3 +257,25 @@ def test_rope_kv_prefill_validation():
     a = list(args)
     a[2] = 0  # no sequences: nothing to do
     assert L.offq_rope_kv_prefill_raw(*a) == L.OFFQ_OK
+
+
+@pytest.mark.parametrize("N,K", [(1, 64), (16, 128), (17, 192), (300, 4096), (33, 8320)])
+def test_blocked_weight_layout(N, K):
+    """The blocked operand layout of the packed weights (include/offq.h,
+    offq_pack_weights): byte kk of row n at ((n / 16) KB + kk / 64) 1024 +
+    (n % 16) 64 + kk % 64, KB = ceil(K / 128), zero padding, and the
+    conversions to and from row-major codes are inverse."""
+    rng = np.random.default_rng(N * 7 + K)
+    rows = rng.integers(0, 256, size=(N, K // 2), dtype=np.uint8)
+    blk = _lib.blocked_weight_codes(rows)
+    KB = -(-K // 128)
+    assert blk.shape == _lib.weight_codes_shape(N, K) == (-(-N // 16), KB, 16, 64)
+    assert blk.size == _lib.offq_weight_codes_bytes(N, K) == -(-N // 16) * KB * 1024
+    flat = blk.reshape(-1)
+    for n, kk in [(0, 0), (N - 1, K // 2 - 1), (N // 2, K // 4), (min(15, N - 1), min(63, K // 2 - 1))]:
+        assert flat[((n // 16) * KB + kk // 64) * 1024 + (n % 16) * 64 + kk % 64] == rows[n, kk]
+    assert int(flat.astype(np.int64).sum()) == int(rows.astype(np.int64).sum())  # zero padding
+    assert np.array_equal(_lib.row_major_weight_codes(blk, N, K), rows)
+    t = torch.from_numpy(rows)
+    assert np.array_equal(_lib.blocked_weight_codes(t).numpy(), blk)
+    assert _lib.offq_weight_codes_bytes(0, K) == 0 and _lib.offq_weight_codes_bytes(N, 0) == 0

@@ -76,7 +76,7 @@ def test_out_must_cover_the_output():
     codes = torch.zeros((M, K // 2), dtype=torch.uint8, device=P.DEV)
     sc = torch.ones((M, 1), dtype=torch.float16, device=P.DEV)
     zp = torch.zeros((M, 1), dtype=torch.int16, device=P.DEV)
-    wc = torch.zeros((N, K // 2), dtype=torch.uint8, device=P.DEV)
+    wc = torch.zeros(offq.weight_codes_shape(N, K), dtype=torch.uint8, device=P.DEV)
     ws = torch.ones(N, dtype=torch.float16, device=P.DEV)
     cs = torch.zeros((1, N), dtype=torch.int32, device=P.DEV)
     short = torch.empty((M - 1, N), dtype=torch.bfloat16, device=P.DEV)
@@ -159,7 +159,8 @@ def test_empty_m_is_noop():
     e = torch.empty((0, K // 2), dtype=torch.uint8, device=P.DEV)
     y, _ = offq.offq_w4a4_gemm(e, torch.empty((0, 1), dtype=torch.float16, device=P.DEV),
                                torch.empty((0, 1), dtype=torch.int16, device=P.DEV),
-                               torch.zeros((N, K // 2), dtype=torch.uint8, device=P.DEV),
+                               torch.zeros(offq.weight_codes_shape(N, K), dtype=torch.uint8,
+                                           device=P.DEV),
                                torch.ones(N, dtype=torch.float16, device=P.DEV),
                                torch.zeros((1, N), dtype=torch.int32, device=P.DEV), g)
     assert y.shape == (0, N)
@@ -174,5 +175,8 @@ def test_pack_weights(N, K, g):
     wc, ws, wcs = offq.offq_pack_weights(torch.from_numpy(w).to(P.DEV), g)
     torch.cuda.synchronize()
     assert np.array_equal(P.fp16_bits(P.host(ws)), P.fp16_bits(sw))
-    assert np.array_equal(P.host(wc), packed)
+    assert tuple(wc.shape) == offq.weight_codes_shape(N, K)
+    assert np.array_equal(offq.row_major_weight_codes(P.host(wc), N, K), packed)
+    # the padding rows and k of the blocked layout hold zero codes
+    assert int(P.host(wc).astype(np.int64).sum()) == int(packed.astype(np.int64).sum())
     assert np.array_equal(P.host(wcs), cs)
