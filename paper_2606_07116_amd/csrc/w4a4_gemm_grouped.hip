@@ -153,7 +153,9 @@ __global__ __launch_bounds__(512) void w4a4_gemm_grouped_kernel(
   };
   // ---- global -> registers -> LDS staging -----------------------------------
   // Chunk s = tid + 512 i of an operand's stage is row s / 4, packed chunk
-  // s % 4 (16 bytes = 32 k); rows past M (N) read as zero.
+  // s % 4 (16 bytes = 32 k); rows past M (N) read as zero.  Activation rows
+  // are row-major (stride K / 2); the weights are in the blocked layout, where
+  // a stage of a row is 64 bytes of a 1 KB block of 16 rows.
   const uint8_t* pbase = XW ? A + (int64_t)tm * ldk : W + (int64_t)tn * ldk;
   const uint8_t* xbase = XW ? W + (int64_t)tn * ldk : A + (int64_t)tm * ldk;
   // (weights: bands of 16 rows of the blocked layout, K a multiple of 128, so a

@@ -13,7 +13,8 @@
 //   waves split K and their fp32 partial sums are added through LDS at the
 //   end.
 // * Per step of 128 k every lane loads 16 packed bytes of one weight row per
-//   tile (lane l: row l % 16, k-block l / 16; 64-byte row segments) and the
+//   tile (lane l: row l % 16, k-block l / 16: the wave reads one 1 KB block
+//   of the blocked weight layout, contiguous in memory) and the
 //   same 16 bytes of its token row l % 16 (rows >= M read as zero through the
 //   buffer descriptor), and runs two MFMAs per tile (low and high nibbles, the
 //   same k-permutation on both operands).  Weight nibbles are widened to 16 q.
